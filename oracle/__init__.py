@@ -1,0 +1,22 @@
+"""Float64 CPU oracle of the fused sub-kernels and the stitched block.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  The library's
+product path (``paper_2609_30059_amd``) never imports it and shares no code
+with it; the two meet only through the seeded inputs of ``fusedsub_data``.
+
+Parity status: every function here is pinned by the CPU tests
+``tests/test_oracle_*.py`` to closed forms, invariants, special cases and
+printed reference values (``tests/golden/``).
+"""
+from .subkernels import (ACTS, apply_act, causal_mask, gelu_erf, gemm_epilogue_reduce,
+                         layernorm_residual, pointwise_chain, relu, residual_store_bf16,
+                         round_to_bf16, row_softmax, sigmoid)
+from .block import block_forward, block_forward_sequence, STAGES
+
+__all__ = [
+    "ACTS", "apply_act", "causal_mask", "gelu_erf", "gemm_epilogue_reduce",
+    "layernorm_residual", "pointwise_chain", "relu", "residual_store_bf16",
+    "round_to_bf16", "row_softmax", "sigmoid", "block_forward",
+    "block_forward_sequence", "STAGES",
+]

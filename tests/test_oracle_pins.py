@@ -1,0 +1,410 @@
+"""Pins of the float64 oracle against values and identities fixed by the
+paper's definitions and by mathematics -- never against the oracle itself
+re-typed.  CPU only.
+
+Each group is built so that a plausible mistake in the oracle (a dropped
+term, a wrong sign or constant, a wrong axis, a swapped order of operations)
+fails at least one test; the mistake each test catches is named in it.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from conftest import read_golden
+
+GOLD = read_golden("normal_cdf.txt")
+PHI = {float(z): float(v) for k, z, v in GOLD if k == "phi"}
+ERF = {float(z): float(v) for k, z, v in GOLD if k == "erf"}
+
+
+# ---------------------------------------------------------------------------
+# activations
+# ---------------------------------------------------------------------------
+class TestGelu:
+    def test_table_values(self):
+        # GELU(z) = z * Phi(z); catches erf(z/2) or erf(z) for erf(z/sqrt 2),
+        # a missing factor 1/2 and a missing "1 +".
+        for z, phi in PHI.items():
+            assert oracle.gelu_erf(z) == pytest.approx(z * phi, abs=2e-15)
+            assert oracle.gelu_erf(-z) == pytest.approx(-z * (1.0 - phi), abs=2e-15)
+
+    def test_erf_table(self):
+        from scipy.special import erf
+        for z, v in ERF.items():
+            assert erf(z) == pytest.approx(v, abs=1e-15)
+
+    def test_zero_and_odd_part(self):
+        assert oracle.gelu_erf(0.0) == 0.0
+        z = np.linspace(-6, 6, 1001)
+        # Phi(z) + Phi(-z) = 1  =>  GELU(z) - GELU(-z) = z
+        np.testing.assert_allclose(oracle.gelu_erf(z) - oracle.gelu_erf(-z), z,
+                                   rtol=0, atol=1e-14)
+
+    def test_tails(self):
+        assert oracle.gelu_erf(12.0) == 12.0
+        g = oracle.gelu_erf(-12.0)
+        assert g <= 0.0 and g > -1e-30
+
+
+class TestSigmoid:
+    def test_closed_forms(self):
+        assert oracle.sigmoid(0.0) == 0.5
+        for k in (2.0, 3.0, 7.0, 99.0):       # sigma(ln k) = k / (k + 1)
+            assert oracle.sigmoid(math.log(k)) == pytest.approx(k / (k + 1), rel=1e-15)
+            assert oracle.sigmoid(-math.log(k)) == pytest.approx(1 / (k + 1), rel=1e-14)
+
+    def test_symmetry_and_extremes(self):
+        t = np.linspace(-30, 30, 601)
+        np.testing.assert_allclose(oracle.sigmoid(-t), 1 - oracle.sigmoid(t), atol=1e-15)
+        assert oracle.sigmoid(-1000.0) == 0.0
+        assert oracle.sigmoid(1000.0) == 1.0
+
+
+# ---------------------------------------------------------------------------
+# a1 pointwise chain
+# ---------------------------------------------------------------------------
+class TestPointwise:
+    def test_order_scale_bias_act_residual(self):
+        x = np.array([[1.0]])
+        # scale before bias: 1*2 + 1 = 3 (not (1+1)*2 = 4)
+        y = oracle.pointwise_chain(x, np.array([1.0]), None, 2.0, "none")
+        assert y[0, 0] == 3.0
+        # residual after the activation: GELU(1) + 1 = Phi(1) + 1 (not GELU(2))
+        y = oracle.pointwise_chain(np.array([[0.0]]), np.array([1.0]), np.array([[1.0]]),
+                                   1.0, "gelu_erf")
+        assert y[0, 0] == pytest.approx(PHI[1.0] + 1.0, abs=2e-15)
+
+    def test_bias_broadcasts_per_column(self):
+        x = np.zeros((2, 3))
+        b = np.array([1.0, 2.0, 3.0])
+        y = oracle.pointwise_chain(x, b, None, 1.0, "none")
+        np.testing.assert_array_equal(y, [[1, 2, 3], [1, 2, 3]])
+
+    def test_zero_scale_bias_gives_residual(self):
+        rng = np.random.default_rng(0)
+        x, r = rng.standard_normal((4, 5)), rng.standard_normal((4, 5))
+        y = oracle.pointwise_chain(x, np.zeros(5), r, 0.0, "gelu_erf")
+        np.testing.assert_array_equal(y, r)
+
+    def test_acts(self):
+        x = np.array([[-2.0, -0.5, 0.0, 0.5, 2.0]])
+        np.testing.assert_array_equal(oracle.pointwise_chain(x, None, None, 1.0, "relu"),
+                                      [[0, 0, 0, 0.5, 2.0]])
+        np.testing.assert_allclose(
+            oracle.pointwise_chain(x, None, None, 1.0, "sigmoid"),
+            [[1 / (1 + math.exp(2)), 1 / (1 + math.exp(0.5)), 0.5,
+              1 / (1 + math.exp(-0.5)), 1 / (1 + math.exp(-2))]], rtol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# a2 row softmax
+# ---------------------------------------------------------------------------
+class TestSoftmax:
+    def test_known_row_and_scale(self):
+        # exp of [0, ln2, ln3] is [1, 2, 3]: softmax = [1/6, 2/6, 3/6].  The
+        # logits are given doubled with scale 1/2, so a divide-by-scale or a
+        # dropped scale fails.
+        x = np.array([[0.0, 2 * math.log(2), 2 * math.log(3)]])
+        y = oracle.row_softmax(x, None, 0.5)
+        np.testing.assert_allclose(y, [[1 / 6, 2 / 6, 3 / 6]], rtol=1e-14)
+
+    def test_large_logits_do_not_overflow(self):
+        # exp(1000) overflows float64: the max must be subtracted first
+        y = oracle.row_softmax(np.array([[1000.0, 1000.0 + math.log(3)]]), None, 1.0)
+        np.testing.assert_allclose(y, [[0.25, 0.75]], rtol=1e-13)
+
+    def test_rows_sum_to_one_along_last_axis(self):
+        rng = np.random.default_rng(1)
+        x = rng.standard_normal((5, 7)) * 3
+        y = oracle.row_softmax(x, None, 0.125)
+        np.testing.assert_allclose(y.sum(axis=1), 1.0, atol=1e-14)
+        assert not np.allclose(y.sum(axis=0), 1.0)
+
+    def test_shift_invariance(self):
+        rng = np.random.default_rng(2)
+        x = rng.standard_normal((6, 9)) * 3
+        c = rng.standard_normal((6, 1)) * 100
+        np.testing.assert_allclose(oracle.row_softmax(x + c, None, 1.0),
+                                   oracle.row_softmax(x, None, 1.0), atol=1e-13)
+
+    def test_mask_uniform_and_pairs(self):
+        ninf = -np.inf
+        x = np.array([[5.0, 5.0, 5.0, 5.0], [1.0, 2.0, 3.0, 4.0]])
+        mask = np.array([[0.0, ninf, 0.0, 0.0], [ninf, 0.0, ninf, 0.0]])
+        y = oracle.row_softmax(x, mask, 1.0)
+        np.testing.assert_allclose(y[0], [1 / 3, 0, 1 / 3, 1 / 3], rtol=1e-15)
+        # two unmasked entries: logistic of the difference
+        np.testing.assert_allclose(y[1], [0, 1 / (1 + math.e ** 2), 0, 1 / (1 + math.e ** -2)],
+                                   rtol=1e-14)
+        assert y[0, 1] == 0.0 and y[1, 0] == 0.0 and y[1, 2] == 0.0
+
+    def test_fully_masked_row_is_zero(self):
+        y = oracle.row_softmax(np.ones((1, 3)), np.full((1, 3), -np.inf), 1.0)
+        np.testing.assert_array_equal(y, 0.0)
+
+    def test_causal_square(self):
+        rng = np.random.default_rng(3)
+        s = 6
+        x = rng.standard_normal((2 * s, s))       # two heads stacked as rows
+        y = oracle.row_softmax(x, None, 1.0, causal_q_len=s)
+        for r in range(2 * s):
+            t = r % s
+            assert np.all(y[r, t + 1:] == 0.0)
+            assert y[r, :t + 1].sum() == pytest.approx(1.0, abs=1e-15)
+        np.testing.assert_array_equal(y[0], [1, 0, 0, 0, 0, 0])     # row 0 one-hot
+        np.testing.assert_array_equal(y[s], [1, 0, 0, 0, 0, 0])
+        d = x[1, 0] - x[1, 1]
+        np.testing.assert_allclose(y[1, :2], [1 / (1 + math.exp(-d)), 1 / (1 + math.exp(d))],
+                                   rtol=1e-14)
+
+    def test_causal_rectangular_offset(self):
+        # q_len 2 queries over 5 keys: query i sees keys 0 .. i + 3
+        m = oracle.causal_mask(4, 5, 2)
+        np.testing.assert_array_equal(m, [[0, 0, 0, 0, 1], [0, 0, 0, 0, 0],
+                                          [0, 0, 0, 0, 1], [0, 0, 0, 0, 0]])
+
+
+# ---------------------------------------------------------------------------
+# a3 LayerNorm + residual
+# ---------------------------------------------------------------------------
+class TestLayerNorm:
+    def test_hand_example(self):
+        # h = [1,2,3,4]: mean 2.5, biased variance 1.25 (unbiased would be 5/3)
+        y, h = oracle.layernorm_residual(np.array([[1.0, 2.0, 3.0, 4.0]]), None, None, None, 0.0)
+        v = 1.5 / math.sqrt(1.25)
+        np.testing.assert_allclose(y, [[-v, -v / 3, v / 3, v]], rtol=1e-15)
+
+    def test_two_elements_biased_variance_and_affine(self):
+        y, _ = oracle.layernorm_residual(np.array([[1.0, 3.0]]), None, None, None, 0.0)
+        np.testing.assert_array_equal(y, [[-1.0, 1.0]])
+        y, _ = oracle.layernorm_residual(np.array([[1.0, 3.0]]), None,
+                                         np.array([2.0, 3.0]), np.array([5.0, 7.0]), 0.0)
+        np.testing.assert_array_equal(y, [[3.0, 10.0]])       # gamma then beta, per column
+
+    def test_eps_inside_sqrt(self):
+        # variance of the normalised row is var / (var + eps) exactly
+        rng = np.random.default_rng(4)
+        h = rng.standard_normal((3, 64))
+        eps = 0.25
+        y, _ = oracle.layernorm_residual(h, None, None, None, eps)
+        var = np.var(h, axis=1)
+        np.testing.assert_allclose(y.mean(axis=1), 0.0, atol=1e-15)
+        np.testing.assert_allclose(np.var(y, axis=1), var / (var + eps), rtol=1e-13)
+
+    def test_constant_row_gives_beta_and_residual_is_added(self):
+        rng = np.random.default_rng(5)
+        x = rng.standard_normal((2, 8))
+        beta = rng.standard_normal(8)
+        gamma = rng.standard_normal(8)
+        y, h = oracle.layernorm_residual(x, 3.0 - x, gamma, beta, 1e-5)
+        np.testing.assert_allclose(h, 3.0, atol=1e-15)
+        np.testing.assert_allclose(y, np.broadcast_to(beta, (2, 8)), atol=1e-10)
+
+    def test_scale_invariance_eps0(self):
+        rng = np.random.default_rng(6)
+        h = rng.standard_normal((4, 33))
+        a, _ = oracle.layernorm_residual(h, None, None, None, 0.0)
+        b, _ = oracle.layernorm_residual(7.5 * h, None, None, None, 0.0)
+        np.testing.assert_allclose(a, b, atol=1e-13)
+
+    def test_round_to_bf16_known_values(self):
+        f = oracle.round_to_bf16
+        assert f(1.0 + 2 ** -8) == 1.0                      # tie -> even (down)
+        assert f(1.0 + 3 * 2 ** -8) == 1.0 + 2 ** -6        # tie -> even (up)
+        assert f(1.0 + 2 ** -8 + 2 ** -20) == 1.0 + 2 ** -7  # above the tie
+        assert f(-(1.0 + 2 ** -8)) == -1.0
+        assert f(2.0 ** -133) == 2.0 ** -133               # smallest subnormal
+        assert f(2.0 ** -135) == 0.0
+        assert f(3.0e38 * 2) == np.inf
+
+    def test_round_to_bf16_matches_library_cast(self):
+        rng = np.random.default_rng(7)
+        v = np.concatenate([rng.standard_normal(20000).astype(np.float32),
+                            (rng.standard_normal(2000) * 1e-39).astype(np.float32),
+                            np.float32(1.0) + np.float32(2.0 ** -8) * np.arange(64,
+                                                                              dtype=np.float32)])
+        ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+        np.testing.assert_array_equal(oracle.round_to_bf16(v.astype(np.float64)), ref)
+
+    def test_residual_store_is_rounded_fp32_sum(self):
+        rng = np.random.default_rng(8)
+        xb = torch.from_numpy(rng.standard_normal(5000).astype(np.float32)).to(torch.bfloat16)
+        rb = torch.from_numpy(rng.standard_normal(5000).astype(np.float32)).to(torch.bfloat16)
+        ref = (xb.float() + rb.float()).to(torch.bfloat16).double().numpy()
+        got = oracle.residual_store_bf16(xb.double().numpy(), rb.double().numpy())
+        np.testing.assert_array_equal(got, ref)
+
+
+# ---------------------------------------------------------------------------
+# a4 GEMM epilogue + row reduction
+# ---------------------------------------------------------------------------
+class TestEpilogue:
+    def test_zero_input_gives_half_count(self):
+        out = oracle.gemm_epilogue_reduce(np.zeros((3, 8192)), np.zeros(8192), np.ones(8192),
+                                          "sigmoid", "sum")
+        np.testing.assert_array_equal(out, 4096.0)
+
+    def test_hand_example_and_bias_axis(self):
+        l3 = math.log(3)
+        c = np.array([[l3, 0.0], [0.0, -l3]])
+        np.testing.assert_allclose(oracle.gemm_epilogue_reduce(c, None, None, "sigmoid", "sum"),
+                                   [1.25, 0.75], rtol=1e-15)
+        # per-column bias on a 2x3 matrix: every row sees [ln3, 0, -ln3]
+        out = oracle.gemm_epilogue_reduce(np.zeros((2, 3)), np.array([l3, 0.0, -l3]),
+                                          None, "sigmoid", "sum")
+        np.testing.assert_allclose(out, [1.5, 1.5], rtol=1e-15)
+
+    def test_bias_before_scale(self):
+        # (1 + 1) * 2 = 4 -> sigma(4); 1*2 + 1 = 3 would give sigma(3)
+        out = oracle.gemm_epilogue_reduce(np.array([[1.0]]), np.array([1.0]), np.array([2.0]),
+                                          "sigmoid", "sum")
+        assert out[0] == pytest.approx(1 / (1 + math.exp(-4)), rel=1e-15)
+
+    def test_sign_flip_symmetry_and_mean(self):
+        rng = np.random.default_rng(9)
+        c = rng.standard_normal((4, 100)) * 0.03
+        b = rng.uniform(-0.5, 0.5, 100)
+        s = rng.uniform(0.5, 1.5, 100)
+        o = oracle.gemm_epilogue_reduce(c, b, s, "sigmoid", "sum")
+        o2 = oracle.gemm_epilogue_reduce(-c, -b, s, "sigmoid", "sum")
+        np.testing.assert_allclose(o + o2, 100.0, atol=1e-12)
+        np.testing.assert_allclose(oracle.gemm_epilogue_reduce(c, b, s, "sigmoid", "mean"),
+                                   o / 100, rtol=1e-15)
+
+    def test_identity_act_is_weighted_row_sum(self):
+        c = np.array([[1.0, 2.0, 3.0], [4.0, 5.0, 6.0]])
+        out = oracle.gemm_epilogue_reduce(c, np.array([1.0, 0.0, -1.0]),
+                                          np.array([1.0, 10.0, 100.0]), "none", "sum")
+        np.testing.assert_array_equal(out, [2 + 20 + 200, 5 + 50 + 500])
+
+
+# ---------------------------------------------------------------------------
+# a5 stitched block
+# ---------------------------------------------------------------------------
+def _tiny_params(rng, hid, mlp, std=0.3):
+    p = {
+        "w_qkv": rng.standard_normal((hid, 3 * hid)) * std,
+        "b_qkv": rng.standard_normal(3 * hid) * std,
+        "w_o": rng.standard_normal((hid, hid)) * std,
+        "b_o": rng.standard_normal(hid) * std,
+        "w_1": rng.standard_normal((hid, mlp)) * std,
+        "b_1": rng.standard_normal(mlp) * std,
+        "w_2": rng.standard_normal((mlp, hid)) * std,
+        "b_2": rng.standard_normal(hid) * std,
+        "ln1_gamma": 1 + 0.1 * rng.standard_normal(hid),
+        "ln1_beta": 0.1 * rng.standard_normal(hid),
+        "ln2_gamma": 1 + 0.1 * rng.standard_normal(hid),
+        "ln2_beta": 0.1 * rng.standard_normal(hid),
+    }
+    return p
+
+
+class TestBlock:
+    S, H, NH, F = 7, 8, 2, 12
+
+    def test_causality(self):
+        rng = np.random.default_rng(10)
+        p = _tiny_params(rng, self.H, self.F)
+        x = rng.standard_normal((self.S, self.H))
+        y = oracle.block_forward_sequence(x, p, self.NH, 1e-5)["out"]
+        for t in range(self.S - 1):
+            x2 = x.copy()
+            x2[t + 1:] = rng.standard_normal((self.S - t - 1, self.H)) * 5
+            y2 = oracle.block_forward_sequence(x2, p, self.NH, 1e-5)["out"]
+            np.testing.assert_allclose(y2[:t + 1], y[:t + 1], atol=1e-12)
+            assert not np.allclose(y2[t + 1:], y[t + 1:])
+
+    def test_token0_attends_to_itself(self):
+        rng = np.random.default_rng(11)
+        p = _tiny_params(rng, self.H, self.F)
+        x = rng.standard_normal((self.S, self.H))
+        r = oracle.block_forward_sequence(x, p, self.NH, 1e-5, keep=("qkv", "o"))
+        np.testing.assert_allclose(r["o"][0], r["qkv"][0, 2 * self.H:], atol=1e-14)
+
+    def test_zero_branches_give_identity(self):
+        rng = np.random.default_rng(12)
+        p = _tiny_params(rng, self.H, self.F)
+        for k in ("w_o", "b_o", "w_2", "b_2"):
+            p[k] = np.zeros_like(p[k])
+        x = rng.standard_normal((self.S, self.H))
+        np.testing.assert_array_equal(oracle.block_forward_sequence(x, p, self.NH, 1e-5)["out"], x)
+
+    def test_uniform_attention_is_prefix_mean_through_permuted_wo(self):
+        # q = 0 -> all scores 0 -> uniform causal attention -> o_t = mean(v_0..v_t).
+        # Wv = I and Wo = a cyclic shift (not symmetric), so a transposed Wo or a
+        # misplaced head lands in the wrong columns.
+        rng = np.random.default_rng(13)
+        H = self.H
+        p = _tiny_params(rng, H, self.F)
+        p["w_qkv"][:, :H] = 0.0
+        p["b_qkv"][:H] = 0.0
+        p["w_qkv"][:, 2 * H:] = np.eye(H)
+        p["b_qkv"][2 * H:] = 0.0
+        shift = np.roll(np.eye(H), 1, axis=1)       # column j of out = column j-1 of in
+        p["w_o"] = shift
+        p["b_o"] = np.zeros(H)
+        x = rng.standard_normal((self.S, H))
+        r = oracle.block_forward_sequence(x, p, self.NH, 1e-5, keep=("a", "att"))
+        prefix = np.cumsum(r["a"], axis=0) / np.arange(1, self.S + 1)[:, None]
+        np.testing.assert_allclose(r["att"], np.roll(prefix, 1, axis=1), atol=1e-13)
+
+    def test_score_scale_is_inverse_sqrt_head_dim(self):
+        # q_t = c * e_0 (bias only), k_t picks a[t, 0] into head 0's first dim,
+        # v = a: head 0 probabilities are softmax over s <= t of c*w*a[s,0]/sqrt(dh).
+        rng = np.random.default_rng(14)
+        H, NH = self.H, self.NH
+        dh = H // NH
+        p = _tiny_params(rng, H, self.F)
+        c, w = 3.0, 2.0
+        p["w_qkv"][:, :H] = 0.0
+        p["b_qkv"][:H] = 0.0
+        p["b_qkv"][0] = c
+        p["w_qkv"][:, H:2 * H] = 0.0
+        p["b_qkv"][H:2 * H] = 0.0
+        p["w_qkv"][0, H] = w
+        p["w_qkv"][:, 2 * H:] = np.eye(H)
+        p["b_qkv"][2 * H:] = 0.0
+        x = rng.standard_normal((self.S, H))
+        r = oracle.block_forward_sequence(x, p, NH, 1e-5, keep=("a", "o"))
+        a = r["a"]
+        for t in range(self.S):
+            logits = [c * w * a[s, 0] / math.sqrt(dh) for s in range(t + 1)]
+            mx = max(logits)
+            e = [math.exp(l - mx) for l in logits]
+            z = sum(e)
+            expect = sum(e[s] / z * a[s, :dh] for s in range(t + 1))
+            np.testing.assert_allclose(r["o"][t, :dh], expect, atol=1e-13)
+
+    def test_mlp_wiring(self):
+        # attention branch off; W1 = [I | 0], W2 = [I ; 0]:
+        # out = x + GELU(LN2(x) + b1[:H]) + b2  (b1 inside the activation)
+        rng = np.random.default_rng(15)
+        H, F = self.H, self.F
+        p = _tiny_params(rng, H, F)
+        p["w_o"][:] = 0.0
+        p["b_o"][:] = 0.0
+        p["w_1"] = np.zeros((H, F))
+        p["w_1"][:, :H] = np.eye(H)
+        p["b_1"] = rng.standard_normal(F)
+        p["w_2"] = np.zeros((F, H))
+        p["w_2"][:H, :] = np.eye(H)
+        x = rng.standard_normal((self.S, H))
+        ln, _ = oracle.layernorm_residual(x, None, p["ln2_gamma"], p["ln2_beta"], 1e-5)
+        expect = x + oracle.gelu_erf(ln + p["b_1"][:H]) + p["b_2"]
+        np.testing.assert_allclose(oracle.block_forward_sequence(x, p, self.NH, 1e-5)["out"],
+                                   expect, atol=1e-14)
+
+    def test_second_residual_carries_attention(self):
+        # MLP branch off: out = h1 = x + att
+        rng = np.random.default_rng(16)
+        p = _tiny_params(rng, self.H, self.F)
+        p["w_2"][:] = 0.0
+        p["b_2"][:] = 0.0
+        x = rng.standard_normal((self.S, self.H))
+        r = oracle.block_forward_sequence(x, p, self.NH, 1e-5, keep=("att", "h1", "out"))
+        assert np.abs(r["att"]).max() > 0.1
+        np.testing.assert_allclose(r["out"], x + r["att"], atol=1e-14)
+        np.testing.assert_array_equal(r["out"], r["h1"])
