@@ -1,0 +1,191 @@
+/*
+ * libfusedsub -- fused sub-kernels of a compiled model graph, for AMD
+ * Instinct MI355X (CDNA4, gfx950).
+ *
+ * A compiled model is a set of generated sub-kernels plus fixed vendor
+ * library calls (KernelOPT, Def. 1 in Section 3).  The GEMMs stay library
+ * calls; this library implements the generated part: fused pointwise chains,
+ * row reductions (softmax, LayerNorm with residual) and GEMM epilogues with a
+ * row reduction (Appendix A, Codegen and Fusion Agent prompts: epilogue
+ * fusion, cross-reduction fusion, pointwise + pointwise, residual + norm).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers are DEVICE pointers; the caller owns every buffer.  The library
+ * allocates no device memory, keeps no state apart from a lazily filled
+ * per-device table of compute-unit counts, and never synchronises the
+ * stream.  Work is enqueued on `stream` (0 = the null stream) and the call
+ * returns after the enqueue.
+ *
+ * Layout: 2-D tensors are row-major with unit inner stride; `ld_*` is the row
+ * stride in ELEMENTS and must be >= cols.  A batched tensor whose leading
+ * dimensions are contiguous is passed flattened to rows (e.g. attention
+ * scores [B, H, S, S] are rows = B*H*S, cols = S).  Vectors indexed by
+ * column (bias, gamma, beta, col_scale) are contiguous [cols].
+ *
+ * rows == 0 or cols == 0 is an empty problem and returns FS_OK without
+ * launching anything (except where an entry point says otherwise).
+ *
+ * Arithmetic is fp32 in registers for every dtype; bf16 values are widened
+ * exactly on load and rounded to nearest even once, on the final store
+ * (Appendix A, Executor prompt: accumulate in fp32, cast on the final store).
+ *
+ * Alignment: every pointer must be aligned to its element size
+ * (FS_ERR_BAD_ARGUMENT otherwise).  Base pointers aligned to 16 bytes with ld*sizeof(elem) a
+ * multiple of 16 (and cols a multiple of the 16-byte vector width) take the
+ * 128-bit vector path; anything else takes a correct scalar path.  This is
+ * never an error.
+ *
+ * Errors: every entry point validates its arguments on the host, before any
+ * HIP call, and returns a status; it never aborts.  A launch failure returns
+ * FS_ERR_HIP with the HIP error text in fs_last_error_message().  Faults that
+ * occur while a kernel runs surface at the caller's next synchronisation.
+ *
+ * Aliasing: an output may coincide exactly (same pointer, same ld) with a
+ * row-shaped input where the entry point says so; any other overlap between
+ * an output and another argument returns FS_ERR_ALIASING.
+ *
+ * Thread safety: calls may be made from several host threads; calls that
+ * share output buffers on overlapping streams race like any kernels do.
+ */
+#ifndef FUSEDSUB_H
+#define FUSEDSUB_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FS_ABI_VERSION 1
+#define FS_API __attribute__((visibility("default")))
+
+typedef enum fs_status {
+  FS_OK = 0,
+  FS_ERR_NULL_POINTER = 1,      /* a required pointer is NULL                  */
+  FS_ERR_BAD_SHAPE = 2,         /* rows/cols negative or beyond a limit        */
+  FS_ERR_BAD_STRIDE = 3,        /* ld < cols                                   */
+  FS_ERR_UNSUPPORTED_DTYPE = 4, /* dtype value or combination not supported    */
+  FS_ERR_ALIASING = 5,          /* forbidden overlap of an output              */
+  FS_ERR_BAD_ARGUMENT = 6,      /* enum out of range, negative q_len, bad eps  */
+  FS_ERR_HIP = 7                /* the HIP runtime reported an error           */
+} fs_status;
+
+typedef enum fs_dtype { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
+
+typedef enum fs_act {
+  FS_ACT_NONE = 0,
+  FS_ACT_GELU_ERF = 1,          /* z * (1 + erf(z / sqrt 2)) / 2               */
+  FS_ACT_SIGMOID = 2,           /* 1 / (1 + exp(-z))                           */
+  FS_ACT_RELU = 3               /* max(z, 0)                                   */
+} fs_act;
+
+typedef enum fs_reduce { FS_REDUCE_SUM = 0, FS_REDUCE_MEAN = 1 } fs_reduce;
+
+/*
+ * Fused pointwise chain (Appendix A, Fusion Agent: pointwise + pointwise and
+ * activation + bias fusion -- load once, apply every op, store once).
+ *
+ *   y[r, j] = act(x[r, j] * scale + bias[j]) + residual[r, j]
+ *
+ * x, residual, y : [rows, cols] of `dtype`, row strides ld_x, ld_r, ld_y.
+ * bias           : [cols] of `dtype`, or NULL (no bias).
+ * residual       : or NULL (no residual; ld_r is then ignored).
+ * y may be x or residual exactly (in place).  scale must be finite.
+ */
+FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bias,
+                             const void* residual, int64_t ld_r, void* y, int64_t ld_y,
+                             int64_t rows, int64_t cols, float scale, fs_act act,
+                             fs_dtype dtype, hipStream_t stream);
+
+/*
+ * Fused row softmax with pre-scale and additive mask (Appendix A, Planner
+ * item 9 and Codegen prompt: fused softmax, online softmax).
+ *
+ *   a[r, j] = x[r, j] * scale + mask[r, j]   (additive mask, e.g. 0 / -inf)
+ *   y[r, :] = exp(a[r, :] - max_j a[r, j]) / sum_j exp(a[r, j] - max)
+ *
+ * x, y   : [rows, cols] of `dtype`; y may be x exactly (in place).
+ * mask   : [rows, cols] of `mask_dtype` with row stride ld_mask, or NULL.
+ * causal_q_len > 0 additionally masks element (r, j) when
+ *          j > (r mod causal_q_len) + (cols - causal_q_len); masked
+ *          elements are not read and are written as +0.  0 = off.
+ * Entries whose logit is -inf come out exactly +0; a fully masked row comes
+ * out all +0.  One pass over HBM: rows up to FS_SOFTMAX_MAX_COLS columns are
+ * held in registers, with a single (max, sum) online combine per row.
+ * scale must be finite; mask values may be any float or -inf.
+ */
+#define FS_SOFTMAX_MAX_COLS 65536
+FS_API fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t ld_mask,
+                         fs_dtype mask_dtype, void* y, int64_t ld_y, int64_t rows,
+                         int64_t cols, float scale, int64_t causal_q_len, fs_dtype dtype,
+                         hipStream_t stream);
+
+/*
+ * LayerNorm fused with the residual add (Appendix A, Fusion Agent:
+ * normalisation fusion -- mean and variance in one pass, normalise, scale and
+ * bias in the same kernel, fp32 accumulation; residual + norm in one memory
+ * pass; Codegen prompt: single-pass LayerNorm).
+ *
+ *   h = x + residual                     (fp32)
+ *   y = (h - mean(h)) / sqrt(var(h) + eps) * gamma + beta   (biased variance)
+ *   residual_out = h rounded to `dtype`
+ *
+ * x, residual, y, residual_out : [rows, cols] of `dtype`.
+ * residual     : or NULL (plain LayerNorm, h = x).
+ * residual_out : or NULL (not stored).
+ * gamma, beta  : [cols] of `dtype`, or NULL (1 and 0).
+ * y and residual_out may each be x or residual exactly; they may not overlap
+ * each other.  eps must be finite and >= 0.  Rows up to
+ * FS_LAYERNORM_MAX_COLS columns (held in registers).
+ */
+#define FS_LAYERNORM_MAX_COLS 65536
+FS_API fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residual,
+                                int64_t ld_r, const void* gamma, const void* beta, void* y,
+                                int64_t ld_y, void* residual_out, int64_t ld_ro, int64_t rows,
+                                int64_t cols, float eps, fs_dtype dtype, hipStream_t stream);
+
+/*
+ * GEMM epilogue with a row reduction, applied to the output C of a library
+ * GEMM (Appendix A, Codegen prompt: keep the matmul a library call and fuse
+ * only its epilogue; Fusion Agent: reduction + pointwise).
+ *
+ *   row_out[i] = reduce_j act((C[i, j] + bias[j]) * col_scale[j])
+ *
+ * c         : [rows, cols] of c_dtype, row stride ld_c.
+ * bias      : [cols] of bias_dtype, or NULL (0).
+ * col_scale : [cols] fp32, or NULL (1).
+ * row_out   : [rows] fp32 (contiguous).  With cols == 0 and rows > 0, SUM
+ *             writes zeros and MEAN returns FS_ERR_BAD_SHAPE.
+ * The sum is accumulated in fp32 (per-thread partial sums, then a tree).
+ */
+FS_API fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype,
+                                  const void* bias, fs_dtype bias_dtype,
+                                  const float* col_scale, fs_act act, fs_reduce reduce,
+                                  float* row_out, int64_t rows, int64_t cols,
+                                  hipStream_t stream);
+
+/*
+ * Calibration utility (not a sub-kernel): copies `bytes` bytes from src to
+ * dst with 128-bit loads and stores when both are 16-byte aligned and bytes
+ * is a multiple of 16, else byte by byte.  Used to measure the achievable
+ * HBM bandwidth and to scale hardware byte counters.  src and dst must not
+ * overlap.
+ */
+FS_API fs_status fs_copy(const void* src, void* dst, int64_t bytes, hipStream_t stream);
+
+/* Static text for a status code (never NULL; unknown codes included). */
+FS_API const char* fs_status_string(fs_status s);
+
+/* Detail of the last non-OK status returned on the calling host thread
+ * ("" if none).  Valid until the next call on that thread. */
+FS_API const char* fs_last_error_message(void);
+
+/* FS_ABI_VERSION of the built library. */
+FS_API int fs_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FUSEDSUB_H */

@@ -1,0 +1,127 @@
+"""Stitched pre-LN transformer block: the fused sub-kernels of libfusedsub
+between hipBLASLt GEMMs, all on the current stream with no host sync.
+
+A compiled model is generated sub-kernels plus fixed library calls (KernelOPT
+Def. 1, Section 3); its model-level check compares the re-stitched model with
+a float64 reference (Gate 3, Section 4.4).  This driver is that re-stitched
+block on MI355X:
+
+    a    = layernorm(x)                                   fs_layernorm_residual
+    qkv  = a @ Wqkv + bqkv                                hipBLASLt (BIAS epilogue)
+    S    = q k^T per (sequence, head), head views of qkv  hipBLASLt strided batched
+    P    = softmax(S / sqrt(dh), causal)                  fs_row_softmax
+    o    = P v  written head-interleaved into [tokens, H] hipBLASLt strided batched
+    att  = o @ Wo + bo                                    hipBLASLt (BIAS epilogue)
+    m, h1 = layernorm(att + x), att + x                   fs_layernorm_residual
+    u    = m @ W1                                         hipBLASLt
+    g    = gelu_erf(u + b1)                               fs_pointwise_chain
+    d    = g @ W2 + b2                                    hipBLASLt (BIAS epilogue)
+    out  = d + h1                                         fs_pointwise_chain
+
+The attention GEMMs read q, k and v as strided views of qkv (no permute
+copies) and write o directly in token-major layout.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, Optional
+
+import torch
+
+from . import ops
+
+PARAM_NAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "ln1_gamma",
+               "ln1_beta", "ln2_gamma", "ln2_beta")
+
+
+class TransformerBlock:
+    """Weights are bf16 device tensors, stored [in, out] (y = x @ W + b)."""
+
+    def __init__(self, params: Dict[str, torch.Tensor], heads: int, eps: float = 1e-5):
+        for k in PARAM_NAMES:
+            t = params[k]
+            if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"{k} must be a contiguous bf16 device tensor")
+        self.p = params
+        self.heads = heads
+        self.eps = float(eps)
+        self.hidden = params["w_o"].shape[0]
+        self.mlp = params["w_1"].shape[1]
+        if self.hidden % heads:
+            raise ValueError("hidden must be divisible by heads")
+        self.dh = self.hidden // heads
+
+    def alloc(self, batch: int, seq: int, device) -> Dict[str, torch.Tensor]:
+        """Activation buffers for one forward pass."""
+        t, H, F, NH = batch * seq, self.hidden, self.mlp, self.heads
+        e = dict(dtype=torch.bfloat16, device=device)
+        return {
+            "a": torch.empty(t, H, **e), "qkv": torch.empty(t, 3 * H, **e),
+            "scores": torch.empty(batch, NH, seq, seq, **e),
+            "probs": torch.empty(batch, NH, seq, seq, **e),
+            "o": torch.empty(t, H, **e), "att": torch.empty(t, H, **e),
+            "h1": torch.empty(t, H, **e), "m": torch.empty(t, H, **e),
+            "u": torch.empty(t, F, **e), "g": torch.empty(t, F, **e),
+            "d": torch.empty(t, H, **e), "out": torch.empty(t, H, **e),
+        }
+
+    # --- stages ----------------------------------------------------------------
+    def attention_gemms_qk(self, buf, batch, seq):
+        H, NH, dh = self.hidden, self.heads, self.dh
+        qkv, s = buf["qkv"], buf["scores"]
+        es = qkv.element_size()
+        for b in range(batch):
+            base = qkv.data_ptr() + b * seq * 3 * H * es
+            # S[b, h] = q_bh @ k_bh^T: q_bh = qkv[rows of b, h*dh:(h+1)*dh], k_bh at +H
+            ops.gemm_strided_batched(base, 3 * H, dh, base + H * es, 3 * H, dh, True,
+                                     s[b].data_ptr(), seq, seq * seq, seq, seq, dh, NH,
+                                     device=qkv.device)
+
+    def attention_gemms_pv(self, buf, batch, seq):
+        H, NH, dh = self.hidden, self.heads, self.dh
+        qkv, p, o = buf["qkv"], buf["probs"], buf["o"]
+        es = qkv.element_size()
+        for b in range(batch):
+            vbase = qkv.data_ptr() + (b * seq * 3 * H + 2 * H) * es
+            obase = o.data_ptr() + b * seq * H * es
+            # o[rows of b, h*dh:(h+1)*dh] = P[b, h] @ v_bh
+            ops.gemm_strided_batched(p[b].data_ptr(), seq, seq * seq, vbase, 3 * H, dh, False,
+                                     obase, H, dh, seq, dh, seq, NH, device=qkv.device)
+
+    def forward(self, x: torch.Tensor, buf: Optional[Dict[str, torch.Tensor]] = None):
+        """x [batch, seq, hidden] bf16 -> dict of every intermediate; 'out' is
+        [batch*seq, hidden]."""
+        batch, seq, H = x.shape
+        if H != self.hidden:
+            raise ValueError("hidden size mismatch")
+        p = self.p
+        if buf is None:
+            buf = self.alloc(batch, seq, x.device)
+        x2 = x.reshape(batch * seq, H)
+        ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
+        ops.gemm(buf["a"], p["w_qkv"], bias=p["b_qkv"], out=buf["qkv"])
+        self.attention_gemms_qk(buf, batch, seq)
+        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
+                        out=buf["probs"])
+        self.attention_gemms_pv(buf, batch, seq)
+        ops.gemm(buf["o"], p["w_o"], bias=p["b_o"], out=buf["att"])
+        ops.layernorm_residual(buf["att"], x2, p["ln2_gamma"], p["ln2_beta"], self.eps,
+                               out=buf["m"], residual_out=buf["h1"])
+        ops.gemm(buf["m"], p["w_1"], out=buf["u"])
+        ops.pointwise_chain(buf["u"], p["b_1"], None, 1.0, "gelu_erf", out=buf["g"])
+        ops.gemm(buf["g"], p["w_2"], bias=p["b_2"], out=buf["d"])
+        ops.pointwise_chain(buf["d"], None, buf["h1"], 1.0, "none", out=buf["out"])
+        return buf
+
+    # the five sub-kernel launches alone, on resident inputs (for timing)
+    def subkernels(self, x: torch.Tensor, buf: Dict[str, torch.Tensor]):
+        batch, seq, H = x.shape
+        p = self.p
+        x2 = x.reshape(batch * seq, H)
+        ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
+        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
+                        out=buf["probs"])
+        ops.layernorm_residual(buf["att"], x2, p["ln2_gamma"], p["ln2_beta"], self.eps,
+                               out=buf["m"], residual_out=buf["h1"])
+        ops.pointwise_chain(buf["u"], p["b_1"], None, 1.0, "gelu_erf", out=buf["g"])
+        ops.pointwise_chain(buf["d"], None, buf["h1"], 1.0, "none", out=buf["out"])

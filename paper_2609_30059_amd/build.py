@@ -1,0 +1,97 @@
+"""Build the native libraries in-tree for gfx950.
+
+    python -m paper_2609_30059_amd.build
+
+produces, next to this file,
+  * libfusedsub.so -- the fused sub-kernels behind the C ABI of include/fusedsub.h
+  * libfsgemm.so   -- the hipBLASLt GEMM wrapper of include/fsgemm.h
+
+Every HIP translation unit is compiled with the packed-FP32 target feature
+switched off (ordinary fp32 code only).  Objects go to ``_build/`` (ignored
+by git); the shared libraries are written atomically.
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(HERE, "_build")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+ARCH = "gfx950"
+
+FUSEDSUB_SOURCES = ["api.hip", "pointwise.hip", "softmax.hip", "layernorm.hip", "epilogue.hip",
+                    "copy.hip"]
+HIP_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-result",
+]
+
+LIB_FUSEDSUB = os.path.join(HERE, "libfusedsub.so")
+LIB_FSGEMM = os.path.join(HERE, "libfsgemm.so")
+
+
+def _hipcc() -> str:
+    p = os.path.join(ROCM, "bin", "hipcc")
+    return p if os.path.exists(p) else "hipcc"
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
+                    if "packed-fp32-ops' is not a recognized feature" not in l)
+    if r.returncode != 0:
+        raise RuntimeError(f"command failed ({r.returncode}): {' '.join(cmd)}\n{out}")
+    if verbose and out.strip():
+        print(out, flush=True)
+
+
+def _compile(src, verbose):
+    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+    _run([_hipcc(), *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),
+          "-o", obj], verbose)
+    return obj
+
+
+def _link(objs, out, extra, verbose):
+    tmp = out + ".tmp"
+    _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp,
+          f"-Wl,-rpath,{ROCM}/lib", *extra], verbose)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False, jobs: int = 8) -> None:
+    os.makedirs(BUILD, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), FUSEDSUB_SOURCES))
+        gemm_obj = os.path.join(BUILD, "gemm_hipblaslt.o")
+        fut = ex.submit(_run, ["g++", "-O2", "-std=c++17", "-fPIC", "-fvisibility=hidden",
+                               "-D__HIP_PLATFORM_AMD__", f"-I{INCLUDE}", f"-I{ROCM}/include",
+                               "-c", os.path.join(CSRC, "gemm_hipblaslt.cpp"), "-o", gemm_obj],
+                        verbose)
+        fut.result()
+    _link(objs, LIB_FUSEDSUB, [], verbose)
+    _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
+          f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
+    os.replace(LIB_FSGEMM + ".tmp", LIB_FSGEMM)
+
+
+def clean() -> None:
+    shutil.rmtree(BUILD, ignore_errors=True)
+    for p in (LIB_FUSEDSUB, LIB_FSGEMM):
+        if os.path.exists(p):
+            os.remove(p)
+
+
+if __name__ == "__main__":
+    build(verbose="-v" in sys.argv)
+    print("built", LIB_FUSEDSUB, LIB_FSGEMM)

@@ -1,0 +1,64 @@
+// Host-side launch interface between the C ABI (api.hip) and the kernels.
+// Arguments arrive here already validated; `vec` selects the 16-byte path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fusedsub.h"
+
+namespace fs {
+
+struct PointwiseArgs {
+  const void* x; int64_t ld_x;
+  const void* bias;
+  const void* res; int64_t ld_r;
+  void* y; int64_t ld_y;
+  int64_t rows, cols;
+  float scale;
+  fs_act act;
+  fs_dtype dtype;
+  bool vec;
+};
+
+struct SoftmaxArgs {
+  const void* x; int64_t ld_x;
+  const void* mask; int64_t ld_mask; fs_dtype mask_dtype;
+  void* y; int64_t ld_y;
+  int64_t rows, cols;
+  float scale;
+  int64_t causal_q_len;
+  fs_dtype dtype;
+  bool vec;
+};
+
+struct LayerNormArgs {
+  const void* x; int64_t ld_x;
+  const void* res; int64_t ld_r;
+  const void* gamma; const void* beta;
+  void* y; int64_t ld_y;
+  void* res_out; int64_t ld_ro;
+  int64_t rows, cols;
+  float eps;
+  fs_dtype dtype;
+  bool vec;
+};
+
+struct EpilogueArgs {
+  const void* c; int64_t ld_c; fs_dtype c_dtype;
+  const void* bias; fs_dtype bias_dtype;
+  const float* col_scale;
+  fs_act act; fs_reduce reduce;
+  float* out;
+  int64_t rows, cols;
+  bool vec;
+};
+
+// `cus` is the compute-unit count of the current device.
+hipError_t launch_pointwise(const PointwiseArgs& a, int cus, hipStream_t s);
+hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s);
+hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s);
+hipError_t launch_epilogue(const EpilogueArgs& a, int cus, hipStream_t s);
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipStream_t s);
+
+}  // namespace fs

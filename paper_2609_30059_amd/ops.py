@@ -1,0 +1,225 @@
+"""Tensor-level calls of the fused sub-kernels and the GEMM wrapper.
+
+Argument marshalling only: each function turns torch tensors into the device
+pointers, row strides and HIP stream the C ABI takes, allocates outputs with
+torch (device memory is torch's job here), calls the native entry point and
+raises on a non-OK status.  No arithmetic happens in Python.
+"""
+from __future__ import annotations
+
+from typing import Optional, Tuple
+
+import torch
+
+from . import _native as N
+
+__all__ = ["pointwise_chain", "row_softmax", "layernorm_residual", "gemm_epilogue_reduce",
+           "copy_", "gemm", "gemm_strided_batched", "as_rows", "fs_dtype"]
+
+
+def fs_dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return N.FS_F32
+    if t.dtype == torch.bfloat16:
+        return N.FS_BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 and bfloat16 only)")
+
+
+def as_rows(t: torch.Tensor) -> Tuple[int, int, int]:
+    """(rows, cols, ld) of a tensor viewed as [prod(leading dims), last dim].
+
+    The last dim must have unit stride and the leading dims must collapse
+    onto one row stride (a contiguous batch of rows)."""
+    if t.dim() == 0:
+        raise ValueError("scalar tensors are not supported")
+    if t.dim() == 1:
+        return 1, t.shape[0], max(t.shape[0], 1)
+    if t.shape[-1] > 1 and t.stride(-1) != 1:
+        raise ValueError("the last dimension must be contiguous")
+    ld = t.stride(-2)
+    for i in range(t.dim() - 2):
+        if t.shape[i] > 1 and t.stride(i) != t.stride(i + 1) * t.shape[i + 1]:
+            raise ValueError("leading dimensions do not collapse onto one row stride")
+    rows = 1
+    for s in t.shape[:-1]:
+        rows *= s
+    cols = t.shape[-1]
+    if rows <= 1:
+        ld = max(cols, 1)
+    return rows, cols, max(ld, cols)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _vec(t: Optional[torch.Tensor], cols: int, name: str):
+    if t is None:
+        return None
+    if t.dim() != 1 or t.shape[0] != cols or (cols > 1 and t.stride(0) != 1):
+        raise ValueError(f"{name} must be a contiguous [{cols}] vector")
+    return t
+
+
+def pointwise_chain(x: torch.Tensor, bias: Optional[torch.Tensor] = None,
+                    residual: Optional[torch.Tensor] = None, scale: float = 1.0,
+                    act: str = "none", out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y = act(x * scale + bias) + residual  (fs_pointwise_chain)."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    _, _, ld_y = as_rows(out)
+    ld_r = 0
+    if residual is not None:
+        if residual.shape != x.shape or residual.dtype != x.dtype:
+            raise ValueError("residual must match x")
+        ld_r = as_rows(residual)[2]
+    if bias is not None and bias.dtype != x.dtype:
+        raise ValueError("bias dtype must match x")
+    _vec(bias, cols, "bias")
+    st = N.fs_pointwise_chain(x.data_ptr(), ld_x, _ptr(bias), _ptr(residual), ld_r,
+                              out.data_ptr(), ld_y, rows, cols, float(scale), N.ACTS[act],
+                              fs_dtype(x), _stream())
+    N.check("fs_pointwise_chain", st)
+    return out
+
+
+def row_softmax(x: torch.Tensor, mask: Optional[torch.Tensor] = None, scale: float = 1.0,
+                causal_q_len: int = 0, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """softmax(x * scale + mask) along the last dim (fs_row_softmax)."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    _, _, ld_y = as_rows(out)
+    ld_m, mdt = 0, fs_dtype(x)
+    if mask is not None:
+        if mask.shape != x.shape:
+            raise ValueError("mask must have the shape of x")
+        ld_m, mdt = as_rows(mask)[2], fs_dtype(mask)
+    st = N.fs_row_softmax(x.data_ptr(), ld_x, _ptr(mask), ld_m, mdt, out.data_ptr(), ld_y, rows,
+                          cols, float(scale), int(causal_q_len), fs_dtype(x), _stream())
+    N.check("fs_row_softmax", st)
+    return out
+
+
+def layernorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
+                       gamma: Optional[torch.Tensor] = None, beta: Optional[torch.Tensor] = None,
+                       eps: float = 1e-5, out: Optional[torch.Tensor] = None,
+                       residual_out: Optional[torch.Tensor] = None,
+                       store_residual: bool = True):
+    """(LN(x + residual), x + residual)  (fs_layernorm_residual).
+
+    Returns (y, residual_out); residual_out is None when there is no residual
+    or ``store_residual`` is False."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    ld_r = ld_ro = 0
+    if residual is not None:
+        if residual.shape != x.shape or residual.dtype != x.dtype:
+            raise ValueError("residual must match x")
+        ld_r = as_rows(residual)[2]
+        if residual_out is None and store_residual:
+            residual_out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    if residual_out is not None:
+        ld_ro = as_rows(residual_out)[2]
+    for v, n in ((gamma, "gamma"), (beta, "beta")):
+        if v is not None and v.dtype != x.dtype:
+            raise ValueError(f"{n} dtype must match x")
+        _vec(v, cols, n)
+    st = N.fs_layernorm_residual(x.data_ptr(), ld_x, _ptr(residual), ld_r, _ptr(gamma),
+                                 _ptr(beta), out.data_ptr(), as_rows(out)[2],
+                                 _ptr(residual_out), ld_ro, rows, cols, float(eps), fs_dtype(x),
+                                 _stream())
+    N.check("fs_layernorm_residual", st)
+    return out, residual_out
+
+
+def gemm_epilogue_reduce(c: torch.Tensor, bias: Optional[torch.Tensor] = None,
+                         col_scale: Optional[torch.Tensor] = None, act: str = "sigmoid",
+                         reduce: str = "sum", out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """out[i] = reduce_j act((c[i, j] + bias[j]) * col_scale[j])  (fs_gemm_epilogue_reduce)."""
+    rows, cols, ld_c = as_rows(c)
+    if out is None:
+        out = torch.empty(rows, dtype=torch.float32, device=c.device)
+    if out.dtype != torch.float32 or out.numel() != rows or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [rows] tensor")
+    _vec(bias, cols, "bias")
+    _vec(col_scale, cols, "col_scale")
+    if col_scale is not None and col_scale.dtype != torch.float32:
+        raise ValueError("col_scale must be float32")
+    st = N.fs_gemm_epilogue_reduce(c.data_ptr(), ld_c, fs_dtype(c), _ptr(bias),
+                                   fs_dtype(bias) if bias is not None else N.FS_F32,
+                                   _ptr(col_scale), N.ACTS[act], N.REDUCES[reduce],
+                                   out.data_ptr(), rows, cols, _stream())
+    N.check("fs_gemm_epilogue_reduce", st)
+    return out
+
+
+def copy_(dst: torch.Tensor, src: torch.Tensor) -> torch.Tensor:
+    """Byte copy of src into dst with the calibration kernel (fs_copy)."""
+    if not (src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("copy_ needs contiguous tensors")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("size mismatch")
+    N.check("fs_copy", N.fs_copy(src.data_ptr(), dst.data_ptr(), nbytes, _stream()))
+    return dst
+
+
+# ---------------------------------------------------------------------------
+# hipBLASLt GEMMs (the fixed library calls)
+# ---------------------------------------------------------------------------
+_WORKSPACE_BYTES = 64 << 20
+_workspaces = {}
+
+
+def _workspace(device) -> torch.Tensor:
+    idx = torch.device(device).index
+    if idx is None:
+        idx = torch.cuda.current_device()
+    ws = _workspaces.get(idx)
+    if ws is None:
+        ws = torch.empty(_WORKSPACE_BYTES, dtype=torch.uint8, device=f"cuda:{idx}")
+        _workspaces[idx] = ws
+    return ws
+
+
+def gemm_strided_batched(a_ptr: int, lda: int, stride_a: int, b_ptr: int, ldb: int,
+                         stride_b: int, trans_b: bool, c_ptr: int, ldc: int, stride_c: int,
+                         m: int, n: int, k: int, batch: int, alpha: float = 1.0,
+                         bias: Optional[torch.Tensor] = None, device="cuda") -> None:
+    """Raw-pointer form of fsg_gemm_bf16 for strided views (attention heads)."""
+    ws = _workspace(device)
+    st = N.fsg_gemm_bf16(a_ptr, lda, stride_a, b_ptr, ldb, stride_b, int(trans_b), c_ptr, ldc,
+                         stride_c, m, n, k, batch, float(alpha), _ptr(bias), ws.data_ptr(),
+                         ws.numel(), _stream())
+    N.check_gemm(st)
+
+
+def gemm(a: torch.Tensor, b: torch.Tensor, bias: Optional[torch.Tensor] = None,
+         out: Optional[torch.Tensor] = None, trans_b: bool = False,
+         alpha: float = 1.0) -> torch.Tensor:
+    """out = alpha * a @ b (+ bias) for bf16 row-major a [m, k] and b [k, n]
+    (or b stored [n, k] with trans_b)."""
+    for t in (a, b):
+        if t.dtype != torch.bfloat16:
+            raise TypeError("gemm takes bfloat16 operands")
+    m, k, lda = as_rows(a)
+    if trans_b:
+        n, kb, ldb = as_rows(b)
+    else:
+        kb, n, ldb = as_rows(b)
+    if kb != k:
+        raise ValueError(f"inner dimensions differ: {k} vs {kb}")
+    if out is None:
+        out = torch.empty((*a.shape[:-1], n), dtype=torch.bfloat16, device=a.device)
+    _, _, ldc = as_rows(out)
+    _vec(bias, n, "bias")
+    gemm_strided_batched(a.data_ptr(), lda, 0, b.data_ptr(), ldb, 0, trans_b, out.data_ptr(),
+                         ldc, 0, m, n, k, 1, alpha, bias, a.device)
+    return out

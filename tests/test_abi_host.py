@@ -1,0 +1,205 @@
+"""Host-side tests of the C ABI: the libraries load, export every symbol
+the headers declare, and reject bad arguments with the documented status
+before any HIP call (so they run without a GPU).  No kernel is launched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_30059_amd import _native as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+NULL = None
+A = 0x10000000          # fake, 16-byte aligned device addresses (never dereferenced:
+B = 0x20000000          # every call below fails validation first)
+C = 0x30000000
+
+
+def declared(header, prefix):
+    txt = open(os.path.join(ROOT, "include", header)).read()
+    return sorted(set(re.findall(r"\b(" + prefix + r"[a-z0-9_]+)\s*\(", txt)))
+
+
+def test_libraries_load_and_export_every_declared_symbol():
+    lib = N.fusedsub()
+    for name in declared("fusedsub.h", "fs_"):
+        assert hasattr(lib, name), name
+    g = N.fsgemm()
+    for name in declared("fsgemm.h", "fsg_"):
+        assert hasattr(g, name), name
+    assert set(declared("fusedsub.h", "fs_")) == set(N.FUSEDSUB_SYMBOLS)
+    assert set(declared("fsgemm.h", "fsg_")) == set(N.FSGEMM_SYMBOLS)
+
+
+def test_only_declared_symbols_are_exported():
+    for lib, pre in ((N.LIB_FUSEDSUB, "fs"), (N.LIB_FSGEMM, "fsg")):
+        out = subprocess.run(["nm", "-D", "--defined-only", lib], capture_output=True,
+                             text=True).stdout
+        syms = {l.split()[-1] for l in out.splitlines() if " T " in l}
+        ours = {s for s in syms if s.startswith(pre + "_")}
+        assert ours == set(declared("fusedsub.h" if pre == "fs" else "fsgemm.h", pre + "_"))
+
+
+def test_single_hip_runtime_in_process():
+    N.fusedsub()
+    N.fsgemm()
+    libs = N.hip_runtimes_mapped()
+    real = {os.path.realpath(p) for p in libs}
+    assert len(real) <= 1, libs
+
+
+def test_version_and_status_strings():
+    assert N.fs_abi_version() == N.FS_ABI_VERSION
+    for code, name in N.STATUS_NAMES.items():
+        assert N.fs_status_string(code).startswith(name)
+    assert "UNKNOWN" in N.fs_status_string(99)
+    assert "UNKNOWN" in N.fs_status_string(-1)
+
+
+# ---- pointwise ---------------------------------------------------------------
+def pw(**kw):
+    a = dict(x=A, ld_x=64, bias=NULL, residual=NULL, ld_r=64, y=B, ld_y=64, rows=4, cols=64,
+             scale=1.0, act=0, dtype=0, stream=None)
+    a.update(kw)
+    return N.fs_pointwise_chain(**a)
+
+
+def test_pointwise_validation():
+    assert pw(x=NULL) == 1
+    assert pw(y=NULL) == 1
+    assert pw(rows=-1) == 2
+    assert pw(cols=-5) == 2
+    assert pw(ld_x=63) == 3
+    assert pw(ld_y=10) == 3
+    assert pw(residual=C, ld_r=3) == 3
+    assert pw(dtype=7) == 4
+    assert pw(act=9) == 6
+    assert pw(scale=float("nan")) == 6
+    assert pw(scale=float("inf")) == 6
+    assert pw(x=A + 2) == 6                      # not aligned to 4 bytes for fp32
+    assert pw(y=A + 4 * 64) == 5                 # y starts inside x (partial overlap)
+    assert pw(y=A + 4, ld_y=64) == 5
+    assert pw(bias=B + 16) == 5                  # bias inside y
+    assert pw(residual=B + 64, ld_r=64) == 5     # residual partially overlaps y
+    assert "overlap" in N.fs_last_error_message()
+
+
+def test_pointwise_empty_problem_is_ok_without_pointers():
+    assert pw(rows=0, x=NULL, y=NULL) == 0
+    assert pw(cols=0, ld_x=0, ld_y=0, x=NULL, y=NULL) == 0
+    assert N.fs_last_error_message() == ""
+
+
+# ---- softmax -----------------------------------------------------------------
+def sm(**kw):
+    a = dict(x=A, ld_x=128, mask=NULL, ld_mask=128, mask_dtype=1, y=B, ld_y=128, rows=4,
+             cols=128, scale=0.125, causal_q_len=0, dtype=1, stream=None)
+    a.update(kw)
+    return N.fs_row_softmax(**a)
+
+
+def test_softmax_validation():
+    assert sm(x=NULL) == 1
+    assert sm(cols=N.FS_SOFTMAX_MAX_COLS + 1, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert sm(rows=-1) == 2
+    assert sm(ld_x=127) == 3
+    assert sm(mask=C, ld_mask=100) == 3
+    assert sm(dtype=3) == 4
+    assert sm(mask=C, mask_dtype=5) == 4
+    assert sm(causal_q_len=-1) == 6
+    assert sm(scale=float("nan")) == 6
+    assert sm(x=A + 1) == 6
+    assert sm(mask=B + 256) == 5                 # mask overlaps y
+    assert sm(y=A + 2) == 5                      # partial overlap with x
+    assert sm(rows=0, x=NULL, y=NULL) == 0
+
+
+# ---- layernorm ---------------------------------------------------------------
+def ln(**kw):
+    a = dict(x=A, ld_x=256, residual=NULL, ld_r=256, gamma=NULL, beta=NULL, y=B, ld_y=256,
+             residual_out=NULL, ld_ro=256, rows=8, cols=256, eps=1e-5, dtype=1, stream=None)
+    a.update(kw)
+    return N.fs_layernorm_residual(**a)
+
+
+def test_layernorm_validation():
+    assert ln(y=NULL) == 1
+    assert ln(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert ln(ld_y=255) == 3
+    assert ln(residual=C, ld_r=1) == 3
+    assert ln(residual_out=C, ld_ro=1) == 3
+    assert ln(dtype=2) == 4
+    assert ln(eps=-1.0) == 6
+    assert ln(eps=float("inf")) == 6
+    assert ln(gamma=A + 1) == 6
+    assert ln(residual_out=B + 512) == 5          # residual_out overlaps y
+    assert ln(gamma=B) == 5                       # gamma inside y
+    assert ln(residual=C, residual_out=C + 2) == 5
+
+
+# ---- epilogue ----------------------------------------------------------------
+def ep(**kw):
+    a = dict(c=A, ld_c=8192, c_dtype=1, bias=NULL, bias_dtype=1, col_scale=NULL, act=2,
+             reduce=0, row_out=B, rows=16, cols=8192, stream=None)
+    a.update(kw)
+    return N.fs_gemm_epilogue_reduce(**a)
+
+
+def test_epilogue_validation():
+    assert ep(row_out=NULL) == 1
+    assert ep(c=NULL) == 1
+    assert ep(rows=-2) == 2
+    assert ep(ld_c=100) == 3
+    assert ep(c_dtype=4) == 4
+    assert ep(bias=C, bias_dtype=9) == 4
+    assert ep(act=11) == 6
+    assert ep(reduce=3) == 6
+    assert ep(row_out=B + 2) == 6
+    assert ep(row_out=A + 64) == 5                # row_out inside C
+    assert ep(col_scale=B) == 5
+    assert ep(rows=0, c=NULL, row_out=NULL) == 0
+    assert ep(cols=0, reduce=1) == 2              # mean over zero columns
+
+
+def test_copy_validation():
+    assert N.fs_copy(A, B, -1, None) == 2
+    assert N.fs_copy(NULL, B, 16, None) == 1
+    assert N.fs_copy(A, A + 8, 16, None) == 5
+    assert N.fs_copy(A, B, 0, None) == 0
+
+
+# ---- gemm wrapper ------------------------------------------------------------
+def gm(**kw):
+    a = dict(a=A, lda=64, stride_a=0, b=B, ldb=32, stride_b=0, trans_b=0, c=C, ldc=32,
+             stride_c=0, m=16, n=32, k=64, batch=1, alpha=1.0, bias=NULL, workspace=NULL,
+             workspace_bytes=0, stream=None)
+    a.update(kw)
+    return N.fsg_gemm_bf16(**a)
+
+
+def test_gemm_validation():
+    assert gm(a=NULL) == 1
+    assert gm(workspace_bytes=1024) == 1
+    assert gm(m=-1) == 2
+    assert gm(batch=0) == 2
+    assert gm(lda=63) == 3
+    assert gm(ldb=31) == 3
+    assert gm(trans_b=1, ldb=63) == 3
+    assert gm(ldc=31) == 3
+    assert gm(trans_b=2) == 4
+    assert gm(alpha=float("nan")) == 4
+    assert gm(m=0, a=NULL, b=NULL, c=NULL) == 0
+    assert "lda" in N.fsg_last_error_message() or N.fsg_last_error_message() == ""
+
+
+def test_header_compiles_as_c():
+    src = '#include "fusedsub.h"\n#include "fsgemm.h"\nint main(void){return fs_abi_version()!=FS_ABI_VERSION;}\n'
+    p = "/tmp/_fs_hdr_test.c"
+    with open(p, "w") as f:
+        f.write(src)
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        f"-I{ROOT}/include", "-I/opt/rocm/include", "-c", p, "-o", "/tmp/_fs_hdr_test.o"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr

@@ -1,0 +1,124 @@
+"""GPU parity of fs_gemm_epilogue_reduce (and of the hipBLASLt GEMM that
+feeds it) against the float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import SEEDS, TOL, announce, assert_close, dev, host64
+
+pytestmark = pytest.mark.gpu
+
+# fp32 tree sum of 8192 terms below 1: |error| <= log2(8192) * ulp(4096) ~ 5e-3
+SUM_ATOL = 5e-3
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_epilogue_only_five_seeds(seed):
+    d = fd.epilogue_inputs(seed, 128, 8192)
+    announce("epilogue cfg4-width", seed)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]), "sigmoid", "sum")
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                      "sigmoid", "sum")
+    got = host64(o)
+    assert_close(f"seed {seed}", got, ref, *TOL["bf16"])
+    # the contract tolerance (~82 at 4096) cannot see a kernel that ignores C
+    assert_close(f"seed {seed} supplementary", got, ref, SUM_ATOL, 0.0)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_cfg4_end_to_end_sampled(seed):
+    c = fd.CONFIGS["cfg4"]
+    m, n, k = c["m"], c["n"], c["k"]
+    d = fd.gemm_epilogue_inputs(seed, m, n, k)
+    announce("cfg4 gemm + epilogue", seed)
+    a, b = dev(d["a"]), dev(d["b"])
+    cmat = fs.gemm(a, b)
+    o = fs.gemm_epilogue_reduce(cmat, dev(d["bias"]), dev(d["col_scale"]), "sigmoid", "sum")
+    idx = np.unique(np.concatenate([[0, m - 1], np.random.default_rng(seed).integers(0, m, 30)]))
+    c64 = d["a"].rows(idx).f64() @ d["b"].f64()
+    # the library GEMM (row-major mapping onto hipBLASLt) against f64
+    assert_close("gemm C", host64(cmat[torch.from_numpy(idx).cuda()]), c64, *TOL["bf16"])
+    ref = oracle.gemm_epilogue_reduce(c64, d["bias"].f64(), d["col_scale"].f64(), "sigmoid", "sum")
+    # C is stored in bf16 (|dC| <= 2^-9 |C|) and sigmoid' <= 1/4, scale <= 1.5:
+    # |d out| <= sum_j 0.25 * 1.5 * 2^-9 |C_ij| plus the fp32 sum error
+    bound = 0.25 * 1.5 * 2.0 ** -9 * np.abs(c64).sum(axis=1) + SUM_ATOL
+    err = np.abs(host64(o[torch.from_numpy(idx).cuda()]) - ref)
+    assert np.all(err <= bound), f"end-to-end error {err.max()} above bound {bound.min()}"
+
+
+def test_zero_input_is_exactly_half_count():
+    cm = torch.zeros(5, 8192, dtype=torch.bfloat16, device="cuda")
+    o = fs.gemm_epilogue_reduce(cm, torch.zeros(8192, dtype=torch.bfloat16, device="cuda"),
+                                torch.ones(8192, device="cuda"), "sigmoid", "sum")
+    np.testing.assert_array_equal(host64(o), 4096.0)
+
+
+def test_sign_flip_symmetry():
+    d = fd.epilogue_inputs(7, 16, 8192)
+    c, b, s = dev(d["c"]), dev(d["bias"]), dev(d["col_scale"])
+    o1 = host64(fs.gemm_epilogue_reduce(c, b, s))
+    o2 = host64(fs.gemm_epilogue_reduce(-c, -b, s))
+    np.testing.assert_allclose(o1 + o2, 8192.0, atol=2 * SUM_ATOL)
+
+
+@pytest.mark.parametrize("c_dtype,b_dtype", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
+                                             ("f32", "bf16")])
+@pytest.mark.parametrize("cols", [1, 7, 8, 100, 512, 1000, 4096, 8192, 8200, 16384, 40000])
+def test_widths_and_dtypes(c_dtype, b_dtype, cols):
+    rows = 11 if cols <= 16384 else 3
+    d = fd.epilogue_inputs(cols, rows, cols, c_dtype, bias_dtype=b_dtype)
+    announce("epilogue width", cols, c_dtype, b_dtype)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]))
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                      "sigmoid", "sum")
+    tol = max(SUM_ATOL * cols / 8192, 1e-5)
+    assert_close(f"cols {cols}", host64(o), ref, tol, 1e-6)
+
+
+@pytest.mark.parametrize("act", ["none", "relu", "gelu_erf", "sigmoid"])
+@pytest.mark.parametrize("reduce", ["sum", "mean"])
+@pytest.mark.parametrize("with_bias,with_scale", [(True, True), (False, True), (True, False),
+                                                  (False, False)])
+def test_acts_reductions_optionals(act, reduce, with_bias, with_scale):
+    d = fd.epilogue_inputs(3, 9, 2048, "f32", c_std=1.0, bias_dtype="f32")
+    announce("epilogue options", act, reduce, with_bias, with_scale)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]) if with_bias else None,
+                                dev(d["col_scale"]) if with_scale else None, act, reduce)
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64() if with_bias else None,
+                                      d["col_scale"].f64() if with_scale else None, act, reduce)
+    assert_close(f"{act} {reduce}", host64(o), ref, 2e-3 if reduce == "sum" else 1e-6, 1e-5)
+
+
+def test_strided_and_misaligned_c():
+    d = fd.epilogue_inputs(4, 17, 3000, "bf16")
+    base = torch.empty(17 * 3072 + 8, dtype=torch.bfloat16, device="cuda")
+    for offset in (0, 1):
+        announce("epilogue strided", offset)
+        view = base[offset:offset + 17 * 3072].view(17, 3072)[:, :3000]
+        view.copy_(dev(d["c"]))
+        o = fs.gemm_epilogue_reduce(view, dev(d["bias"]), dev(d["col_scale"]))
+        ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                          "sigmoid", "sum")
+        assert_close(f"strided offset {offset}", host64(o), ref, SUM_ATOL, 0)
+
+
+def test_zero_columns_sum_writes_zeros():
+    out = torch.full((6,), 7.0, device="cuda")
+    fs.gemm_epilogue_reduce(torch.empty(6, 0, dtype=torch.bfloat16, device="cuda"), out=out)
+    np.testing.assert_array_equal(host64(out), 0.0)
+
+
+@pytest.mark.slow
+def test_beyond_2_31_elements():
+    rows, cols = (1 << 18) + 3, 8192
+    d = fd.epilogue_inputs(12, 64, cols)
+    announce("epilogue > 2^31 elements", rows, cols)
+    c = dev(d["c"]).repeat((rows + 63) // 64, 1)[:rows]
+    o = fs.gemm_epilogue_reduce(c, dev(d["bias"]), dev(d["col_scale"]))
+    idx = np.array([0, 1, 64, rows // 2, rows - 1])
+    ref = oracle.gemm_epilogue_reduce(d["c"].rows(idx % 64).f64(), d["bias"].f64(),
+                                      d["col_scale"].f64(), "sigmoid", "sum")
+    assert_close("beyond 2^31", host64(o[torch.from_numpy(idx).cuda()]), ref, SUM_ATOL, 0)

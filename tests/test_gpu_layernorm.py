@@ -1,0 +1,143 @@
+"""GPU parity of fs_layernorm_residual against the float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import (SEEDS, TOL, Guarded, announce, assert_close, bf16_ulp_close, dev, host64)
+
+pytestmark = pytest.mark.gpu
+
+
+def check(name, d, y, ro, dtype, has_res=True, affine=True):
+    g = d["gamma"].f64() if affine else None
+    b = d["beta"].f64() if affine else None
+    r = d["residual"].f64() if has_res else None
+    ref_y, _ = oracle.layernorm_residual(d["x"].f64(), r, g, b, d["eps"])
+    got = host64(y)
+    assert_close(name + " y", got, ref_y, *TOL[dtype])
+    if dtype == "bf16":
+        # fp32 statistics keep y within one bf16 rounding of exact (+ fp32 noise)
+        bf16_ulp_close(name + " y", got, ref_y, ulps=1.0, atol=2e-5)
+    if ro is not None:
+        if dtype == "bf16":
+            want = oracle.residual_store_bf16(d["x"].f64(), d["residual"].f64())
+            np.testing.assert_array_equal(host64(ro), want, err_msg=name + " residual_out")
+        else:
+            want = d["x"].data + d["residual"].data        # the fp32 sum
+            np.testing.assert_array_equal(host64(ro), want.astype(np.float64))
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_cfg3_rows_five_seeds(seed):
+    d = fd.layernorm_inputs(seed, 80, 4096)
+    announce("layernorm cfg3-width", seed)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                  dev(d["beta"]), d["eps"])
+    check(f"seed {seed}", d, y, ro, "bf16")
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_cfg3_full_size_sampled(seed):
+    d = fd.make_inputs("cfg3", seed)
+    rows = fd.CONFIGS["cfg3"]["rows"]
+    announce("layernorm cfg3 full", seed)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                  dev(d["beta"]), d["eps"])
+    idx = np.unique(np.concatenate([[0, rows - 1], np.random.default_rng(seed).integers(0, rows, 62)]))
+    ti = torch.from_numpy(idx).cuda()
+    sub = {k: d[k].rows(idx) for k in ("x", "residual")}
+    sub.update(gamma=d["gamma"], beta=d["beta"], eps=d["eps"])
+    check(f"cfg3 seed {seed}", sub, y[ti], ro[ti], "bf16")
+    # every row: residual_out is bit-exactly the rounded fp32 sum
+    want = (dev(d["x"]).float() + dev(d["residual"]).float()).to(torch.bfloat16)
+    assert torch.equal(ro.view(torch.int16), want.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [1, 2, 7, 64, 100, 1024, 4096, 4099, 8192, 20000, 65536])
+def test_widths(dtype, cols):
+    rows = 9 if cols <= 8192 else 3
+    d = fd.layernorm_inputs(cols, rows, cols, dtype)
+    announce("layernorm width", cols, dtype)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                  dev(d["beta"]), d["eps"])
+    check(f"cols {cols}", d, y, ro, dtype)
+
+
+@pytest.mark.parametrize("has_res,affine,store", [(False, True, False), (True, False, True),
+                                                  (True, True, False), (False, False, False)])
+def test_optional_operands(has_res, affine, store):
+    d = fd.layernorm_inputs(3, 33, 1024, "bf16")
+    announce("layernorm optional", has_res, affine, store)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]) if has_res else None,
+                                  dev(d["gamma"]) if affine else None,
+                                  dev(d["beta"]) if affine else None, d["eps"],
+                                  store_residual=store)
+    assert (ro is None) == (not (has_res and store))
+    check("optional", d, y, ro, "bf16", has_res, affine)
+
+
+def test_statistics_properties_fp32():
+    # gamma = 1, beta = 0: each row has mean 0 and variance var/(var+eps)
+    d = fd.layernorm_inputs(9, 16, 4096, "f32")
+    y, _ = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), None, None, 0.25)
+    y = host64(y)
+    h = d["x"].f64() + d["residual"].f64()
+    var = h.var(axis=1)
+    np.testing.assert_allclose(y.mean(axis=1), 0.0, atol=1e-6)
+    np.testing.assert_allclose(y.var(axis=1), var / (var + 0.25), rtol=1e-5)
+
+
+def test_constant_rows_give_beta():
+    x = torch.full((4, 1024), 3.0, device="cuda")
+    beta = torch.linspace(-1, 1, 1024, device="cuda")
+    gamma = torch.ones(1024, device="cuda")
+    y, _ = fs.layernorm_residual(x, None, gamma, beta, 1e-5)
+    assert_close("constant rows", host64(y), np.broadcast_to(host64(beta), (4, 1024)), 1e-6, 0)
+
+
+def test_in_place_outputs():
+    d = fd.layernorm_inputs(4, 40, 4096, "bf16")
+    x, r = dev(d["x"]), dev(d["residual"])
+    fs.layernorm_residual(x, r, dev(d["gamma"]), dev(d["beta"]), d["eps"], out=x,
+                          residual_out=r)             # y == x, residual_out == residual
+    torch.cuda.synchronize()
+    check("in place", d, x, r, "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_misaligned_and_guards(dtype):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 13, 1500, 1536
+    d = fd.layernorm_inputs(13, rows, cols, dtype)
+    for offset in (0, 1):
+        announce("layernorm guard", dtype, offset)
+        xg = Guarded(rows, cols, ld, tdt, offset=offset)
+        xg.view.copy_(dev(d["x"]))
+        yg = Guarded(rows, cols, ld + 16, tdt, offset=offset)
+        og = Guarded(rows, cols, ld + 32, tdt, offset=offset)
+        fs.layernorm_residual(xg.view, dev(d["residual"]), dev(d["gamma"]), dev(d["beta"]),
+                              d["eps"], out=yg.view, residual_out=og.view)
+        torch.cuda.synchronize()
+        check(f"strided offset {offset}", d, yg.view, og.view, dtype)
+        yg.check_untouched("layernorm y")
+        og.check_untouched("layernorm residual_out")
+
+
+@pytest.mark.slow
+def test_beyond_2_31_elements():
+    rows, cols = (1 << 19) + 9, 4096
+    d = fd.layernorm_inputs(6, 64, cols, "bf16")
+    announce("layernorm > 2^31 elements", rows, cols)
+    rep = (rows + 63) // 64
+    x = dev(d["x"]).repeat(rep, 1)[:rows]
+    r = dev(d["residual"]).repeat(rep, 1)[:rows]
+    y, ro = fs.layernorm_residual(x, r, dev(d["gamma"]), dev(d["beta"]), d["eps"])
+    idx = np.array([0, 5, 64, rows // 3, rows - 1])
+    ti = torch.from_numpy(idx).cuda()
+    sub = {"x": d["x"].rows(idx % 64), "residual": d["residual"].rows(idx % 64),
+           "gamma": d["gamma"], "beta": d["beta"], "eps": d["eps"]}
+    check("beyond 2^31", sub, y[ti], ro[ti], "bf16")

@@ -1,0 +1,166 @@
+"""GPU parity of fs_row_softmax against the float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import (SEEDS, TOL, Guarded, announce, assert_close, bf16_ulp_close, dev, host64)
+
+pytestmark = pytest.mark.gpu
+
+
+def supplementary_bf16(name, got, ref, masked):
+    """The contract atol (1e-2) exceeds every probability of a 4096-wide row,
+    so also: about one bf16 rounding of the exact value, row sums near 1,
+    masked entries exactly +0."""
+    assert_close(name + " supplementary", got, ref, 1e-6, 8e-3)
+    sums = got.sum(axis=1)
+    live = ref.sum(axis=1) > 0
+    np.testing.assert_allclose(sums[live], 1.0, atol=2e-2, err_msg=name + " row sums")
+    assert np.all(got[masked] == 0.0), name + " masked entries not zero"
+    assert not np.any(np.signbit(got[masked])), name + " masked entries are -0"
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_cfg2_rows_five_seeds(seed):
+    d = fd.softmax_inputs(seed, 96, 4096)
+    announce("softmax cfg2-width", seed)
+    y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
+    got = host64(y)
+    ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
+    assert_close(f"seed {seed}", got, ref, *TOL["bf16"])
+    supplementary_bf16(f"seed {seed}", got, ref, np.isinf(d["mask"].f64()))
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_cfg2_full_size_sampled(seed):
+    c = fd.CONFIGS["cfg2"]
+    d = fd.make_inputs("cfg2", seed)
+    announce("softmax cfg2 full", seed)
+    y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
+    rows = c["rows"]
+    idx = np.unique(np.concatenate([[0, 1, rows - 1],
+                                    np.random.default_rng(seed).integers(0, rows, 61)]))
+    got = host64(y[torch.from_numpy(idx).cuda()])
+    ref = oracle.row_softmax(d["x"].rows(idx).f64(), d["mask"].rows(idx).f64(), d["scale"])
+    assert_close(f"cfg2 seed {seed}", got, ref, *TOL["bf16"])
+    supplementary_bf16(f"cfg2 seed {seed}", got, ref, np.isinf(d["mask"].rows(idx).f64()))
+    # property at every row: sums of the whole output
+    s = y.float().sum(dim=1)
+    assert torch.all((s - 1).abs() < 2e-2), "a row sum is off"
+
+
+@pytest.mark.parametrize("dtype,mask_dtype", [("f32", "f32"), ("f32", "bf16"), ("bf16", "bf16"),
+                                              ("bf16", "f32"), ("bf16", None), ("f32", None)])
+@pytest.mark.parametrize("cols", [1, 3, 8, 37, 511, 512, 513, 1000, 4095, 4096, 4104, 8192,
+                                  16384 + 8, 65536])
+def test_widths(dtype, mask_dtype, cols):
+    rows = 7 if cols <= 16384 else 3
+    d = fd.softmax_inputs(cols, rows, cols, dtype, mask_dtype=mask_dtype)
+    announce("softmax width", cols, dtype, mask_dtype)
+    y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
+    got = host64(y)
+    m = d["mask"].f64() if mask_dtype else None
+    ref = oracle.row_softmax(d["x"].f64(), m, d["scale"])
+    assert_close(f"cols {cols}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"cols {cols}", got, ref, ulps=1.0, atol=1e-7)
+    if m is not None:
+        assert np.all(got[np.isinf(m)] == 0.0)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_causal_attention_scores(seed):
+    # [2, 16, 512, 512] scores, causal, scale 1/8: the block's softmax shape
+    b, h, s = 2, 16, 512
+    d = fd.softmax_inputs(seed, b * h * s, s, "bf16", sigma=3.0, mask_dtype=None, scale=0.125)
+    announce("softmax causal", seed)
+    y = fs.row_softmax(dev(d["x"]), None, d["scale"], causal_q_len=s)
+    got = host64(y)
+    ref = oracle.row_softmax(d["x"].f64(), None, d["scale"], causal_q_len=s)
+    assert_close(f"causal seed {seed}", got, ref, *TOL["bf16"])
+    masked = oracle.causal_mask(b * h * s, s, s)
+    supplementary_bf16(f"causal seed {seed}", got, ref, masked)
+    one_hot = np.zeros(s)
+    one_hot[0] = 1.0
+    for r in range(0, b * h * s, s):          # row 0 of every head: exactly [1, 0, ...]
+        np.testing.assert_array_equal(got[r], one_hot)
+
+
+@pytest.mark.parametrize("q_len,cols", [(3, 10), (64, 512), (100, 4096), (512, 512)])
+def test_causal_offsets_and_widths(q_len, cols):
+    rows = 3 * q_len
+    d = fd.softmax_inputs(q_len + cols, rows, cols, "f32", mask_dtype="f32", p_masked=0.2)
+    announce("softmax causal offset", q_len, cols)
+    y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"], causal_q_len=q_len)
+    ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"], causal_q_len=q_len)
+    assert_close("causal offset", host64(y), ref, *TOL["f32"])
+
+
+def test_fully_masked_rows_and_large_logits():
+    x = torch.tensor([[1.0, 2.0, 3.0, 4.0], [3e4, 3e4 + np.log(3.0), -3e4, 0.0],
+                      [5.0, 5.0, 5.0, 5.0]], device="cuda")
+    mask = torch.tensor([[-np.inf] * 4, [0, 0, -np.inf, -np.inf], [0, -np.inf, 0, -np.inf]],
+                        device="cuda", dtype=torch.float32)
+    announce("softmax masked rows")
+    y = host64(fs.row_softmax(x, mask, 1.0))
+    np.testing.assert_array_equal(y[0], 0.0)
+    assert not np.any(np.signbit(y[0]))
+    np.testing.assert_allclose(y[1], [0.25, 0.75, 0, 0], rtol=1e-6)
+    np.testing.assert_allclose(y[2], [0.5, 0, 0.5, 0], rtol=1e-6)
+
+
+def test_general_additive_mask():
+    # a finite additive bias (not only 0/-inf)
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((9, 300)).astype(np.float32)
+    m = (rng.standard_normal((9, 300)) * 2).astype(np.float32)
+    y = fs.row_softmax(torch.from_numpy(x).cuda(), torch.from_numpy(m).cuda(), 0.5)
+    ref = oracle.row_softmax(x.astype(np.float64), m.astype(np.float64), 0.5)
+    assert_close("finite mask", host64(y), ref, *TOL["f32"])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_misaligned_in_place_and_guards(dtype):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 21, 777, 800
+    d = fd.softmax_inputs(21, rows, cols, dtype, mask_dtype=dtype)
+    ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
+    for offset in (0, 1):
+        announce("softmax guard", dtype, offset)
+        xg = Guarded(rows, cols, ld, tdt, offset=offset)
+        xg.view.copy_(dev(d["x"]))
+        mg = Guarded(rows, cols, ld + 8, tdt, offset=offset)
+        mg.view.copy_(dev(d["mask"]))
+        fs.row_softmax(xg.view, mg.view, d["scale"], out=xg.view)       # in place
+        torch.cuda.synchronize()
+        assert_close(f"strided in place offset {offset}", host64(xg.view), ref, *TOL[dtype])
+        xg.check_untouched("softmax y")
+        mg.check_untouched("softmax mask")
+
+
+def test_repeatable():
+    d = fd.softmax_inputs(5, 64, 4096)
+    x, m = dev(d["x"]), dev(d["mask"])
+    y1 = fs.row_softmax(x, m, d["scale"])
+    y2 = fs.row_softmax(x, m, d["scale"])
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.slow
+def test_beyond_2_31_elements():
+    rows, cols = (1 << 19) + 5, 4096
+    d = fd.softmax_inputs(8, 64, cols, "bf16")
+    announce("softmax > 2^31 elements", rows, cols)
+    rep = (rows + 63) // 64
+    x = dev(d["x"]).repeat(rep, 1)[:rows]
+    m = dev(d["mask"]).repeat(rep, 1)[:rows]
+    y = fs.row_softmax(x, m, d["scale"])
+    idx = np.array([0, 1, 64, rows // 2 + 7, rows - 1])
+    got = host64(y[torch.from_numpy(idx).cuda()])
+    ref = oracle.row_softmax(d["x"].rows(idx % 64).f64(), d["mask"].rows(idx % 64).f64(),
+                             d["scale"])
+    assert_close("beyond 2^31", got, ref, *TOL["bf16"])
+    bf16_ulp_close("beyond 2^31", got, ref, atol=1e-7)
