@@ -55,10 +55,10 @@ def _run(cmd, verbose):
         print(out, flush=True)
 
 
-def _compile(src, verbose):
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    _run([_hipcc(), *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),
-          "-o", obj], verbose)
+def _compile(src, verbose, build_dir=BUILD, defines=()):
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    _run([_hipcc(), *HIP_FLAGS, *defines, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+          os.path.join(CSRC, src), "-o", obj], verbose)
     return obj
 
 
@@ -83,6 +83,17 @@ def build(verbose: bool = False, jobs: int = 8) -> None:
     _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
           f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
     os.replace(LIB_FSGEMM + ".tmp", LIB_FSGEMM)
+
+
+def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8) -> str:
+    """Build libfusedsub.so into ``out_dir`` with extra ``-D`` build-time
+    tuning parameters (see the FS_* macros in csrc/); returns its path."""
+    os.makedirs(out_dir, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose, out_dir, defines), FUSEDSUB_SOURCES))
+    out = os.path.join(out_dir, "libfusedsub.so")
+    _link(objs, out, [], verbose)
+    return out
 
 
 def clean() -> None:

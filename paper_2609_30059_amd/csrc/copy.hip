@@ -4,12 +4,19 @@
 #include "device_common.hpp"
 #include "launch.hpp"
 
+#ifndef FS_COPY_UNROLL
+#define FS_COPY_UNROLL 1
+#endif
+#ifndef FS_COPY_BLOCKS_PER_CU
+#define FS_COPY_BLOCKS_PER_CU 64
+#endif
+
 namespace fs {
 namespace {
 
 __global__ __launch_bounds__(256) void copy128_kernel(const u32x4* __restrict__ src,
                                                        u32x4* __restrict__ dst, int64_t n) {
-  constexpr int U = 4;
+  constexpr int U = FS_COPY_UNROLL;
   const int64_t stride = int64_t(gridDim.x) * 256;
   int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   for (; i + (U - 1) * stride < n; i += U * stride) {
@@ -35,7 +42,7 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipSt
                    (reinterpret_cast<uintptr_t>(dst) % 16 == 0) && (bytes % 16 == 0);
   const int64_t n = vec ? bytes / 16 : bytes;
   int64_t grid = (n + 255) / 256;
-  const int64_t cap = int64_t(cus) * 8;
+  const int64_t cap = int64_t(cus) * FS_COPY_BLOCKS_PER_CU;
   if (grid > cap) grid = cap;
   if (grid < 1) grid = 1;
   if (vec)

@@ -12,7 +12,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// Build-time tuning parameters (defaults measured on MI355X).  Streaming
+// loads and stores use the non-temporal hint unless these are set to 0.
+#ifndef FS_NT_LOAD
+#define FS_NT_LOAD 1
+#endif
+#ifndef FS_NT_STORE
+#define FS_NT_STORE 1
+#endif
+
 namespace fs {
+
+constexpr bool kNtLoad = FS_NT_LOAD != 0;
+constexpr bool kNtStore = FS_NT_STORE != 0;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -74,15 +86,16 @@ template <> struct Elem<uint16_t> {   // bf16 bit patterns
 };
 
 // 128-bit loads/stores.  Streaming data is touched once, so it is loaded and
-// stored non-temporally (it should not displace reused data from the caches).
+// stored non-temporally (it should not displace reused data from the caches);
+// NT = true means "streaming", subject to the build-time switches above.
 template <bool NT>
 __device__ __forceinline__ u32x4 ld128(const void* p) {
-  if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  if constexpr (NT && kNtLoad) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
   else return *reinterpret_cast<const u32x4*>(p);
 }
 template <bool NT>
 __device__ __forceinline__ void st128(void* p, const u32x4& v) {
-  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+  if constexpr (NT && kNtStore) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
   else *reinterpret_cast<u32x4*>(p) = v;
 }
 
@@ -103,12 +116,65 @@ __device__ __forceinline__ void ldv(const T* p, float* out) {
     Elem<T>::unpack(ld128<NT>(p + kPer16), out + kPer16);
   } else if constexpr (kBytes == 8 && sizeof(T) == 2) {
     u32x2 w;
-    if constexpr (NT) w = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+    if constexpr (NT && kNtLoad) w = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
     else w = *reinterpret_cast<const u32x2*>(p);
     out[0] = bf16_lo(w.x); out[1] = bf16_hi(w.x); out[2] = bf16_lo(w.y); out[3] = bf16_hi(w.y);
   } else {
     static_assert(kBytes == 16, "unsupported vector load width");
   }
+}
+
+// V consecutive elements of T held in registers exactly as loaded (bf16 stays
+// packed two per dword until unpacked).  Loads are unconditional: callers
+// clamp out-of-range addresses onto an in-bounds vector and mask the values
+// afterwards, so the compiler can keep every load of a row in flight at once
+// (a load under a per-lane branch forces a wait for all older loads).
+template <typename T, int V>
+struct Raw {
+  static constexpr int kBytes = int(sizeof(T)) * V;
+  static constexpr int kWords = V == 1 ? 1 : kBytes / 4;
+  uint32_t w[kWords];
+
+  template <bool NT = true>
+  __device__ __forceinline__ void load(const T* p) {
+    if constexpr (V == 1) {
+      w[0] = __float_as_uint(Elem<T>::load1(p));
+    } else if constexpr (kBytes == 16) {
+      const u32x4 v = ld128<NT>(p);
+      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else if constexpr (kBytes == 32) {
+      const u32x4 a = ld128<NT>(p), b = ld128<NT>(p + 16 / sizeof(T));
+      w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+      w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+    } else {
+      static_assert(kBytes == 8, "unsupported raw vector width");
+      u32x2 v;
+      if constexpr (NT && kNtLoad) v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+      else v = *reinterpret_cast<const u32x2*>(p);
+      w[0] = v.x; w[1] = v.y;
+    }
+  }
+  __device__ __forceinline__ void unpack(float* out) const {
+    if constexpr (V == 1) {
+      out[0] = __uint_as_float(w[0]);
+    } else if constexpr (sizeof(T) == 4) {
+#pragma unroll
+      for (int i = 0; i < V; ++i) out[i] = __uint_as_float(w[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < V / 2; ++i) {
+        out[2 * i] = bf16_lo(w[i]);
+        out[2 * i + 1] = bf16_hi(w[i]);
+      }
+    }
+  }
+};
+
+// Store V fp32 values as T (16 bytes when V > 1).
+template <typename T, int V>
+__device__ __forceinline__ void stv(T* p, const float* v) {
+  if constexpr (V == 1) Elem<T>::store1(p, v[0]);
+  else st128<true>(p, Elem<T>::pack(v));
 }
 
 // ---------------------------------------------------------------------------
@@ -164,6 +230,66 @@ __device__ __forceinline__ P group_allreduce(P p, P* lds, int wave, int lane) {
     return acc;
   }
 }
+
+// ---------------------------------------------------------------------------
+// activations
+// ---------------------------------------------------------------------------
+// GELU(z) = z * Phi(z) = max(z, 0) - |z| * Q(|z|), where Q(x) = erfc(x/sqrt 2)/2
+// is the upper tail of the standard normal.  erfc(u) = (1 + a1 u + ... +
+// a6 u^6)^-16 with the coefficients of Abramowitz & Stegun, Handbook of
+// Mathematical Functions, formula 7.1.28 (|error of erf| <= 3e-7, u >= 0).
+// The 1/sqrt(2) of the argument (a_i / 2^(i/2)) and the 1/2 of Q (2^(1/16)
+// on the whole polynomial) are folded into the coefficients, so
+// Q(x) = 1 / q(x)^16: six FMAs, four squarings, one v_rcp_f32 and two more
+// operations, with no branch.  Large |z| overflow q^16 to +inf, giving Q = 0;
+// |z| is clamped in the product so that GELU(+inf) = +inf.
+__device__ __forceinline__ float gelu_erf(float z) {
+  constexpr double k = 1.0442737824274138;       // 2^(1/16)
+  constexpr double r2 = 1.4142135623730951;      // sqrt 2
+  constexpr float c0 = float(k);
+  constexpr float c1 = float(k * 0.0705230784 / r2);
+  constexpr float c2 = float(k * 0.0422820123 / 2.0);
+  constexpr float c3 = float(k * 0.0092705272 / (2.0 * r2));
+  constexpr float c4 = float(k * 0.0001520143 / 4.0);
+  constexpr float c5 = float(k * 0.0002765672 / (4.0 * r2));
+  constexpr float c6 = float(k * 0.0000430638 / 8.0);
+  const float x = fabsf(z);
+  float q = fmaf(c6, x, c5);
+  q = fmaf(q, x, c4);
+  q = fmaf(q, x, c3);
+  q = fmaf(q, x, c2);
+  q = fmaf(q, x, c1);
+  q = fmaf(q, x, c0);
+  q = q * q;   // q^2
+  q = q * q;   // q^4
+  q = q * q;   // q^8
+  q = q * q;   // q^16
+  const float tail = __builtin_amdgcn_rcpf(q);     // Q(|z|)
+  return fmaf(-fminf(x, 1e30f), tail, fmaxf(z, 0.f));
+}
+
+// logistic 1 / (1 + 2^(-z log2 e)): one v_exp_f32 and one v_rcp_f32
+__device__ __forceinline__ float sigmoid(float z) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-z * kLog2e));
+}
+
+// R independent partials reduced together (one shuffle sequence for R rows)
+template <class P, int R>
+struct Multi {
+  P p[R];
+  __device__ __forceinline__ static Multi combine(const Multi& a, const Multi& b) {
+    Multi o;
+#pragma unroll
+    for (int r = 0; r < R; ++r) o.p[r] = P::combine(a.p[r], b.p[r]);
+    return o;
+  }
+  template <class F> __device__ __forceinline__ static Multi map(const Multi& a, F f) {
+    Multi o;
+#pragma unroll
+    for (int r = 0; r < R; ++r) o.p[r] = P::map(a.p[r], f);
+    return o;
+  }
+};
 
 // plain sum
 struct SumP {

@@ -5,27 +5,38 @@
 // KernelOPT Appendix A (Codegen prompt: keep the matmul a library call and
 // fuse only its epilogue; Fusion Agent: reduction + pointwise).
 //
-// Design (gfx950): a block of W wave64s owns ALL columns of the matrix and
-// walks down the rows (grid-stride).  Each thread owns NV 16-byte column
-// vectors and keeps their epilogue coefficients in registers for the whole
-// kernel, so C is the only HBM stream; bias and scale are read once per
-// block.  (C + b) * s is evaluated as C * s + b * s (one FMA); for the
-// sigmoid the factor -log2(e) is folded into both coefficients so that
-// sigmoid = 1 / (1 + 2^u) costs one v_exp_f32 and one v_rcp_f32.  R rows are
-// processed per trip; their W per-wave partial sums meet in LDS
-// (double-buffered, one barrier per trip) and R threads finish them.
+// Design (gfx950).  (C + b) * s is evaluated as C * s + b * s (one FMA per
+// element); for the sigmoid the factor -log2(e) is folded into both
+// coefficients so that sigmoid = 1 / (1 + 2^u) costs one v_exp_f32 and one
+// v_rcp_f32.  The per-column coefficients (s, b*s) are staged once per block
+// in LDS; then every wave reduces whole rows on its own -- no block barrier
+// in the row loop.  A wave reads its row in chunks of CH 16-byte vectors per
+// lane and software-pipelines them: the loads of the next chunk (of this row
+// or of its next row) are in flight while the current chunk is evaluated, so
+// HBM traffic and the transcendental work overlap inside every wave.
+//
+// LDS layout: vector v = k*64 + lane of a row holds V columns; its V scale
+// factors are H = V/4 float4s at index (k*H + h)*64 + lane, so each
+// ds_read_b128 of a wave touches 64 consecutive float4s (no bank conflicts).
+// The biases times scale use the same layout in a second array.
+//
+// Rows wider than the LDS staging capacity, or C that is not 16-byte
+// aligned, take a block-per-row kernel that reads the coefficients through
+// the cache.
 #include "device_common.hpp"
 #include "launch.hpp"
 
 namespace fs {
 namespace {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 template <int ACT>
 __device__ __forceinline__ float epi_act(float u) {
   if constexpr (ACT == FS_ACT_SIGMOID) {
     return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(u));   // u = -t*log2(e)
   } else if constexpr (ACT == FS_ACT_GELU_ERF) {
-    return 0.5f * u * (1.f + erff(u * 0.70710678118654752f));
+    return gelu_erf(u);
   } else if constexpr (ACT == FS_ACT_RELU) {
     return u > 0.f ? u : 0.f;
   } else {
@@ -33,111 +44,131 @@ __device__ __forceinline__ float epi_act(float u) {
   }
 }
 
-template <int R>
-struct RowSums {
-  float s[R];
-  __device__ __forceinline__ static RowSums combine(const RowSums& a, const RowSums& b) {
-    RowSums o;
-#pragma unroll
-    for (int r = 0; r < R; ++r) o.s[r] = a.s[r] + b.s[r];
-    return o;
-  }
-  template <class F> __device__ __forceinline__ static RowSums map(const RowSums& a, F f) {
-    RowSums o;
-#pragma unroll
-    for (int r = 0; r < R; ++r) o.s[r] = f(a.s[r]);
-    return o;
-  }
-};
+template <int ACT>
+__device__ __forceinline__ float coef_sign() {
+  return ACT == FS_ACT_SIGMOID ? -kLog2e : 1.f;
+}
 
-template <typename CT, typename BT, int ACT, int W, int NV, int R, bool VEC>
-__global__ __launch_bounds__(64 * W) void epilogue_kernel(
+// Coefficients of the NVEC*64 vectors of a row into LDS (zeros past the row).
+template <typename BT, int V, int H, int NVEC, int W, bool HB, bool HS>
+__device__ __forceinline__ void fill_coef(f32x4* sc, f32x4* bs, const BT* __restrict__ bias,
+                                          const float* __restrict__ col_scale, int nvec,
+                                          float sgn) {
+  for (int i = threadIdx.x; i < NVEC * 64 * H; i += 64 * W) {
+    // i enumerates (vector, half): vector vi = i / H, half h = i % H
+    const int vi = i / H, h = i % H;
+    const int k = vi / 64, ln = vi % 64;
+    const bool live = vi < nvec;
+    const int c0 = (live ? vi : nvec - 1) * V + h * 4;   // clamped: always in bounds
+    float sv[4], bv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sv[e] = HS ? col_scale[c0 + e] : 1.f;
+      bv[e] = HB ? Elem<BT>::load1(bias + c0 + e) : 0.f;
+    }
+    f32x4 s4, b4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float s = sv[e] * sgn;
+      s4[e] = live ? s : 0.f;
+      b4[e] = live ? bv[e] * s : 0.f;
+    }
+    sc[(k * H + h) * 64 + ln] = s4;
+    bs[(k * H + h) * 64 + ln] = b4;
+  }
+}
+
+// NVEC: 16-byte vectors per lane per row (compile-time ceiling); CHMAX:
+// vectors per pipelined chunk (at most NVEC); W: waves per block.
+template <typename CT, typename BT, int ACT, int NVEC, int CHMAX, int W>
+__global__ __launch_bounds__(64 * W) void epilogue_lds_kernel(
     const CT* __restrict__ c, int64_t ld_c, const BT* __restrict__ bias,
     const float* __restrict__ col_scale, float* __restrict__ out, int64_t rows, int cols,
     int mean) {
-  constexpr int kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<CT>::kVec : 1;
-  __shared__ float lds[2][R][W];
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  constexpr int V = Elem<CT>::kVec;    // columns per vector
+  constexpr int H = V / 4;             // float4s of coefficients per vector
+  constexpr int CH = CHMAX < NVEC ? CHMAX : NVEC;
+  constexpr int NCH = NVEC / CH;
+  static_assert(NVEC % CH == 0, "NVEC must be a multiple of CH");
+  extern __shared__ f32x4 lds_coef[];
+  f32x4* sc = lds_coef;                       // [NVEC * H * 64]
+  f32x4* bs = lds_coef + NVEC * H * 64;       // [NVEC * H * 64]
 
-  // per-column coefficients: u = C * sc + bs
-  float sc[NV][V], bs[NV][V];
-  const float sgn = (ACT == FS_ACT_SIGMOID) ? -kLog2e : 1.f;
-#pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    const int c0 = (k * kThreads + tid) * V;
-#pragma unroll
-    for (int i = 0; i < V; ++i) {
-      const int col = c0 + i;
-      float s = 0.f, b = 0.f;
-      if (col < cols) {
-        s = col_scale ? col_scale[col] : 1.f;
-        b = bias ? Elem<BT>::load1(bias + col) : 0.f;
-      }
-      sc[k][i] = s * sgn;
-      bs[k][i] = b * s * sgn;
-    }
+  const int nvec = cols / V;                  // vectors in a row
+  const float sgn = coef_sign<ACT>();
+  // stage (s, b*s): the null checks sit outside the loop so that each body is
+  // branch-free and its loads are issued together
+  if (bias) {
+    if (col_scale) fill_coef<BT, V, H, NVEC, W, true, true>(sc, bs, bias, col_scale, nvec, sgn);
+    else fill_coef<BT, V, H, NVEC, W, true, false>(sc, bs, bias, col_scale, nvec, sgn);
+  } else {
+    if (col_scale) fill_coef<BT, V, H, NVEC, W, false, true>(sc, bs, bias, col_scale, nvec, sgn);
+    else fill_coef<BT, V, H, NVEC, W, false, false>(sc, bs, bias, col_scale, nvec, sgn);
   }
+  __syncthreads();
 
-  int parity = 0;
-  for (int64_t r0 = int64_t(blockIdx.x) * R; r0 < rows; r0 += int64_t(gridDim.x) * R) {
-    float cv[R][NV][V];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int64_t stride = int64_t(gridDim.x) * W;
+  int64_t row = int64_t(blockIdx.x) * W + wave;
+  if (row >= rows) return;            // no barrier after this point
+
+  // raw chunks: CH vectors of 4 dwords each, double-buffered.  Loads are
+  // unconditional (a lane past the row end re-reads the row's last vector)
+  // so the next chunk stays in flight while the current one is evaluated.
+  u32x4 buf[2][CH];
+  auto load_chunk = [&](u32x4 (&dst)[CH], int64_t r, int j) {
+    const CT* cr = c + r * ld_c;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
+    for (int q = 0; q < CH; ++q) {
+      const int vi = (j * CH + q) * 64 + lane;
+      dst[q] = ld128<true>(cr + (vi < nvec ? vi : nvec - 1) * V);
+    }
+  };
+  load_chunk(buf[0], row, 0);
+  while (true) {
+    float acc = 0.f;
+    const int64_t next = row + stride;
+    // the coefficients are re-read from LDS for every row: the opaque copy of
+    // the lane index stops the compiler from hoisting 2*NVEC*H float4s of
+    // loop-invariant LDS reads into registers (which would spill)
+    int li = lane;
+    asm volatile("" : "+v"(li));
+    const int64_t pre = next < rows ? next : row;   // prefetch target of the last chunk
 #pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
-        if (r0 + r < rows && c0 < cols) {
-          ldv<CT, V>(c + (r0 + r) * ld_c + c0, cv[r][k]);
-        } else {
+    for (int j = 0; j < NCH; ++j) {
+      // prefetch: next chunk of this row, or chunk 0 of the next row
+      if (j + 1 < NCH) load_chunk(buf[(j + 1) & 1], row, j + 1);
+      else load_chunk(buf[(j + 1) & 1], pre, 0);
 #pragma unroll
-          for (int i = 0; i < V; ++i) cv[r][k][i] = 0.f;
+      for (int q = 0; q < CH; ++q) {
+        const int vi = (j * CH + q) * 64 + lane;
+        float v[V];
+        Elem<CT>::unpack(buf[j & 1][q], v);
+        const int kq = j * CH + q;
+        float part = 0.f;
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+          const f32x4 s4 = sc[(kq * H + h) * 64 + li];
+          const f32x4 b4 = bs[(kq * H + h) * 64 + li];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) part += epi_act<ACT>(fmaf(v[h * 4 + e], s4[e], b4[e]));
         }
+        acc += vi < nvec ? part : 0.f;
       }
     }
-    RowSums<R> ps;
+    const SumP t = wave_allreduce(SumP{acc});
+    if (lane == 0) out[row] = mean ? t.s / float(cols) : t.s;
+    if (next >= rows) break;
+    row = next;
+    if constexpr (NCH % 2 == 1) {
+      // with an odd chunk count the next row's chunk 0 landed in buf[1]
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      float acc = 0.f;
-#pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
-        if (c0 < cols) {
-#pragma unroll
-          for (int i = 0; i < V; ++i) {
-            const float v = epi_act<ACT>(fmaf(cv[r][k][i], sc[k][i], bs[k][i]));
-            if (VEC || c0 + i < cols) acc += v;
-          }
-        }
-      }
-      ps.s[r] = acc;
-    }
-    ps = wave_allreduce(ps);
-    if constexpr (W == 1) {
-      // every lane holds the R sums; lane r stores row r0 + r
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        if (lane == r && r0 + r < rows) out[r0 + r] = mean ? ps.s[r] / float(cols) : ps.s[r];
-      }
-    } else {
-      if (lane == 0) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) lds[parity][r][wave] = ps.s[r];
-      }
-      __syncthreads();
-      if (tid < R && r0 + tid < rows) {
-        float t = 0.f;
-#pragma unroll
-        for (int w = 0; w < W; ++w) t += lds[parity][tid][w];
-        out[r0 + tid] = mean ? t / float(cols) : t;
-      }
-      parity ^= 1;
+      for (int q = 0; q < CH; ++q) buf[0][q] = buf[1][q];
     }
   }
 }
 
-// Rows longer than the register-resident capacity: one block per row, the
-// coefficients read through the cache for every element.
+// Any width, any alignment: one block per row, coefficients through the cache.
 template <typename CT, typename BT, int ACT>
 __global__ __launch_bounds__(256) void epilogue_wide_kernel(
     const CT* __restrict__ c, int64_t ld_c, const BT* __restrict__ bias,
@@ -145,7 +176,7 @@ __global__ __launch_bounds__(256) void epilogue_wide_kernel(
     int mean) {
   __shared__ SumP lds[2][4];
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
-  const float sgn = (ACT == FS_ACT_SIGMOID) ? -kLog2e : 1.f;
+  const float sgn = coef_sign<ACT>();
   int parity = 0;
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const CT* cr = c + row * ld_c;
@@ -161,62 +192,63 @@ __global__ __launch_bounds__(256) void epilogue_wide_kernel(
   }
 }
 
-template <typename CT, typename BT, int ACT, bool VEC>
+#ifndef FS_EPI_WAVES
+#define FS_EPI_WAVES 8
+#endif
+#ifndef FS_EPI_CHUNK
+#define FS_EPI_CHUNK 2
+#endif
+#ifndef FS_EPI_BLOCKS_PER_CU
+#define FS_EPI_BLOCKS_PER_CU 2
+#endif
+constexpr int kLdsW = FS_EPI_WAVES;    // waves per block of the staged kernel
+constexpr int kLdsCH = FS_EPI_CHUNK;   // vectors per pipelined chunk
+
+template <typename CT, typename BT, int ACT>
 hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
-  constexpr int V = VEC ? Elem<CT>::kVec : 1;
-  constexpr int R = 2;
-  const int64_t c = a.cols;
+  constexpr int V = Elem<CT>::kVec;
   const int mean = a.reduce == FS_REDUCE_MEAN;
-  auto launch = [&](auto kern, int threads, int blocks_per_cu) {
-    int64_t want = (a.rows + R - 1) / R;
-    int64_t cap = int64_t(cus) * blocks_per_cu;
+  const int64_t per_lane = (a.cols / V + 63) / 64;
+  auto staged = [&](auto kern, int nvec) {
+    const size_t lds = size_t(2) * nvec * (V / 4) * 64 * 16;
+    int64_t want = (a.rows + kLdsW - 1) / kLdsW;
+    int64_t cap = int64_t(cus) * FS_EPI_BLOCKS_PER_CU;
     int grid = int(want < cap ? want : cap);
     if (grid < 1) grid = 1;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s, static_cast<const CT*>(a.c), a.ld_c,
-                       static_cast<const BT*>(a.bias), a.col_scale, a.out, a.rows, int(a.cols),
-                       mean);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kLdsW), lds, s, static_cast<const CT*>(a.c),
+                       a.ld_c, static_cast<const BT*>(a.bias), a.col_scale, a.out, a.rows,
+                       int(a.cols), mean);
     return hipGetLastError();
   };
-#define FS_EP(Wv, NVv, BPC)                                                           \
-  if (c <= int64_t(64) * Wv * NVv * V)                                                 \
-    return launch(epilogue_kernel<CT, BT, ACT, Wv, NVv, R, VEC>, 64 * Wv, BPC);
-  if constexpr (VEC) {
-    FS_EP(1, 1, 16)
-    FS_EP(1, 2, 16)
-    FS_EP(2, 2, 8)
-    FS_EP(4, 2, 4)
-    FS_EP(4, 4, 4)
-    FS_EP(8, 4, 2)
-  } else {
-    FS_EP(1, 1, 16)
-    FS_EP(1, 4, 16)
-    FS_EP(4, 4, 4)
-    FS_EP(4, 16, 4)
-    FS_EP(16, 16, 1)
+  if (a.vec && a.cols > 0) {
+    if (per_lane <= 4) return staged(epilogue_lds_kernel<CT, BT, ACT, 4, kLdsCH, kLdsW>, 4);
+    if (per_lane <= 8) return staged(epilogue_lds_kernel<CT, BT, ACT, 8, kLdsCH, kLdsW>, 8);
+    if (per_lane <= 16) return staged(epilogue_lds_kernel<CT, BT, ACT, 16, kLdsCH, kLdsW>, 16);
+    if constexpr (V == 4) {   // fp32 C: 64 KiB of coefficients cover 8192 columns
+      if (per_lane <= 32) return staged(epilogue_lds_kernel<CT, BT, ACT, 32, kLdsCH, kLdsW>, 32);
+    }
   }
-#undef FS_EP
   int64_t grid = a.rows < int64_t(cus) * 8 ? a.rows : int64_t(cus) * 8;
+  if (grid < 1) grid = 1;
   hipLaunchKernelGGL((epilogue_wide_kernel<CT, BT, ACT>), dim3(unsigned(grid)), dim3(256), 0, s,
                      static_cast<const CT*>(a.c), a.ld_c, static_cast<const BT*>(a.bias),
                      a.col_scale, a.out, a.rows, a.cols, mean);
   return hipGetLastError();
 }
 
-template <typename CT, typename BT, bool VEC>
+template <typename CT, typename BT>
 hipError_t by_act(const EpilogueArgs& a, int cus, hipStream_t s) {
   switch (a.act) {
-    case FS_ACT_SIGMOID: return dispatch<CT, BT, FS_ACT_SIGMOID, VEC>(a, cus, s);
-    case FS_ACT_GELU_ERF: return dispatch<CT, BT, FS_ACT_GELU_ERF, VEC>(a, cus, s);
-    case FS_ACT_RELU: return dispatch<CT, BT, FS_ACT_RELU, VEC>(a, cus, s);
-    default: return dispatch<CT, BT, FS_ACT_NONE, VEC>(a, cus, s);
+    case FS_ACT_SIGMOID: return dispatch<CT, BT, FS_ACT_SIGMOID>(a, cus, s);
+    case FS_ACT_GELU_ERF: return dispatch<CT, BT, FS_ACT_GELU_ERF>(a, cus, s);
+    case FS_ACT_RELU: return dispatch<CT, BT, FS_ACT_RELU>(a, cus, s);
+    default: return dispatch<CT, BT, FS_ACT_NONE>(a, cus, s);
   }
 }
 
 template <typename CT>
 hipError_t by_bias(const EpilogueArgs& a, int cus, hipStream_t s) {
-  if (a.bias_dtype == FS_BF16)
-    return a.vec ? by_act<CT, uint16_t, true>(a, cus, s) : by_act<CT, uint16_t, false>(a, cus, s);
-  return a.vec ? by_act<CT, float, true>(a, cus, s) : by_act<CT, float, false>(a, cus, s);
+  return a.bias_dtype == FS_BF16 ? by_act<CT, uint16_t>(a, cus, s) : by_act<CT, float>(a, cus, s);
 }
 
 }  // namespace

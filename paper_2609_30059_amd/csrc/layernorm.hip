@@ -17,6 +17,19 @@
 #include "device_common.hpp"
 #include "launch.hpp"
 
+// Build-time tuning: rows of at least FS_LN_SPLIT_COLS columns use at least
+// FS_LN_MIN_WAVES waves per row; the grid holds at most FS_LN_GRID_SCALE/4 times
+// the per-variant blocks-per-CU figure.
+#ifndef FS_LN_MIN_WAVES
+#define FS_LN_MIN_WAVES 1
+#endif
+#ifndef FS_LN_SPLIT_COLS
+#define FS_LN_SPLIT_COLS 2048
+#endif
+#ifndef FS_LN_GRID_SCALE
+#define FS_LN_GRID_SCALE 16
+#endif
+
 namespace fs {
 namespace {
 
@@ -35,7 +48,10 @@ struct MeanM2P {
   }
 };
 
-template <typename T, int W, int EPT, bool VEC, int G>
+// W waves per row, EPT elements per thread, G row groups per block (W == 1
+// only), R rows per group per trip: narrow rows are batched so that a wave
+// keeps R rows of loads in flight and reduces them with one shuffle sequence.
+template <typename T, bool HAS_RES, int W, int EPT, bool VEC, int G, int R>
 __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
     const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
     const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
@@ -43,110 +59,147 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   constexpr int kThreads = 64 * W;
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;
+  // gamma and beta stay in registers for the whole kernel when they fit;
+  // wider rows re-read them (cache-resident) after each trip's statistics
+  constexpr bool kAffineResident = EPT <= 32;
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
-  __shared__ MeanM2P lds[2][W];
+  using P = Multi<MeanM2P, R>;
+  __shared__ P lds[2][W];
 
   const int tid = threadIdx.x % kThreads;
   const int wave = tid / 64, lane = tid % 64;
   const int g = threadIdx.x / kThreads;
   int parity = 0;
 
-  // columns this thread owns and how many are inside the row
+  // the columns this thread owns; out-of-row vectors read the last vector of
+  // the row (an in-bounds address) and are masked
   int n_local = 0;
 #pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    const int c0 = (k * kThreads + tid) * V;
-    n_local += (c0 < cols) ? V : 0;
-  }
+  for (int k = 0; k < NV; ++k) n_local += ((k * kThreads + tid) * V < cols) ? V : 0;
+  const int clast = cols - V;
+  const float nl = float(n_local);
 
-  for (int64_t row = int64_t(blockIdx.x) * G + g; row < rows; row += int64_t(gridDim.x) * G) {
-    const T* xr = x + row * ld_x;
-    const T* rr = res ? res + row * ld_r : nullptr;
-    float h[EPT];
+  Raw<T, V> rg[NV], rb[NV];
+  auto load_affine = [&]() {
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int c0 = (k * kThreads + tid) * V;
-      if (c0 < cols) {
-        ldv<T, V>(xr + c0, h + k * V);
-        if (rr) {
-          float rv[V];
-          ldv<T, V>(rr + c0, rv);
-#pragma unroll
-          for (int i = 0; i < V; ++i) h[k * V + i] += rv[i];
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < V; ++i) h[k * V + i] = 0.f;
-      }
+      const int cl = c0 < cols ? c0 : clast;
+      if (gamma) rg[k].template load<false>(gamma + cl);
+      if (beta) rb[k].template load<false>(beta + cl);
     }
-    if (res_out) {
-      T* ro = res_out + row * ld_ro;
+  };
+
+  if constexpr (kAffineResident) load_affine();
+
+  for (int64_t row0 = (int64_t(blockIdx.x) * G + g) * R; row0 < rows;
+       row0 += int64_t(gridDim.x) * G * R) {
+    Raw<T, V> rx[R][NV], rres[R][HAS_RES ? NV : 1];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      // rows past the end re-read the last row (in bounds) and are not stored
+      const int64_t row = row0 + r < rows ? row0 + r : rows - 1;
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
         const int c0 = (k * kThreads + tid) * V;
-        if (c0 < cols) {
-          if constexpr (VEC) st128<true>(ro + c0, Elem<T>::pack(h + k * V));
-          else Elem<T>::store1(ro + c0, h[k]);
-        }
+        const int cl = c0 < cols ? c0 : clast;
+        rx[r][k].load(x + row * ld_x + cl);
+        if constexpr (HAS_RES) rres[r][k].load(res + row * ld_r + cl);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
 
-    // per-thread exact two-pass statistics over the owned columns
-    float s = 0.f;
+    float h[R][EPT];
+    P part;
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) s += h[i];     // out-of-row slots hold 0
-    const float nl = float(n_local);
-    const float mean_l = n_local ? s / nl : 0.f;
-    float m2 = 0.f;
+    for (int r = 0; r < R; ++r) {
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const int c0 = (k * kThreads + tid) * V;
-      if (c0 < cols) {
+      for (int k = 0; k < NV; ++k) {
+        const bool in = (k * kThreads + tid) * V < cols;
+        float xv[V];
+        rx[r][k].unpack(xv);
+        if constexpr (HAS_RES) {
+          float rv[V];
+          rres[r][k].unpack(rv);
+#pragma unroll
+          for (int i = 0; i < V; ++i) xv[i] += rv[i];
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) h[r][k * V + i] = in ? xv[i] : 0.f;
+      }
+      if (res_out && row0 + r < rows) {
+        T* ro = res_out + (row0 + r) * ld_ro;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const int c0 = (k * kThreads + tid) * V;
+          if (c0 < cols) stv<T, V>(ro + c0, h[r] + k * V);
+        }
+      }
+      // per-thread exact two-pass statistics over the owned columns
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) sum += h[r][i];     // out-of-row slots hold 0
+      const float mean_l = n_local ? sum / nl : 0.f;
+      float m2 = 0.f;
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        const bool in = (k * kThreads + tid) * V < cols;
 #pragma unroll
         for (int i = 0; i < V; ++i) {
-          const float d = h[k * V + i] - mean_l;
+          const float d = in ? h[r][k * V + i] - mean_l : 0.f;
           m2 = fmaf(d, d, m2);
         }
       }
+      part.p[r] = MeanM2P{nl, mean_l, m2};
     }
-    const MeanM2P st = group_allreduce<W>(MeanM2P{nl, mean_l, m2}, lds[parity], wave, lane);
+    const P st = group_allreduce<W>(part, lds[parity], wave, lane);
     parity ^= 1;
-    const float rstd = rsqrtf(st.m2 / st.n + eps);
-    const float mean = st.mean;
+    if constexpr (!kAffineResident) load_affine();
 
-    T* yr = y + row * ld_y;
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const int c0 = (k * kThreads + tid) * V;
-      if (c0 < cols) {
-        float gv[V], bv[V];
-        if (gamma) ldv<T, V, false>(gamma + c0, gv);
-        else {
+    for (int r = 0; r < R; ++r) {
+      const float rstd = rsqrtf(st.p[r].m2 / st.p[r].n + eps);
+      const float mean = st.p[r].mean;
+      if (row0 + r < rows) {
+        T* yr = y + (row0 + r) * ld_y;
 #pragma unroll
-          for (int i = 0; i < V; ++i) gv[i] = 1.f;
+        for (int k = 0; k < NV; ++k) {
+          const int c0 = (k * kThreads + tid) * V;
+          float gv[V], bv[V];
+          if (gamma) rg[k].unpack(gv);
+          else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) gv[i] = 1.f;
+          }
+          if (beta) rb[k].unpack(bv);
+          else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) bv[i] = 0.f;
+          }
+          float o[V];
+#pragma unroll
+          for (int i = 0; i < V; ++i) o[i] = fmaf((h[r][k * V + i] - mean) * rstd, gv[i], bv[i]);
+          if (c0 < cols) stv<T, V>(yr + c0, o);
         }
-        if (beta) ldv<T, V, false>(beta + c0, bv);
-        else {
-#pragma unroll
-          for (int i = 0; i < V; ++i) bv[i] = 0.f;
-        }
-        float o[V];
-#pragma unroll
-        for (int i = 0; i < V; ++i) o[i] = fmaf((h[k * V + i] - mean) * rstd, gv[i], bv[i]);
-        if constexpr (VEC) st128<true>(yr + c0, Elem<T>::pack(o));
-        else Elem<T>::store1(yr + c0, o[0]);
       }
     }
   }
 }
 
-template <typename T, bool VEC>
+// rows batched per group: enough that a one-wave group handles ~32 elements
+// per lane per trip
+template <int W, int EPT>
+struct RowsPerGroup {
+  static constexpr int value = (W == 1 && EPT < 32) ? 32 / EPT : 1;
+};
+
+template <typename T, bool HAS_RES, bool VEC>
 hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   const int64_t c = a.cols;
   auto launch = [&](auto kern, int threads, int rows_per_block, int blocks_per_cu) {
     int64_t want = (a.rows + rows_per_block - 1) / rows_per_block;
-    int64_t cap = int64_t(cus) * blocks_per_cu;
+    int64_t cap = int64_t(cus) * blocks_per_cu * FS_LN_GRID_SCALE / 4;
     int grid = int(want < cap ? want : cap);
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s, static_cast<const T*>(a.x), a.ld_x,
@@ -155,30 +208,45 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
                        static_cast<T*>(a.res_out), a.ld_ro, a.rows, int(a.cols), a.eps);
     return hipGetLastError();
   };
-#define FS_LN(Wv, E, Gv, BPC)                                                   \
-  if (c <= int64_t(64) * Wv * E)                                                 \
-    return launch(layernorm_kernel<T, Wv, E, VEC, Gv>, 64 * Wv * Gv, Gv, BPC);
-  if constexpr (V <= 1) { FS_LN(1, 1, 4, 64) }
-  if constexpr (V <= 2) { FS_LN(1, 2, 4, 64) }
-  if constexpr (V <= 4) { FS_LN(1, 4, 4, 64) }
-  FS_LN(1, 8, 4, 64)
-  FS_LN(1, 16, 4, 64)
-  FS_LN(1, 32, 4, 32)
-  FS_LN(1, 64, 4, 16)
-  FS_LN(2, 64, 1, 32)
-  FS_LN(4, 64, 1, 16)
-  FS_LN(8, 64, 1, 8)
-  FS_LN(16, 64, 1, 4)
+// Variant ladder, in order: the first rung with at least min_w waves per row
+  // and a row capacity 64 * W * EPT >= cols is launched.
+  const int min_w = c >= FS_LN_SPLIT_COLS ? FS_LN_MIN_WAVES : 1;
+#define FS_LN(Wv, E, Gv, BPC)                                                       \
+  if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                   \
+    return launch(layernorm_kernel<T, HAS_RES, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
+                  64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
+  if constexpr (V <= 1) { FS_LN(1, 1, 4, 8) }
+  if constexpr (V <= 2) { FS_LN(1, 2, 4, 8) }
+  if constexpr (V <= 4) { FS_LN(1, 4, 4, 8) }
+  FS_LN(1, 8, 4, 8)
+  FS_LN(1, 16, 4, 8)
+  FS_LN(1, 32, 4, 8)
+  FS_LN(1, 64, 4, 8)
+  FS_LN(2, 32, 1, 16)
+  FS_LN(2, 64, 1, 16)
+  FS_LN(4, 16, 1, 8)
+  FS_LN(4, 32, 1, 8)
+  FS_LN(4, 64, 1, 8)
+  FS_LN(8, 8, 1, 4)
+  FS_LN(8, 16, 1, 4)
+  FS_LN(8, 32, 1, 4)
+  FS_LN(8, 64, 1, 4)
+  FS_LN(16, 64, 1, 2)
 #undef FS_LN
   return hipErrorInvalidValue;   // unreachable: the host checks cols
+}
+
+template <typename T>
+hipError_t by_res(const LayerNormArgs& a, int cus, hipStream_t s) {
+  if (a.res == nullptr)
+    return a.vec ? dispatch<T, false, true>(a, cus, s) : dispatch<T, false, false>(a, cus, s);
+  return a.vec ? dispatch<T, true, true>(a, cus, s) : dispatch<T, true, false>(a, cus, s);
 }
 
 }  // namespace
 
 hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s) {
-  if (a.dtype == FS_BF16)
-    return a.vec ? dispatch<uint16_t, true>(a, cus, s) : dispatch<uint16_t, false>(a, cus, s);
-  return a.vec ? dispatch<float, true>(a, cus, s) : dispatch<float, false>(a, cus, s);
+  return a.dtype == FS_BF16 ? by_res<uint16_t>(a, cus, s) : by_res<float>(a, cus, s);
 }
 
 }  // namespace fs

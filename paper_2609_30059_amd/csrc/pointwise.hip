@@ -14,6 +14,13 @@
 #include "device_common.hpp"
 #include "launch.hpp"
 
+#ifndef FS_PW_ROWS_PER_TRIP
+#define FS_PW_ROWS_PER_TRIP 4
+#endif
+#ifndef FS_PW_BLOCKS_PER_CU
+#define FS_PW_BLOCKS_PER_CU 16
+#endif
+
 namespace fs {
 namespace {
 
@@ -22,9 +29,9 @@ constexpr int kBlock = 256;
 template <int ACT>
 __device__ __forceinline__ float act_fn(float z) {
   if constexpr (ACT == FS_ACT_GELU_ERF) {
-    return 0.5f * z * (1.f + erff(z * 0.70710678118654752f));
+    return gelu_erf(z);
   } else if constexpr (ACT == FS_ACT_SIGMOID) {
-    return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-z * kLog2e));
+    return sigmoid(z);
   } else if constexpr (ACT == FS_ACT_RELU) {
     return z > 0.f ? z : 0.f;
   } else {
@@ -32,7 +39,7 @@ __device__ __forceinline__ float act_fn(float z) {
   }
 }
 
-template <typename T, int ACT, bool VEC, int U>
+template <typename T, int ACT, bool HAS_RES, bool VEC, int U>
 __global__ __launch_bounds__(kBlock) void pointwise_kernel(
     const T* x, int64_t ld_x, const T* __restrict__ bias, const T* res, int64_t ld_r, T* y,
     int64_t ld_y, int64_t rows, int cols, float scale, int col_blocks) {
@@ -44,56 +51,59 @@ __global__ __launch_bounds__(kBlock) void pointwise_kernel(
   if (c0 >= cols) return;               // no barriers below: early exit is safe
 
   float b[V];
-  if (bias) ldv<T, V, false>(bias + c0, b);
-  else {
+  if (bias) {
+    Raw<T, V> rb;
+    rb.template load<false>(bias + c0);
+    rb.unpack(b);
+  } else {
 #pragma unroll
     for (int i = 0; i < V; ++i) b[i] = 0.f;
   }
 
   for (int64_t r0 = rg * U; r0 < rows; r0 += nrg * U) {
-    float xv[U][V], rv[U][V];
+    // all 2U loads of the trip are issued before any use; rows past the end
+    // re-read the last row (in bounds) and are not stored
+    Raw<T, V> rx[U], rr[HAS_RES ? U : 1];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t r = r0 + u;
-      if (r < rows) {
-        ldv<T, V>(x + r * ld_x + c0, xv[u]);
-        if (res) ldv<T, V>(res + r * ld_r + c0, rv[u]);
-      }
+      const int64_t r = r0 + u < rows ? r0 + u : rows - 1;
+      rx[u].load(x + r * ld_x + c0);
+      if constexpr (HAS_RES) rr[u].load(res + r * ld_r + c0);
     }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t r = r0 + u;
-      if (r < rows) {
-        float o[V];
+      float xv[V], o[V];
+      rx[u].unpack(xv);
 #pragma unroll
-        for (int i = 0; i < V; ++i) {
-          o[i] = act_fn<ACT>(fmaf(xv[u][i], scale, b[i]));
-          if (res) o[i] += rv[u][i];
-        }
-        T* yp = y + r * ld_y + c0;
-        if constexpr (VEC) st128<true>(yp, Elem<T>::pack(o));
-        else Elem<T>::store1(yp, o[0]);
+      for (int i = 0; i < V; ++i) o[i] = act_fn<ACT>(fmaf(xv[i], scale, b[i]));
+      if constexpr (HAS_RES) {
+        float rv[V];
+        rr[u].unpack(rv);
+#pragma unroll
+        for (int i = 0; i < V; ++i) o[i] += rv[i];
       }
+      if (r0 + u < rows) stv<T, V>(y + (r0 + u) * ld_y + c0, o);
     }
   }
 }
 
-template <typename T, int ACT, bool VEC>
+template <typename T, int ACT, bool HAS_RES, bool VEC>
 hipError_t dispatch(const PointwiseArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   const int64_t vecs = (a.cols + V - 1) / V;
   const int col_blocks = int((vecs + kBlock - 1) / kBlock);
   // U rows per trip; fewer when the problem is too small to fill the chip
-  constexpr int U = 4;
+  constexpr int U = FS_PW_ROWS_PER_TRIP;
   const int64_t row_groups_needed = (a.rows + U - 1) / U;
-  const int64_t target_blocks = int64_t(cus) * 8;
+  const int64_t target_blocks = int64_t(cus) * FS_PW_BLOCKS_PER_CU;
   int64_t rg = target_blocks / col_blocks;
   if (rg < 1) rg = 1;
   if (row_groups_needed < int64_t(cus) * 2) {
     // small problem: one row per trip, as many blocks as rows
     int64_t r1 = a.rows < target_blocks ? a.rows : target_blocks;
     int64_t grid = r1 * col_blocks;
-    hipLaunchKernelGGL((pointwise_kernel<T, ACT, VEC, 1>), dim3(unsigned(grid)), dim3(kBlock), 0,
+    hipLaunchKernelGGL((pointwise_kernel<T, ACT, HAS_RES, VEC, 1>), dim3(unsigned(grid)), dim3(kBlock), 0,
                        s, static_cast<const T*>(a.x), a.ld_x, static_cast<const T*>(a.bias),
                        static_cast<const T*>(a.res), a.ld_r, static_cast<T*>(a.y), a.ld_y, a.rows,
                        int(a.cols), a.scale, col_blocks);
@@ -101,29 +111,34 @@ hipError_t dispatch(const PointwiseArgs& a, int cus, hipStream_t s) {
   }
   if (rg > row_groups_needed) rg = row_groups_needed;
   const int64_t grid = rg * col_blocks;
-  hipLaunchKernelGGL((pointwise_kernel<T, ACT, VEC, U>), dim3(unsigned(grid)), dim3(kBlock), 0, s,
+  hipLaunchKernelGGL((pointwise_kernel<T, ACT, HAS_RES, VEC, U>), dim3(unsigned(grid)), dim3(kBlock), 0, s,
                      static_cast<const T*>(a.x), a.ld_x, static_cast<const T*>(a.bias),
                      static_cast<const T*>(a.res), a.ld_r, static_cast<T*>(a.y), a.ld_y, a.rows,
                      int(a.cols), a.scale, col_blocks);
   return hipGetLastError();
 }
 
-template <typename T, bool VEC>
+template <typename T, bool HAS_RES, bool VEC>
 hipError_t by_act(const PointwiseArgs& a, int cus, hipStream_t s) {
   switch (a.act) {
-    case FS_ACT_GELU_ERF: return dispatch<T, FS_ACT_GELU_ERF, VEC>(a, cus, s);
-    case FS_ACT_SIGMOID: return dispatch<T, FS_ACT_SIGMOID, VEC>(a, cus, s);
-    case FS_ACT_RELU: return dispatch<T, FS_ACT_RELU, VEC>(a, cus, s);
-    default: return dispatch<T, FS_ACT_NONE, VEC>(a, cus, s);
+    case FS_ACT_GELU_ERF: return dispatch<T, FS_ACT_GELU_ERF, HAS_RES, VEC>(a, cus, s);
+    case FS_ACT_SIGMOID: return dispatch<T, FS_ACT_SIGMOID, HAS_RES, VEC>(a, cus, s);
+    case FS_ACT_RELU: return dispatch<T, FS_ACT_RELU, HAS_RES, VEC>(a, cus, s);
+    default: return dispatch<T, FS_ACT_NONE, HAS_RES, VEC>(a, cus, s);
   }
+}
+
+template <typename T>
+hipError_t by_res(const PointwiseArgs& a, int cus, hipStream_t s) {
+  if (a.res == nullptr)
+    return a.vec ? by_act<T, false, true>(a, cus, s) : by_act<T, false, false>(a, cus, s);
+  return a.vec ? by_act<T, true, true>(a, cus, s) : by_act<T, true, false>(a, cus, s);
 }
 
 }  // namespace
 
 hipError_t launch_pointwise(const PointwiseArgs& a, int cus, hipStream_t s) {
-  if (a.dtype == FS_BF16)
-    return a.vec ? by_act<uint16_t, true>(a, cus, s) : by_act<uint16_t, false>(a, cus, s);
-  return a.vec ? by_act<float, true>(a, cus, s) : by_act<float, false>(a, cus, s);
+  return a.dtype == FS_BF16 ? by_res<uint16_t>(a, cus, s) : by_res<float>(a, cus, s);
 }
 
 }  // namespace fs

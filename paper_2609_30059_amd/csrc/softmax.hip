@@ -5,15 +5,29 @@
 //
 // Design (gfx950): one row per group of W wave64s; each thread holds EPT
 // elements of the row in registers, so HBM is read once and written once.
-// Per thread the logits are turned into base-2 exponents
-// a = (x * scale + mask) * log2(e), the local max m and the local sum d of
-// exp2(a - m) are formed with the exponentials kept in registers, and a
-// single all-reduce combines the (m, d) pairs:
+// Per thread: logits a = x * scale + mask, the local max m, and the local
+// sum d of 2^(a*log2e - m*log2e) with the exponentials kept in registers.
+// The exponent is one fma, a*log2e - m', with m' = m*log2e rounded once, so
+// large logits keep full relative accuracy in their differences.  A single
+// all-reduce combines the (m', d) pairs:
 //     (m1, d1) + (m2, d2) = (M, d1 * 2^(m1 - M) + d2 * 2^(m2 - M)),  M = max
 // with m = -inf acting as the identity (never evaluating -inf - -inf).  The
-// output is the stored exponential times 2^(m - M) / D: one exp2 per element.
+// output is the stored exponential times 2^(m' - M) / D: one exp2 per element.
 #include "device_common.hpp"
 #include "launch.hpp"
+
+// Build-time tuning: rows of at least FS_SM_SPLIT_COLS columns use at least
+// FS_SM_MIN_WAVES waves per row; the grid holds at most FS_SM_GRID_SCALE/4 times
+// the per-variant blocks-per-CU figure.
+#ifndef FS_SM_MIN_WAVES
+#define FS_SM_MIN_WAVES 1
+#endif
+#ifndef FS_SM_SPLIT_COLS
+#define FS_SM_SPLIT_COLS 2048
+#endif
+#ifndef FS_SM_GRID_SCALE
+#define FS_SM_GRID_SCALE 64
+#endif
 
 namespace fs {
 namespace {
@@ -31,10 +45,12 @@ struct MaxSumP {
   }
 };
 
-// T: storage type of x and y; MT: storage type of the mask.
-// W waves per row; EPT elements per thread; VEC: 16-byte vector path.
-// G rows per block (W == 1 only).
-template <typename T, typename MT, int W, int EPT, bool VEC, int G>
+// T: storage type of x and y; MT: storage type of the mask (used when
+// HAS_MASK).  W waves per row; EPT elements per thread; VEC: 16-byte vector
+// path; G row groups per block (W == 1 only); R rows per group per trip --
+// narrow rows are batched so that a wave keeps R rows of loads in flight and
+// reduces them with one shuffle sequence.
+template <typename T, typename MT, bool HAS_MASK, int W, int EPT, bool VEC, int G, int R>
 __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m,
     T* y, int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len) {
@@ -42,108 +58,123 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;                       // vectors per thread
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
-  __shared__ MaxSumP lds[2][W];
+  using P = Multi<MaxSumP, R>;
+  __shared__ P lds[2][W];
 
   const int tid = threadIdx.x % kThreads;
   const int wave = tid / 64, lane = tid % 64;
   const int g = threadIdx.x / kThreads;
-  const bool has_mask = mask != nullptr;
-  const float scale_log2e = scale * kLog2e;
   int parity = 0;
 
-  for (int64_t row = int64_t(blockIdx.x) * G + g; row < rows; row += int64_t(gridDim.x) * G) {
-    const T* xr = x + row * ld_x;
-    const MT* mr = has_mask ? mask + row * ld_m : nullptr;
-    // last unmasked column (inclusive) under the causal rule
-    const int64_t limit = q_len > 0 ? (row % q_len) + (cols - q_len) : int64_t(cols) - 1;
-    const int lim = int(limit < int64_t(cols) - 1 ? limit : int64_t(cols) - 1);
+  for (int64_t row0 = (int64_t(blockIdx.x) * G + g) * R; row0 < rows;
+       row0 += int64_t(gridDim.x) * G * R) {
+    Raw<T, V> rx[R][NV];
+    Raw<MT, V> rm[R][HAS_MASK ? NV : 1];
+    int lim[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      // rows past the end re-read the last row (in bounds) and are not stored
+      const int64_t row = row0 + r < rows ? row0 + r : rows - 1;
+      const T* xr = x + row * ld_x;
+      const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
+      // last live column (inclusive) under the causal rule; -1 if none
+      const int64_t limit = q_len > 0 ? (row % q_len) + (cols - q_len) : int64_t(cols) - 1;
+      lim[r] = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+      // vectors past lim are not read: their address is clamped onto the
+      // vector holding column lim (fetched by a live lane), then masked
+      const int limv = lim[r] < 0 ? 0 : (lim[r] / V) * V;
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        const int c0 = (k * kThreads + tid) * V;
+        const int cl = c0 <= lim[r] ? c0 : limv;
+        rx[r][k].load(xr + cl);
+        if constexpr (HAS_MASK) rm[r][k].load(mr + cl);
+      }
+    }
+    // keep every load of the trip ahead of the first use (one HBM round trip)
+    __builtin_amdgcn_sched_barrier(0);
 
-    // a = (x * scale + mask) * log2(e): base-2 exponents
-    float a[EPT];
-    if constexpr (VEC) {
+    // logits a = x * scale + mask (-inf past lim); local (m', d) in base-2
+    // units with the exponentials kept in a[]
+    float a[R][EPT];
+    P part;
+    bool empty[R];
+    float ml2[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
         const int c0 = (k * kThreads + tid) * V;
         float xv[V];
-        if (c0 <= lim) {
-          ldv<T, V>(xr + c0, xv);
-          if (has_mask) {
-            float mv[V];
-            ldv<MT, V>(mr + c0, mv);
+        rx[r][k].unpack(xv);
+        if constexpr (HAS_MASK) {
+          float mv[V];
+          rm[r][k].unpack(mv);
 #pragma unroll
-            for (int i = 0; i < V; ++i) xv[i] = fmaf(xv[i], scale, mv[i]) * kLog2e;
-          } else {
-#pragma unroll
-            for (int i = 0; i < V; ++i) xv[i] *= scale_log2e;
-          }
-#pragma unroll
-          for (int i = 0; i < V; ++i) a[k * V + i] = (c0 + i <= lim) ? xv[i] : -INFINITY;
+          for (int i = 0; i < V; ++i) xv[i] = fmaf(xv[i], scale, mv[i]);
         } else {
 #pragma unroll
-          for (int i = 0; i < V; ++i) a[k * V + i] = -INFINITY;
+          for (int i = 0; i < V; ++i) xv[i] *= scale;
         }
-      }
-    } else {
 #pragma unroll
-      for (int k = 0; k < EPT; ++k) {
-        const int c = k * kThreads + tid;
-        float v = -INFINITY;
-        if (c <= lim) {
-          const float xv = Elem<T>::load1(xr + c);
-          v = has_mask ? fmaf(xv, scale, Elem<MT>::load1(mr + c)) * kLog2e : xv * scale_log2e;
-        }
-        a[k] = v;
+        for (int i = 0; i < V; ++i) a[r][k * V + i] = (c0 + i <= lim[r]) ? xv[i] : -INFINITY;
       }
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
+      empty[r] = (m == -INFINITY);
+      ml2[r] = empty[r] ? 0.f : m * kLog2e;   // m' (0 for an all-masked slice)
+      float d = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) {
+        a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2[r]));   // exp2(-inf) = 0
+        d += a[r][i];
+      }
+      part.p[r] = MaxSumP{empty[r] ? -INFINITY : ml2[r], d};
     }
 
-    // local (m, d), exponentials kept in a[]
-    float m = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[i]);
-    const float m_safe = (m == -INFINITY) ? 0.f : m;
-    float d = 0.f;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      a[i] = __builtin_amdgcn_exp2f(a[i] - m_safe);   // exp2(-inf) = 0
-      d += a[i];
-    }
-
-    MaxSumP p = group_allreduce<W>(MaxSumP{m, d}, lds[parity], wave, lane);
+    const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
     parity ^= 1;
-    // fully masked row: p.m = -inf, every a[i] = 0 -> output 0
-    const float f = (p.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_safe - p.m) / p.d;
 
-    T* yr = y + row * ld_y;
-    if constexpr (VEC) {
 #pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
-        if (c0 < cols) {
-          float o[V];
+    for (int r = 0; r < R; ++r) {
+      // a slice with no live element contributes zeros (and must not form
+      // 0*inf); a fully masked row has M = -inf and comes out all zeros
+      const MaxSumP p = tot.p[r];
+      const float f =
+          (empty[r] || p.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml2[r] - p.m) / p.d;
+      if (row0 + r < rows) {
+        T* yr = y + (row0 + r) * ld_y;
 #pragma unroll
-          for (int i = 0; i < V; ++i) o[i] = a[k * V + i] * f;
-          st128<true>(yr + c0, Elem<T>::pack(o));
+        for (int k = 0; k < NV; ++k) {
+          const int c0 = (k * kThreads + tid) * V;
+          if (c0 < cols) {
+            float o[V];
+#pragma unroll
+            for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f;
+            stv<T, V>(yr + c0, o);
+          }
         }
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < EPT; ++k) {
-        const int c = k * kThreads + tid;
-        if (c < cols) Elem<T>::store1(yr + c, a[k] * f);
       }
     }
   }
 }
 
+// rows batched per group: enough that a one-wave group handles ~32 elements
+// per lane per trip
+template <int W, int EPT>
+struct RowsPerGroup {
+  static constexpr int value = (W == 1 && EPT < 32) ? 32 / EPT : 1;
+};
 
-template <typename T, typename MT, bool VEC>
+template <typename T, typename MT, bool HAS_MASK, bool VEC>
 hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   // smallest capacity >= cols; the vector path needs EPT >= V
   const int64_t c = a.cols;
   auto launch = [&](auto kern, int threads, int rows_per_block, int blocks_per_cu) {
     int64_t want = (a.rows + rows_per_block - 1) / rows_per_block;
-    int64_t cap = int64_t(cus) * blocks_per_cu;
+    int64_t cap = int64_t(cus) * blocks_per_cu * FS_SM_GRID_SCALE / 4;
     int grid = int(want < cap ? want : cap);
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s,
@@ -152,38 +183,48 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
                        a.scale, a.causal_q_len);
     return hipGetLastError();
   };
-#define FS_SM(Wv, E, Gv, BPC)                                                      \
-  if (c <= int64_t(64) * Wv * E)                                                    \
-    return launch(softmax_kernel<T, MT, Wv, E, VEC, Gv>, 64 * Wv * Gv, Gv, BPC);
-  if constexpr (V <= 1) { FS_SM(1, 1, 4, 64) }
-  if constexpr (V <= 2) { FS_SM(1, 2, 4, 64) }
-  if constexpr (V <= 4) { FS_SM(1, 4, 4, 64) }
-  FS_SM(1, 8, 4, 64)
-  FS_SM(1, 16, 4, 64)
-  FS_SM(1, 32, 4, 32)
-  FS_SM(1, 64, 4, 16)
-  FS_SM(2, 64, 1, 32)
-  FS_SM(4, 64, 1, 16)
-  FS_SM(8, 64, 1, 8)
-  FS_SM(16, 64, 1, 4)
+// Variant ladder, in order: the first rung with at least min_w waves per row
+  // and a row capacity 64 * W * EPT >= cols is launched.
+  const int min_w = c >= FS_SM_SPLIT_COLS ? FS_SM_MIN_WAVES : 1;
+#define FS_SM(Wv, E, Gv, BPC)                                                       \
+  if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                   \
+    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
+                  64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
+  if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }
+  if constexpr (V <= 2) { FS_SM(1, 2, 4, 8) }
+  if constexpr (V <= 4) { FS_SM(1, 4, 4, 8) }
+  FS_SM(1, 8, 4, 8)
+  FS_SM(1, 16, 4, 8)
+  FS_SM(1, 32, 4, 8)
+  FS_SM(1, 64, 4, 8)
+  FS_SM(2, 32, 1, 16)
+  FS_SM(2, 64, 1, 16)
+  FS_SM(4, 16, 1, 8)
+  FS_SM(4, 32, 1, 8)
+  FS_SM(4, 64, 1, 8)
+  FS_SM(8, 8, 1, 4)
+  FS_SM(8, 16, 1, 4)
+  FS_SM(8, 32, 1, 4)
+  FS_SM(8, 64, 1, 4)
+  FS_SM(16, 64, 1, 2)
 #undef FS_SM
   return hipErrorInvalidValue;   // unreachable: the host checks cols
+}
+
+template <typename T, typename MT>
+hipError_t by_vec(const SoftmaxArgs& a, int cus, hipStream_t s) {
+  if (a.mask == nullptr)
+    return a.vec ? dispatch<T, T, false, true>(a, cus, s) : dispatch<T, T, false, false>(a, cus, s);
+  return a.vec ? dispatch<T, MT, true, true>(a, cus, s) : dispatch<T, MT, true, false>(a, cus, s);
 }
 
 }  // namespace
 
 hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s) {
-  const bool bf16 = a.dtype == FS_BF16;
   const bool mbf16 = a.mask_dtype == FS_BF16;
-  if (bf16) {
-    if (mbf16) return a.vec ? dispatch<uint16_t, uint16_t, true>(a, cus, s)
-                            : dispatch<uint16_t, uint16_t, false>(a, cus, s);
-    return a.vec ? dispatch<uint16_t, float, true>(a, cus, s)
-                 : dispatch<uint16_t, float, false>(a, cus, s);
-  }
-  if (mbf16) return a.vec ? dispatch<float, uint16_t, true>(a, cus, s)
-                          : dispatch<float, uint16_t, false>(a, cus, s);
-  return a.vec ? dispatch<float, float, true>(a, cus, s) : dispatch<float, float, false>(a, cus, s);
+  if (a.dtype == FS_BF16)
+    return mbf16 ? by_vec<uint16_t, uint16_t>(a, cus, s) : by_vec<uint16_t, float>(a, cus, s);
+  return mbf16 ? by_vec<float, uint16_t>(a, cus, s) : by_vec<float, float>(a, cus, s);
 }
 
 }  // namespace fs

@@ -100,16 +100,31 @@ def test_causal_offsets_and_widths(q_len, cols):
 
 
 def test_fully_masked_rows_and_large_logits():
-    x = torch.tensor([[1.0, 2.0, 3.0, 4.0], [3e4, 3e4 + np.log(3.0), -3e4, 0.0],
-                      [5.0, 5.0, 5.0, 5.0]], device="cuda")
-    mask = torch.tensor([[-np.inf] * 4, [0, 0, -np.inf, -np.inf], [0, -np.inf, 0, -np.inf]],
-                        device="cuda", dtype=torch.float32)
+    # fp32 logits near 3e4 whose difference is ln 3: the exponent difference
+    # must keep full relative accuracy
+    x = torch.tensor([[1.0, 2.0, 3.0, 4.0], [3e4, 3e4 + float(np.log(3.0)), -3e4, 0.0],
+                      [5.0, 5.0, 5.0, 5.0], [-3e4, -3e4, -3e4, -3e4 + 1.0]],
+                     dtype=torch.float32, device="cuda")
+    mask = torch.tensor([[-np.inf] * 4, [0, 0, -np.inf, -np.inf], [0, -np.inf, 0, -np.inf],
+                         [-np.inf, -np.inf, 0, 0]], device="cuda", dtype=torch.float32)
     announce("softmax masked rows")
     y = host64(fs.row_softmax(x, mask, 1.0))
     np.testing.assert_array_equal(y[0], 0.0)
     assert not np.any(np.signbit(y[0]))
-    np.testing.assert_allclose(y[1], [0.25, 0.75, 0, 0], rtol=1e-6)
+    x64 = host64(x)
+    ref = oracle.row_softmax(x64, host64(mask), 1.0)
+    assert_close("large and masked logits", y, ref, *TOL["f32"])
     np.testing.assert_allclose(y[2], [0.5, 0, 0.5, 0], rtol=1e-6)
+    # very negative logits with an all-masked slice: no NaN, exact zeros where masked
+    xs = torch.full((2, 4096), -3e4, dtype=torch.float32, device="cuda")
+    xs[:, -1] = -2.9e4
+    ms = torch.zeros_like(xs)
+    ms[:, :2048] = float("-inf")
+    ys = host64(fs.row_softmax(xs, ms, 1.0))
+    assert not np.isnan(ys).any()
+    assert np.all(ys[:, :2048] == 0.0)
+    assert_close("negative logits", ys, oracle.row_softmax(host64(xs), host64(ms), 1.0),
+                 *TOL["f32"])
 
 
 def test_general_additive_mask():
