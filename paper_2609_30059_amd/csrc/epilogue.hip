@@ -133,12 +133,15 @@ __global__ __launch_bounds__(64 * W) void epilogue_lds_kernel(
     // loop-invariant LDS reads into registers (which would spill)
     int li = lane;
     asm volatile("" : "+v"(li));
-    const int64_t pre = next < rows ? next : row;   // prefetch target of the last chunk
+    // the last chunk prefetches chunk 0 of the wave's next row; on its last
+    // row it re-reads the chunk just fetched (cache-resident) instead, which
+    // keeps the code free of branches
+    const int64_t pre_row = next < rows ? next : row;
+    const int pre_chunk = next < rows ? 0 : NCH - 1;
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
-      // prefetch: next chunk of this row, or chunk 0 of the next row
       if (j + 1 < NCH) load_chunk(buf[(j + 1) & 1], row, j + 1);
-      else load_chunk(buf[(j + 1) & 1], pre, 0);
+      else load_chunk(buf[(j + 1) & 1], pre_row, pre_chunk);
 #pragma unroll
       for (int q = 0; q < CH; ++q) {
         const int vi = (j * CH + q) * 64 + lane;
