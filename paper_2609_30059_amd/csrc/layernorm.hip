@@ -7,24 +7,26 @@
 //
 // Design (gfx950): one row per group of W wave64s, EPT elements per thread
 // held in registers: x and residual are read from HBM once, residual_out and
-// y written once.  The statistics are exact two-pass values per thread (mean
-// of the thread's elements, then the sum of squared deviations from it) and
-// one all-reduce merges the (count, mean, M2) triples with the pairwise
-// update of Chan, Golub and LeVeque (1979):
-//     n = na + nb, mean = (na*ma + nb*mb) / n, M2 = M2a + M2b + (mb-ma)^2 na nb / n
-// written so that combine(a, b) and combine(b, a) round identically, so every
-// lane ends with the same statistics.  No E[h^2] - mean^2 cancellation.
+// y written once.  The statistics are exact two-pass values over the
+// register-resident row -- an all-reduce of sum(h) gives the mean, then an
+// all-reduce of sum((h - mean)^2) the biased variance -- so there is no
+// E[h^2] - mean^2 cancellation and no second HBM pass.  Both all-reduces are
+// plain sums, which fold into DPP adds.
 #include "device_common.hpp"
 #include "launch.hpp"
 
 // Build-time tuning: rows of at least FS_LN_SPLIT_COLS columns use at least
-// FS_LN_MIN_WAVES waves per row; the grid holds at most FS_LN_GRID_SCALE/4 times
-// the per-variant blocks-per-CU figure.
+// FS_LN_MIN_WAVES waves per row; one-wave rows are batched to about
+// FS_LN_BATCH_ELEMS elements per lane per trip; the grid holds at most
+// FS_LN_GRID_SCALE/4 times the per-variant blocks-per-CU figure.
 #ifndef FS_LN_MIN_WAVES
-#define FS_LN_MIN_WAVES 1
+#define FS_LN_MIN_WAVES 2
 #endif
 #ifndef FS_LN_SPLIT_COLS
 #define FS_LN_SPLIT_COLS 2048
+#endif
+#ifndef FS_LN_BATCH_ELEMS
+#define FS_LN_BATCH_ELEMS 16
 #endif
 #ifndef FS_LN_GRID_SCALE
 #define FS_LN_GRID_SCALE 16
@@ -32,21 +34,6 @@
 
 namespace fs {
 namespace {
-
-struct MeanM2P {
-  float n, mean, m2;
-  __device__ __forceinline__ static MeanM2P combine(const MeanM2P& a, const MeanM2P& b) {
-    if (a.n == 0.f) return b;
-    if (b.n == 0.f) return a;
-    const float n = a.n + b.n;
-    const float mean = (a.n * a.mean + b.n * b.mean) / n;
-    const float d = b.mean - a.mean;
-    return {n, mean, (a.m2 + b.m2) + d * d * ((a.n * b.n) / n)};
-  }
-  template <class F> __device__ __forceinline__ static MeanM2P map(const MeanM2P& a, F f) {
-    return {f(a.n), f(a.mean), f(a.m2)};
-  }
-};
 
 // W waves per row, EPT elements per thread, G row groups per block (W == 1
 // only), R rows per group per trip: narrow rows are batched so that a wave
@@ -63,7 +50,7 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   // wider rows re-read them (cache-resident) after each trip's statistics
   constexpr bool kAffineResident = EPT <= 32;
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
-  using P = Multi<MeanM2P, R>;
+  using P = Multi<SumP, R>;
   __shared__ P lds[2][W];
 
   const int tid = threadIdx.x % kThreads;
@@ -71,13 +58,10 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   const int g = threadIdx.x / kThreads;
   int parity = 0;
 
-  // the columns this thread owns; out-of-row vectors read the last vector of
-  // the row (an in-bounds address) and are masked
-  int n_local = 0;
-#pragma unroll
-  for (int k = 0; k < NV; ++k) n_local += ((k * kThreads + tid) * V < cols) ? V : 0;
+  // out-of-row vectors read the last vector of the row (an in-bounds address)
+  // and are masked
   const int clast = cols - V;
-  const float nl = float(n_local);
+  const float inv_cols = 1.f / float(cols);
 
   Raw<T, V> rg[NV], rb[NV];
   auto load_affine = [&]() {
@@ -135,31 +119,38 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
           if (c0 < cols) stv<T, V>(ro + c0, h[r] + k * V);
         }
       }
-      // per-thread exact two-pass statistics over the owned columns
       float sum = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) sum += h[r][i];     // out-of-row slots hold 0
-      const float mean_l = n_local ? sum / nl : 0.f;
+      part.p[r] = SumP{sum};
+    }
+    // pass 1: the row means
+    const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
+    parity ^= 1;
+    float mean[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      mean[r] = tot.p[r].s * inv_cols;
+      // pass 2: squared deviations from the row mean, over the owned columns
       float m2 = 0.f;
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
         const bool in = (k * kThreads + tid) * V < cols;
 #pragma unroll
         for (int i = 0; i < V; ++i) {
-          const float d = in ? h[r][k * V + i] - mean_l : 0.f;
+          const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
           m2 = fmaf(d, d, m2);
         }
       }
-      part.p[r] = MeanM2P{nl, mean_l, m2};
+      part.p[r] = SumP{m2};
     }
-    const P st = group_allreduce<W>(part, lds[parity], wave, lane);
+    const P sq = group_allreduce<W>(part, lds[parity], wave, lane);
     parity ^= 1;
     if constexpr (!kAffineResident) load_affine();
 
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      const float rstd = rsqrtf(st.p[r].m2 / st.p[r].n + eps);
-      const float mean = st.p[r].mean;
+      const float rstd = rsqrtf(sq.p[r].s * inv_cols + eps);
       if (row0 + r < rows) {
         T* yr = y + (row0 + r) * ld_y;
 #pragma unroll
@@ -178,7 +169,7 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
           }
           float o[V];
 #pragma unroll
-          for (int i = 0; i < V; ++i) o[i] = fmaf((h[r][k * V + i] - mean) * rstd, gv[i], bv[i]);
+          for (int i = 0; i < V; ++i) o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, gv[i], bv[i]);
           if (c0 < cols) stv<T, V>(yr + c0, o);
         }
       }
@@ -186,11 +177,11 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   }
 }
 
-// rows batched per group: enough that a one-wave group handles ~32 elements
-// per lane per trip
+// rows batched per group: enough that a one-wave group handles about
+// FS_LN_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
 struct RowsPerGroup {
-  static constexpr int value = (W == 1 && EPT < 32) ? 32 / EPT : 1;
+  static constexpr int value = (W == 1 && EPT < FS_LN_BATCH_ELEMS) ? FS_LN_BATCH_ELEMS / EPT : 1;
 };
 
 template <typename T, bool HAS_RES, bool VEC>

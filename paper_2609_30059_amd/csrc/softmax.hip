@@ -17,13 +17,17 @@
 #include "launch.hpp"
 
 // Build-time tuning: rows of at least FS_SM_SPLIT_COLS columns use at least
-// FS_SM_MIN_WAVES waves per row; the grid holds at most FS_SM_GRID_SCALE/4 times
-// the per-variant blocks-per-CU figure.
+// FS_SM_MIN_WAVES waves per row; one-wave rows are batched to about
+// FS_SM_BATCH_ELEMS elements per lane per trip; the grid holds at most
+// FS_SM_GRID_SCALE/4 times the per-variant blocks-per-CU figure.
 #ifndef FS_SM_MIN_WAVES
-#define FS_SM_MIN_WAVES 1
+#define FS_SM_MIN_WAVES 2
 #endif
 #ifndef FS_SM_SPLIT_COLS
 #define FS_SM_SPLIT_COLS 2048
+#endif
+#ifndef FS_SM_BATCH_ELEMS
+#define FS_SM_BATCH_ELEMS 16
 #endif
 #ifndef FS_SM_GRID_SCALE
 #define FS_SM_GRID_SCALE 64
@@ -34,11 +38,17 @@ namespace {
 
 struct MaxSumP {
   float m, d;
+  // (m1, d1) + (m2, d2) = (M, d_big + d_small * 2^-|m1 - m2|): the pair with
+  // the larger max keeps weight 1, so one exp2 per combine.  Symmetric in its
+  // arguments (swapping them selects the same big/small pair), so every lane
+  // ends with identical bits.  m = -inf is the identity (d = 0).
   __device__ __forceinline__ static MaxSumP combine(const MaxSumP& a, const MaxSumP& b) {
     const float M = fmaxf(a.m, b.m);
     if (M == -INFINITY) return {-INFINITY, 0.f};
-    // symmetric in (a, b): both products are formed the same way
-    return {M, a.d * __builtin_amdgcn_exp2f(a.m - M) + b.d * __builtin_amdgcn_exp2f(b.m - M)};
+    const bool a_big = a.m > b.m;
+    const float big = a_big ? a.d : b.d, small = a_big ? b.d : a.d;
+    const float e = __builtin_amdgcn_exp2f(-fabsf(a.m - b.m));   // 2^-inf = 0
+    return {M, fmaf(small, e, big)};
   }
   template <class F> __device__ __forceinline__ static MaxSumP map(const MaxSumP& a, F f) {
     return {f(a.m), f(a.d)};
@@ -160,11 +170,11 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   }
 }
 
-// rows batched per group: enough that a one-wave group handles ~32 elements
-// per lane per trip
+// rows batched per group: enough that a one-wave group handles about
+// FS_SM_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
 struct RowsPerGroup {
-  static constexpr int value = (W == 1 && EPT < 32) ? 32 / EPT : 1;
+  static constexpr int value = (W == 1 && EPT < FS_SM_BATCH_ELEMS) ? FS_SM_BATCH_ELEMS / EPT : 1;
 };
 
 template <typename T, typename MT, bool HAS_MASK, bool VEC>
