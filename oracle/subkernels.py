@@ -46,7 +46,8 @@ from scipy import special as _sp
 __all__ = [
     "ACTS", "gelu_erf", "sigmoid", "relu", "apply_act",
     "pointwise_chain", "causal_mask", "row_softmax", "layernorm_residual",
-    "residual_store_bf16", "round_to_bf16", "gemm_epilogue_reduce",
+    "rmsnorm_residual", "residual_store_bf16", "round_to_bf16", "gemm_epilogue_reduce",
+    "row_reduce", "row_argmax",
 ]
 
 ACTS = ("none", "gelu_erf", "sigmoid", "relu")
@@ -164,6 +165,22 @@ def layernorm_residual(x, residual=None, gamma=None, beta=None, eps: float = 1e-
     return y, h
 
 
+def rmsnorm_residual(x, residual=None, gamma=None, eps: float = 1e-6):
+    """h = x + residual; y = h / sqrt(mean(h^2) + eps) * gamma.
+
+    The RMS variant of the normalisation fusion (Appendix A, Fusion Agent:
+    LayerNorm/RMSNorm sequences): no mean subtraction and no bias.  Returns
+    (y, h)."""
+    h = np.asarray(x, dtype=np.float64)
+    if residual is not None:
+        h = h + np.asarray(residual, dtype=np.float64)
+    ms = (h * h).sum(axis=1, keepdims=True) / h.shape[1]
+    y = h / np.sqrt(ms + float(eps))
+    if gamma is not None:
+        y = y * np.asarray(gamma, dtype=np.float64)[None, :]
+    return y, h
+
+
 def round_to_bf16(v) -> np.ndarray:
     """Round float64 values to the nearest bf16 value (8 significant bits,
     ties to even, bf16 exponent range), returned as float64.
@@ -217,3 +234,41 @@ def gemm_epilogue_reduce(c, bias=None, col_scale=None, act: str = "sigmoid",
     if reduce == "mean":
         return s / c.shape[1]
     raise ValueError(f"unknown reduction {reduce!r}")
+
+
+# ---------------------------------------------------------------------------
+# plain row reductions
+# ---------------------------------------------------------------------------
+def row_reduce(x, op: str = "sum"):
+    """out[i] = sum_j x[i, j] ("sum"), that divided by cols ("mean") or
+    max_j x[i, j] ("max").  Section 6 lists sum/mean reductions among the
+    optimised sub-kernel classes; the reduction + pointwise fusion pattern is
+    in Appendix A (Fusion Agent)."""
+    x = np.asarray(x, dtype=np.float64)
+    if op == "sum":
+        return x.sum(axis=1)
+    if op == "mean":
+        return x.sum(axis=1) / x.shape[1]
+    if op == "max":
+        return x.max(axis=1)
+    raise ValueError(f"unknown reduction {op!r}")
+
+
+def row_argmax(x):
+    """Index of the largest element of every row; the lowest index wins a
+    tie and a NaN counts as larger than any number (the first NaN wins).
+
+    Exact by definition: it is written as an explicit comparison scan, not
+    as a library call, so the tie and NaN rules are visible."""
+    x = np.asarray(x, dtype=np.float64)
+    rows, cols = x.shape
+    out = np.zeros(rows, dtype=np.int64)
+    nan = np.isnan(x)
+    for i in range(rows):
+        if nan[i].any():
+            out[i] = int(np.flatnonzero(nan[i])[0])
+            continue
+        row = x[i]
+        best = row.max()
+        out[i] = int(np.flatnonzero(row == best)[0])   # lowest index of the maximum
+    return out

@@ -408,3 +408,61 @@ class TestBlock:
         assert np.abs(r["att"]).max() > 0.1
         np.testing.assert_allclose(r["out"], x + r["att"], atol=1e-14)
         np.testing.assert_array_equal(r["out"], r["h1"])
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm + residual
+# ---------------------------------------------------------------------------
+class TestRMSNorm:
+    def test_hand_example(self):
+        # h = [3, 4]: mean square 12.5 -> y = h / sqrt(12.5) (no mean subtraction)
+        y, _ = oracle.rmsnorm_residual(np.array([[3.0, 4.0]]), None, None, 0.0)
+        np.testing.assert_allclose(y, [[3 / math.sqrt(12.5), 4 / math.sqrt(12.5)]], rtol=1e-15)
+
+    def test_unit_rms_and_scale_invariance(self):
+        rng = np.random.default_rng(20)
+        h = rng.standard_normal((4, 64)) + 2.0
+        y, _ = oracle.rmsnorm_residual(h, None, None, 0.0)
+        np.testing.assert_allclose((y * y).mean(axis=1), 1.0, rtol=1e-14)
+        y2, _ = oracle.rmsnorm_residual(5.0 * h, None, None, 0.0)
+        np.testing.assert_allclose(y, y2, atol=1e-14)
+        assert np.all(y.mean(axis=1) > 0.5)          # the mean is not removed
+
+    def test_eps_gamma_and_residual(self):
+        x = np.array([[1.0, 1.0, 1.0, 1.0]])
+        y, h = oracle.rmsnorm_residual(x, -x + 2.0, np.array([1.0, 2.0, 3.0, 4.0]), 12.0)
+        np.testing.assert_array_equal(h, 2.0)
+        # mean square 4, eps 12 -> 2 / sqrt(16) = 0.5, times gamma
+        np.testing.assert_allclose(y, [[0.5, 1.0, 1.5, 2.0]], rtol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# row reductions
+# ---------------------------------------------------------------------------
+class TestRowReduce:
+    def test_closed_forms(self):
+        x = np.arange(12, dtype=np.float64).reshape(3, 4)
+        np.testing.assert_array_equal(oracle.row_reduce(x, "sum"), [6, 22, 38])
+        np.testing.assert_array_equal(oracle.row_reduce(x, "mean"), [1.5, 5.5, 9.5])
+        np.testing.assert_array_equal(oracle.row_reduce(x, "max"), [3, 7, 11])
+        # sum of 1..n = n(n+1)/2 along the last axis only
+        y = np.tile(np.arange(1, 101, dtype=np.float64), (2, 1))
+        np.testing.assert_array_equal(oracle.row_reduce(y, "sum"), [5050, 5050])
+
+    def test_argmax_ties_and_nan(self):
+        x = np.array([[1.0, 3.0, 3.0, 2.0],        # tie -> lowest index
+                      [-5.0, -5.0, -5.0, -5.0],     # all equal -> 0
+                      [0.0, np.nan, 9.0, np.nan],   # first NaN
+                      [-np.inf, -np.inf, -1.0, 7.0]])
+        np.testing.assert_array_equal(oracle.row_argmax(x), [1, 0, 1, 3])
+
+    def test_argmax_matches_brute_force_comparisons(self):
+        rng = np.random.default_rng(21)
+        x = rng.integers(-3, 4, size=(50, 17)).astype(np.float64)   # many ties
+        got = oracle.row_argmax(x)
+        for i in range(50):
+            best = 0
+            for j in range(1, 17):
+                if x[i, j] > x[i, best]:
+                    best = j
+            assert got[i] == best
