@@ -26,7 +26,8 @@ import numpy as np
 __all__ = [
     "f32_to_bf16_bits", "bf16_bits_to_f64", "bf16_bits_to_f32", "Tensor",
     "pointwise_inputs", "softmax_inputs", "layernorm_inputs", "epilogue_inputs",
-    "gemm_epilogue_inputs", "block_inputs", "CONFIGS", "make_inputs",
+    "gemm_epilogue_inputs", "block_inputs", "row_inputs", "integer_inputs", "CONFIGS",
+    "make_inputs",
     "BLOCK_DIMS",
 ]
 
@@ -200,6 +201,21 @@ def gemm_epilogue_inputs(seed: int, m: int, n: int, k: int) -> Dict[str, object]
     s = _uniform(rng, (n,), 0.5, 1.5)
     return {"a": _store(a, "bf16"), "b": _store(b, "bf16"),
             "bias": _store(bias, "bf16"), "col_scale": _store(s, "f32")}
+
+
+def row_inputs(seed: int, rows: int, cols: int, dtype: str = "bf16", mean: float = 0.0,
+               std: float = 1.0) -> Tensor:
+    """x ~ N(mean, std) [rows, cols] in the storage dtype."""
+    rng = np.random.default_rng(seed)
+    return _store(_normal(rng, (rows, cols), mean, std), dtype)
+
+
+def integer_inputs(seed: int, rows: int, cols: int, dtype: str = "bf16", lo: int = -3,
+                   hi: int = 4) -> Tensor:
+    """Small integers drawn uniformly from [lo, hi) -- exact in bf16 and fp32,
+    so rows hold many exact ties."""
+    rng = np.random.default_rng(seed)
+    return _store(rng.integers(lo, hi, size=(rows, cols)).astype(np.float64), dtype)
 
 
 BLOCK_DIMS = dict(batch=32, seq=512, hidden=1024, heads=16, mlp=4096)

@@ -83,6 +83,8 @@ typedef enum fs_act {
 
 typedef enum fs_reduce { FS_REDUCE_SUM = 0, FS_REDUCE_MEAN = 1 } fs_reduce;
 
+typedef enum fs_row_op { FS_ROW_SUM = 0, FS_ROW_MEAN = 1, FS_ROW_MAX = 2 } fs_row_op;
+
 /*
  * Fused pointwise chain (Appendix A, Fusion Agent: pointwise + pointwise and
  * activation + bias fusion -- load once, apply every op, store once).
@@ -145,6 +147,50 @@ FS_API fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* 
                                 int64_t ld_r, const void* gamma, const void* beta, void* y,
                                 int64_t ld_y, void* residual_out, int64_t ld_ro, int64_t rows,
                                 int64_t cols, float eps, fs_dtype dtype, hipStream_t stream);
+
+/*
+ * RMSNorm fused with the residual add (Appendix A, Fusion Agent: the
+ * LayerNorm/RMSNorm normalisation fusion; residual + norm in one memory pass).
+ *
+ *   h = x + residual                     (fp32)
+ *   y = h / sqrt(mean(h^2) + eps) * gamma
+ *   residual_out = h rounded to `dtype`
+ *
+ * Arguments, layouts, aliasing rules and limits as fs_layernorm_residual,
+ * without beta.
+ */
+FS_API fs_status fs_rmsnorm_residual(const void* x, int64_t ld_x, const void* residual,
+                                     int64_t ld_r, const void* gamma, void* y, int64_t ld_y,
+                                     void* residual_out, int64_t ld_ro, int64_t rows,
+                                     int64_t cols, float eps, fs_dtype dtype,
+                                     hipStream_t stream);
+
+/*
+ * Plain row reduction (Section 6 counts sum/mean reductions among the
+ * optimised sub-kernel classes; Appendix A, Executor prompt: accumulate in
+ * fp32).
+ *
+ *   out[i] = sum_j x[i, j]   (FS_ROW_SUM)
+ *          = that / cols     (FS_ROW_MEAN)
+ *          = max_j x[i, j]   (FS_ROW_MAX; a NaN in the row gives NaN)
+ *
+ * x   : [rows, cols] of `dtype`, row stride ld_x.  Rows of any length: the
+ *       row is streamed, not held in registers.
+ * out : [rows] fp32, contiguous; must not overlap x.
+ * cols == 0 with rows > 0: SUM writes zeros, MEAN and MAX return
+ * FS_ERR_BAD_SHAPE.
+ */
+FS_API fs_status fs_row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op,
+                               float* out, int64_t rows, int64_t cols, hipStream_t stream);
+
+/*
+ * Row argmax, bit-exact: out[i] is the index of the largest x[i, j]; the
+ * lowest index wins a tie, and a NaN counts as larger than any number (the
+ * first NaN wins).  x as in fs_row_reduce; out: [rows] int64, contiguous,
+ * not overlapping x.  cols must be >= 1.
+ */
+FS_API fs_status fs_row_argmax(const void* x, int64_t ld_x, fs_dtype dtype, int64_t* out,
+                               int64_t rows, int64_t cols, hipStream_t stream);
 
 /*
  * GEMM epilogue with a row reduction, applied to the output C of a library

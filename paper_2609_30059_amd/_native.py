@@ -29,12 +29,14 @@ STATUS_NAMES = {0: "FS_OK", 1: "FS_ERR_NULL_POINTER", 2: "FS_ERR_BAD_SHAPE",
 FS_F32, FS_BF16 = 0, 1
 ACTS = {"none": 0, "gelu_erf": 1, "sigmoid": 2, "relu": 3}
 REDUCES = {"sum": 0, "mean": 1}
+ROW_OPS = {"sum": 0, "mean": 1, "max": 2}
 FS_ABI_VERSION = 1
 FS_SOFTMAX_MAX_COLS = 65536
 FS_LAYERNORM_MAX_COLS = 65536
 
 # every symbol the headers declare
 FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_layernorm_residual",
+                    "fs_rmsnorm_residual", "fs_row_reduce", "fs_row_argmax",
                     "fs_gemm_epilogue_reduce", "fs_copy", "fs_status_string",
                     "fs_last_error_message", "fs_abi_version")
 FSGEMM_SYMBOLS = ("fsg_gemm_bf16", "fsg_last_error_message")
@@ -60,6 +62,9 @@ _SIGS = {
     "fs_row_softmax": [_P, _I64, _P, _I64, _I, _P, _I64, _I64, _I64, _F, _I64, _I, _P],
     "fs_layernorm_residual": [_P, _I64, _P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _F, _I,
                               _P],
+    "fs_rmsnorm_residual": [_P, _I64, _P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64, _F, _I, _P],
+    "fs_row_reduce": [_P, _I64, _I, _I, _P, _I64, _I64, _P],
+    "fs_row_argmax": [_P, _I64, _I, _P, _I64, _I64, _P],
     "fs_gemm_epilogue_reduce": [_P, _I64, _I, _P, _I, _P, _I, _I, _P, _I64, _I64, _P],
     "fs_copy": [_P, _P, _I64, _P],
     "fs_status_string": [_I],
@@ -140,6 +145,20 @@ def fs_layernorm_residual(x, ld_x, residual, ld_r, gamma, beta, y, ld_y, residua
                           rows, cols, eps, dtype, stream):
     return fusedsub().fs_layernorm_residual(x, ld_x, residual, ld_r, gamma, beta, y, ld_y,
                                             residual_out, ld_ro, rows, cols, eps, dtype, stream)
+
+
+def fs_rmsnorm_residual(x, ld_x, residual, ld_r, gamma, y, ld_y, residual_out, ld_ro, rows, cols,
+                        eps, dtype, stream):
+    return fusedsub().fs_rmsnorm_residual(x, ld_x, residual, ld_r, gamma, y, ld_y, residual_out,
+                                          ld_ro, rows, cols, eps, dtype, stream)
+
+
+def fs_row_reduce(x, ld_x, dtype, op, out, rows, cols, stream):
+    return fusedsub().fs_row_reduce(x, ld_x, dtype, op, out, rows, cols, stream)
+
+
+def fs_row_argmax(x, ld_x, dtype, out, rows, cols, stream):
+    return fusedsub().fs_row_argmax(x, ld_x, dtype, out, rows, cols, stream)
 
 
 def fs_gemm_epilogue_reduce(c, ld_c, c_dtype, bias, bias_dtype, col_scale, act, reduce, row_out,

@@ -200,10 +200,15 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
   return e == hipSuccess ? FS_OK : hip_fail(e, "row_softmax launch");
 }
 
-fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residual, int64_t ld_r,
-                                const void* gamma, const void* beta, void* y, int64_t ld_y,
-                                void* residual_out, int64_t ld_ro, int64_t rows, int64_t cols,
-                                float eps, fs_dtype dtype, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// shared by LayerNorm and RMSNorm (rms: no mean, no beta)
+fs_status norm_residual(const void* x, int64_t ld_x, const void* residual, int64_t ld_r,
+                        const void* gamma, const void* beta, void* y, int64_t ld_y,
+                        void* residual_out, int64_t ld_ro, int64_t rows, int64_t cols, float eps,
+                        fs_dtype dtype, hipStream_t stream, bool rms) {
   clear_msg();
   if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
   if (!std::isfinite(eps) || eps < 0.f) return fail(FS_ERR_BAD_ARGUMENT, "eps must be finite, >= 0");
@@ -232,14 +237,80 @@ fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residua
   if (overlap(ey, eo)) return fail(FS_ERR_ALIASING, "y overlaps residual_out");
 
   fs::LayerNormArgs a{x, ld_x, residual, ld_r, gamma, beta, y, ld_y, residual_out, ld_ro,
-                      rows, cols, eps, dtype, false};
+                      rows, cols, eps, dtype, false, rms};
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(residual, ld_r, es) && vec_ok(residual_out, ld_ro, es) &&
           (gamma == nullptr || aligned(gamma, 16)) && (beta == nullptr || aligned(beta, 16));
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_layernorm(a, cus, stream);
-  return e == hipSuccess ? FS_OK : hip_fail(e, "layernorm_residual launch");
+  return e == hipSuccess ? FS_OK : hip_fail(e, rms ? "rmsnorm_residual launch"
+                                                   : "layernorm_residual launch");
+}
+
+// shared by the row reductions (argmax when out_i is set)
+fs_status row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op, float* out_f,
+                     int64_t* out_i, int64_t rows, int64_t cols, hipStream_t stream) {
+  clear_msg();
+  if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
+  if (!out_i && op != FS_ROW_SUM && op != FS_ROW_MEAN && op != FS_ROW_MAX)
+    return fail(FS_ERR_BAD_ARGUMENT, "op=%d", int(op));
+  fs_status st = check_shape(rows, cols, INT32_MAX / 2);
+  if (st != FS_OK) return st;
+  if ((st = check_ld("ld_x", ld_x, rows, cols)) != FS_OK) return st;
+  if (rows == 0) return FS_OK;
+  if (cols == 0 && (out_i || op != FS_ROW_SUM))
+    return fail(FS_ERR_BAD_SHAPE, "this reduction needs cols >= 1");
+  if (!(out_f || out_i) || (cols > 0 && !x)) return fail(FS_ERR_NULL_POINTER, "x and out are required");
+  const int es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(out_f, 4) || !aligned(out_i, 8))
+    return fail(FS_ERR_BAD_ARGUMENT, "pointers must be aligned to the element size");
+  const Extent eo = out_i ? vec_extent(out_i, rows, 8) : vec_extent(out_f, rows, 4);
+  const Extent ex = cols ? mat_extent(x, rows, cols, ld_x, es) : Extent{};
+  if (overlap(eo, ex)) return fail(FS_ERR_ALIASING, "out overlaps x");
+  fs::ReduceArgs a{x, ld_x, dtype, op, out_f, out_i, rows, cols, false};
+  a.vec = cols > 0 && cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es);
+  int cus = 0;
+  if ((st = device_cus(&cus)) != FS_OK) return st;
+  hipError_t e = fs::launch_reduce(a, cus, stream);
+  return e == hipSuccess ? FS_OK : hip_fail(e, out_i ? "row_argmax launch" : "row_reduce launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residual, int64_t ld_r,
+                                const void* gamma, const void* beta, void* y, int64_t ld_y,
+                                void* residual_out, int64_t ld_ro, int64_t rows, int64_t cols,
+                                float eps, fs_dtype dtype, hipStream_t stream) {
+  return norm_residual(x, ld_x, residual, ld_r, gamma, beta, y, ld_y, residual_out, ld_ro, rows,
+                       cols, eps, dtype, stream, false);
+}
+
+fs_status fs_rmsnorm_residual(const void* x, int64_t ld_x, const void* residual, int64_t ld_r,
+                              const void* gamma, void* y, int64_t ld_y, void* residual_out,
+                              int64_t ld_ro, int64_t rows, int64_t cols, float eps,
+                              fs_dtype dtype, hipStream_t stream) {
+  return norm_residual(x, ld_x, residual, ld_r, gamma, nullptr, y, ld_y, residual_out, ld_ro,
+                       rows, cols, eps, dtype, stream, true);
+}
+
+fs_status fs_row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op, float* out,
+                        int64_t rows, int64_t cols, hipStream_t stream) {
+  return row_reduce(x, ld_x, dtype, op, out, nullptr, rows, cols, stream);
+}
+
+fs_status fs_row_argmax(const void* x, int64_t ld_x, fs_dtype dtype, int64_t* out, int64_t rows,
+                        int64_t cols, hipStream_t stream) {
+  if (!out) {
+    clear_msg();
+    if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
+    if (rows < 0 || cols < 0) return fail(FS_ERR_BAD_SHAPE, "negative shape");
+    if (rows == 0) return FS_OK;
+    return fail(FS_ERR_NULL_POINTER, "out is required");
+  }
+  return row_reduce(x, ld_x, dtype, FS_ROW_MAX, nullptr, out, rows, cols, stream);
 }
 
 fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype, const void* bias,

@@ -42,6 +42,7 @@ struct LayerNormArgs {
   float eps;
   fs_dtype dtype;
   bool vec;
+  bool rms;        // RMSNorm: no mean, no beta
 };
 
 struct EpilogueArgs {
@@ -60,5 +61,15 @@ hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s);
 hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs& a, int cus, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipStream_t s);
+
+struct ReduceArgs {
+  const void* x; int64_t ld_x; fs_dtype dtype;
+  fs_row_op op;
+  float* out_f;      // sum / mean / max
+  int64_t* out_i;    // argmax
+  int64_t rows, cols;
+  bool vec;
+};
+hipError_t launch_reduce(const ReduceArgs& a, int cus, hipStream_t s);
 
 }  // namespace fs

@@ -1,4 +1,4 @@
-// LayerNorm fused with the residual add.
+// LayerNorm (and RMSNorm) fused with the residual add.
 //
 // h = x + residual; y = (h - mean) / sqrt(var + eps) * gamma + beta;
 // residual_out = h -- KernelOPT Appendix A (Fusion Agent: normalisation
@@ -11,7 +11,9 @@
 // register-resident row -- an all-reduce of sum(h) gives the mean, then an
 // all-reduce of sum((h - mean)^2) the biased variance -- so there is no
 // E[h^2] - mean^2 cancellation and no second HBM pass.  Both all-reduces are
-// plain sums, which fold into DPP adds.
+// plain sums, which fold into DPP adds.  RMSNorm (y = h / sqrt(mean(h^2) +
+// eps) * gamma, the RMS form of the same normalisation fusion) shares the
+// kernel with a single all-reduce of sum(h^2) and no mean.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -38,7 +40,7 @@ namespace {
 // W waves per row, EPT elements per thread, G row groups per block (W == 1
 // only), R rows per group per trip: narrow rows are batched so that a wave
 // keeps R rows of loads in flight and reduces them with one shuffle sequence.
-template <typename T, bool HAS_RES, int W, int EPT, bool VEC, int G, int R>
+template <typename T, bool HAS_RES, bool RMS, int W, int EPT, bool VEC, int G, int R>
 __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
     const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
     const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
@@ -50,6 +52,9 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   // wider rows re-read them (cache-resident) after each trip's statistics
   constexpr bool kAffineResident = EPT <= 32;
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
+  // one LDS fold area and one barrier sequence per block: rows wider than a
+  // wave take the whole block (the row loop is then uniform across it)
+  static_assert(W == 1 || G == 1, "multi-wave rows use one row group per block");
   using P = Multi<SumP, R>;
   __shared__ P lds[2][W];
 
@@ -121,28 +126,34 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
       }
       float sum = 0.f;
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) sum += h[r][i];     // out-of-row slots hold 0
-      part.p[r] = SumP{sum};
+      for (int i = 0; i < EPT; ++i) sum = RMS ? fmaf(h[r][i], h[r][i], sum) : sum + h[r][i];
+      part.p[r] = SumP{sum};      // out-of-row slots hold 0
     }
-    // pass 1: the row means
-    const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
-    parity ^= 1;
     float mean[R];
+    if constexpr (RMS) {
+      // RMSNorm: the single reduction above is already sum(h^2)
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      mean[r] = tot.p[r].s * inv_cols;
-      // pass 2: squared deviations from the row mean, over the owned columns
-      float m2 = 0.f;
+      for (int r = 0; r < R; ++r) mean[r] = 0.f;
+    } else {
+      // pass 1: the row means
+      const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
+      parity ^= 1;
 #pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        const bool in = (k * kThreads + tid) * V < cols;
+      for (int r = 0; r < R; ++r) {
+        mean[r] = tot.p[r].s * inv_cols;
+        // pass 2: squared deviations from the row mean, over the owned columns
+        float m2 = 0.f;
 #pragma unroll
-        for (int i = 0; i < V; ++i) {
-          const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
-          m2 = fmaf(d, d, m2);
+        for (int k = 0; k < NV; ++k) {
+          const bool in = (k * kThreads + tid) * V < cols;
+#pragma unroll
+          for (int i = 0; i < V; ++i) {
+            const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
+            m2 = fmaf(d, d, m2);
+          }
         }
+        part.p[r] = SumP{m2};
       }
-      part.p[r] = SumP{m2};
     }
     const P sq = group_allreduce<W>(part, lds[parity], wave, lane);
     parity ^= 1;
@@ -184,7 +195,7 @@ struct RowsPerGroup {
   static constexpr int value = (W == 1 && EPT < FS_LN_BATCH_ELEMS) ? FS_LN_BATCH_ELEMS / EPT : 1;
 };
 
-template <typename T, bool HAS_RES, bool VEC>
+template <typename T, bool HAS_RES, bool RMS, bool VEC>
 hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   const int64_t c = a.cols;
@@ -204,7 +215,7 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   const int min_w = c >= FS_LN_SPLIT_COLS ? FS_LN_MIN_WAVES : 1;
 #define FS_LN(Wv, E, Gv, BPC)                                                       \
   if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                   \
-    return launch(layernorm_kernel<T, HAS_RES, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
+    return launch(layernorm_kernel<T, HAS_RES, RMS, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_LN(1, 1, 4, 8) }
   if constexpr (V <= 2) { FS_LN(1, 2, 4, 8) }
@@ -227,17 +238,18 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   return hipErrorInvalidValue;   // unreachable: the host checks cols
 }
 
-template <typename T>
+template <typename T, bool RMS>
 hipError_t by_res(const LayerNormArgs& a, int cus, hipStream_t s) {
   if (a.res == nullptr)
-    return a.vec ? dispatch<T, false, true>(a, cus, s) : dispatch<T, false, false>(a, cus, s);
-  return a.vec ? dispatch<T, true, true>(a, cus, s) : dispatch<T, true, false>(a, cus, s);
+    return a.vec ? dispatch<T, false, RMS, true>(a, cus, s) : dispatch<T, false, RMS, false>(a, cus, s);
+  return a.vec ? dispatch<T, true, RMS, true>(a, cus, s) : dispatch<T, true, RMS, false>(a, cus, s);
 }
 
 }  // namespace
 
 hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s) {
-  return a.dtype == FS_BF16 ? by_res<uint16_t>(a, cus, s) : by_res<float>(a, cus, s);
+  if (a.rms) return a.dtype == FS_BF16 ? by_res<uint16_t, true>(a, cus, s) : by_res<float, true>(a, cus, s);
+  return a.dtype == FS_BF16 ? by_res<uint16_t, false>(a, cus, s) : by_res<float, false>(a, cus, s);
 }
 
 }  // namespace fs

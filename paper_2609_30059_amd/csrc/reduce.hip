@@ -1,0 +1,164 @@
+// Plain row reductions: sum, mean, max (fp32 out) and bit-exact argmax
+// (int64 out, lowest index on ties, first NaN wins).
+//
+// KernelOPT Section 6 counts sum/mean reductions among the optimised
+// sub-kernel classes; Appendix A (Executor prompt) asks for fp32 accumulation.
+//
+// Design (gfx950): a group of W wave64s per row; the row is streamed in trips
+// of U 16-byte vectors per lane, all U loads issued before any use, with a
+// trip count that is uniform across the group (lanes past the row end re-read
+// the row's last vector and mask it).  Rows of any length are supported; the
+// per-lane partials meet in one wave all-reduce (plus an LDS fold when W > 1).
+#include "device_common.hpp"
+#include "launch.hpp"
+
+#ifndef FS_RED_UNROLL
+#define FS_RED_UNROLL 4
+#endif
+
+namespace fs {
+namespace {
+
+struct MaxP {   // NaN-propagating maximum
+  float m;
+  __device__ __forceinline__ static MaxP combine(const MaxP& a, const MaxP& b) {
+    if (a.m != a.m) return a;
+    if (b.m != b.m) return b;
+    return {fmaxf(a.m, b.m)};
+  }
+  template <class F> __device__ __forceinline__ static MaxP map(const MaxP& a, F f) {
+    return {f(a.m)};
+  }
+};
+
+// (value, index): larger value wins, NaN above every number, lowest index on
+// a tie (between two NaNs too).  combine(a, b) == combine(b, a).
+struct ArgP {
+  float v;
+  int i;
+  __device__ __forceinline__ static ArgP combine(const ArgP& a, const ArgP& b) {
+    const bool an = a.v != a.v, bn = b.v != b.v;
+    if (an || bn) {
+      if (an && bn) return a.i < b.i ? a : b;
+      return an ? a : b;
+    }
+    if (a.v > b.v) return a;
+    if (b.v > a.v) return b;
+    return a.i < b.i ? a : b;
+  }
+  template <class F> __device__ __forceinline__ static ArgP map(const ArgP& a, F f) {
+    return {f(a.v), __float_as_int(f(__int_as_float(a.i)))};
+  }
+};
+
+constexpr int kOpSum = 0, kOpMax = 2, kOpArg = 3;   // MEAN runs as SUM
+
+template <int OP> struct AccOf;
+template <> struct AccOf<kOpSum> { using type = SumP; };
+template <> struct AccOf<kOpMax> { using type = MaxP; };
+template <> struct AccOf<kOpArg> { using type = ArgP; };
+
+template <int OP>
+__device__ __forceinline__ typename AccOf<OP>::type identity() {
+  if constexpr (OP == kOpSum) return SumP{0.f};
+  else if constexpr (OP == kOpMax) return MaxP{-INFINITY};
+  else return ArgP{-INFINITY, 0x7fffffff};
+}
+
+template <int OP>
+__device__ __forceinline__ void accumulate(typename AccOf<OP>::type& acc, float v, int col) {
+  if constexpr (OP == kOpSum) acc.s += v;
+  else if constexpr (OP == kOpMax) acc = MaxP::combine(acc, MaxP{v});
+  else acc = ArgP::combine(acc, ArgP{v, col});
+}
+
+template <typename T, int OP, int W, int G, bool VEC>
+__global__ __launch_bounds__(64 * W * G) void reduce_kernel(
+    const T* __restrict__ x, int64_t ld_x, float* __restrict__ out_f,
+    int64_t* __restrict__ out_i, int64_t rows, int cols, int trips, float post_scale) {
+  constexpr int kThreads = 64 * W;
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int U = FS_RED_UNROLL;
+  // one LDS fold area and one barrier sequence per block: rows wider than a
+  // wave take the whole block (the row loop is then uniform across it)
+  static_assert(W == 1 || G == 1, "multi-wave rows use one row group per block");
+  using P = typename AccOf<OP>::type;
+  __shared__ P lds[2][W];
+  const int tid = threadIdx.x % kThreads;
+  const int wave = tid / 64, lane = tid % 64;
+  const int g = threadIdx.x / kThreads;
+  const int clast = cols - V;     // start of the row's last vector
+  int parity = 0;
+
+  for (int64_t row = int64_t(blockIdx.x) * G + g; row < rows; row += int64_t(gridDim.x) * G) {
+    const T* xr = x + row * ld_x;
+    P acc = identity<OP>();
+    for (int t = 0; t < trips; ++t) {
+      Raw<T, V> rv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        rv[u].load(xr + (c0 < cols ? c0 : clast));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        float v[V];
+        rv[u].unpack(v);
+        if (c0 < cols) {   // the whole vector is in the row (cols % V == 0 on this path)
+#pragma unroll
+          for (int i = 0; i < V; ++i) accumulate<OP>(acc, v[i], c0 + i);
+        }
+      }
+    }
+    const P tot = group_allreduce<W>(acc, lds[parity], wave, lane);
+    parity ^= 1;
+    if (tid == 0) {
+      if constexpr (OP == kOpArg) out_i[row] = tot.i;
+      else if constexpr (OP == kOpSum) out_f[row] = tot.s * post_scale;
+      else out_f[row] = tot.m;
+    }
+  }
+}
+
+template <typename T, int OP, bool VEC>
+hipError_t dispatch(const ReduceArgs& a, int cus, hipStream_t s) {
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int U = FS_RED_UNROLL;
+  // waves per row: enough that a trip covers about half the row, at most 8
+  const int64_t per_wave_trip = int64_t(64) * V * U;
+  const int64_t want_w = (a.cols + 2 * per_wave_trip - 1) / (2 * per_wave_trip);
+  const float post = (a.op == FS_ROW_MEAN && a.cols > 0) ? 1.f / float(a.cols) : 1.f;
+  auto launch = [&](auto kern, int w, int g) {
+    const int trips = int((a.cols + int64_t(64) * w * V * U - 1) / (int64_t(64) * w * V * U));
+    int64_t want = (a.rows + g - 1) / g;
+    int64_t cap = int64_t(cus) * (32 / (w * g) > 0 ? 32 / (w * g) : 1) * 4;
+    int grid = int(want < cap ? want : cap);
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * w * g), 0, s, static_cast<const T*>(a.x),
+                       a.ld_x, a.out_f, a.out_i, a.rows, int(a.cols), trips, post);
+    return hipGetLastError();
+  };
+  if (want_w <= 1) return launch(reduce_kernel<T, OP, 1, 4, VEC>, 1, 4);
+  if (want_w <= 2) return launch(reduce_kernel<T, OP, 2, 1, VEC>, 2, 1);
+  if (want_w <= 4) return launch(reduce_kernel<T, OP, 4, 1, VEC>, 4, 1);
+  return launch(reduce_kernel<T, OP, 8, 1, VEC>, 8, 1);
+}
+
+template <typename T>
+hipError_t by_op(const ReduceArgs& a, bool argmax, int cus, hipStream_t s) {
+  if (argmax) return a.vec ? dispatch<T, kOpArg, true>(a, cus, s) : dispatch<T, kOpArg, false>(a, cus, s);
+  if (a.op == FS_ROW_MAX)
+    return a.vec ? dispatch<T, kOpMax, true>(a, cus, s) : dispatch<T, kOpMax, false>(a, cus, s);
+  return a.vec ? dispatch<T, kOpSum, true>(a, cus, s) : dispatch<T, kOpSum, false>(a, cus, s);
+}
+
+}  // namespace
+
+hipError_t launch_reduce(const ReduceArgs& a, int cus, hipStream_t s) {
+  const bool argmax = a.out_i != nullptr;
+  return a.dtype == FS_BF16 ? by_op<uint16_t>(a, argmax, cus, s) : by_op<float>(a, argmax, cus, s);
+}
+
+}  // namespace fs

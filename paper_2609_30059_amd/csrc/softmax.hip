@@ -68,6 +68,9 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;                       // vectors per thread
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
+  // one LDS fold area and one barrier sequence per block: rows wider than a
+  // wave take the whole block (the row loop is then uniform across it)
+  static_assert(W == 1 || G == 1, "multi-wave rows use one row group per block");
   using P = Multi<MaxSumP, R>;
   __shared__ P lds[2][W];
 

@@ -13,8 +13,9 @@ import torch
 
 from . import _native as N
 
-__all__ = ["pointwise_chain", "row_softmax", "layernorm_residual", "gemm_epilogue_reduce",
-           "copy_", "gemm", "gemm_strided_batched", "as_rows", "fs_dtype"]
+__all__ = ["pointwise_chain", "row_softmax", "layernorm_residual", "rmsnorm_residual",
+           "row_reduce", "row_argmax", "gemm_epilogue_reduce", "copy_", "gemm",
+           "gemm_strided_batched", "as_rows", "fs_dtype"]
 
 
 def fs_dtype(t: torch.Tensor) -> int:
@@ -137,6 +138,58 @@ def layernorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
                                  _stream())
     N.check("fs_layernorm_residual", st)
     return out, residual_out
+
+
+def rmsnorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
+                     gamma: Optional[torch.Tensor] = None, eps: float = 1e-6,
+                     out: Optional[torch.Tensor] = None,
+                     residual_out: Optional[torch.Tensor] = None, store_residual: bool = True):
+    """(RMSNorm(x + residual), x + residual)  (fs_rmsnorm_residual)."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    ld_r = ld_ro = 0
+    if residual is not None:
+        if residual.shape != x.shape or residual.dtype != x.dtype:
+            raise ValueError("residual must match x")
+        ld_r = as_rows(residual)[2]
+        if residual_out is None and store_residual:
+            residual_out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    if residual_out is not None:
+        ld_ro = as_rows(residual_out)[2]
+    if gamma is not None and gamma.dtype != x.dtype:
+        raise ValueError("gamma dtype must match x")
+    _vec(gamma, cols, "gamma")
+    st = N.fs_rmsnorm_residual(x.data_ptr(), ld_x, _ptr(residual), ld_r, _ptr(gamma),
+                               out.data_ptr(), as_rows(out)[2], _ptr(residual_out), ld_ro, rows,
+                               cols, float(eps), fs_dtype(x), _stream())
+    N.check("fs_rmsnorm_residual", st)
+    return out, residual_out
+
+
+def row_reduce(x: torch.Tensor, op: str = "sum", out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Row sum / mean / max as float32 [rows]  (fs_row_reduce)."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty(rows, dtype=torch.float32, device=x.device)
+    if out.dtype != torch.float32 or out.numel() != rows or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [rows] tensor")
+    st = N.fs_row_reduce(x.data_ptr() if x.numel() else None, ld_x, fs_dtype(x), N.ROW_OPS[op],
+                         out.data_ptr(), rows, cols, _stream())
+    N.check("fs_row_reduce", st)
+    return out
+
+
+def row_argmax(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Row argmax as int64 [rows]: lowest index on ties, first NaN wins  (fs_row_argmax)."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty(rows, dtype=torch.int64, device=x.device)
+    if out.dtype != torch.int64 or out.numel() != rows or not out.is_contiguous():
+        raise ValueError("out must be a contiguous int64 [rows] tensor")
+    st = N.fs_row_argmax(x.data_ptr(), ld_x, fs_dtype(x), out.data_ptr(), rows, cols, _stream())
+    N.check("fs_row_argmax", st)
+    return out
 
 
 def gemm_epilogue_reduce(c: torch.Tensor, bias: Optional[torch.Tensor] = None,

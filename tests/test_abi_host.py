@@ -139,6 +139,46 @@ def test_layernorm_validation():
     assert ln(residual=C, residual_out=C + 2) == 5
 
 
+def rms(**kw):
+    a = dict(x=A, ld_x=256, residual=NULL, ld_r=256, gamma=NULL, y=B, ld_y=256,
+             residual_out=NULL, ld_ro=256, rows=8, cols=256, eps=1e-6, dtype=1, stream=None)
+    a.update(kw)
+    return N.fs_rmsnorm_residual(**a)
+
+
+def test_rmsnorm_validation():
+    assert rms(x=NULL) == 1
+    assert rms(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert rms(ld_x=7) == 3
+    assert rms(dtype=5) == 4
+    assert rms(eps=float("nan")) == 6
+    assert rms(gamma=B + 64) == 5
+    assert rms(residual=C, residual_out=B + 2) == 5
+    assert rms(rows=0, x=NULL, y=NULL) == 0
+
+
+def test_row_reduce_and_argmax_validation():
+    red = lambda **kw: N.fs_row_reduce(**{**dict(x=A, ld_x=64, dtype=0, op=0, out=B, rows=4,  # noqa: E731
+                                              cols=64, stream=None), **kw})
+    arg = lambda **kw: N.fs_row_argmax(**{**dict(x=A, ld_x=64, dtype=0, out=B, rows=4,  # noqa: E731
+                                              cols=64, stream=None), **kw})
+    assert red(out=NULL) == 1
+    assert red(rows=-1) == 2
+    assert red(ld_x=3) == 3
+    assert red(dtype=9) == 4
+    assert red(op=7) == 6
+    assert red(out=A + 8) == 5              # out inside x
+    assert red(out=B + 2) == 6              # misaligned float*
+    assert red(cols=0, op=1) == 2           # mean of nothing
+    assert red(cols=0, op=2) == 2           # max of nothing
+    assert red(rows=0, x=NULL, out=NULL) == 0
+    assert arg(out=NULL) == 1
+    assert arg(cols=0, ld_x=0) == 2
+    assert arg(out=B + 4) == 6              # misaligned int64*
+    assert arg(out=A) == 5
+    assert arg(rows=0, out=NULL) == 0
+
+
 # ---- epilogue ----------------------------------------------------------------
 def ep(**kw):
     a = dict(c=A, ld_c=8192, c_dtype=1, bias=NULL, bias_dtype=1, col_scale=NULL, act=2,

@@ -141,3 +141,45 @@ def test_beyond_2_31_elements():
     sub = {"x": d["x"].rows(idx % 64), "residual": d["residual"].rows(idx % 64),
            "gamma": d["gamma"], "beta": d["beta"], "eps": d["eps"]}
     check("beyond 2^31", sub, y[ti], ro[ti], "bf16")
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm + residual (the same kernel family)
+# ---------------------------------------------------------------------------
+def check_rms(name, d, y, ro, dtype, has_res=True, affine=True, eps=1e-6):
+    ref_y, _ = oracle.rmsnorm_residual(d["x"].f64(), d["residual"].f64() if has_res else None,
+                                       d["gamma"].f64() if affine else None, eps)
+    got = host64(y)
+    assert_close(name + " y", got, ref_y, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(name + " y", got, ref_y, ulps=1.0, atol=2e-5)
+    if ro is not None and dtype == "bf16":
+        np.testing.assert_array_equal(host64(ro), oracle.residual_store_bf16(
+            d["x"].f64(), d["residual"].f64()), err_msg=name + " residual_out")
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_rmsnorm_five_seeds(seed):
+    d = fd.layernorm_inputs(seed, 80, 4096)
+    announce("rmsnorm", seed)
+    eps = float(np.float32(1e-6))
+    y, ro = fs.rmsnorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]), eps)
+    check_rms(f"seed {seed}", d, y, ro, "bf16", eps=eps)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [1, 7, 64, 1024, 4099, 8192, 20000])
+def test_rmsnorm_widths(dtype, cols):
+    d = fd.layernorm_inputs(cols + 1, 9 if cols <= 8192 else 3, cols, dtype)
+    announce("rmsnorm width", cols, dtype)
+    eps = float(np.float32(1e-6))
+    y, ro = fs.rmsnorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]), eps)
+    check_rms(f"cols {cols}", d, y, ro, dtype, eps=eps)
+
+
+def test_rmsnorm_without_residual_or_gamma():
+    d = fd.layernorm_inputs(5, 16, 1024, "bf16")
+    eps = float(np.float32(1e-6))
+    y, ro = fs.rmsnorm_residual(dev(d["x"]), None, None, eps)
+    assert ro is None
+    check_rms("plain", d, y, None, "bf16", has_res=False, affine=False, eps=eps)

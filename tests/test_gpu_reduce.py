@@ -1,0 +1,99 @@
+"""GPU parity of fs_row_reduce (sum, mean, max) and fs_row_argmax against the
+float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import SEEDS, Guarded, announce, assert_close, dev, host64
+
+pytestmark = pytest.mark.gpu
+
+
+def sum_tol(x64):
+    # fp32 accumulation (sequential per lane, then a tree): a few fp32 units
+    # of the sum of magnitudes
+    return 1e-6 * np.abs(x64).sum(axis=1) + 1e-6
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sum_mean_max_seeds(seed, dtype):
+    x = fd.row_inputs(seed, 97, 4096, dtype, mean=0.25, std=2.0)
+    t = dev(x)
+    announce("row_reduce seeds", seed, dtype)
+    x64 = x.f64()
+    assert_close("sum", host64(fs.row_reduce(t, "sum")), oracle.row_reduce(x64, "sum"),
+                 sum_tol(x64), 0)
+    assert_close("mean", host64(fs.row_reduce(t, "mean")), oracle.row_reduce(x64, "mean"),
+                 sum_tol(x64) / 4096, 0)
+    np.testing.assert_array_equal(host64(fs.row_reduce(t, "max")), oracle.row_reduce(x64, "max"))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,cols", [(5, 1), (9, 7), (33, 8), (17, 100), (8, 4099),
+                                       (3, 65536 + 24), (2, (1 << 20) + 3)])
+def test_widths(dtype, rows, cols):
+    x = fd.row_inputs(cols, rows, cols, dtype)
+    t = dev(x)
+    announce("row_reduce width", rows, cols, dtype)
+    x64 = x.f64()
+    assert_close("sum", host64(fs.row_reduce(t, "sum")), oracle.row_reduce(x64, "sum"),
+                 sum_tol(x64), 0)
+    np.testing.assert_array_equal(host64(fs.row_reduce(t, "max")), oracle.row_reduce(x64, "max"))
+    np.testing.assert_array_equal(fs.row_argmax(t).cpu().numpy(), oracle.row_argmax(x64))
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [64, 1000, 4096, 70000])
+def test_argmax_bit_exact_with_ties(seed, dtype, cols):
+    # small integers: every row is full of exact ties, so only the
+    # lowest-index rule picks the right answer
+    x = fd.integer_inputs(seed, 41, cols, dtype)
+    announce("row_argmax ties", seed, dtype, cols)
+    got = fs.row_argmax(dev(x)).cpu().numpy()
+    np.testing.assert_array_equal(got, oracle.row_argmax(x.f64()))
+
+
+def test_argmax_nan_inf_and_constant_rows():
+    rows = np.zeros((6, 300), dtype=np.float32)
+    rows[0, :] = 2.0                          # constant -> 0
+    rows[1, 123] = np.nan                     # NaN wins
+    rows[1, 200] = np.nan
+    rows[1, 5] = 1e30
+    rows[2, :] = -np.inf                      # all -inf -> 0
+    rows[3, :] = -np.inf
+    rows[3, 299] = -1.0                       # last element
+    rows[4, 17] = np.inf                      # +inf
+    rows[4, 250] = np.inf
+    rows[5, :] = np.arange(300, dtype=np.float32)[::-1]   # first element
+    t = torch.from_numpy(rows).cuda()
+    got = fs.row_argmax(t).cpu().numpy()
+    np.testing.assert_array_equal(got, oracle.row_argmax(rows.astype(np.float64)))
+    np.testing.assert_array_equal(got, [0, 123, 0, 299, 17, 0])
+    mx = host64(fs.row_reduce(t, "max"))
+    assert np.isnan(mx[1]) and mx[2] == -np.inf and mx[4] == np.inf
+
+
+def test_zero_columns_sum_and_empty_rows():
+    out = torch.full((4,), 3.0, device="cuda")
+    fs.row_reduce(torch.empty(4, 0, device="cuda"), "sum", out=out)
+    np.testing.assert_array_equal(host64(out), 0.0)
+    assert fs.row_reduce(torch.empty(0, 9, device="cuda")).numel() == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_and_misaligned(dtype):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 13, 1500, 1536
+    x = fd.integer_inputs(31, rows, cols, dtype, -50, 50)
+    for offset in (0, 1):
+        announce("row_reduce strided", dtype, offset)
+        g = Guarded(rows, cols, ld, tdt, offset=offset)
+        g.view.copy_(dev(x))
+        np.testing.assert_array_equal(fs.row_argmax(g.view).cpu().numpy(), oracle.row_argmax(x.f64()))
+        assert_close("sum", host64(fs.row_reduce(g.view, "sum")), oracle.row_reduce(x.f64(), "sum"),
+                     sum_tol(x.f64()), 0)
