@@ -114,11 +114,14 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  *          j > (r mod causal_q_len) + (cols - causal_q_len); masked
  *          elements are not read and are written as +0.  0 = off.
  * Entries whose logit is -inf come out exactly +0; a fully masked row comes
- * out all +0.  One pass over HBM: rows up to FS_SOFTMAX_MAX_COLS columns are
- * held in registers, with a single (max, sum) online combine per row.
+ * out all +0.  Rows up to 16384 columns are held in registers and read from
+ * HBM once, with a single (max, sum) online combine per row; longer rows, up
+ * to FS_SOFTMAX_MAX_COLS columns, are streamed: one pass keeps a running
+ * (max, sum) and a second re-reads x (and mask) to write y, so they move
+ * 2 reads + 1 write per element.
  * scale must be finite; mask values may be any float or -inf.
  */
-#define FS_SOFTMAX_MAX_COLS 65536
+#define FS_SOFTMAX_MAX_COLS 16777216
 FS_API fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t ld_mask,
                          fs_dtype mask_dtype, void* y, int64_t ld_y, int64_t rows,
                          int64_t cols, float scale, int64_t causal_q_len, fs_dtype dtype,
@@ -139,10 +142,13 @@ FS_API fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, i
  * residual_out : or NULL (not stored).
  * gamma, beta  : [cols] of `dtype`, or NULL (1 and 0).
  * y and residual_out may each be x or residual exactly; they may not overlap
- * each other.  eps must be finite and >= 0.  Rows up to
- * FS_LAYERNORM_MAX_COLS columns (held in registers).
+ * each other.  eps must be finite and >= 0.  Rows up to 16384 columns are held
+ * in registers (x and residual read once, statistics in two exact passes over
+ * the registers); longer rows, up to FS_LAYERNORM_MAX_COLS columns, are
+ * streamed: a first pass merges per-chunk (count, mean, M2) statistics, a
+ * second re-reads x and residual and writes residual_out and y.
  */
-#define FS_LAYERNORM_MAX_COLS 65536
+#define FS_LAYERNORM_MAX_COLS 16777216
 FS_API fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residual,
                                 int64_t ld_r, const void* gamma, const void* beta, void* y,
                                 int64_t ld_y, void* residual_out, int64_t ld_ro, int64_t rows,

@@ -6,7 +6,8 @@ as hipBLASLt library calls.
 The native libraries are loaded on first use; a missing or unloadable
 library raises ``NativeLibraryError`` -- there is no CPU fallback.
 """
-from ._native import FusedSubError, GemmError, NativeLibraryError  # noqa: F401
+from ._native import (FS_LAYERNORM_MAX_COLS, FS_SOFTMAX_MAX_COLS, FusedSubError,  # noqa: F401
+                      GemmError, NativeLibraryError)
 from .ops import (as_rows, copy_, gemm, gemm_epilogue_reduce, gemm_strided_batched,  # noqa: F401
                   layernorm_residual, pointwise_chain, rmsnorm_residual, row_argmax, row_reduce,
                   row_softmax)

@@ -31,8 +31,8 @@ ACTS = {"none": 0, "gelu_erf": 1, "sigmoid": 2, "relu": 3}
 REDUCES = {"sum": 0, "mean": 1}
 ROW_OPS = {"sum": 0, "mean": 1, "max": 2}
 FS_ABI_VERSION = 1
-FS_SOFTMAX_MAX_COLS = 65536
-FS_LAYERNORM_MAX_COLS = 65536
+FS_SOFTMAX_MAX_COLS = 16777216
+FS_LAYERNORM_MAX_COLS = 16777216
 
 # every symbol the headers declare
 FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_layernorm_residual",

@@ -188,6 +188,151 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   }
 }
 
+// (count, mean, M2) merged with the pairwise update of Chan, Golub and
+// LeVeque (1979), written so that combine(a, b) and combine(b, a) round
+// identically: the statistics of a streamed row.
+struct MeanM2P {
+  float n, mean, m2;
+  __device__ __forceinline__ static MeanM2P combine(const MeanM2P& a, const MeanM2P& b) {
+    if (a.n == 0.f) return b;
+    if (b.n == 0.f) return a;
+    const float n = a.n + b.n;
+    const float d = b.mean - a.mean;
+    return {n, (a.n * a.mean + b.n * b.mean) / n, (a.m2 + b.m2) + d * d * ((a.n * b.n) / n)};
+  }
+  template <class F> __device__ __forceinline__ static MeanM2P map(const MeanM2P& a, F f) {
+    return {f(a.n), f(a.mean), f(a.m2)};
+  }
+};
+
+// Rows longer than the register-resident capacity: one block of W waves per
+// row streams it twice.  Pass 1 reads x (+ residual) in trips of U vectors
+// per lane and merges each trip's exact two-pass statistics into a running
+// (count, mean, M2) (RMSNorm: a running sum of squares); pass 2 re-reads
+// them, writes residual_out and y.  Writing both in pass 2 keeps in-place
+// outputs (y == x, residual_out == residual) correct.
+template <typename T, bool HAS_RES, bool RMS, int W, bool VEC>
+__global__ __launch_bounds__(64 * W) void layernorm_stream_kernel(
+    const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
+    const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
+    int64_t ld_ro, int64_t rows, int cols, float eps, int trips) {
+  constexpr int kThreads = 64 * W;
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int U = 4;
+  using P = MeanM2P;
+  __shared__ P lds[2][W];
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int clast = cols - V;
+  int parity = 0;
+
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+    const T* xr = x + row * ld_x;
+    const T* rr = HAS_RES ? res + row * ld_r : nullptr;
+    auto trip_h = [&](int t, float (&h)[U * V]) {
+      Raw<T, V> rx[U], rres[HAS_RES ? U : 1];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        const int cl = c0 < cols ? c0 : clast;
+        rx[u].load(xr + cl);
+        if constexpr (HAS_RES) rres[u].load(rr + cl);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float xv[V];
+        rx[u].unpack(xv);
+        if constexpr (HAS_RES) {
+          float rv[V];
+          rres[u].unpack(rv);
+#pragma unroll
+          for (int i = 0; i < V; ++i) xv[i] += rv[i];
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) h[u * V + i] = xv[i];
+      }
+    };
+
+    // pass 1: statistics
+    P run{0.f, 0.f, 0.f};
+    for (int t = 0; t < trips; ++t) {
+      float h[U * V];
+      trip_h(t, h);
+      float n = 0.f, sum = 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool in = ((t * U + u) * kThreads + tid) * V < cols;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          const float v = in ? h[u * V + i] : 0.f;
+          sum = RMS ? fmaf(v, v, sum) : sum + v;
+        }
+        n += in ? float(V) : 0.f;
+      }
+      if constexpr (RMS) {
+        run.m2 += sum;                        // running sum of squares
+      } else {
+        const float mt = n > 0.f ? sum / n : 0.f;
+        float m2 = 0.f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const bool in = ((t * U + u) * kThreads + tid) * V < cols;
+#pragma unroll
+          for (int i = 0; i < V; ++i) {
+            const float d = in ? h[u * V + i] - mt : 0.f;
+            m2 = fmaf(d, d, m2);
+          }
+        }
+        run = P::combine(run, P{n, mt, m2});
+      }
+    }
+    if constexpr (RMS) run.n = 1.f;          // keep the fold from skipping lanes
+    const P st = group_allreduce<W>(run, lds[parity], wave, lane);
+    parity ^= 1;
+    const float inv_cols = 1.f / float(cols);
+    const float mean = RMS ? 0.f : st.mean;
+    // RMS: every lane carried mean 0, so the fold added the sums of squares
+    const float rstd = rsqrtf(st.m2 * inv_cols + eps);
+
+    // pass 2: residual_out and y
+    T* yr = y + row * ld_y;
+    T* ro = res_out ? res_out + row * ld_ro : nullptr;
+    for (int t = 0; t < trips; ++t) {
+      float h[U * V];
+      trip_h(t, h);
+      Raw<T, V> rg[U], rb[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        const int cl = c0 < cols ? c0 : clast;
+        if (gamma) rg[u].template load<false>(gamma + cl);
+        if (beta) rb[u].template load<false>(beta + cl);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        if (c0 < cols) {
+          if (ro) stv<T, V>(ro + c0, h + u * V);
+          float gv[V], bv[V], o[V];
+          if (gamma) rg[u].unpack(gv);
+          else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) gv[i] = 1.f;
+          }
+          if (beta) rb[u].unpack(bv);
+          else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) bv[i] = 0.f;
+          }
+#pragma unroll
+          for (int i = 0; i < V; ++i) o[i] = fmaf((h[u * V + i] - mean) * rstd, gv[i], bv[i]);
+          stv<T, V>(yr + c0, o);
+        }
+      }
+    }
+  }
+}
+
 // rows batched per group: enough that a one-wave group handles about
 // FS_LN_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
@@ -232,10 +377,19 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   FS_LN(8, 8, 1, 4)
   FS_LN(8, 16, 1, 4)
   FS_LN(8, 32, 1, 4)
-  FS_LN(8, 64, 1, 4)
-  FS_LN(16, 64, 1, 2)
 #undef FS_LN
-  return hipErrorInvalidValue;   // unreachable: the host checks cols
+  // longer rows: streamed, one 8-wave block per row
+  {
+    constexpr int W = 8, U = 4;
+    const int trips = int((c + int64_t(64) * W * V * U - 1) / (int64_t(64) * W * V * U));
+    int64_t grid = a.rows < int64_t(cus) * 4 ? a.rows : int64_t(cus) * 4;
+    hipLaunchKernelGGL((layernorm_stream_kernel<T, HAS_RES, RMS, W, VEC>), dim3(unsigned(grid)),
+                       dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
+                       static_cast<const T*>(a.res), a.ld_r, static_cast<const T*>(a.gamma),
+                       static_cast<const T*>(a.beta), static_cast<T*>(a.y), a.ld_y,
+                       static_cast<T*>(a.res_out), a.ld_ro, a.rows, int(a.cols), a.eps, trips);
+    return hipGetLastError();
+  }
 }
 
 template <typename T, bool RMS>

@@ -173,6 +173,100 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   }
 }
 
+// Rows longer than the register-resident capacity: one block of W waves per
+// row streams the row twice.  Pass 1 keeps a running online (m', d) per lane
+// (one rescale exp2 per trip of U vectors) and combines the lanes once; pass 2
+// re-reads the row and writes 2^(a*log2e - M) / D.  Two HBM reads of x (the
+// second is often served from L2 or the Infinity Cache) and one write.
+template <typename T, typename MT, bool HAS_MASK, int W, bool VEC>
+__global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
+    const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
+    int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trips) {
+  constexpr int kThreads = 64 * W;
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int U = 4;
+  __shared__ MaxSumP lds[2][W];
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  int parity = 0;
+
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+    const T* xr = x + row * ld_x;
+    const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
+    const int64_t limit = q_len > 0 ? (row % q_len) + (cols - q_len) : int64_t(cols) - 1;
+    const int lim = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+    const int limv = lim < 0 ? 0 : (lim / V) * V;
+
+    // logits of one trip: U vectors per lane, -inf past lim
+    auto trip_logits = [&](int t, float (&a)[U * V]) {
+      Raw<T, V> rx[U];
+      Raw<MT, V> rm[HAS_MASK ? U : 1];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        const int cl = c0 <= lim ? c0 : limv;
+        rx[u].load(xr + cl);
+        if constexpr (HAS_MASK) rm[u].load(mr + cl);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        float xv[V];
+        rx[u].unpack(xv);
+        if constexpr (HAS_MASK) {
+          float mv[V];
+          rm[u].unpack(mv);
+#pragma unroll
+          for (int i = 0; i < V; ++i) xv[i] = fmaf(xv[i], scale, mv[i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < V; ++i) xv[i] *= scale;
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) a[u * V + i] = (c0 + i <= lim) ? xv[i] : -INFINITY;
+      }
+    };
+
+    // pass 1: running (m', d) per lane
+    float mrun = -INFINITY, drun = 0.f;
+    for (int t = 0; t < trips; ++t) {
+      float a[U * V];
+      trip_logits(t, a);
+      float tm = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < U * V; ++i) tm = fmaxf(tm, a[i]);
+      const float mnew = fmaxf(mrun, tm == -INFINITY ? -INFINITY : tm * kLog2e);
+      const float msafe = mnew == -INFINITY ? 0.f : mnew;
+      float dt = 0.f;
+#pragma unroll
+      for (int i = 0; i < U * V; ++i) dt += __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
+      drun = fmaf(drun, __builtin_amdgcn_exp2f(mrun - msafe), dt);   // 2^-inf = 0
+      mrun = mnew;
+    }
+    const MaxSumP p = group_allreduce<W>(MaxSumP{mrun, drun}, lds[parity], wave, lane);
+    parity ^= 1;
+    const bool empty = p.m == -INFINITY;
+    const float M = empty ? 0.f : p.m;
+    const float inv_d = empty ? 0.f : 1.f / p.d;
+
+    // pass 2: outputs
+    T* yr = y + row * ld_y;
+    for (int t = 0; t < trips; ++t) {
+      float a[U * V];
+      trip_logits(t, a);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        float o[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+          o[i] = __builtin_amdgcn_exp2f(fmaf(a[u * V + i], kLog2e, -M)) * inv_d;
+        if (c0 < cols) stv<T, V>(yr + c0, o);
+      }
+    }
+  }
+}
+
 // rows batched per group: enough that a one-wave group handles about
 // FS_SM_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
@@ -196,7 +290,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
                        a.scale, a.causal_q_len);
     return hipGetLastError();
   };
-// Variant ladder, in order: the first rung with at least min_w waves per row
+  // Variant ladder, in order: the first rung with at least min_w waves per row
   // and a row capacity 64 * W * EPT >= cols is launched.
   const int min_w = c >= FS_SM_SPLIT_COLS ? FS_SM_MIN_WAVES : 1;
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
@@ -218,10 +312,18 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   FS_SM(8, 8, 1, 4)
   FS_SM(8, 16, 1, 4)
   FS_SM(8, 32, 1, 4)
-  FS_SM(8, 64, 1, 4)
-  FS_SM(16, 64, 1, 2)
 #undef FS_SM
-  return hipErrorInvalidValue;   // unreachable: the host checks cols
+  // longer rows: streamed, one 8-wave block per row
+  {
+    constexpr int W = 8, U = 4;
+    const int trips = int((c + int64_t(64) * W * V * U - 1) / (int64_t(64) * W * V * U));
+    int64_t grid = a.rows < int64_t(cus) * 4 ? a.rows : int64_t(cus) * 4;
+    hipLaunchKernelGGL((softmax_stream_kernel<T, MT, HAS_MASK, W, VEC>), dim3(unsigned(grid)),
+                       dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
+                       static_cast<const MT*>(a.mask), a.ld_mask, static_cast<T*>(a.y), a.ld_y,
+                       a.rows, int(a.cols), a.scale, a.causal_q_len, trips);
+    return hipGetLastError();
+  }
 }
 
 template <typename T, typename MT>

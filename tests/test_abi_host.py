@@ -102,7 +102,7 @@ def sm(**kw):
 
 def test_softmax_validation():
     assert sm(x=NULL) == 1
-    assert sm(cols=N.FS_SOFTMAX_MAX_COLS + 1, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert sm(cols=N.FS_SOFTMAX_MAX_COLS + 1, ld_x=1 << 25, ld_y=1 << 25) == 2
     assert sm(rows=-1) == 2
     assert sm(ld_x=127) == 3
     assert sm(mask=C, ld_mask=100) == 3
@@ -126,7 +126,7 @@ def ln(**kw):
 
 def test_layernorm_validation():
     assert ln(y=NULL) == 1
-    assert ln(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert ln(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 25, ld_y=1 << 25) == 2
     assert ln(ld_y=255) == 3
     assert ln(residual=C, ld_r=1) == 3
     assert ln(residual_out=C, ld_ro=1) == 3
@@ -148,7 +148,7 @@ def rms(**kw):
 
 def test_rmsnorm_validation():
     assert rms(x=NULL) == 1
-    assert rms(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 20, ld_y=1 << 20) == 2
+    assert rms(cols=N.FS_LAYERNORM_MAX_COLS + 8, ld_x=1 << 25, ld_y=1 << 25) == 2
     assert rms(ld_x=7) == 3
     assert rms(dtype=5) == 4
     assert rms(eps=float("nan")) == 6
