@@ -88,6 +88,26 @@ class TransformerBlock:
             ops.gemm_strided_batched(p[b].data_ptr(), seq, seq * seq, vbase, 3 * H, dh, False,
                                      obase, H, dh, seq, dh, seq, NH, device=qkv.device)
 
+    # --- the five sub-kernels (the generated part of the compiled model) --------
+    def layernorm1(self, x2, buf):
+        p = self.p
+        ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
+
+    def softmax(self, buf, seq):
+        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
+                        out=buf["probs"])
+
+    def layernorm2_residual(self, x2, buf):
+        p = self.p
+        ops.layernorm_residual(buf["att"], x2, p["ln2_gamma"], p["ln2_beta"], self.eps,
+                               out=buf["m"], residual_out=buf["h1"])
+
+    def bias_gelu(self, buf):
+        ops.pointwise_chain(buf["u"], self.p["b_1"], None, 1.0, "gelu_erf", out=buf["g"])
+
+    def residual_add(self, buf):
+        ops.pointwise_chain(buf["d"], None, buf["h1"], 1.0, "none", out=buf["out"])
+
     def forward(self, x: torch.Tensor, buf: Optional[Dict[str, torch.Tensor]] = None):
         """x [batch, seq, hidden] bf16 -> dict of every intermediate; 'out' is
         [batch*seq, hidden]."""
@@ -98,30 +118,25 @@ class TransformerBlock:
         if buf is None:
             buf = self.alloc(batch, seq, x.device)
         x2 = x.reshape(batch * seq, H)
-        ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
+        self.layernorm1(x2, buf)
         ops.gemm(buf["a"], p["w_qkv"], bias=p["b_qkv"], out=buf["qkv"])
         self.attention_gemms_qk(buf, batch, seq)
-        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
-                        out=buf["probs"])
+        self.softmax(buf, seq)
         self.attention_gemms_pv(buf, batch, seq)
         ops.gemm(buf["o"], p["w_o"], bias=p["b_o"], out=buf["att"])
-        ops.layernorm_residual(buf["att"], x2, p["ln2_gamma"], p["ln2_beta"], self.eps,
-                               out=buf["m"], residual_out=buf["h1"])
+        self.layernorm2_residual(x2, buf)
         ops.gemm(buf["m"], p["w_1"], out=buf["u"])
-        ops.pointwise_chain(buf["u"], p["b_1"], None, 1.0, "gelu_erf", out=buf["g"])
+        self.bias_gelu(buf)
         ops.gemm(buf["g"], p["w_2"], bias=p["b_2"], out=buf["d"])
-        ops.pointwise_chain(buf["d"], None, buf["h1"], 1.0, "none", out=buf["out"])
+        self.residual_add(buf)
         return buf
 
     # the five sub-kernel launches alone, on resident inputs (for timing)
     def subkernels(self, x: torch.Tensor, buf: Dict[str, torch.Tensor]):
         batch, seq, H = x.shape
-        p = self.p
         x2 = x.reshape(batch * seq, H)
-        ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
-        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
-                        out=buf["probs"])
-        ops.layernorm_residual(buf["att"], x2, p["ln2_gamma"], p["ln2_beta"], self.eps,
-                               out=buf["m"], residual_out=buf["h1"])
-        ops.pointwise_chain(buf["u"], p["b_1"], None, 1.0, "gelu_erf", out=buf["g"])
-        ops.pointwise_chain(buf["d"], None, buf["h1"], 1.0, "none", out=buf["out"])
+        self.layernorm1(x2, buf)
+        self.softmax(buf, seq)
+        self.layernorm2_residual(x2, buf)
+        self.bias_gelu(buf)
+        self.residual_add(buf)

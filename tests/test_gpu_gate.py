@@ -1,0 +1,61 @@
+"""GPU checks of the model-level performance gate (Eq. 5): the baseline
+models compute the same block as the float64 oracle, and the block stitched
+with libfusedsub passes the gate against the block with PyTorch eager
+sub-kernels at the full block shape [32, 512, 1024]."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+from gpu_util import TOL, announce, assert_close, dev, host64
+from paper_2609_30059_amd import gate
+from paper_2609_30059_amd.block import PARAM_NAMES
+
+pytestmark = pytest.mark.gpu
+
+SMALL = dict(batch=3, seq=64, hidden=256, heads=4, mlp=1024)
+
+
+def _oracle_out(d, seqs):
+    p64 = {k: d[k].f64() for k in PARAM_NAMES}
+    return oracle.block_forward(d["x"].f64(), p64, d["heads"], d["eps"], sequences=seqs,
+                                keep=("out", "h1", "d"))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_baseline_models_match_oracle(seed):
+    d = fd.block_inputs(seed, **SMALL)
+    announce("gate baselines", seed)
+    params = {k: dev(d[k]) for k in PARAM_NAMES}
+    x = dev(d["x"])
+    blk = gate._baseline_block_class()(params, heads=d["heads"], eps=d["eps"])
+    buf = blk.forward(x)
+    eager = gate.eager_block(params, x, d["heads"], d["eps"])
+    torch.cuda.synchronize()
+    ref = _oracle_out(d, [0, 1, 2])
+    atol, rtol = TOL["bf16"]
+    # residual adds in bf16 may cancel: one bf16 rounding of each operand
+    a = atol + 2.0 ** -8 * (np.abs(ref["h1"]) + np.abs(ref["d"]))
+    for name, out in (("eager sub-kernels", buf["out"]), ("eager block", eager)):
+        got = host64(out).reshape(3, SMALL["seq"], SMALL["hidden"])
+        assert_close(name, got, ref["out"], a, rtol)
+
+
+def test_fused_block_passes_the_gate_at_full_shape():
+    announce("gate full shape")
+    t = {v: gate.measure(v, seed=0, warmup_ms=10.0, rep_ms=60.0)
+         for v in ("fused", "eager_subkernels")}
+    for v in t.values():
+        assert v["out_finite"]
+    # the two models compute the same block: their outputs agree in mean size
+    assert abs(t["fused"]["out_abs_mean"] / t["eager_subkernels"]["out_abs_mean"] - 1) < 1e-2
+    r = gate.report(t)
+    print("gate", r, flush=True)
+    assert r["pass"], r
+
+
+def test_isolated_measurement_round_trip():
+    announce("gate isolated")
+    r = gate.run_isolated("fused", 0, 5.0, 20.0, timeout_s=300)
+    assert r["variant"] == "fused" and r["median_ms"] > 0 and r["out_finite"]
