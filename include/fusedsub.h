@@ -219,6 +219,32 @@ FS_API fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c
                                   hipStream_t stream);
 
 /*
+ * Batched strided 2-D copy: the layout transforms a compiled graph places
+ * between library GEMMs (the .contiguous() copies that transposed or
+ * permuted strides force, Section 4.4, Gate 4), e.g. splitting a token-major
+ * [tokens, 3 * hidden] QKV projection into head-major [3 * heads, tokens,
+ * head_dim] operands for one strided-batched attention GEMM, and merging
+ * head-major attention output back into [tokens, hidden].
+ *
+ *   dst[b * stride_dst + r * ld_dst + c] = src[b * stride_src + r * ld_src + c]
+ *   for b < batch, r < rows, c < cols
+ *
+ * Strides and leading dimensions are in elements of `dtype` (only the size
+ * matters: bits are copied unchanged, NaN payloads included).
+ * ld_src, ld_dst >= cols; stride_src, stride_dst >= 0 (0 broadcasts the
+ * source).  batch * cols < 2^30.  Destination elements must be distinct:
+ * either stride_dst >= (rows - 1) * ld_dst + cols (batches one after another)
+ * or stride_dst >= cols and ld_dst >= (batch - 1) * stride_dst + cols
+ * (batches interleaved within each row), else FS_ERR_BAD_STRIDE.  The spans
+ * of src and dst must not overlap (FS_ERR_ALIASING).  16-byte units are used
+ * when every address, stride and row length is a multiple of 16 bytes.
+ */
+FS_API fs_status fs_copy_strided(const void* src, int64_t ld_src, int64_t stride_src, void* dst,
+                                 int64_t ld_dst, int64_t stride_dst, int64_t rows,
+                                 int64_t cols, int64_t batch, fs_dtype dtype,
+                                 hipStream_t stream);
+
+/*
  * Calibration utility (not a sub-kernel): copies `bytes` bytes from src to
  * dst with 128-bit loads and stores when both are 16-byte aligned and bytes
  * is a multiple of 16, else byte by byte.  Used to measure the achievable

@@ -12,13 +12,13 @@ printed reference values (``tests/golden/``).
 from .subkernels import (ACTS, apply_act, causal_mask, gelu_erf, gemm_epilogue_reduce,
                          layernorm_residual, pointwise_chain, relu, residual_store_bf16,
                          rmsnorm_residual, round_to_bf16, row_argmax, row_reduce, row_softmax,
-                         sigmoid)
+                         sigmoid, strided_copy)
 from .block import block_forward, block_forward_sequence, STAGES
 
 __all__ = [
     "ACTS", "apply_act", "causal_mask", "gelu_erf", "gemm_epilogue_reduce",
     "layernorm_residual", "pointwise_chain", "relu", "residual_store_bf16",
     "rmsnorm_residual", "row_reduce", "row_argmax",
-    "round_to_bf16", "row_softmax", "sigmoid", "block_forward",
+    "round_to_bf16", "row_softmax", "sigmoid", "strided_copy", "block_forward",
     "block_forward_sequence", "STAGES",
 ]

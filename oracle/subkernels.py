@@ -272,3 +272,23 @@ def row_argmax(x):
         best = row.max()
         out[i] = int(np.flatnonzero(row == best)[0])   # lowest index of the maximum
     return out
+
+
+# ---------------------------------------------------------------------------
+# layout transform
+# ---------------------------------------------------------------------------
+def strided_copy(src_flat, dst_flat, rows: int, cols: int, batch: int, ld_src: int,
+                 stride_src: int, ld_dst: int, stride_dst: int):
+    """The copy a compiled graph inserts when permuted strides must become
+    contiguous (Section 4.4, Gate 4): returns a copy of the flat destination
+    with dst[b*stride_dst + r*ld_dst + c] = src[b*stride_src + r*ld_src + c]
+    for every b < batch, r < rows, c < cols; other destination elements keep
+    their values.  Works on any 1-D array (values or raw bit patterns)."""
+    src = np.asarray(src_flat).reshape(-1)
+    out = np.array(dst_flat, copy=True).reshape(-1)
+    for b in range(batch):
+        for r in range(rows):
+            s0 = b * stride_src + r * ld_src
+            d0 = b * stride_dst + r * ld_dst
+            out[d0:d0 + cols] = src[s0:s0 + cols]
+    return out

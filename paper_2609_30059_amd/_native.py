@@ -37,7 +37,8 @@ FS_LAYERNORM_MAX_COLS = 16777216
 # every symbol the headers declare
 FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_layernorm_residual",
                     "fs_rmsnorm_residual", "fs_row_reduce", "fs_row_argmax",
-                    "fs_gemm_epilogue_reduce", "fs_copy", "fs_status_string",
+                    "fs_gemm_epilogue_reduce", "fs_copy_strided", "fs_copy",
+                    "fs_status_string",
                     "fs_last_error_message", "fs_abi_version")
 FSGEMM_SYMBOLS = ("fsg_gemm_bf16", "fsg_last_error_message")
 
@@ -66,6 +67,7 @@ _SIGS = {
     "fs_row_reduce": [_P, _I64, _I, _I, _P, _I64, _I64, _P],
     "fs_row_argmax": [_P, _I64, _I, _P, _I64, _I64, _P],
     "fs_gemm_epilogue_reduce": [_P, _I64, _I, _P, _I, _P, _I, _I, _P, _I64, _I64, _P],
+    "fs_copy_strided": [_P, _I64, _I64, _P, _I64, _I64, _I64, _I64, _I64, _I, _P],
     "fs_copy": [_P, _P, _I64, _P],
     "fs_status_string": [_I],
     "fs_last_error_message": [],
@@ -165,6 +167,12 @@ def fs_gemm_epilogue_reduce(c, ld_c, c_dtype, bias, bias_dtype, col_scale, act, 
                             rows, cols, stream):
     return fusedsub().fs_gemm_epilogue_reduce(c, ld_c, c_dtype, bias, bias_dtype, col_scale, act,
                                               reduce, row_out, rows, cols, stream)
+
+
+def fs_copy_strided(src, ld_src, stride_src, dst, ld_dst, stride_dst, rows, cols, batch, dtype,
+                    stream):
+    return fusedsub().fs_copy_strided(src, ld_src, stride_src, dst, ld_dst, stride_dst, rows, cols,
+                                      batch, dtype, stream)
 
 
 def fs_copy(src, dst, nbytes, stream):

@@ -8,9 +8,11 @@ block on MI355X:
 
     a    = layernorm(x)                                   fs_layernorm_residual
     qkv  = a @ Wqkv + bqkv                                hipBLASLt (BIAS epilogue)
-    S    = q k^T per (sequence, head), head views of qkv  hipBLASLt strided batched
+    q, k, v head-major  [3 * heads, tokens, dh]           fs_copy_strided
+    S    = q k^T for all (head, sequence) pairs           hipBLASLt strided batched
     P    = softmax(S / sqrt(dh), causal)                  fs_row_softmax
-    o    = P v  written head-interleaved into [tokens, H] hipBLASLt strided batched
+    o_h  = P v for all pairs                              hipBLASLt strided batched
+    o    = o_h merged to token-major [tokens, H]          fs_copy_strided
     att  = o @ Wo + bo                                    hipBLASLt (BIAS epilogue)
     m, h1 = layernorm(att + x), att + x                   fs_layernorm_residual
     u    = m @ W1                                         hipBLASLt
@@ -18,8 +20,9 @@ block on MI355X:
     d    = g @ W2 + b2                                    hipBLASLt (BIAS epilogue)
     out  = d + h1                                         fs_pointwise_chain
 
-The attention GEMMs read q, k and v as strided views of qkv (no permute
-copies) and write o directly in token-major layout.
+The head split and merge cost one pass over qkv and one over o; in exchange
+each attention GEMM is a single launch over heads * batch pairs instead of
+one launch per sequence.
 """
 from __future__ import annotations
 
@@ -52,41 +55,60 @@ class TransformerBlock:
         self.dh = self.hidden // heads
 
     def alloc(self, batch: int, seq: int, device) -> Dict[str, torch.Tensor]:
-        """Activation buffers for one forward pass."""
+        """Activation buffers for one forward pass.  Attention operands are
+        head-major: qkv_h [3 * heads, tokens, dh], scores and probs
+        [heads, batch, seq, seq], o_h [heads, tokens, dh]."""
         t, H, F, NH = batch * seq, self.hidden, self.mlp, self.heads
         e = dict(dtype=torch.bfloat16, device=device)
         return {
             "a": torch.empty(t, H, **e), "qkv": torch.empty(t, 3 * H, **e),
-            "scores": torch.empty(batch, NH, seq, seq, **e),
-            "probs": torch.empty(batch, NH, seq, seq, **e),
+            "qkv_h": torch.empty(3 * NH, t, self.dh, **e),
+            "scores": torch.empty(NH, batch, seq, seq, **e),
+            "probs": torch.empty(NH, batch, seq, seq, **e),
+            "o_h": torch.empty(NH, t, self.dh, **e),
             "o": torch.empty(t, H, **e), "att": torch.empty(t, H, **e),
             "h1": torch.empty(t, H, **e), "m": torch.empty(t, H, **e),
             "u": torch.empty(t, F, **e), "g": torch.empty(t, F, **e),
             "d": torch.empty(t, H, **e), "out": torch.empty(t, H, **e),
         }
 
-    # --- stages ----------------------------------------------------------------
+    # --- attention: head split, two strided-batched GEMMs, head merge ---------
+    # Batch index i = head * batch + sequence.  In head-major storage the
+    # operands of pair i start i * seq * dh elements apart, so each attention
+    # GEMM is one launch over all heads * batch pairs.
+    def split_heads(self, buf):
+        qkv = buf["qkv"]
+        t = qkv.shape[0]
+        ops.copy_strided(buf["qkv_h"], qkv, rows=t, cols=self.dh, batch=3 * self.heads,
+                         ld_src=3 * self.hidden, stride_src=self.dh, ld_dst=self.dh,
+                         stride_dst=t * self.dh)
+
     def attention_gemms_qk(self, buf, batch, seq):
-        H, NH, dh = self.hidden, self.heads, self.dh
-        qkv, s = buf["qkv"], buf["scores"]
-        es = qkv.element_size()
-        for b in range(batch):
-            base = qkv.data_ptr() + b * seq * 3 * H * es
-            # S[b, h] = q_bh @ k_bh^T: q_bh = qkv[rows of b, h*dh:(h+1)*dh], k_bh at +H
-            ops.gemm_strided_batched(base, 3 * H, dh, base + H * es, 3 * H, dh, True,
-                                     s[b].data_ptr(), seq, seq * seq, seq, seq, dh, NH,
-                                     device=qkv.device)
+        NH, dh = self.heads, self.dh
+        qh, s = buf["qkv_h"], buf["scores"]
+        es = qh.element_size()
+        head = qh.shape[1] * dh * es                       # bytes of one [tokens, dh] slab
+        q = qh.data_ptr()
+        k = q + NH * head
+        # S_i = q_i @ k_i^T
+        ops.gemm_strided_batched(q, dh, seq * dh, k, dh, seq * dh, True, s.data_ptr(), seq,
+                                 seq * seq, seq, seq, dh, NH * batch, device=qh.device)
 
     def attention_gemms_pv(self, buf, batch, seq):
-        H, NH, dh = self.hidden, self.heads, self.dh
-        qkv, p, o = buf["qkv"], buf["probs"], buf["o"]
-        es = qkv.element_size()
-        for b in range(batch):
-            vbase = qkv.data_ptr() + (b * seq * 3 * H + 2 * H) * es
-            obase = o.data_ptr() + b * seq * H * es
-            # o[rows of b, h*dh:(h+1)*dh] = P[b, h] @ v_bh
-            ops.gemm_strided_batched(p[b].data_ptr(), seq, seq * seq, vbase, 3 * H, dh, False,
-                                     obase, H, dh, seq, dh, seq, NH, device=qkv.device)
+        NH, dh = self.heads, self.dh
+        qh, p, oh = buf["qkv_h"], buf["probs"], buf["o_h"]
+        es = qh.element_size()
+        v = qh.data_ptr() + 2 * NH * qh.shape[1] * dh * es
+        # o_i = P_i @ v_i
+        ops.gemm_strided_batched(p.data_ptr(), seq, seq * seq, v, dh, seq * dh, False,
+                                 oh.data_ptr(), dh, seq * dh, seq, dh, seq, NH * batch,
+                                 device=qh.device)
+
+    def merge_heads(self, buf):
+        oh = buf["o_h"]
+        t = oh.shape[1]
+        ops.copy_strided(buf["o"], oh, rows=t, cols=self.dh, batch=self.heads, ld_src=self.dh,
+                         stride_src=t * self.dh, ld_dst=self.hidden, stride_dst=self.dh)
 
     # --- the five sub-kernels (the generated part of the compiled model) --------
     def layernorm1(self, x2, buf):
@@ -120,9 +142,11 @@ class TransformerBlock:
         x2 = x.reshape(batch * seq, H)
         self.layernorm1(x2, buf)
         ops.gemm(buf["a"], p["w_qkv"], bias=p["b_qkv"], out=buf["qkv"])
+        self.split_heads(buf)
         self.attention_gemms_qk(buf, batch, seq)
         self.softmax(buf, seq)
         self.attention_gemms_pv(buf, batch, seq)
+        self.merge_heads(buf)
         ops.gemm(buf["o"], p["w_o"], bias=p["b_o"], out=buf["att"])
         self.layernorm2_residual(x2, buf)
         ops.gemm(buf["m"], p["w_1"], out=buf["u"])

@@ -1,6 +1,7 @@
 // C ABI of libfusedsub: argument validation (host only, before any HIP call),
 // choice of the 16-byte vector path, aliasing checks, and dispatch to the
 // kernels.  The contract of every entry point is documented in fusedsub.h.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdarg>
@@ -364,6 +365,48 @@ fs_status fs_copy(const void* src, void* dst, int64_t bytes, hipStream_t stream)
   if (st != FS_OK) return st;
   hipError_t e = fs::launch_copy(src, dst, bytes, cus, stream);
   return e == hipSuccess ? FS_OK : hip_fail(e, "copy launch");
+}
+
+fs_status fs_copy_strided(const void* src, int64_t ld_src, int64_t stride_src, void* dst,
+                          int64_t ld_dst, int64_t stride_dst, int64_t rows, int64_t cols,
+                          int64_t batch, fs_dtype dtype, hipStream_t stream) {
+  clear_msg();
+  if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
+  if (rows < 0 || cols < 0 || batch < 0)
+    return fail(FS_ERR_BAD_SHAPE, "rows=%lld cols=%lld batch=%lld must be >= 0",
+                (long long)rows, (long long)cols, (long long)batch);
+  if (batch > 0 && cols > ((int64_t(1) << 30) - 1) / batch)
+    return fail(FS_ERR_BAD_SHAPE, "batch * cols must be < 2^30");
+  if (stride_src < 0 || stride_dst < 0)
+    return fail(FS_ERR_BAD_STRIDE, "batch strides must be >= 0");
+  fs_status st;
+  if ((st = check_ld("ld_src", ld_src, rows, cols)) != FS_OK) return st;
+  if ((st = check_ld("ld_dst", ld_dst, rows, cols)) != FS_OK) return st;
+  if (rows == 0 || cols == 0 || batch == 0) return FS_OK;
+  // the last element offset of each side must fit in int64 bytes
+  for (int64_t sb : {stride_src, stride_dst})
+    if (batch > 1 && sb > 0 && (batch - 1) > (INT64_MAX / 8 - (rows - 1) * std::max(ld_src, ld_dst) - cols) / sb)
+      return fail(FS_ERR_BAD_SHAPE, "batch * stride overflows");
+  // every destination element distinct: batches one after another, or
+  // interleaved within each destination row
+  const bool outer = stride_dst >= (rows - 1) * ld_dst + cols;
+  const bool inner = stride_dst >= cols && ld_dst >= (batch - 1) * stride_dst + cols;
+  if (batch > 1 && !outer && !inner)
+    return fail(FS_ERR_BAD_STRIDE, "destination batches overlap each other");
+  if (!src || !dst) return fail(FS_ERR_NULL_POINTER, "src and dst are required");
+  const int es = elem_size(dtype);
+  if (!aligned(src, es) || !aligned(dst, es))
+    return fail(FS_ERR_BAD_ARGUMENT, "pointers must be aligned to the element size");
+  auto span = [&](const void* p, int64_t ld, int64_t sb) {
+    return vec_extent(p, (batch - 1) * sb + (rows - 1) * ld + cols, es);
+  };
+  if (overlap(span(src, ld_src, stride_src), span(dst, ld_dst, stride_dst)))
+    return fail(FS_ERR_ALIASING, "the spans of src and dst overlap");
+  int cus = 0;
+  if ((st = device_cus(&cus)) != FS_OK) return st;
+  fs::CopyStridedArgs a{src, ld_src, stride_src, dst, ld_dst, stride_dst, rows, cols, batch, es};
+  hipError_t e = fs::launch_copy_strided(a, cus, stream);
+  return e == hipSuccess ? FS_OK : hip_fail(e, "strided copy launch");
 }
 
 }  // extern "C"

@@ -1,6 +1,9 @@
 // Calibration copy: the achievable HBM bandwidth of a plain streaming kernel
 // on this device (16-byte loads and stores, grid-stride), and the reference
-// against which hardware byte counters are scaled.
+// against which hardware byte counters are scaled.  Also the batched strided
+// copy that moves activations between token-major and head-major layouts.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -9,6 +12,15 @@
 #endif
 #ifndef FS_COPY_BLOCKS_PER_CU
 #define FS_COPY_BLOCKS_PER_CU 64
+#endif
+#ifndef FS_STRIDED_UNROLL
+#define FS_STRIDED_UNROLL 4
+#endif
+#ifndef FS_STRIDED_TILE_UNITS
+#define FS_STRIDED_TILE_UNITS 4096
+#endif
+#ifndef FS_STRIDED_BLOCKS_PER_CU
+#define FS_STRIDED_BLOCKS_PER_CU 8
 #endif
 
 namespace fs {
@@ -35,6 +47,44 @@ __global__ __launch_bounds__(256) void copy8_kernel(const uint8_t* __restrict__ 
     dst[i] = src[i];
 }
 
+
+// Batched strided 2-D copy (a layout transform such as a head split or
+// merge): dst[b, r, c] = src[b, r, c].  Work items are ordered (row, batch,
+// unit) with the unit (16 bytes, or one element) fastest, so the items of one
+// row of a head split read one contiguous source row and write whole 128-byte
+// segments.  A block walks tiles of kRB rows; its loads for FS_STRIDED_UNROLL
+// items are issued before their stores (indices past the tile are clamped
+// onto its last item and not stored).
+template <typename U>
+__global__ __launch_bounds__(256) void copy_strided_kernel(
+    const U* __restrict__ src, int64_t ld_s, int64_t st_s, U* __restrict__ dst, int64_t ld_d,
+    int64_t st_d, int64_t rows, int upr, int per_row, int rb) {
+  constexpr int UN = FS_STRIDED_UNROLL;
+  for (int64_t r0 = int64_t(blockIdx.x) * rb; r0 < rows; r0 += int64_t(gridDim.x) * rb) {
+    const int nr = int(rows - r0 < rb ? rows - r0 : rb);
+    const int n = nr * per_row;
+    for (int j0 = threadIdx.x; j0 < n; j0 += 256 * UN) {
+      U v[UN];
+      int64_t di[UN];
+#pragma unroll
+      for (int u = 0; u < UN; ++u) {
+        int j = j0 + u * 256;
+        j = j < n ? j : n - 1;
+        const int rr = j / per_row;
+        const int rem = j - rr * per_row;
+        const int b = rem / upr;
+        const int c = rem - b * upr;
+        const int64_t r = r0 + rr;
+        v[u] = src[b * st_s + r * ld_s + c];
+        di[u] = b * st_d + r * ld_d + c;
+      }
+#pragma unroll
+      for (int u = 0; u < UN; ++u)
+        if (j0 + u * 256 < n) dst[di[u]] = v[u];
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipStream_t s) {
@@ -52,6 +102,36 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipSt
     hipLaunchKernelGGL(copy8_kernel, dim3(unsigned(grid)), dim3(256), 0, s,
                        static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), n);
   return hipGetLastError();
+}
+
+hipError_t launch_copy_strided(const CopyStridedArgs& a, int cus, hipStream_t s) {
+  // units: 16-byte vectors when every address, stride and row is a multiple
+  // of 16 bytes, else single elements
+  const int es = a.es;
+  const bool vec = (reinterpret_cast<uintptr_t>(a.src) % 16 == 0) &&
+                   (reinterpret_cast<uintptr_t>(a.dst) % 16 == 0) && (a.cols * es) % 16 == 0 &&
+                   (a.ld_src * es) % 16 == 0 && (a.ld_dst * es) % 16 == 0 &&
+                   (a.stride_src * es) % 16 == 0 && (a.stride_dst * es) % 16 == 0;
+  const int ue = vec ? 16 : es;                      // bytes per unit
+  const int upr = int(a.cols * es / ue);
+  const int per_row = int(a.batch) * upr;
+  int rb = FS_STRIDED_TILE_UNITS / per_row;
+  if (rb < 1) rb = 1;
+  int64_t grid = (a.rows + rb - 1) / rb;
+  const int64_t cap = int64_t(cus) * FS_STRIDED_BLOCKS_PER_CU;
+  if (grid > cap) grid = cap;
+  auto go = [&](auto* tag) {
+    using U = std::remove_pointer_t<decltype(tag)>;
+    const int64_t k = ue / es;                       // elements per unit
+    hipLaunchKernelGGL(copy_strided_kernel<U>, dim3(unsigned(grid)), dim3(256), 0, s,
+                       static_cast<const U*>(a.src), a.ld_src / k, a.stride_src / k,
+                       static_cast<U*>(a.dst), a.ld_dst / k, a.stride_dst / k, a.rows, upr,
+                       per_row, rb);
+    return hipGetLastError();
+  };
+  if (vec) return go(static_cast<u32x4*>(nullptr));
+  if (es == 4) return go(static_cast<uint32_t*>(nullptr));
+  return go(static_cast<uint16_t*>(nullptr));
 }
 
 }  // namespace fs

@@ -62,6 +62,14 @@ hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs& a, int cus, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipStream_t s);
 
+struct CopyStridedArgs {
+  const void* src; int64_t ld_src, stride_src;
+  void* dst; int64_t ld_dst, stride_dst;
+  int64_t rows, cols, batch;   // batch * cols < 2^30, rows * ld within int64
+  int es;                      // element size in bytes (2 or 4)
+};
+hipError_t launch_copy_strided(const CopyStridedArgs& a, int cus, hipStream_t s);
+
 struct ReduceArgs {
   const void* x; int64_t ld_x; fs_dtype dtype;
   fs_row_op op;

@@ -213,6 +213,26 @@ def gemm_epilogue_reduce(c: torch.Tensor, bias: Optional[torch.Tensor] = None,
     return out
 
 
+def copy_strided(dst: torch.Tensor, src: torch.Tensor, rows: int, cols: int, batch: int,
+                 ld_src: int, stride_src: int, ld_dst: int, stride_dst: int) -> torch.Tensor:
+    """dst[b, r, c] = src[b, r, c] over the flat storage of two contiguous
+    tensors of one dtype (fs_copy_strided), with element strides
+    src offset b * stride_src + r * ld_src + c and likewise for dst."""
+    if src.dtype != dst.dtype:
+        raise ValueError("src and dst must have one dtype")
+    if not (src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("copy_strided addresses contiguous tensors")
+    if rows > 0 and cols > 0 and batch > 0:
+        for t, ld, st, name in ((src, ld_src, stride_src, "src"), (dst, ld_dst, stride_dst, "dst")):
+            last = (batch - 1) * st + (rows - 1) * ld + cols
+            if last > t.numel():
+                raise ValueError(f"{name} is too small for the requested strides")
+    N.check("fs_copy_strided",
+            N.fs_copy_strided(src.data_ptr(), ld_src, stride_src, dst.data_ptr(), ld_dst,
+                              stride_dst, rows, cols, batch, fs_dtype(src), _stream()))
+    return dst
+
+
 def copy_(dst: torch.Tensor, src: torch.Tensor) -> torch.Tensor:
     """Byte copy of src into dst with the calibration kernel (fs_copy)."""
     if not (src.is_contiguous() and dst.is_contiguous()):

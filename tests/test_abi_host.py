@@ -243,3 +243,25 @@ def test_header_compiles_as_c():
                         f"-I{ROOT}/include", "-I/opt/rocm/include", "-c", p, "-o", "/tmp/_fs_hdr_test.o"],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_copy_strided_validation():
+    cs = lambda **kw: N.fs_copy_strided(**{**dict(src=A, ld_src=192, stride_src=64, dst=B,  # noqa: E731
+                                             ld_dst=64, stride_dst=64 * 100, rows=100, cols=64,
+                                             batch=3, dtype=1, stream=None), **kw})
+    assert cs(src=NULL) == 1
+    assert cs(rows=-1) == 2
+    assert cs(batch=-2) == 2
+    assert cs(batch=1 << 20, cols=1 << 11, ld_src=1 << 11, ld_dst=1 << 11) == 2   # batch*cols >= 2^30
+    assert cs(ld_src=63) == 3
+    assert cs(ld_dst=10) == 3
+    assert cs(stride_src=-1) == 3
+    assert cs(stride_dst=64) == 3          # destination batches overlap
+    assert cs(dtype=5) == 4
+    assert cs(dst=B + 1) == 6              # misaligned bf16 pointer
+    assert cs(dst=A + 128) == 5            # spans overlap
+    assert cs(rows=0, src=NULL, dst=NULL) == 0
+    assert cs(batch=0, src=NULL, dst=NULL) == 0
+    # interleaved destination (a head merge) is accepted by validation:
+    # batches 64 apart inside rows of 192
+    assert cs(ld_src=64, stride_src=6400, ld_dst=192, stride_dst=64, src=NULL) == 1

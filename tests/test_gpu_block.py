@@ -38,7 +38,8 @@ def compare(buf, ref, seqs, batch, seq, name, x64=None):
     atol, rtol = TOL["bf16"]
     for st in STAGES:
         if st == "probs":
-            got = host64(buf["probs"][seqs])
+            # device probs are head-major [heads, batch, seq, seq]
+            got = host64(buf["probs"][:, seqs].transpose(0, 1))
         else:
             got = host64(buf[st].view(batch, seq, -1)[seqs])
         want = ref[st]

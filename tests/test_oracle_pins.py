@@ -466,3 +466,52 @@ class TestRowReduce:
                 if x[i, j] > x[i, best]:
                     best = j
             assert got[i] == best
+
+
+# ---------------------------------------------------------------------------
+# layout transform
+# ---------------------------------------------------------------------------
+class TestStridedCopy:
+    def test_head_split_is_a_numpy_transpose(self):
+        # [tokens, 3, heads, dh] -> [3, heads, tokens, dh]; catches swapped
+        # strides, a wrong source or destination batch stride
+        t, nh, dh = 6, 4, 3
+        src = np.arange(t * 3 * nh * dh, dtype=np.int64)
+        got = oracle.strided_copy(src, np.zeros(src.size, np.int64), rows=t, cols=dh,
+                                  batch=3 * nh, ld_src=3 * nh * dh, stride_src=dh, ld_dst=dh,
+                                  stride_dst=t * dh)
+        want = src.reshape(t, 3, nh, dh).transpose(1, 2, 0, 3).reshape(-1)
+        np.testing.assert_array_equal(got, want)
+
+    def test_split_then_merge_round_trips(self):
+        t, nh, dh = 5, 3, 4
+        h = nh * dh
+        src = np.random.default_rng(4).standard_normal(t * h)
+        heads = oracle.strided_copy(src, np.zeros(t * h), rows=t, cols=dh, batch=nh, ld_src=h,
+                                    stride_src=dh, ld_dst=dh, stride_dst=t * dh)
+        back = oracle.strided_copy(heads, np.zeros(t * h), rows=t, cols=dh, batch=nh,
+                                   ld_src=dh, stride_src=t * dh, ld_dst=h, stride_dst=dh)
+        np.testing.assert_array_equal(back, src)
+        assert not np.array_equal(heads, src)              # the split really moved data
+
+    def test_gaps_keep_their_values_and_bits(self):
+        # padding between rows and batches is not written; bit patterns
+        # (here including a NaN payload) are copied unchanged
+        src = np.arange(1, 13, dtype=np.uint16)
+        src[5] = 0x7FC1
+        dst = np.full(40, 0xAAAA, dtype=np.uint16)
+        got = oracle.strided_copy(src, dst, rows=2, cols=3, batch=2, ld_src=3, stride_src=6,
+                                  ld_dst=5, stride_dst=20)
+        want = dst.copy()
+        for b in range(2):
+            for r in range(2):
+                for c in range(3):
+                    want[b * 20 + r * 5 + c] = src[b * 6 + r * 3 + c]
+        np.testing.assert_array_equal(got, want)
+        assert got[39] == 0xAAAA and got[3] == 0xAAAA
+
+    def test_zero_source_stride_broadcasts(self):
+        src = np.array([7.0, 8.0])
+        got = oracle.strided_copy(src, np.zeros(6), rows=1, cols=2, batch=3, ld_src=2,
+                                  stride_src=0, ld_dst=2, stride_dst=2)
+        np.testing.assert_array_equal(got, [7, 8, 7, 8, 7, 8])
