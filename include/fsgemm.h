@@ -56,6 +56,40 @@ FSG_API fsg_status fsg_gemm_bf16(const void* a, int64_t lda, int64_t stride_a, c
                                  int64_t batch, float alpha, const void* bias, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream);
 
+/* Activation applied by the GEMM's own epilogue, after bias.  hipBLASLt's
+ * SIGMOID epilogue is not offered: with this ROCm release it returns success
+ * for bf16 output without applying the activation or the bias. */
+typedef enum fsg_act {
+  FSG_ACT_NONE = 0,
+  FSG_ACT_GELU = 1,       /* hipBLASLt's GELU (its own approximation, not erf) */
+  FSG_ACT_RELU = 2
+} fsg_act;
+
+/*
+ * The GEMM with hipBLASLt's built-in epilogue, for placing a thin epilogue
+ * inside the library call instead of in a separate sub-kernel (the paper's
+ * observation that thin epilogues after a GEMM can lose to dispatch overhead,
+ * Sections 5.2-5.3):
+ *
+ *   C_i = act( alpha_col (.) (A_i @ op(B_i)) + beta * Cin_i + bias )
+ *
+ * alpha_col : [n] fp32 per-column scale (device), or NULL for the scalar
+ *             alpha; with a vector, alpha must be 1.
+ * bias      : [n] per-column, bf16 (bias_f32 = 0) or fp32 (bias_f32 = 1), or NULL.
+ * c_in      : [m, n] bf16 with row stride ld_cin >= n and batch stride
+ *             stride_cin, read when beta != 0 (e.g. a residual added inside
+ *             the GEMM); may equal c exactly.  beta != 0 requires c_in.
+ * Other arguments as fsg_gemm_bf16.
+ */
+FSG_API fsg_status fsg_gemm_bf16_ex(const void* a, int64_t lda, int64_t stride_a, const void* b,
+                                    int64_t ldb, int64_t stride_b, int trans_b, void* c,
+                                    int64_t ldc, int64_t stride_c, int64_t m, int64_t n,
+                                    int64_t k, int64_t batch, float alpha,
+                                    const float* alpha_col, const void* bias, int bias_f32,
+                                    fsg_act act, const void* c_in, int64_t ld_cin,
+                                    int64_t stride_cin, float beta, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
+
 /* Detail of the last non-OK status on the calling thread (never NULL). */
 FSG_API const char* fsg_last_error_message(void);
 

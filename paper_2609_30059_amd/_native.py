@@ -40,7 +40,7 @@ FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_layernorm_residu
                     "fs_gemm_epilogue_reduce", "fs_copy_strided", "fs_copy",
                     "fs_status_string",
                     "fs_last_error_message", "fs_abi_version")
-FSGEMM_SYMBOLS = ("fsg_gemm_bf16", "fsg_last_error_message")
+FSGEMM_SYMBOLS = ("fsg_gemm_bf16", "fsg_gemm_bf16_ex", "fsg_last_error_message")
 
 
 class NativeLibraryError(ImportError):
@@ -74,6 +74,8 @@ _SIGS = {
     "fs_abi_version": [],
     "fsg_gemm_bf16": [_P, _I64, _I64, _P, _I64, _I64, _I, _P, _I64, _I64, _I64, _I64, _I64, _I64,
                       _F, _P, _P, ctypes.c_size_t, _P],
+    "fsg_gemm_bf16_ex": [_P, _I64, _I64, _P, _I64, _I64, _I, _P, _I64, _I64, _I64, _I64, _I64,
+                         _I64, _F, _P, _P, _I, _I, _P, _I64, _I64, _F, _P, ctypes.c_size_t, _P],
     "fsg_last_error_message": [],
 }
 _RESTYPES = {"fs_status_string": ctypes.c_char_p, "fs_last_error_message": ctypes.c_char_p,
@@ -195,6 +197,14 @@ def fsg_gemm_bf16(a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c,
                   alpha, bias, workspace, workspace_bytes, stream):
     return fsgemm().fsg_gemm_bf16(a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c,
                                   m, n, k, batch, alpha, bias, workspace, workspace_bytes, stream)
+
+
+def fsg_gemm_bf16_ex(a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c, m, n, k, batch,
+                     alpha, alpha_col, bias, bias_f32, act, c_in, ld_cin, stride_cin, beta,
+                     workspace, workspace_bytes, stream):
+    return fsgemm().fsg_gemm_bf16_ex(a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c,
+                                     m, n, k, batch, alpha, alpha_col, bias, bias_f32, act, c_in,
+                                     ld_cin, stride_cin, beta, workspace, workspace_bytes, stream)
 
 
 def fsg_last_error_message():

@@ -149,11 +149,18 @@ class TransformerBlock:
         self.merge_heads(buf)
         ops.gemm(buf["o"], p["w_o"], bias=p["b_o"], out=buf["att"])
         self.layernorm2_residual(x2, buf)
-        ops.gemm(buf["m"], p["w_1"], out=buf["u"])
-        self.bias_gelu(buf)
-        ops.gemm(buf["g"], p["w_2"], bias=p["b_2"], out=buf["d"])
-        self.residual_add(buf)
+        self.mlp_up(buf)
+        self.mlp_down(buf)
         return buf
+
+    # --- MLP: library GEMMs with the epilogue sub-kernels after them ----------
+    def mlp_up(self, buf):
+        ops.gemm(buf["m"], self.p["w_1"], out=buf["u"])
+        self.bias_gelu(buf)
+
+    def mlp_down(self, buf):
+        ops.gemm(buf["g"], self.p["w_2"], bias=self.p["b_2"], out=buf["d"])
+        self.residual_add(buf)
 
     # the five sub-kernel launches alone, on resident inputs (for timing)
     def subkernels(self, x: torch.Tensor, buf: Dict[str, torch.Tensor]):

@@ -29,12 +29,24 @@ fsg_status fail(fsg_status st, const char* fmt, ...) {
   return st;
 }
 
+struct Req {
+  const void* a; int64_t lda, stride_a;
+  const void* b; int64_t ldb, stride_b; int trans_b;
+  void* c; int64_t ldc, stride_c;
+  int64_t m, n, k, batch;
+  float alpha; const float* alpha_col;
+  const void* bias; int bias_f32;
+  fsg_act act;
+  const void* c_in; int64_t ld_cin, stride_cin; float beta;
+  void* workspace; size_t workspace_bytes;
+};
+
 using Key = std::tuple<int, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int, int64_t,
-                       int64_t, int64_t, int64_t, bool, size_t>;
+                       int64_t, int64_t, int64_t, size_t, int, int, int, int, int64_t, int64_t>;
 
 struct Plan {
   hipblasLtMatmulDesc_t desc = nullptr;
-  hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr;
+  hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr, lcin = nullptr;
   hipblasLtMatmulAlgo_t algo{};
 };
 
@@ -66,31 +78,50 @@ fsg_status make_layout(hipblasLtMatrixLayout_t* l, uint64_t rows, uint64_t cols,
   return FSG_OK;
 }
 
-}  // namespace
+uint32_t epilogue_of(bool bias, fsg_act act) {
+  switch (act) {
+    case FSG_ACT_GELU: return bias ? HIPBLASLT_EPILOGUE_GELU_BIAS : HIPBLASLT_EPILOGUE_GELU;
+    case FSG_ACT_RELU: return bias ? HIPBLASLT_EPILOGUE_RELU_BIAS : HIPBLASLT_EPILOGUE_RELU;
+    default: return bias ? HIPBLASLT_EPILOGUE_BIAS : HIPBLASLT_EPILOGUE_DEFAULT;
+  }
+}
 
-extern "C" {
+hipblasStatus_t launch(hipblasLtHandle_t h, const Plan& p, const Req& r,
+                       const hipblasLtMatmulAlgo_t* algo, hipStream_t stream) {
+  const void* alpha = r.alpha_col ? static_cast<const void*>(r.alpha_col)
+                                  : static_cast<const void*>(&r.alpha);
+  const bool has_cin = r.c_in != nullptr && r.beta != 0.f;
+  return hipblasLtMatmul(h, p.desc, alpha, r.b, p.la, r.a, p.lb, &r.beta,
+                         has_cin ? r.c_in : r.c, has_cin ? p.lcin : p.lc, r.c, p.lc, algo,
+                         r.workspace, r.workspace_bytes, stream);
+}
 
-const char* fsg_last_error_message(void) { return g_msg; }
-
-fsg_status fsg_gemm_bf16(const void* a, int64_t lda, int64_t stride_a, const void* b, int64_t ldb,
-                         int64_t stride_b, int trans_b, void* c, int64_t ldc, int64_t stride_c,
-                         int64_t m, int64_t n, int64_t k, int64_t batch, float alpha,
-                         const void* bias, void* workspace, size_t workspace_bytes,
-                         hipStream_t stream) {
-  g_msg[0] = '\0';
-  if (trans_b != 0 && trans_b != 1) return fail(FSG_ERR_BAD_ARGUMENT, "trans_b=%d", trans_b);
-  if (!std::isfinite(alpha)) return fail(FSG_ERR_BAD_ARGUMENT, "alpha is not finite");
-  if (m < 0 || n < 0 || k < 0 || batch < 1 || batch > INT32_MAX)
-    return fail(FSG_ERR_BAD_SHAPE, "m=%lld n=%lld k=%lld batch=%lld", (long long)m, (long long)n,
-                (long long)k, (long long)batch);
-  if (lda < k || ldc < n || ldb < (trans_b ? k : n))
-    return fail(FSG_ERR_BAD_STRIDE, "lda=%lld ldb=%lld ldc=%lld", (long long)lda,
-                (long long)ldb, (long long)ldc);
-  if (m == 0 || n == 0) return FSG_OK;
-  if (k == 0) return fail(FSG_ERR_BAD_SHAPE, "k=0 is not supported");
-  if (!a || !b || !c) return fail(FSG_ERR_NULL_POINTER, "a, b and c are required");
-  if (workspace_bytes && !workspace) return fail(FSG_ERR_NULL_POINTER, "workspace is NULL");
-  if (batch == 1) stride_a = stride_b = stride_c = 0;
+fsg_status run(const Req& r, hipStream_t stream) {
+  if (r.trans_b != 0 && r.trans_b != 1) return fail(FSG_ERR_BAD_ARGUMENT, "trans_b=%d", r.trans_b);
+  if (!std::isfinite(r.alpha) || !std::isfinite(r.beta))
+    return fail(FSG_ERR_BAD_ARGUMENT, "alpha and beta must be finite");
+  if (r.act < FSG_ACT_NONE || r.act > FSG_ACT_RELU)
+    return fail(FSG_ERR_BAD_ARGUMENT, "act=%d", int(r.act));
+  if (r.bias_f32 != 0 && r.bias_f32 != 1) return fail(FSG_ERR_BAD_ARGUMENT, "bias_f32=%d", r.bias_f32);
+  if (r.alpha_col && r.alpha != 1.f)
+    return fail(FSG_ERR_BAD_ARGUMENT, "alpha must be 1 with a per-column alpha vector");
+  if (r.m < 0 || r.n < 0 || r.k < 0 || r.batch < 1 || r.batch > INT32_MAX)
+    return fail(FSG_ERR_BAD_SHAPE, "m=%lld n=%lld k=%lld batch=%lld", (long long)r.m,
+                (long long)r.n, (long long)r.k, (long long)r.batch);
+  if (r.lda < r.k || r.ldc < r.n || r.ldb < (r.trans_b ? r.k : r.n))
+    return fail(FSG_ERR_BAD_STRIDE, "lda=%lld ldb=%lld ldc=%lld", (long long)r.lda,
+                (long long)r.ldb, (long long)r.ldc);
+  const bool has_cin = r.c_in != nullptr && r.beta != 0.f;
+  if (has_cin && r.ld_cin < r.n)
+    return fail(FSG_ERR_BAD_STRIDE, "ld_cin=%lld < n", (long long)r.ld_cin);
+  if (r.m == 0 || r.n == 0) return FSG_OK;
+  if (r.k == 0) return fail(FSG_ERR_BAD_SHAPE, "k=0 is not supported");
+  if (!r.a || !r.b || !r.c) return fail(FSG_ERR_NULL_POINTER, "a, b and c are required");
+  if (r.beta != 0.f && !r.c_in) return fail(FSG_ERR_NULL_POINTER, "beta != 0 needs c_in");
+  if (r.workspace_bytes && !r.workspace) return fail(FSG_ERR_NULL_POINTER, "workspace is NULL");
+  Req q = r;
+  if (q.batch == 1) q.stride_a = q.stride_b = q.stride_c = q.stride_cin = 0;
+  if (!has_cin) q.ld_cin = q.stride_cin = 0;
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(FSG_ERR_HIP, "hipGetDevice failed");
@@ -105,40 +136,50 @@ fsg_status fsg_gemm_bf16(const void* a, int64_t lda, int64_t stride_a, const voi
   }
   hipblasLtHandle_t handle = hit->second;
 
-  const Key key{dev, m, n, k, lda, ldb, ldc, trans_b, stride_a, stride_b, stride_c, batch,
-                bias != nullptr, workspace_bytes};
+  const Key key{dev, q.m, q.n, q.k, q.lda, q.ldb, q.ldc, q.trans_b, q.stride_a, q.stride_b,
+                q.stride_c, q.batch, q.workspace_bytes, (q.bias ? 1 : 0) | (q.bias_f32 << 1),
+                int(q.act), q.alpha_col ? 1 : 0, has_cin ? 1 : 0, q.ld_cin, q.stride_cin};
   auto pit = st.plans.find(key);
   if (pit == st.plans.end()) {
     Plan p;
     LT(hipblasLtMatmulDescCreate(&p.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F));
     // hipBLASLt "A" = row-major B: column-major [n, k] (trans_b = 0) or
     // stored column-major [k, n] used transposed (trans_b = 1).
-    int32_t opa = trans_b ? HIPBLAS_OP_T : HIPBLAS_OP_N, opb = HIPBLAS_OP_N;
+    int32_t opa = q.trans_b ? HIPBLAS_OP_T : HIPBLAS_OP_N, opb = HIPBLAS_OP_N;
     LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &opa, sizeof(opa)));
     LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &opb, sizeof(opb)));
-    if (bias) {
-      uint32_t epi = HIPBLASLT_EPILOGUE_BIAS;
-      int32_t bt = HIP_R_16BF;
+    const uint32_t epi = epilogue_of(q.bias != nullptr, q.act);
+    if (epi != HIPBLASLT_EPILOGUE_DEFAULT)
       LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_EPILOGUE, &epi, sizeof(epi)));
+    if (q.bias) {
+      int32_t bt = q.bias_f32 ? HIP_R_32F : HIP_R_16BF;
       LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_DATA_TYPE, &bt,
                                          sizeof(bt)));
     }
+    if (q.alpha_col) {
+      int32_t pm = HIPBLASLT_POINTER_MODE_ALPHA_DEVICE_VECTOR_BETA_HOST;
+      LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_POINTER_MODE, &pm,
+                                         sizeof(pm)));
+    }
     fsg_status s2;
-    if ((s2 = trans_b ? make_layout(&p.la, k, n, ldb, batch, stride_b)
-                      : make_layout(&p.la, n, k, ldb, batch, stride_b)) != FSG_OK)
+    if ((s2 = q.trans_b ? make_layout(&p.la, q.k, q.n, q.ldb, q.batch, q.stride_b)
+                        : make_layout(&p.la, q.n, q.k, q.ldb, q.batch, q.stride_b)) != FSG_OK)
       return s2;
-    if ((s2 = make_layout(&p.lb, k, m, lda, batch, stride_a)) != FSG_OK) return s2;
-    if ((s2 = make_layout(&p.lc, n, m, ldc, batch, stride_c)) != FSG_OK) return s2;
-
+    if ((s2 = make_layout(&p.lb, q.k, q.m, q.lda, q.batch, q.stride_a)) != FSG_OK) return s2;
+    if ((s2 = make_layout(&p.lc, q.n, q.m, q.ldc, q.batch, q.stride_c)) != FSG_OK) return s2;
+    if (has_cin &&
+        (s2 = make_layout(&p.lcin, q.n, q.m, q.ld_cin, q.batch, q.stride_cin)) != FSG_OK)
+      return s2;
     hipblasLtMatmulPreference_t pref = nullptr;
     LT(hipblasLtMatmulPreferenceCreate(&pref));
-    uint64_t ws = workspace_bytes;
+    uint64_t ws = q.workspace_bytes;
     LT(hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &ws,
                                              sizeof(ws)));
     hipblasLtMatmulHeuristicResult_t res[1];
     int found = 0;
-    hipblasStatus_t hs = hipblasLtMatmulAlgoGetHeuristic(handle, p.desc, p.la, p.lb, p.lc, p.lc,
-                                                         pref, 1, res, &found);
+    hipblasStatus_t hs = hipblasLtMatmulAlgoGetHeuristic(handle, p.desc, p.la, p.lb,
+                                                         has_cin ? p.lcin : p.lc, p.lc, pref, 1,
+                                                         res, &found);
     hipblasLtMatmulPreferenceDestroy(pref);
     if (hs != HIPBLAS_STATUS_SUCCESS || found < 1)
       return fail(FSG_ERR_NO_ALGO, "no hipBLASLt algorithm (status %d, found %d)", int(hs), found);
@@ -146,14 +187,42 @@ fsg_status fsg_gemm_bf16(const void* a, int64_t lda, int64_t stride_a, const voi
     pit = st.plans.emplace(key, p).first;
   }
   Plan& p = pit->second;
-  if (bias) {
-    LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias,
-                                       sizeof(bias)));
-  }
-  const float beta = 0.f;
-  LT(hipblasLtMatmul(handle, p.desc, &alpha, b, p.la, a, p.lb, &beta, c, p.lc, c, p.lc, &p.algo,
-                     workspace, workspace_bytes, stream));
+  if (q.bias)
+    LT(hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &q.bias,
+                                       sizeof(q.bias)));
+  LT(launch(handle, p, q, &p.algo, stream));
   return FSG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fsg_last_error_message(void) { return g_msg; }
+
+fsg_status fsg_gemm_bf16(const void* a, int64_t lda, int64_t stride_a, const void* b, int64_t ldb,
+                         int64_t stride_b, int trans_b, void* c, int64_t ldc, int64_t stride_c,
+                         int64_t m, int64_t n, int64_t k, int64_t batch, float alpha,
+                         const void* bias, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+  g_msg[0] = '\0';
+  Req r{a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c, m, n, k, batch,
+        alpha, nullptr, bias, 0, FSG_ACT_NONE, nullptr, 0, 0, 0.f, workspace, workspace_bytes};
+  return run(r, stream);
+}
+
+fsg_status fsg_gemm_bf16_ex(const void* a, int64_t lda, int64_t stride_a, const void* b,
+                            int64_t ldb, int64_t stride_b, int trans_b, void* c, int64_t ldc,
+                            int64_t stride_c, int64_t m, int64_t n, int64_t k, int64_t batch,
+                            float alpha, const float* alpha_col, const void* bias, int bias_f32,
+                            fsg_act act, const void* c_in, int64_t ld_cin, int64_t stride_cin,
+                            float beta, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  g_msg[0] = '\0';
+  Req r{a, lda, stride_a, b, ldb, stride_b, trans_b, c, ldc, stride_c, m, n, k, batch,
+        alpha, alpha_col, bias, bias_f32, act, c_in, ld_cin, stride_cin, beta, workspace,
+        workspace_bytes};
+  return run(r, stream);
 }
 
 }  // extern "C"

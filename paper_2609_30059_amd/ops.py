@@ -274,14 +274,22 @@ def gemm_strided_batched(a_ptr: int, lda: int, stride_a: int, b_ptr: int, ldb: i
     N.check_gemm(st)
 
 
+GEMM_ACTS = {"none": 0, "gelu": 1, "relu": 2}
+
+
 def gemm(a: torch.Tensor, b: torch.Tensor, bias: Optional[torch.Tensor] = None,
          out: Optional[torch.Tensor] = None, trans_b: bool = False,
-         alpha: float = 1.0) -> torch.Tensor:
-    """out = alpha * a @ b (+ bias) for bf16 row-major a [m, k] and b [k, n]
-    (or b stored [n, k] with trans_b)."""
+         alpha: float = 1.0, act: str = "none", col_scale: Optional[torch.Tensor] = None,
+         c_in: Optional[torch.Tensor] = None, beta: float = 0.0) -> torch.Tensor:
+    """out = act(alpha * a @ b (* col_scale) + beta * c_in + bias) for bf16
+    row-major a [m, k] and b [k, n] (or b stored [n, k] with trans_b).  The
+    activation, column scale and c_in use hipBLASLt's own epilogue
+    (fsg_gemm_bf16_ex); bias is bf16, or fp32 on that path."""
     for t in (a, b):
         if t.dtype != torch.bfloat16:
             raise TypeError("gemm takes bfloat16 operands")
+    if act not in GEMM_ACTS:
+        raise ValueError(f"act must be one of {sorted(GEMM_ACTS)}")
     m, k, lda = as_rows(a)
     if trans_b:
         n, kb, ldb = as_rows(b)
@@ -293,6 +301,30 @@ def gemm(a: torch.Tensor, b: torch.Tensor, bias: Optional[torch.Tensor] = None,
         out = torch.empty((*a.shape[:-1], n), dtype=torch.bfloat16, device=a.device)
     _, _, ldc = as_rows(out)
     _vec(bias, n, "bias")
-    gemm_strided_batched(a.data_ptr(), lda, 0, b.data_ptr(), ldb, 0, trans_b, out.data_ptr(),
-                         ldc, 0, m, n, k, 1, alpha, bias, a.device)
+    if bias is not None and bias.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError("bias must be bf16 or fp32")
+    extended = act != "none" or col_scale is not None or c_in is not None or beta != 0.0 or (
+        bias is not None and bias.dtype == torch.float32)
+    if not extended:
+        gemm_strided_batched(a.data_ptr(), lda, 0, b.data_ptr(), ldb, 0, trans_b,
+                             out.data_ptr(), ldc, 0, m, n, k, 1, alpha, bias, a.device)
+        return out
+    if col_scale is not None:
+        if col_scale.dtype != torch.float32:
+            raise TypeError("col_scale must be fp32")
+        _vec(col_scale, n, "col_scale")
+    ld_cin = 0
+    if c_in is not None:
+        if c_in.dtype != torch.bfloat16:
+            raise TypeError("c_in must be bf16")
+        mc, nc, ld_cin = as_rows(c_in)
+        if (mc, nc) != (m, n):
+            raise ValueError("c_in must be [m, n]")
+    ws = _workspace(a.device)
+    st = N.fsg_gemm_bf16_ex(a.data_ptr(), lda, 0, b.data_ptr(), ldb, 0, int(trans_b),
+                            out.data_ptr(), ldc, 0, m, n, k, 1, float(alpha), _ptr(col_scale),
+                            _ptr(bias), int(bias is not None and bias.dtype == torch.float32),
+                            GEMM_ACTS[act], _ptr(c_in), ld_cin, 0, float(beta), ws.data_ptr(),
+                            ws.numel(), _stream())
+    N.check_gemm(st)
     return out

@@ -265,3 +265,22 @@ def test_copy_strided_validation():
     # interleaved destination (a head merge) is accepted by validation:
     # batches 64 apart inside rows of 192
     assert cs(ld_src=64, stride_src=6400, ld_dst=192, stride_dst=64, src=NULL) == 1
+
+
+def test_gemm_ex_validation():
+    ge = lambda **kw: N.fsg_gemm_bf16_ex(**{**dict(a=A, lda=64, stride_a=0, b=B, ldb=32,  # noqa: E731
+                                              stride_b=0, trans_b=0, c=C, ldc=32, stride_c=0,
+                                              m=16, n=32, k=64, batch=1, alpha=1.0,
+                                              alpha_col=NULL, bias=NULL, bias_f32=0, act=0,
+                                              c_in=NULL, ld_cin=32, stride_cin=0, beta=0.0,
+                                              workspace=NULL, workspace_bytes=0,
+                                              stream=None), **kw})
+    assert ge(act=7) == 4
+    assert ge(act=3) == 4                           # no sigmoid epilogue is offered
+    assert ge(bias_f32=2) == 4
+    assert ge(alpha=2.0, alpha_col=A + 4096) == 4     # a vector replaces the scalar
+    assert ge(beta=float("nan")) == 4
+    assert ge(beta=1.0) == 1                          # beta != 0 needs c_in
+    assert ge(beta=1.0, c_in=A + 8192, ld_cin=31) == 3
+    assert ge(m=-1) == 2
+    assert ge(m=0, a=NULL, b=NULL, c=NULL) == 0
