@@ -69,7 +69,7 @@ typedef enum fsg_act {
  * The GEMM with hipBLASLt's built-in epilogue, for placing a thin epilogue
  * inside the library call instead of in a separate sub-kernel (the paper's
  * observation that thin epilogues after a GEMM can lose to dispatch overhead,
- * Sections 5.2-5.3):
+ * Section 6.2, library dominance; Section 6.3):
  *
  *   C_i = act( alpha_col (.) (A_i @ op(B_i)) + beta * Cin_i + bias )
  *

@@ -4,7 +4,7 @@ cheapest on MI355X.
 KernelOPT keeps GEMMs as library calls and rewrites only the generated
 sub-kernels around them; it reports that in GEMM-dominated models a thin
 epilogue gains little and an extra dispatch can make the model slower
-(Sections 5.2-5.3).  This module measures the alternatives for the two
+(Section 6.2, library dominance; Section 6.3).  This module measures the alternatives for the two
 epilogues of this library:
 
 GEMM + bias/scale/sigmoid + row sum  (C = A @ B, A [8192, 4096], B [4096, 8192])
