@@ -60,7 +60,7 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
 
   const int tid = threadIdx.x % kThreads;
   const int wave = tid / 64, lane = tid % 64;
-  const int g = threadIdx.x / kThreads;
+  const int g = __builtin_amdgcn_readfirstlane(threadIdx.x / kThreads);   // wave-uniform
   int parity = 0;
 
   // out-of-row vectors read the last vector of the row (an in-bounds address)

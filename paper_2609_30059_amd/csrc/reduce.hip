@@ -86,7 +86,7 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
   __shared__ P lds[2][W];
   const int tid = threadIdx.x % kThreads;
   const int wave = tid / 64, lane = tid % 64;
-  const int g = threadIdx.x / kThreads;
+  const int g = __builtin_amdgcn_readfirstlane(threadIdx.x / kThreads);   // wave-uniform
   const int clast = cols - V;     // start of the row's last vector
   int parity = 0;
 

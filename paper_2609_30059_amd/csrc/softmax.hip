@@ -55,6 +55,17 @@ struct MaxSumP {
   }
 };
 
+// Plain maximum (one-wave rows reduce the max and the sum separately).
+struct MaxF {
+  float m;
+  __device__ __forceinline__ static MaxF combine(const MaxF& a, const MaxF& b) {
+    return {fmaxf(a.m, b.m)};
+  }
+  template <class F> __device__ __forceinline__ static MaxF map(const MaxF& a, F f) {
+    return {f(a.m)};
+  }
+};
+
 // T: storage type of x and y; MT: storage type of the mask (used when
 // HAS_MASK).  W waves per row; EPT elements per thread; VEC: 16-byte vector
 // path; G row groups per block (W == 1 only); R rows per group per trip --
@@ -71,16 +82,25 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   // one LDS fold area and one barrier sequence per block: rows wider than a
   // wave take the whole block (the row loop is then uniform across it)
   static_assert(W == 1 || G == 1, "multi-wave rows use one row group per block");
-  using P = Multi<MaxSumP, R>;
-  __shared__ P lds[2][W];
+  __shared__ Multi<MaxSumP, R> lds[W == 1 ? 1 : 2][W];
 
   const int tid = threadIdx.x % kThreads;
   const int wave = tid / 64, lane = tid % 64;
-  const int g = threadIdx.x / kThreads;
+  // the row group is uniform across a wave: keep it (and all row
+  // arithmetic) in scalar registers
+  const int g = __builtin_amdgcn_readfirstlane(threadIdx.x / kThreads);
   int parity = 0;
 
-  for (int64_t row0 = (int64_t(blockIdx.x) * G + g) * R; row0 < rows;
-       row0 += int64_t(gridDim.x) * G * R) {
+  // causal position of row0 (row0 mod q_len), advanced by the loop step
+  // without a division per row
+  const int64_t step = int64_t(gridDim.x) * G * R;
+  int64_t row0 = (int64_t(blockIdx.x) * G + g) * R;
+  int64_t pos0 = 0, step_mod = 0;
+  if (q_len > 0) {
+    pos0 = row0 % q_len;
+    step_mod = step % q_len;
+  }
+  for (; row0 < rows; row0 += step) {
     Raw<T, V> rx[R][NV];
     Raw<MT, V> rm[R][HAS_MASK ? NV : 1];
     int lim[R];
@@ -91,7 +111,12 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       const T* xr = x + row * ld_x;
       const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
       // last live column (inclusive) under the causal rule; -1 if none
-      const int64_t limit = q_len > 0 ? (row % q_len) + (cols - q_len) : int64_t(cols) - 1;
+      int64_t limit = int64_t(cols) - 1;
+      if (q_len > 0) {
+        int64_t pos = pos0 + r;
+        if (pos >= q_len) pos = q_len >= R ? pos - q_len : pos % q_len;
+        limit = pos + (cols - q_len);
+      }
       lim[r] = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
       // vectors past lim are not read: their address is clamped onto the
       // vector holding column lim (fetched by a live lane), then masked
@@ -104,15 +129,15 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         if constexpr (HAS_MASK) rm[r][k].load(mr + cl);
       }
     }
+    if (q_len > 0) {
+      pos0 += step_mod;
+      if (pos0 >= q_len) pos0 -= q_len;
+    }
     // keep every load of the trip ahead of the first use (one HBM round trip)
     __builtin_amdgcn_sched_barrier(0);
 
-    // logits a = x * scale + mask (-inf past lim); local (m', d) in base-2
-    // units with the exponentials kept in a[]
+    // logits a = x * scale + mask (-inf past lim)
     float a[R][EPT];
-    P part;
-    bool empty[R];
-    float ml2[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
@@ -132,30 +157,78 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 #pragma unroll
         for (int i = 0; i < V; ++i) a[r][k * V + i] = (c0 + i <= lim[r]) ? xv[i] : -INFINITY;
       }
-      float m = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
-      empty[r] = (m == -INFINITY);
-      ml2[r] = empty[r] ? 0.f : m * kLog2e;   // m' (0 for an all-masked slice)
-      float d = 0.f;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i) {
-        a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2[r]));   // exp2(-inf) = 0
-        d += a[r][i];
-      }
-      part.p[r] = MaxSumP{empty[r] ? -INFINITY : ml2[r], d};
     }
 
-    const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
-    parity ^= 1;
+    // f[r]: the factor that turns the stored exponentials into probabilities
+    float f[R];
+    if constexpr (W == 1) {
+      // One-wave rows: a max all-reduce, exponentials against the row max,
+      // a sum all-reduce.  Two cheap shuffle sequences instead of one of
+      // (max, sum) pairs, whose every combine costs an exp2 -- with only
+      // EPT * R elements per lane that combine dominated the ALU work.
+      Multi<MaxF, R> mx;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
+        mx.p[r].m = m;
+      }
+      mx = wave_allreduce(mx);
+      Multi<SumP, R> sm;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        // M' = M log2(e) rounded once; an all-masked row keeps 0 (its
+        // exponentials are exp2(-inf) = 0)
+        const float ml2 = mx.p[r].m == -INFINITY ? 0.f : mx.p[r].m * kLog2e;
+        float d = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2));
+          d += a[r][i];
+        }
+        sm.p[r].s = d;
+      }
+      sm = wave_allreduce(sm);
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        f[r] = sm.p[r].s > 0.f ? __builtin_amdgcn_rcpf(sm.p[r].s) : 0.f;   // D >= 1 when live
+    } else {
+      // Multi-wave rows: local (m', d) per thread in base-2 units with the
+      // exponentials kept in a[], one all-reduce of the pairs across waves
+      using P = Multi<MaxSumP, R>;
+      P part;
+      bool empty[R];
+      float ml2[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
+        empty[r] = (m == -INFINITY);
+        ml2[r] = empty[r] ? 0.f : m * kLog2e;   // m' (0 for an all-masked slice)
+        float d = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2[r]));   // exp2(-inf) = 0
+          d += a[r][i];
+        }
+        part.p[r] = MaxSumP{empty[r] ? -INFINITY : ml2[r], d};
+      }
+      const P tot = group_allreduce<W>(part, lds[parity], wave, lane);
+      parity ^= 1;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        // a slice with no live element contributes zeros (and must not form
+        // 0*inf); a fully masked row has M = -inf and comes out all zeros
+        const MaxSumP p = tot.p[r];
+        f[r] = (empty[r] || p.m == -INFINITY) ? 0.f
+                                              : __builtin_amdgcn_exp2f(ml2[r] - p.m) / p.d;
+      }
+    }
 
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      // a slice with no live element contributes zeros (and must not form
-      // 0*inf); a fully masked row has M = -inf and comes out all zeros
-      const MaxSumP p = tot.p[r];
-      const float f =
-          (empty[r] || p.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml2[r] - p.m) / p.d;
       if (row0 + r < rows) {
         T* yr = y + (row0 + r) * ld_y;
 #pragma unroll
@@ -164,7 +237,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
           if (c0 < cols) {
             float o[V];
 #pragma unroll
-            for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f;
+            for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f[r];
             stv<T, V>(yr + c0, o);
           }
         }
