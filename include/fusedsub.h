@@ -128,6 +128,31 @@ FS_API fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, i
                          hipStream_t stream);
 
 /*
+ * Causal row softmax that leaves the zero blocks no consumer reads unwritten
+ * (fused softmax with the causal mask, Appendix A, Planner item 9; the
+ * writes it skips are dead stores once the P.V product is issued per row
+ * block with K limited to the causal extent, the way the stitched block
+ * does it).
+ *
+ *   a[r, j] = x[r, j] * scale, masked (-inf) when j > s + (cols - q),
+ *   s = r mod causal_q_len, q = causal_q_len
+ *   y[r, j] = softmax_j(a[r, :]) for j < w(r),
+ *   w(r) = min(cols, (floor(s / block) + 1) * block + (cols - q)), clamped at 0
+ *
+ * Columns j >= w(r) of y are not written (they keep their contents); masked
+ * columns below w(r) are written as +0.  For square attention (cols == q)
+ * and block B, the rows of causal positions [i B, (i+1) B) write their first
+ * (i+1) B columns: exactly what a P.V product over K = (i+1) B reads.
+ * block must be a power of two (1 ... 2^30) and causal_q_len >= 1
+ * (FS_ERR_BAD_ARGUMENT otherwise).  x, y, dtype, scale, shapes, strides and
+ * aliasing as fs_row_softmax without a mask.
+ */
+FS_API fs_status fs_causal_softmax_trimmed(const void* x, int64_t ld_x, void* y, int64_t ld_y,
+                                           int64_t rows, int64_t cols, float scale,
+                                           int64_t causal_q_len, int64_t block, fs_dtype dtype,
+                                           hipStream_t stream);
+
+/*
  * LayerNorm fused with the residual add (Appendix A, Fusion Agent:
  * normalisation fusion -- mean and variance in one pass, normalise, scale and
  * bias in the same kernel, fp32 accumulation; residual + norm in one memory

@@ -118,6 +118,18 @@ def causal_mask(rows: int, cols: int, q_len: int) -> np.ndarray:
     return j > (r % q_len) + (cols - q_len)
 
 
+def causal_written_width(rows: int, cols: int, q_len: int, block: int) -> np.ndarray:
+    """Columns of each row that a causal softmax trimmed to row blocks
+    writes: w(r) = min(cols, (floor(s / block) + 1) * block + (cols - q_len)),
+    at least 0, with s = r mod q_len.  Row r's live columns j <= s + (cols -
+    q_len) all lie below w(r); the columns from w(r) on are all masked and are
+    the ones a P.V product issued per row block of `block` rows never reads
+    (the dead stores of the causal mask, Appendix A, Planner item 9)."""
+    s = np.arange(rows, dtype=np.int64) % q_len
+    w = (s // block + 1) * block + (cols - q_len)
+    return np.clip(w, 0, cols)
+
+
 def row_softmax(x, mask=None, scale: float = 1.0, causal_q_len: int = 0):
     """y[r] = softmax_j(x[r, j] * scale + mask[r, j]) along the last dim.
 

@@ -35,7 +35,8 @@ FS_SOFTMAX_MAX_COLS = 16777216
 FS_LAYERNORM_MAX_COLS = 16777216
 
 # every symbol the headers declare
-FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_layernorm_residual",
+FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_causal_softmax_trimmed",
+                    "fs_layernorm_residual",
                     "fs_rmsnorm_residual", "fs_row_reduce", "fs_row_argmax",
                     "fs_gemm_epilogue_reduce", "fs_copy_strided", "fs_copy",
                     "fs_status_string",
@@ -67,6 +68,7 @@ _SIGS = {
     "fs_row_reduce": [_P, _I64, _I, _I, _P, _I64, _I64, _P],
     "fs_row_argmax": [_P, _I64, _I, _P, _I64, _I64, _P],
     "fs_gemm_epilogue_reduce": [_P, _I64, _I, _P, _I, _P, _I, _I, _P, _I64, _I64, _P],
+    "fs_causal_softmax_trimmed": [_P, _I64, _P, _I64, _I64, _I64, _F, _I64, _I64, _I, _P],
     "fs_copy_strided": [_P, _I64, _I64, _P, _I64, _I64, _I64, _I64, _I64, _I, _P],
     "fs_copy": [_P, _P, _I64, _P],
     "fs_status_string": [_I],
@@ -169,6 +171,12 @@ def fs_gemm_epilogue_reduce(c, ld_c, c_dtype, bias, bias_dtype, col_scale, act, 
                             rows, cols, stream):
     return fusedsub().fs_gemm_epilogue_reduce(c, ld_c, c_dtype, bias, bias_dtype, col_scale, act,
                                               reduce, row_out, rows, cols, stream)
+
+
+def fs_causal_softmax_trimmed(x, ld_x, y, ld_y, rows, cols, scale, causal_q_len, block, dtype,
+                              stream):
+    return fusedsub().fs_causal_softmax_trimmed(x, ld_x, y, ld_y, rows, cols, scale, causal_q_len,
+                                                block, dtype, stream)
 
 
 def fs_copy_strided(src, ld_src, stride_src, dst, ld_dst, stride_dst, rows, cols, batch, dtype,

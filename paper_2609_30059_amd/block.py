@@ -10,7 +10,7 @@ block on MI355X:
     qkv  = a @ Wqkv + bqkv                                hipBLASLt (BIAS epilogue)
     q, k, v head-major  [3 * heads, tokens, dh]           fs_copy_strided
     S    = q k^T for all (head, sequence) pairs           hipBLASLt strided batched
-    P    = softmax(S / sqrt(dh), causal)                  fs_row_softmax
+    P    = softmax(S / sqrt(dh), causal)                  fs_row_softmax (or fs_causal_softmax_trimmed)
     o_h  = P v for all pairs                              hipBLASLt strided batched
     o    = o_h merged to token-major [tokens, H]          fs_copy_strided
     att  = o @ Wo + bo                                    hipBLASLt (BIAS epilogue)
@@ -21,8 +21,16 @@ block on MI355X:
     out  = d + h1                                         fs_pointwise_chain
 
 The head split and merge cost one pass over qkv and one over o; in exchange
-each attention GEMM is a single launch over heads * batch pairs instead of
-one launch per sequence.
+each attention GEMM is one launch over all heads * batch pairs.
+
+attn_block (a power of two) issues the products per causal row block of that
+many rows instead, with K limited to the block's causal extent, and the
+softmax (fs_causal_softmax_trimmed) leaves the all-masked blocks above the
+diagonal unwritten: with 4 blocks, 5/8 of the score and probability matrices
+are computed, written and read, and entries beyond a row's block are left
+unwritten.  At [32, 512] with 16 heads this measured no faster on MI355X
+(hipBLASLt's kernels for the narrower products are less efficient, and the
+shortened rows write less efficiently), so it is off by default.
 """
 from __future__ import annotations
 
@@ -40,7 +48,8 @@ PARAM_NAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "ln1_
 class TransformerBlock:
     """Weights are bf16 device tensors, stored [in, out] (y = x @ W + b)."""
 
-    def __init__(self, params: Dict[str, torch.Tensor], heads: int, eps: float = 1e-5):
+    def __init__(self, params: Dict[str, torch.Tensor], heads: int, eps: float = 1e-5,
+                 attn_block: Optional[int] = None):
         for k in PARAM_NAMES:
             t = params[k]
             if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
@@ -53,6 +62,9 @@ class TransformerBlock:
         if self.hidden % heads:
             raise ValueError("hidden must be divisible by heads")
         self.dh = self.hidden // heads
+        if attn_block is not None and (attn_block < 1 or attn_block & (attn_block - 1)):
+            raise ValueError("attn_block must be a power of two (or None)")
+        self.attn_block = None if attn_block is None else int(attn_block)
 
     def alloc(self, batch: int, seq: int, device) -> Dict[str, torch.Tensor]:
         """Activation buffers for one forward pass.  Attention operands are
@@ -83,6 +95,14 @@ class TransformerBlock:
                          ld_src=3 * self.hidden, stride_src=self.dh, ld_dst=self.dh,
                          stride_dst=t * self.dh)
 
+    def row_blocks(self, seq):
+        """Causal row blocks of one (head, sequence) pair: (first row, rows,
+        columns its rows can see).  Rows of block i only see columns below
+        the block's end, so the q k^T and P v products of block i stop there
+        and the softmax leaves the zero blocks beyond it unwritten."""
+        bs = seq if self.attn_block is None else min(self.attn_block, seq)
+        return [(r0, min(bs, seq - r0), min(seq, r0 + bs)) for r0 in range(0, seq, bs)]
+
     def attention_gemms_qk(self, buf, batch, seq):
         NH, dh = self.heads, self.dh
         qh, s = buf["qkv_h"], buf["scores"]
@@ -90,19 +110,22 @@ class TransformerBlock:
         head = qh.shape[1] * dh * es                       # bytes of one [tokens, dh] slab
         q = qh.data_ptr()
         k = q + NH * head
-        # S_i = q_i @ k_i^T
-        ops.gemm_strided_batched(q, dh, seq * dh, k, dh, seq * dh, True, s.data_ptr(), seq,
-                                 seq * seq, seq, seq, dh, NH * batch, device=qh.device)
+        # S_i[rows r0.., cols < n] = q_i[r0..] @ k_i[:n]^T for every pair i
+        for r0, m, n in self.row_blocks(seq):
+            ops.gemm_strided_batched(q + r0 * dh * es, dh, seq * dh, k, dh, seq * dh, True,
+                                     s.data_ptr() + r0 * seq * es, seq, seq * seq, m, n, dh,
+                                     NH * batch, device=qh.device)
 
     def attention_gemms_pv(self, buf, batch, seq):
         NH, dh = self.heads, self.dh
         qh, p, oh = buf["qkv_h"], buf["probs"], buf["o_h"]
         es = qh.element_size()
         v = qh.data_ptr() + 2 * NH * qh.shape[1] * dh * es
-        # o_i = P_i @ v_i
-        ops.gemm_strided_batched(p.data_ptr(), seq, seq * seq, v, dh, seq * dh, False,
-                                 oh.data_ptr(), dh, seq * dh, seq, dh, seq, NH * batch,
-                                 device=qh.device)
+        # o_i[rows r0..] = P_i[rows r0.., cols < n] @ v_i[:n] for every pair i
+        for r0, m, n in self.row_blocks(seq):
+            ops.gemm_strided_batched(p.data_ptr() + r0 * seq * es, seq, seq * seq, v, dh, seq * dh,
+                                     False, oh.data_ptr() + r0 * dh * es, dh, seq * dh, m, dh, n,
+                                     NH * batch, device=qh.device)
 
     def merge_heads(self, buf):
         oh = buf["o_h"]
@@ -116,8 +139,15 @@ class TransformerBlock:
         ops.layernorm_residual(x2, None, p["ln1_gamma"], p["ln1_beta"], self.eps, out=buf["a"])
 
     def softmax(self, buf, seq):
-        ops.row_softmax(buf["scores"], None, 1.0 / math.sqrt(self.dh), causal_q_len=seq,
-                        out=buf["probs"])
+        scale = 1.0 / math.sqrt(self.dh)
+        if self.attn_block is None:
+            ops.row_softmax(buf["scores"], None, scale, causal_q_len=seq, out=buf["probs"])
+        else:
+            # each row up to the end of its causal row block: the blocks
+            # beyond are never read by the P v products
+            ops.causal_softmax_trimmed(buf["scores"], scale, seq,
+                                       min(self.attn_block, 1 << (seq - 1).bit_length()),
+                                       out=buf["probs"])
 
     def layernorm2_residual(self, x2, buf):
         p = self.p

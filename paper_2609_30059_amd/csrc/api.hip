@@ -201,6 +201,42 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
   return e == hipSuccess ? FS_OK : hip_fail(e, "row_softmax launch");
 }
 
+fs_status fs_causal_softmax_trimmed(const void* x, int64_t ld_x, void* y, int64_t ld_y,
+                                    int64_t rows, int64_t cols, float scale,
+                                    int64_t causal_q_len, int64_t block, fs_dtype dtype,
+                                    hipStream_t stream) {
+  clear_msg();
+  if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
+  if (!std::isfinite(scale)) return fail(FS_ERR_BAD_ARGUMENT, "scale is not finite");
+  if (causal_q_len < 1)
+    return fail(FS_ERR_BAD_ARGUMENT, "causal_q_len=%lld must be >= 1", (long long)causal_q_len);
+  if (block < 1 || block > (int64_t(1) << 30) || (block & (block - 1)) != 0)
+    return fail(FS_ERR_BAD_ARGUMENT, "block=%lld must be a power of two", (long long)block);
+  fs_status st = check_shape(rows, cols, FS_SOFTMAX_MAX_COLS);
+  if (st != FS_OK) return st;
+  if ((st = check_ld("ld_x", ld_x, rows, cols)) != FS_OK) return st;
+  if ((st = check_ld("ld_y", ld_y, rows, cols)) != FS_OK) return st;
+  if (rows == 0 || cols == 0) return FS_OK;
+  if (!x || !y) return fail(FS_ERR_NULL_POINTER, "x and y are required");
+  const int es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(y, es))
+    return fail(FS_ERR_BAD_ARGUMENT, "pointers must be aligned to the element size");
+  const Extent ex = mat_extent(x, rows, cols, ld_x, es), ey = mat_extent(y, rows, cols, ld_y, es);
+  if (overlap(ey, ex) && !identical(ey, ex))
+    return fail(FS_ERR_ALIASING, "y partially overlaps x");
+
+  fs::SoftmaxArgs a{x, ld_x, nullptr, 0, dtype, y, ld_y, rows, cols, scale,
+                    causal_q_len, dtype, false};
+  a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es);
+  int shift = 0;
+  while ((int64_t(1) << shift) < block) ++shift;
+  a.trim_shift = shift;
+  int cus = 0;
+  if ((st = device_cus(&cus)) != FS_OK) return st;
+  hipError_t e = fs::launch_softmax(a, cus, stream);
+  return e == hipSuccess ? FS_OK : hip_fail(e, "causal_softmax_trimmed launch");
+}
+
 }  // extern "C"
 
 namespace {

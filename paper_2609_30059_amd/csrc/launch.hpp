@@ -30,6 +30,7 @@ struct SoftmaxArgs {
   int64_t causal_q_len;
   fs_dtype dtype;
   bool vec;
+  int trim_shift = -1;   // causal block trimming: log2(block), or -1 (write whole rows)
 };
 
 struct LayerNormArgs {

@@ -66,6 +66,19 @@ struct MaxF {
   }
 };
 
+// Stores the V values of the vector at column c0 that lie before column
+// `end` (a whole vector, a leading part of it, or nothing).
+template <typename T, int V>
+__device__ __forceinline__ void store_until(T* row, int c0, int end, const float (&o)[V]) {
+  if (c0 + V <= end) {
+    stv<T, V>(row + c0, o);
+  } else if (c0 < end) {
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (c0 + i < end) stv<T, 1>(row + c0 + i, &o[i]);
+  }
+}
+
 // T: storage type of x and y; MT: storage type of the mask (used when
 // HAS_MASK).  W waves per row; EPT elements per thread; VEC: 16-byte vector
 // path; G row groups per block (W == 1 only); R rows per group per trip --
@@ -74,7 +87,7 @@ struct MaxF {
 template <typename T, typename MT, bool HAS_MASK, int W, int EPT, bool VEC, int G, int R>
 __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m,
-    T* y, int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len) {
+    T* y, int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift) {
   constexpr int kThreads = 64 * W;
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;                       // vectors per thread
@@ -103,21 +116,24 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   for (; row0 < rows; row0 += step) {
     Raw<T, V> rx[R][NV];
     Raw<MT, V> rm[R][HAS_MASK ? NV : 1];
-    int lim[R];
+    int lim[R], wend[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       // rows past the end re-read the last row (in bounds) and are not stored
       const int64_t row = row0 + r < rows ? row0 + r : rows - 1;
       const T* xr = x + row * ld_x;
       const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
-      // last live column (inclusive) under the causal rule; -1 if none
-      int64_t limit = int64_t(cols) - 1;
+      // last live column (inclusive) under the causal rule; -1 if none; and
+      // the end of the written columns
+      int64_t limit = int64_t(cols) - 1, we = cols;
       if (q_len > 0) {
         int64_t pos = pos0 + r;
         if (pos >= q_len) pos = q_len >= R ? pos - q_len : pos % q_len;
         limit = pos + (cols - q_len);
+        if (trim_shift >= 0) we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
       }
       lim[r] = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+      wend[r] = int(we < cols ? (we < 0 ? 0 : we) : cols);
       // vectors past lim are not read: their address is clamped onto the
       // vector holding column lim (fetched by a live lane), then masked
       const int limv = lim[r] < 0 ? 0 : (lim[r] / V) * V;
@@ -234,12 +250,10 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
           const int c0 = (k * kThreads + tid) * V;
-          if (c0 < cols) {
-            float o[V];
+          float o[V];
 #pragma unroll
-            for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f[r];
-            stv<T, V>(yr + c0, o);
-          }
+          for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f[r];
+          store_until(yr, c0, wend[r], o);
         }
       }
     }
@@ -254,7 +268,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 template <typename T, typename MT, bool HAS_MASK, int W, bool VEC>
 __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
-    int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trips) {
+    int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift, int trips) {
   constexpr int kThreads = 64 * W;
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int U = 4;
@@ -265,8 +279,13 @@ __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const T* xr = x + row * ld_x;
     const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
-    const int64_t limit = q_len > 0 ? (row % q_len) + (cols - q_len) : int64_t(cols) - 1;
+    const int64_t pos = q_len > 0 ? row % q_len : 0;   // one division per (long) row
+    const int64_t limit = q_len > 0 ? pos + (cols - q_len) : int64_t(cols) - 1;
     const int lim = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+    int64_t we = cols;
+    if (q_len > 0 && trim_shift >= 0)
+      we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
+    const int wend = int(we < cols ? (we < 0 ? 0 : we) : cols);
     const int limv = lim < 0 ? 0 : (lim / V) * V;
 
     // logits of one trip: U vectors per lane, -inf past lim
@@ -334,7 +353,7 @@ __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
 #pragma unroll
         for (int i = 0; i < V; ++i)
           o[i] = __builtin_amdgcn_exp2f(fmaf(a[u * V + i], kLog2e, -M)) * inv_d;
-        if (c0 < cols) stv<T, V>(yr + c0, o);
+        store_until(yr, c0, wend, o);
       }
     }
   }
@@ -360,7 +379,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
     hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s,
                        static_cast<const T*>(a.x), a.ld_x, static_cast<const MT*>(a.mask),
                        a.ld_mask, static_cast<T*>(a.y), a.ld_y, a.rows, int(a.cols),
-                       a.scale, a.causal_q_len);
+                       a.scale, a.causal_q_len, a.trim_shift);
     return hipGetLastError();
   };
   // Variant ladder, in order: the first rung with at least min_w waves per row
@@ -394,7 +413,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
     hipLaunchKernelGGL((softmax_stream_kernel<T, MT, HAS_MASK, W, VEC>), dim3(unsigned(grid)),
                        dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
                        static_cast<const MT*>(a.mask), a.ld_mask, static_cast<T*>(a.y), a.ld_y,
-                       a.rows, int(a.cols), a.scale, a.causal_q_len, trips);
+                       a.rows, int(a.cols), a.scale, a.causal_q_len, a.trim_shift, trips);
     return hipGetLastError();
   }
 }

@@ -58,6 +58,33 @@ def _stream() -> int:
     return torch.cuda.current_stream().cuda_stream
 
 
+def _cuda(**tensors) -> None:
+    """Every tensor handed to a kernel must live on the current GPU."""
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a CUDA (HIP) device tensor")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, expected {dev}")
+    if dev is not None and dev.index is not None and dev.index != torch.cuda.current_device():
+        raise ValueError(f"tensors are on {dev}; make it the current device")
+
+
+def _like(out: torch.Tensor, x: torch.Tensor, name: str) -> int:
+    """out must have x's rows, columns and dtype; returns its row stride."""
+    if out.dtype != x.dtype:
+        raise ValueError(f"{name} must have dtype {x.dtype}")
+    r, c, ld = as_rows(out)
+    rx, cx, _ = as_rows(x)
+    if (r, c) != (rx, cx):
+        raise ValueError(f"{name} must be [{rx}, {cx}] as rows, got [{r}, {c}]")
+    return ld
+
+
 def _vec(t: Optional[torch.Tensor], cols: int, name: str):
     if t is None:
         return None
@@ -73,7 +100,8 @@ def pointwise_chain(x: torch.Tensor, bias: Optional[torch.Tensor] = None,
     rows, cols, ld_x = as_rows(x)
     if out is None:
         out = torch.empty_like(x, memory_format=torch.contiguous_format)
-    _, _, ld_y = as_rows(out)
+    _cuda(x=x, bias=bias, residual=residual, out=out)
+    ld_y = _like(out, x, "out")
     ld_r = 0
     if residual is not None:
         if residual.shape != x.shape or residual.dtype != x.dtype:
@@ -95,7 +123,8 @@ def row_softmax(x: torch.Tensor, mask: Optional[torch.Tensor] = None, scale: flo
     rows, cols, ld_x = as_rows(x)
     if out is None:
         out = torch.empty_like(x, memory_format=torch.contiguous_format)
-    _, _, ld_y = as_rows(out)
+    _cuda(x=x, mask=mask, out=out)
+    ld_y = _like(out, x, "out")
     ld_m, mdt = 0, fs_dtype(x)
     if mask is not None:
         if mask.shape != x.shape:
@@ -104,6 +133,23 @@ def row_softmax(x: torch.Tensor, mask: Optional[torch.Tensor] = None, scale: flo
     st = N.fs_row_softmax(x.data_ptr(), ld_x, _ptr(mask), ld_m, mdt, out.data_ptr(), ld_y, rows,
                           cols, float(scale), int(causal_q_len), fs_dtype(x), _stream())
     N.check("fs_row_softmax", st)
+    return out
+
+
+def causal_softmax_trimmed(x: torch.Tensor, scale: float, causal_q_len: int, block: int,
+                           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Causal softmax(x * scale) writing only the columns j < w(r) of each
+    row, w(r) = min(cols, (floor(s / block) + 1) * block + cols - q) with
+    s = r mod q  (fs_causal_softmax_trimmed); the rest of out is untouched."""
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    _cuda(x=x, out=out)
+    ld_y = _like(out, x, "out")
+    st = N.fs_causal_softmax_trimmed(x.data_ptr(), ld_x, out.data_ptr(), ld_y, rows, cols,
+                                     float(scale), int(causal_q_len), int(block), fs_dtype(x),
+                                     _stream())
+    N.check("fs_causal_softmax_trimmed", st)
     return out
 
 
@@ -127,7 +173,9 @@ def layernorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
         if residual_out is None and store_residual:
             residual_out = torch.empty_like(x, memory_format=torch.contiguous_format)
     if residual_out is not None:
-        ld_ro = as_rows(residual_out)[2]
+        ld_ro = _like(residual_out, x, "residual_out")
+    _cuda(x=x, residual=residual, gamma=gamma, beta=beta, out=out, residual_out=residual_out)
+    _like(out, x, "out")
     for v, n in ((gamma, "gamma"), (beta, "beta")):
         if v is not None and v.dtype != x.dtype:
             raise ValueError(f"{n} dtype must match x")
@@ -156,7 +204,9 @@ def rmsnorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
         if residual_out is None and store_residual:
             residual_out = torch.empty_like(x, memory_format=torch.contiguous_format)
     if residual_out is not None:
-        ld_ro = as_rows(residual_out)[2]
+        ld_ro = _like(residual_out, x, "residual_out")
+    _cuda(x=x, residual=residual, gamma=gamma, out=out, residual_out=residual_out)
+    _like(out, x, "out")
     if gamma is not None and gamma.dtype != x.dtype:
         raise ValueError("gamma dtype must match x")
     _vec(gamma, cols, "gamma")
@@ -174,6 +224,7 @@ def row_reduce(x: torch.Tensor, op: str = "sum", out: Optional[torch.Tensor] = N
         out = torch.empty(rows, dtype=torch.float32, device=x.device)
     if out.dtype != torch.float32 or out.numel() != rows or not out.is_contiguous():
         raise ValueError("out must be a contiguous float32 [rows] tensor")
+    _cuda(x=x, out=out)
     st = N.fs_row_reduce(x.data_ptr() if x.numel() else None, ld_x, fs_dtype(x), N.ROW_OPS[op],
                          out.data_ptr(), rows, cols, _stream())
     N.check("fs_row_reduce", st)
@@ -187,6 +238,7 @@ def row_argmax(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Ten
         out = torch.empty(rows, dtype=torch.int64, device=x.device)
     if out.dtype != torch.int64 or out.numel() != rows or not out.is_contiguous():
         raise ValueError("out must be a contiguous int64 [rows] tensor")
+    _cuda(x=x, out=out)
     st = N.fs_row_argmax(x.data_ptr(), ld_x, fs_dtype(x), out.data_ptr(), rows, cols, _stream())
     N.check("fs_row_argmax", st)
     return out
@@ -201,6 +253,7 @@ def gemm_epilogue_reduce(c: torch.Tensor, bias: Optional[torch.Tensor] = None,
         out = torch.empty(rows, dtype=torch.float32, device=c.device)
     if out.dtype != torch.float32 or out.numel() != rows or not out.is_contiguous():
         raise ValueError("out must be a contiguous float32 [rows] tensor")
+    _cuda(c=c, bias=bias, col_scale=col_scale, out=out)
     _vec(bias, cols, "bias")
     _vec(col_scale, cols, "col_scale")
     if col_scale is not None and col_scale.dtype != torch.float32:
@@ -222,6 +275,7 @@ def copy_strided(dst: torch.Tensor, src: torch.Tensor, rows: int, cols: int, bat
         raise ValueError("src and dst must have one dtype")
     if not (src.is_contiguous() and dst.is_contiguous()):
         raise ValueError("copy_strided addresses contiguous tensors")
+    _cuda(src=src, dst=dst)
     if rows > 0 and cols > 0 and batch > 0:
         for t, ld, st, name in ((src, ld_src, stride_src, "src"), (dst, ld_dst, stride_dst, "dst")):
             last = (batch - 1) * st + (rows - 1) * ld + cols
@@ -237,6 +291,7 @@ def copy_(dst: torch.Tensor, src: torch.Tensor) -> torch.Tensor:
     """Byte copy of src into dst with the calibration kernel (fs_copy)."""
     if not (src.is_contiguous() and dst.is_contiguous()):
         raise ValueError("copy_ needs contiguous tensors")
+    _cuda(src=src, dst=dst)
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() != nbytes:
         raise ValueError("size mismatch")
@@ -299,7 +354,10 @@ def gemm(a: torch.Tensor, b: torch.Tensor, bias: Optional[torch.Tensor] = None,
         raise ValueError(f"inner dimensions differ: {k} vs {kb}")
     if out is None:
         out = torch.empty((*a.shape[:-1], n), dtype=torch.bfloat16, device=a.device)
-    _, _, ldc = as_rows(out)
+    _cuda(a=a, b=b, bias=bias, out=out, col_scale=col_scale, c_in=c_in)
+    mo, no, ldc = as_rows(out)
+    if out.dtype != torch.bfloat16 or (mo, no) != (m, n):
+        raise ValueError(f"out must be bf16 [{m}, {n}] as rows")
     _vec(bias, n, "bias")
     if bias is not None and bias.dtype not in (torch.bfloat16, torch.float32):
         raise TypeError("bias must be bf16 or fp32")

@@ -284,3 +284,18 @@ def test_gemm_ex_validation():
     assert ge(beta=1.0, c_in=A + 8192, ld_cin=31) == 3
     assert ge(m=-1) == 2
     assert ge(m=0, a=NULL, b=NULL, c=NULL) == 0
+
+
+def test_causal_softmax_trimmed_validation():
+    ct = lambda **kw: N.fs_causal_softmax_trimmed(**{**dict(x=A, ld_x=512, y=B, ld_y=512, rows=64,  # noqa: E731
+                                                      cols=512, scale=0.125, causal_q_len=512,
+                                                      block=128, dtype=1, stream=None), **kw})
+    assert ct(x=NULL) == 1
+    assert ct(block=96) == 6                 # not a power of two
+    assert ct(block=0) == 6
+    assert ct(causal_q_len=0) == 6           # the trimming needs a causal rule
+    assert ct(scale=float("inf")) == 6
+    assert ct(ld_y=100) == 3
+    assert ct(dtype=9) == 4
+    assert ct(y=A + 2) == 5
+    assert ct(rows=0, x=NULL, y=NULL) == 0

@@ -15,9 +15,9 @@ pytestmark = pytest.mark.gpu
 STAGES = ("a", "qkv", "probs", "o", "att", "h1", "m", "u", "g", "d", "out")
 
 
-def run_block(d, heads, seqs):
+def run_block(d, heads, seqs, attn_block=None):
     params = {k: dev(d[k]) for k in fs.block.PARAM_NAMES}
-    blk = fs.TransformerBlock(params, heads=heads, eps=d["eps"])
+    blk = fs.TransformerBlock(params, heads=heads, eps=d["eps"], attn_block=attn_block)
     x = dev(d["x"])
     buf = blk.forward(x)
     torch.cuda.synchronize()
@@ -34,12 +34,16 @@ def run_block(d, heads, seqs):
 RESIDUAL_OPERANDS = {"h1": ("x", "att"), "out": ("h1", "d")}
 
 
-def compare(buf, ref, seqs, batch, seq, name, x64=None):
+def compare(buf, ref, seqs, batch, seq, name, x64=None, block=None):
     atol, rtol = TOL["bf16"]
     for st in STAGES:
         if st == "probs":
-            # device probs are head-major [heads, batch, seq, seq]
+            # device probs are head-major [heads, batch, seq, seq]; with
+            # causal row blocks, columns beyond a row's block are unwritten
             got = host64(buf["probs"][:, seqs].transpose(0, 1))
+            if block is not None:
+                w = oracle.causal_written_width(seq, seq, seq, block)
+                got = np.where(np.arange(seq)[None, :] < w[:, None], got, 0.0)
         else:
             got = host64(buf[st].view(batch, seq, -1)[seqs])
         want = ref[st]
@@ -56,6 +60,16 @@ def test_small_block_all_stages(seed):
     announce("block small", seed)
     buf, ref = run_block(d, 4, [0, 1, 2])
     compare(buf, ref, [0, 1, 2], 3, 64, f"small seed {seed}", d["x"].f64()[[0, 1, 2]])
+
+
+@pytest.mark.parametrize("attn_block", [1, 16, 32, 64])
+def test_small_block_causal_row_blocks(attn_block):
+    # the q k^T and P v products issued per causal row block, down to one row
+    d = fd.block_inputs(attn_block, batch=2, seq=64, hidden=256, heads=4, mlp=1024)
+    announce("block row blocks", attn_block)
+    buf, ref = run_block(d, 4, [0, 1], attn_block=attn_block)
+    compare(buf, ref, [0, 1], 2, 64, f"row block {attn_block}", d["x"].f64()[[0, 1]],
+            block=attn_block)
 
 
 @pytest.mark.parametrize("seed", SEEDS)

@@ -515,3 +515,32 @@ class TestStridedCopy:
         got = oracle.strided_copy(src, np.zeros(6), rows=1, cols=2, batch=3, ld_src=2,
                                   stride_src=0, ld_dst=2, stride_dst=2)
         np.testing.assert_array_equal(got, [7, 8, 7, 8, 7, 8])
+
+
+# ---------------------------------------------------------------------------
+# causal softmax trimmed to row blocks
+# ---------------------------------------------------------------------------
+class TestCausalWrittenWidth:
+    def test_hand_worked_widths(self):
+        # square, block 2: positions 0..5 write 2, 2, 4, 4, 6, 6 columns
+        np.testing.assert_array_equal(oracle.causal_written_width(6, 6, 6, 2), [2, 2, 4, 4, 6, 6])
+        # rows wrap every q_len rows (two heads of 3 positions)
+        np.testing.assert_array_equal(oracle.causal_written_width(6, 3, 3, 2), [2, 2, 3, 2, 2, 3])
+        # rectangular: 6 extra leading columns visible to every row
+        np.testing.assert_array_equal(oracle.causal_written_width(4, 10, 4, 2), [8, 8, 10, 10])
+
+    def test_special_blocks(self):
+        # block 1 writes exactly the live columns (the causal limit + 1)
+        rows, cols, q = 7, 9, 5
+        live = (~oracle.causal_mask(rows, cols, q)).sum(axis=1)
+        np.testing.assert_array_equal(oracle.causal_written_width(rows, cols, q, 1), live)
+        # a block at least as long as the row writes every column
+        np.testing.assert_array_equal(oracle.causal_written_width(5, 8, 5, 8), [8] * 5)
+
+    def test_live_columns_always_written(self):
+        for rows, cols, q, b in ((64, 64, 64, 16), (30, 40, 10, 4), (12, 5, 7, 2)):
+            w = oracle.causal_written_width(rows, cols, q, b)
+            live = ~oracle.causal_mask(rows, cols, q)
+            last_live = np.where(live.any(axis=1), cols - 1 - np.argmax(live[:, ::-1], axis=1), -1)
+            assert np.all(w > last_live)           # every live column lies below w
+            assert np.all(w <= cols)
