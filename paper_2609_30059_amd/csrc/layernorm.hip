@@ -21,6 +21,9 @@
 // FS_LN_MIN_WAVES waves per row; one-wave rows are batched to about
 // FS_LN_BATCH_ELEMS elements per lane per trip; the grid holds at most
 // FS_LN_GRID_SCALE/4 times the per-variant blocks-per-CU figure.
+#ifndef FS_LN_FULL_PATH
+#define FS_LN_FULL_PATH 1   // mask-free code for rows that fill every lane's slots
+#endif
 #ifndef FS_LN_MIN_WAVES
 #define FS_LN_MIN_WAVES 2
 #endif
@@ -67,6 +70,9 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   // and are masked
   const int clast = cols - V;
   const float inv_cols = 1.f / float(cols);
+  // rows that fill every slot of every lane need no masking (uniform)
+  const bool full = FS_LN_FULL_PATH && cols == kThreads * EPT;
+  const bool affine = FS_LN_FULL_PATH && gamma != nullptr && (RMS || beta != nullptr);
 
   Raw<T, V> rg[NV], rb[NV];
   auto load_affine = [&]() {
@@ -104,7 +110,6 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
     for (int r = 0; r < R; ++r) {
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
-        const bool in = (k * kThreads + tid) * V < cols;
         float xv[V];
         rx[r][k].unpack(xv);
         if constexpr (HAS_RES) {
@@ -114,7 +119,16 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
           for (int i = 0; i < V; ++i) xv[i] += rv[i];
         }
 #pragma unroll
-        for (int i = 0; i < V; ++i) h[r][k * V + i] = in ? xv[i] : 0.f;
+        for (int i = 0; i < V; ++i) h[r][k * V + i] = xv[i];
+      }
+      if (!full) {
+        // slots past the row end hold 0 (they re-read the row's last vector)
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const bool in = (k * kThreads + tid) * V < cols;
+#pragma unroll
+          for (int i = 0; i < V; ++i) h[r][k * V + i] = in ? h[r][k * V + i] : 0.f;
+        }
       }
       if (res_out && row0 + r < rows) {
         T* ro = res_out + (row0 + r) * ld_ro;
@@ -143,13 +157,21 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
         mean[r] = tot.p[r].s * inv_cols;
         // pass 2: squared deviations from the row mean, over the owned columns
         float m2 = 0.f;
+        if (full) {
 #pragma unroll
-        for (int k = 0; k < NV; ++k) {
-          const bool in = (k * kThreads + tid) * V < cols;
-#pragma unroll
-          for (int i = 0; i < V; ++i) {
-            const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
+          for (int i = 0; i < EPT; ++i) {
+            const float d = h[r][i] - mean[r];
             m2 = fmaf(d, d, m2);
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < NV; ++k) {
+            const bool in = (k * kThreads + tid) * V < cols;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+              const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
+              m2 = fmaf(d, d, m2);
+            }
           }
         }
         part.p[r] = SumP{m2};
@@ -164,24 +186,58 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
       const float rstd = rsqrtf(sq.p[r].s * inv_cols + eps);
       if (row0 + r < rows) {
         T* yr = y + (row0 + r) * ld_y;
+        // the affine form is uniform: one loop for gamma and beta both given
+        // (no per-element choice of 1 / 0), one for the other cases
+        if (affine) {
+          // keep gamma and beta packed between rows: unpacked copies hoisted
+          // out of the row loop would double their registers
+          if constexpr (kAffineResident) {
 #pragma unroll
-        for (int k = 0; k < NV; ++k) {
-          const int c0 = (k * kThreads + tid) * V;
-          float gv[V], bv[V];
-          if (gamma) rg[k].unpack(gv);
-          else {
+            for (int k = 0; k < NV; ++k) {
 #pragma unroll
-            for (int i = 0; i < V; ++i) gv[i] = 1.f;
+              for (int j = 0; j < Raw<T, V>::kWords; ++j) {
+                asm volatile("" : "+v"(rg[k].w[j]));
+                if constexpr (!RMS) asm volatile("" : "+v"(rb[k].w[j]));
+              }
+            }
           }
-          if (beta) rb[k].unpack(bv);
-          else {
 #pragma unroll
-            for (int i = 0; i < V; ++i) bv[i] = 0.f;
+          for (int k = 0; k < NV; ++k) {
+            const int c0 = (k * kThreads + tid) * V;
+            float gv[V], bv[V], o[V];
+            rg[k].unpack(gv);
+            if constexpr (RMS) {
+#pragma unroll
+              for (int i = 0; i < V; ++i) bv[i] = 0.f;     // RMSNorm has no beta
+            } else {
+              rb[k].unpack(bv);
+            }
+#pragma unroll
+            for (int i = 0; i < V; ++i)
+              o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, gv[i], bv[i]);
+            if (full || c0 < cols) stv<T, V>(yr + c0, o);
           }
-          float o[V];
+        } else {
 #pragma unroll
-          for (int i = 0; i < V; ++i) o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, gv[i], bv[i]);
-          if (c0 < cols) stv<T, V>(yr + c0, o);
+          for (int k = 0; k < NV; ++k) {
+            const int c0 = (k * kThreads + tid) * V;
+            float gv[V], bv[V];
+            if (gamma) rg[k].unpack(gv);
+            else {
+#pragma unroll
+              for (int i = 0; i < V; ++i) gv[i] = 1.f;
+            }
+            if (beta) rb[k].unpack(bv);
+            else {
+#pragma unroll
+              for (int i = 0; i < V; ++i) bv[i] = 0.f;
+            }
+            float o[V];
+#pragma unroll
+            for (int i = 0; i < V; ++i)
+              o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, gv[i], bv[i]);
+            if (c0 < cols) stv<T, V>(yr + c0, o);
+          }
         }
       }
     }

@@ -20,6 +20,9 @@
 // FS_SM_MIN_WAVES waves per row; one-wave rows are batched to about
 // FS_SM_BATCH_ELEMS elements per lane per trip; the grid holds at most
 // FS_SM_GRID_SCALE/4 times the per-variant blocks-per-CU figure.
+#ifndef FS_SM_FULL_PATH
+#define FS_SM_FULL_PATH 1   // no per-element mask for non-causal rows that fill every slot
+#endif
 #ifndef FS_SM_MIN_WAVES
 #define FS_SM_MIN_WAVES 2
 #endif
@@ -103,6 +106,9 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   // arithmetic) in scalar registers
   const int g = __builtin_amdgcn_readfirstlane(threadIdx.x / kThreads);
   int parity = 0;
+  // rows without a causal rule that fill every slot of every lane have no
+  // column to mask (uniform)
+  const bool whole = FS_SM_FULL_PATH && q_len == 0 && cols == kThreads * EPT;
 
   // causal position of row0 (row0 mod q_len), advanced by the loop step
   // without a division per row
@@ -170,8 +176,13 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 #pragma unroll
           for (int i = 0; i < V; ++i) xv[i] *= scale;
         }
+        if (whole) {
 #pragma unroll
-        for (int i = 0; i < V; ++i) a[r][k * V + i] = (c0 + i <= lim[r]) ? xv[i] : -INFINITY;
+          for (int i = 0; i < V; ++i) a[r][k * V + i] = xv[i];
+        } else {
+#pragma unroll
+          for (int i = 0; i < V; ++i) a[r][k * V + i] = (c0 + i <= lim[r]) ? xv[i] : -INFINITY;
+        }
       }
     }
 
