@@ -312,30 +312,56 @@ def main():
     setup_s = time.perf_counter() - t_setup
 
     nk = len(wl.kernels)
-    for _ in range(args.warmup):
-        wl.step()
+
+    def interval_pass(steps):
+        """Per-kernel intervals between events recorded after every kernel."""
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)]
+               for _ in range(steps)]
+        for s in range(steps):
+            evs[s][0].record()
+            wl.step(evs[s])
+        torch.cuda.synchronize()
+        return [sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)) / steps
+                for i in range(nk)]
+
+    # warmup (untimed); its per-kernel intervals pick the dominant kernel
+    if args.warmup > 0:
+        warm = interval_pass(args.warmup)
+        dom = max(range(nk), key=lambda i: warm[i])
+    else:
+        dom = max(range(nk), key=lambda i: wl.kernels[i][2])
     torch.cuda.synchronize()
 
-    # timed region: K steps, boundary events between consecutive kernels
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)]
+    # timed region: exactly K steps.  Events mark its two ends and bracket the
+    # dominant kernel of every step; no other event sits between kernels (an
+    # event costs the GPU about 3 us, so one after every kernel would inflate
+    # the step by about 10 %).
+    t_beg = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    dev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
+    dom_fn = wl.kernels[dom][3]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    t_beg.record()
     for s in range(args.steps):
-        evs[s][0].record()
-        wl.step(evs[s])
+        for i, (_, _, _, fn) in enumerate(wl.kernels):
+            if i == dom:
+                dev[s][0].record()
+                dom_fn()
+                dev[s][1].record()
+            else:
+                fn()
+    t_end.record()
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t0
-
-    per = [0.0] * nk
-    step_ms = 0.0
-    for s in range(args.steps):
-        for i in range(nk):
-            per[i] += evs[s][i].elapsed_time(evs[s][i + 1])
-        step_ms += evs[s][0].elapsed_time(evs[s][nk])
-    per = [p / args.steps for p in per]
-    step_ms /= args.steps
+    step_ms = t_beg.elapsed_time(t_end) / args.steps
+    dom_ms = sum(a.elapsed_time(b) for a, b in dev) / args.steps
     value = wl.step_bytes / (step_ms * 1e-3) / 1e9
+
+    # per-kernel breakdown (context, after the timed region): K more steps with
+    # an event after every kernel; each interval includes that event's cost
+    per = interval_pass(args.steps)
 
     traffic = load_traffic()
     per_kernel = {}
@@ -343,9 +369,8 @@ def main():
         gbs = nbytes / (ms * 1e-3) / 1e9
         per_kernel[name] = {"us": round(ms * 1e3, 2), "bytes": nbytes, "GB/s": round(gbs, 1),
                             "frac": round(gbs / PEAK_HBM_GBS, 4)}
-    dom = max(range(nk), key=lambda i: per[i])
     dname, dkind, dbytes, _ = wl.kernels[dom]
-    achieved = dbytes / (per[dom] * 1e-3) / 1e9
+    achieved = dbytes / (dom_ms * 1e-3) / 1e9
     t = traffic.get(dname)
     tr = None
     if t and t.get("source_hash") == source_hash(dkind):
@@ -376,8 +401,10 @@ def main():
         "roofline": {"kernel": dname, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": tr,
-                     "algorithmic_bytes": dbytes},
+                     "algorithmic_bytes": dbytes, "launch_us": round(dom_ms * 1e3, 2)},
         "per_kernel": per_kernel,
+        "per_kernel_note": "intervals between events recorded after every kernel, in a pass "
+                           "after the timed region; each includes the cost of one event",
         "copy_calibration_GBs": round(copy_gbs, 1),
         "context": {"block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
                     "gemm_cfg4_ms": round(wl.gemm_cfg4_ms, 3),
