@@ -22,7 +22,17 @@ separated from its previous launch by more than the 256 MB Infinity Cache of
 other traffic, so inputs come from HBM (pw_cfg1, 3 MiB, stays cache
 resident and is latency-bound).
 
-Prints one JSON line.
+Timing: the K timed steps are bracketed by two events; inside them only the
+dominant kernel (the longest, picked from the warmup steps) is bracketed, for
+`roofline.achieved`.  A HIP event costs the GPU about 3 us, so events after
+every kernel would lengthen the step by about 10 %; the per-kernel breakdown
+therefore comes from a separate pass after the timed region.
+
+Prints one JSON line.  Two GPU-free modes turn rocprofv3 CSV output of this
+script into the summaries under profiles/:
+  --report-trace STATS_CSV          per-kernel durations (Markdown table)
+  --write-traffic FETCH_CSV WRITE_CSV
+                                    HBM bytes per launch -> profiles/traffic.json
 """
 from __future__ import annotations
 
@@ -45,6 +55,98 @@ KERNEL_SOURCES = {
 }
 
 
+# Each bench kernel by its (demangled, anonymous-namespace-free) kernel name in
+# rocprofv3 output: the template arguments tell the launches apart.
+KERNEL_PATTERNS = {
+    "pw_cfg1": r"pointwise_kernel<float, 1, true,",
+    "sm_cfg2": r"softmax_kernel<unsigned short, unsigned short, true,",
+    "ln_cfg3": r"layernorm_kernel<unsigned short, true, false, 2,",
+    "ep_cfg4": r"epilogue_lds_kernel<unsigned short, unsigned short, 2,",
+    "blk_ln1": r"layernorm_kernel<unsigned short, false, false, 1,",
+    "blk_sm": r"softmax_kernel<unsigned short, unsigned short, false,",
+    "blk_ln2": r"layernorm_kernel<unsigned short, true, false, 1,",
+    "blk_gelu": r"pointwise_kernel<unsigned short, 1, false,",
+    "blk_res": r"pointwise_kernel<unsigned short, 0, true,",
+    "copy_1GiB": r"copy128_kernel",
+}
+KIND = {"pw_cfg1": "pw", "sm_cfg2": "sm", "ln_cfg3": "ln", "ep_cfg4": "ep", "blk_ln1": "ln",
+        "blk_sm": "sm", "blk_ln2": "ln", "blk_gelu": "pw", "blk_res": "pw"}
+# compulsory bytes per launch (block: batch 32, seq 512, hidden 1024, 16 heads, MLP 4096)
+_T, _H, _F, _NH, _S = 32 * 512, 1024, 4096, 16, 512
+STEP_BYTES = {
+    "pw_cfg1": 256 * 1024 * 4 * 3 + 1024 * 4,
+    "sm_cfg2": 8192 * 4096 * 2 * 3,
+    "ln_cfg3": 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
+    "ep_cfg4": 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
+    "blk_ln1": _T * _H * 2 * 2 + _H * 2 * 2,
+    "blk_sm": 32 * _NH * (_S * (_S + 1) // 2) * 2 + 32 * _NH * _S * _S * 2,
+    "blk_ln2": _T * _H * 2 * 4 + _H * 2 * 2,
+    "blk_gelu": _T * _F * 2 * 2 + _F * 2,
+    "blk_res": _T * _H * 2 * 3,
+    "copy_1GiB": 2 << 30,
+}
+
+
+def _match(names, label):
+    import re
+    hits = [n for n in names if re.search(KERNEL_PATTERNS[label], n)]
+    if len(hits) > 1:
+        raise ValueError(f"{label}: pattern matches {len(hits)} kernels: {hits}")
+    return hits[0] if hits else None
+
+
+def report_trace(stats_csv: str) -> None:
+    """Markdown table of the bench kernels' rocprofv3 durations."""
+    import csv
+    rows = {}
+    with open(stats_csv, newline="") as f:
+        for r in csv.DictReader(f):
+            rows[r["Name"].replace("(anonymous namespace)::", "")] = r
+    total = sum(float(r["TotalDurationNs"]) for r in rows.values())
+    print("| kernel | calls | avg us | min us | max us | % of GPU time | GB/s (avg) | % of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|")
+    for label in KERNEL_PATTERNS:
+        n = _match(rows, label)
+        if n is None:
+            continue
+        r = rows[n]
+        avg = float(r["AverageNs"])
+        gbs = STEP_BYTES[label] / avg
+        print(f"| {label} | {r['Calls']} | {avg / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+              f"{float(r['MaxNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.1f} | "
+              f"{gbs:.0f} | {100 * gbs / PEAK_HBM_GBS:.1f} |")
+
+
+def write_traffic(fetch_csv: str, write_csv: str, measured_at: str, cmd_fetch: str,
+                  cmd_write: str) -> dict:
+    """HBM bytes per launch of every bench kernel from FETCH_SIZE and
+    WRITE_SIZE runs, each counter scaled by what it reads for the 1 GiB
+    calibration copy of the same run; written to profiles/traffic.json with
+    the hash of each kernel's sources (bench.py reports a kernel's traffic
+    only while its sources still hash the same)."""
+    from paper_2609_30059_amd import tiers
+    prof = {}
+    tiers.read_counters(fetch_csv, prof)
+    tiers.read_counters(write_csv, prof)
+    fs_, ws_ = tiers.copy_scales(prof, KERNEL_PATTERNS["copy_1GiB"], float(1 << 30),
+                                 float(1 << 30))
+    out = {"fetch_scale": fs_, "write_scale": ws_, "measured_at": measured_at,
+           "command_fetch": cmd_fetch, "command_write": cmd_write}
+    for label in KERNEL_PATTERNS:
+        n = _match(prof, label)
+        if n is None or label not in KIND:
+            continue
+        p = prof[n]
+        out[label] = {"source_hash": source_hash(KIND[label]),
+                      "fetch_kib": round(p.fetch_kib, 1), "write_kib": round(p.write_kib, 1),
+                      "bytes_per_launch": round(p.hbm_bytes(fs_, ws_)),
+                      "algorithmic_bytes": STEP_BYTES[label]}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    return out
+
+
 def source_hash(kind: str) -> str:
     csrc = os.path.join(ROOT, "paper_2609_30059_amd", "csrc")
     h = hashlib.sha256()
@@ -63,6 +165,13 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of each sub-kernel's rows the CPU oracle baseline runs over")
+    ap.add_argument("--report-trace", metavar="STATS_CSV",
+                    help="print the bench kernels' durations from a rocprofv3 kernel-stats CSV")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic.json from FETCH_SIZE and WRITE_SIZE runs")
+    ap.add_argument("--measured-at", default="", help="commit the counter runs measured")
+    ap.add_argument("--commands", nargs=2, default=("", ""), metavar=("FETCH_CMD", "WRITE_CMD"),
+                    help="the rocprofv3 commands of the two counter runs (recorded)")
     return ap.parse_args()
 
 
@@ -171,6 +280,13 @@ class Workload:
                                         out=buf["out"])),
         ]
         self.step_bytes = sum(k[2] for k in self.kernels)
+        for name, _, nbytes, _ in self.kernels:
+            assert nbytes == STEP_BYTES[name], name
+        # one launch of each kernel, so that loading its code object is not
+        # part of any measured interval
+        for _, _, _, fn in self.kernels:
+            fn()
+        torch.cuda.synchronize()
 
     def step(self, events=None):
         for i, (_, _, _, fn) in enumerate(self.kernels):
@@ -299,6 +415,13 @@ def load_traffic():
 
 def main():
     args = parse()
+    if args.report_trace:
+        report_trace(args.report_trace)
+        return
+    if args.write_traffic:
+        out = write_traffic(*args.write_traffic, args.measured_at, *args.commands)
+        print(json.dumps(out, indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): every sub-kernel shards "
               f"by rows with no exchange, so each GPU of a larger job runs this same "
@@ -313,7 +436,7 @@ def main():
 
     nk = len(wl.kernels)
 
-    def interval_pass(steps):
+    def interval_pass(steps, reduce=lambda v: sum(v) / len(v)):
         """Per-kernel intervals between events recorded after every kernel."""
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)]
                for _ in range(steps)]
@@ -321,12 +444,13 @@ def main():
             evs[s][0].record()
             wl.step(evs[s])
         torch.cuda.synchronize()
-        return [sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)) / steps
+        return [reduce([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)])
                 for i in range(nk)]
 
-    # warmup (untimed); its per-kernel intervals pick the dominant kernel
+    # warmup (untimed); the medians of its per-kernel intervals pick the
+    # dominant kernel
     if args.warmup > 0:
-        warm = interval_pass(args.warmup)
+        warm = interval_pass(args.warmup, lambda v: sorted(v)[len(v) // 2])
         dom = max(range(nk), key=lambda i: warm[i])
     else:
         dom = max(range(nk), key=lambda i: wl.kernels[i][2])

@@ -5,6 +5,7 @@
 produces, next to this file,
   * libfusedsub.so -- the fused sub-kernels behind the C ABI of include/fusedsub.h
   * libfsgemm.so   -- the hipBLASLt GEMM wrapper of include/fsgemm.h
+  * issue_rate     -- the issue-rate calibration program of tiers.py
 
 Every HIP translation unit is compiled with the packed-FP32 target feature
 switched off (ordinary fp32 code only).  Objects go to ``_build/`` (ignored
@@ -36,6 +37,7 @@ HIP_FLAGS = [
 
 LIB_FUSEDSUB = os.path.join(HERE, "libfusedsub.so")
 LIB_FSGEMM = os.path.join(HERE, "libfsgemm.so")
+ISSUE_RATE = os.path.join(HERE, "issue_rate")     # calibration program of tiers.py
 
 
 def _hipcc() -> str:
@@ -78,7 +80,11 @@ def build(verbose: bool = False, jobs: int = 8) -> None:
                                "-D__HIP_PLATFORM_AMD__", f"-I{INCLUDE}", f"-I{ROCM}/include",
                                "-c", os.path.join(CSRC, "gemm_hipblaslt.cpp"), "-o", gemm_obj],
                         verbose)
+        probe = ex.submit(_run, [_hipcc(), *HIP_FLAGS, os.path.join(CSRC, "issue_rate.hip"),
+                                 "-o", ISSUE_RATE + ".tmp"], verbose)
         fut.result()
+        probe.result()
+    os.replace(ISSUE_RATE + ".tmp", ISSUE_RATE)
     _link(objs, LIB_FUSEDSUB, [], verbose)
     _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
           f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
@@ -98,7 +104,7 @@ def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8
 
 def clean() -> None:
     shutil.rmtree(BUILD, ignore_errors=True)
-    for p in (LIB_FUSEDSUB, LIB_FSGEMM):
+    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE):
         if os.path.exists(p):
             os.remove(p)
 

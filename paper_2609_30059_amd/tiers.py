@@ -17,9 +17,11 @@ duration t of a kernel-trace run:
              calibration dispatch of the same run);
   SOL_comp = the busiest issue pipe, as a fraction of its capacity at the
              2.4 GHz peak engine clock:
-               VALU  (4 (N_valu - N_mfma - N_trans) + 16 N_trans) / (1024 SIMDs * f * t)
-                     (a wave64 instruction occupies a 16-lane SIMD for 4
-                     cycles; fp32 transcendentals run at a quarter rate)
+               VALU  (2 (N_valu - N_mfma - N_trans) + 8 N_trans) / (1024 SIMDs * f * t)
+                     (issue costs measured on MI355X by csrc/issue_rate.hip:
+                     a wave64 fp32 FMA occupies a SIMD for 2.3 cycles -- the
+                     157 TFLOP/s fp32 vector peak without packed math -- and
+                     v_exp_f32 / v_rcp_f32 for 8.3, a quarter of that rate)
                SALU  N_salu / (256 CUs * f * t)      (one scalar issue per CU cycle)
                MFMA  MfmaUtil / 100                  (matrix-core busy cycles)
              from SQ_INSTS_VALU, SQ_INSTS_MFMA, SQ_INSTS_VALU_TRANS_F32,
@@ -46,6 +48,8 @@ HBM_PEAK_BYTES_PER_S = 8.0e12
 SIMDS = 1024                 # 256 CUs x 4 SIMDs
 CUS = 256
 CLOCK_HZ = 2.4e9             # peak engine clock
+VALU_CYCLES = 2.0            # SIMD cycles per wave64 VALU instruction
+TRANS_CYCLES = 8.0           # SIMD cycles per wave64 fp32 transcendental
 
 TIERS = ("near-optimal", "memory-bound", "compute-bound", "underutilized")
 
@@ -87,7 +91,7 @@ class KernelProfile:
         if "SQ_INSTS_VALU" in r:
             trans = r.get("SQ_INSTS_VALU_TRANS_F32", 0.0)
             plain = max(r["SQ_INSTS_VALU"] - r.get("SQ_INSTS_MFMA", 0.0) - trans, 0.0)
-            out["VALU"] = (4.0 * plain + 16.0 * trans) / (SIMDS * cyc)
+            out["VALU"] = (VALU_CYCLES * plain + TRANS_CYCLES * trans) / (SIMDS * cyc)
         if "SQ_INSTS_SALU" in r:
             out["SALU"] = r["SQ_INSTS_SALU"] / (CUS * cyc)
         if "MfmaUtil" in r:

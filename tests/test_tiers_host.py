@@ -35,7 +35,7 @@ def test_sol_from_scaled_counters():
     # reads (scale 2) and all the writes: 4.295 TB/s = 53.7 % of 8 TB/s
     cyc = 2.4e9 * 5e-4                                  # engine cycles in 0.5 ms
     p = T.KernelProfile("k", duration_ns=5e5, fetch_kib=(1 << 20) / 2, write_kib=1 << 20,
-                        raw={"SQ_INSTS_VALU": 0.1 * 1024 * cyc / 4 + 1000.0,
+                        raw={"SQ_INSTS_VALU": 0.1 * 1024 * cyc / T.VALU_CYCLES + 1000.0,
                              "SQ_INSTS_MFMA": 1000.0,      # counted among VALU, removed
                              "SQ_INSTS_SALU": 0.05 * 256 * cyc, "MfmaUtil": 2.0,
                              "VALUBusy": 130.0})          # context only, never the SOL
@@ -45,10 +45,13 @@ def test_sol_from_scaled_counters():
     assert math.isclose(pp["VALU"], 0.1) and math.isclose(pp["SALU"], 0.05)
     assert pp["MFMA"] == 0.02 and comp == pp["VALU"]
     assert T.classify(mem, comp) == "memory-bound"
-    # transcendentals cost four VALU issue slots
-    q = T.KernelProfile("t", duration_ns=5e5, raw={"SQ_INSTS_VALU": 1024 * cyc / 16,
-                                                   "SQ_INSTS_VALU_TRANS_F32": 1024 * cyc / 16})
+    # a transcendental costs four FMA issue slots (2 and 8 cycles per wave64)
+    assert (T.VALU_CYCLES, T.TRANS_CYCLES) == (2.0, 8.0)
+    q = T.KernelProfile("t", duration_ns=5e5, raw={"SQ_INSTS_VALU": 1024 * cyc / 8,
+                                                   "SQ_INSTS_VALU_TRANS_F32": 1024 * cyc / 8})
     assert math.isclose(q.pipes()["VALU"], 1.0)
+    q4 = T.KernelProfile("f", duration_ns=5e5, raw={"SQ_INSTS_VALU": 4 * 1024 * cyc / 8})
+    assert math.isclose(q4.pipes()["VALU"], 1.0)
     with pytest.raises(ValueError):
         T.KernelProfile("empty").sol()
 
@@ -81,12 +84,12 @@ def test_reads_rocprof_csv_and_calibrates(tmp_path):
     sm = prof["void fs::softmax_kernel<a>(b)"]
     assert sm.duration_ns == 100000 and sm.fetch_kib == 65536
     assert sm.raw["SQ_INSTS_VALU"] == 3840000             # per-dispatch average
-    # 4 * 3.84e6 / (1024 * 2.4e9 * 1e-4) = 6.25 %
+    # 2 * 3.84e6 / (1024 * 2.4e9 * 1e-4) = 3.125 %
     fs_, ws_ = T.copy_scales(prof, "copy128_kernel", float(1 << 30), float(1 << 30))
     assert fs_ == 2.0 and ws_ == 1.0
     rows = T.table([sm], fs_, ws_)
-    # (2 * 64 + 64) MiB in 100 us = 2013 GB/s = 25.2 % of 8 TB/s > VALU 6.25 %
-    assert rows[2] == ("| void fs::softmax_kernel<a>(b) | 100.0 | 2013 | 25.2 | 6.2 (VALU) | 90.0 "
+    # (2 * 64 + 64) MiB in 100 us = 2013 GB/s = 25.2 % of 8 TB/s > VALU 3.125 %
+    assert rows[2] == ("| void fs::softmax_kernel<a>(b) | 100.0 | 2013 | 25.2 | 3.1 (VALU) | 90.0 "
                        "| memory-bound |")
     with pytest.raises(ValueError):
         T.copy_scales(prof, "nothing", 1.0, 1.0)
