@@ -163,6 +163,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-reference", action="store_true",
+                    help="skip the same-size copies (profiling runs: every copy dispatch is "
+                         "then the 1 GiB calibration that scales the byte counters)")
     ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of each sub-kernel's rows the CPU oracle baseline runs over")
     ap.add_argument("--report-trace", metavar="STATS_CSV",
@@ -309,6 +312,34 @@ class Workload:
         ms = e0.elapsed_time(e1) / iters
         del src, dst
         return 2 * nbytes / (ms * 1e-3) / 1e9
+
+    def same_size_copies(self, sizes, reps):
+        """Median interval of a calibration copy moving the same number of
+        bytes as each kernel (half read, half written), timed like the
+        per-kernel pass (an event after every launch).  Successive copies
+        take different slices of 1 GiB buffers, so their inputs come from
+        HBM, not the Infinity Cache."""
+        torch, fs = self.torch, self.fs
+        span = 1 << 30
+        src = torch.empty(span, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(span, dtype=torch.uint8, device="cuda")
+        out = []
+        for nbytes in sizes:
+            half = (nbytes // 2 + 4095) // 4096 * 4096
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            off = 0
+            evs[0].record()
+            for i in range(reps):
+                if off + half > span:
+                    off = 0
+                fs.copy_(dst[off:off + half], src[off:off + half])
+                off += half
+                evs[i + 1].record()
+            torch.cuda.synchronize()
+            ts = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(reps))
+            out.append(ts[reps // 2])
+        del src, dst
+        return out
 
 
 # ---------------------------------------------------------------------------
@@ -486,13 +517,18 @@ def main():
     # per-kernel breakdown (context, after the timed region): K more steps with
     # an event after every kernel; each interval includes that event's cost
     per = interval_pass(args.steps)
+    # the practical ceiling of a kernel that moves as many bytes: a copy of
+    # that size, measured the same way
+    copies = ([float("nan")] * nk if args.no_copy_reference
+              else wl.same_size_copies([k[2] for k in wl.kernels], max(args.steps, 5)))
 
     traffic = load_traffic()
     per_kernel = {}
-    for (name, kind, nbytes, _), ms in zip(wl.kernels, per):
+    for (name, kind, nbytes, _), ms, cms in zip(wl.kernels, per, copies):
         gbs = nbytes / (ms * 1e-3) / 1e9
         per_kernel[name] = {"us": round(ms * 1e3, 2), "bytes": nbytes, "GB/s": round(gbs, 1),
-                            "frac": round(gbs / PEAK_HBM_GBS, 4)}
+                            "frac": round(gbs / PEAK_HBM_GBS, 4),
+                            "same_size_copy_us": None if cms != cms else round(cms * 1e3, 2)}
     dname, dkind, dbytes, _ = wl.kernels[dom]
     achieved = dbytes / (dom_ms * 1e-3) / 1e9
     t = traffic.get(dname)
@@ -528,7 +564,9 @@ def main():
                      "algorithmic_bytes": dbytes, "launch_us": round(dom_ms * 1e3, 2)},
         "per_kernel": per_kernel,
         "per_kernel_note": "intervals between events recorded after every kernel, in a pass "
-                           "after the timed region; each includes the cost of one event",
+                           "after the timed region; each includes the cost of one event. "
+                           "same_size_copy_us: the calibration copy moving the same bytes "
+                           "(half read, half written), timed the same way",
         "copy_calibration_GBs": round(copy_gbs, 1),
         "context": {"block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
                     "gemm_cfg4_ms": round(wl.gemm_cfg4_ms, 3),
