@@ -126,6 +126,25 @@ def _short(name: str) -> str:
     return name.replace("(anonymous namespace)::", "")
 
 
+def label(name: str) -> str:
+    """A table label: a kernel's name with its template arguments, without
+    the return type, namespace and parameter list (library kernels keep
+    their first 64 characters)."""
+    n = re.sub(r"^void ", "", name)
+    n = n.replace("fs::", "")
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0 and i > 0:
+            cut = i
+            break
+    n = n[:cut]
+    return n if len(n) <= 64 or "<" in n else n[:64] + "..."
+
+
 def read_kernel_stats(path: str, into: Dict[str, KernelProfile]) -> None:
     """Average durations from a ``*_kernel_stats.csv`` (--kernel-trace --stats)."""
     with open(path, newline="") as f:
@@ -189,7 +208,7 @@ def main(argv: Optional[List[str]] = None) -> int:
     fs_, ws_ = copy_scales(prof, a.calibration, a.calibration_bytes, a.calibration_bytes)
     print(f"FETCH_SIZE scale x{fs_:.4f}, WRITE_SIZE scale x{ws_:.4f}")
     by_time = sorted(prof.values(), key=lambda p: -p.duration_ns if p.duration_ns > 0 else 0.0)
-    for line in table(by_time, fs_, ws_, tie=a.tie):
+    for line in table(by_time, fs_, ws_, label=label, tie=a.tie):
         print(line)
     return 0
 
