@@ -36,15 +36,13 @@ struct MaxP {   // NaN-propagating maximum
 struct ArgP {
   float v;
   int i;
+  // written with selects only: early returns of the struct kept it in
+  // scratch memory
   __device__ __forceinline__ static ArgP combine(const ArgP& a, const ArgP& b) {
     const bool an = a.v != a.v, bn = b.v != b.v;
-    if (an || bn) {
-      if (an && bn) return a.i < b.i ? a : b;
-      return an ? a : b;
-    }
-    if (a.v > b.v) return a;
-    if (b.v > a.v) return b;
-    return a.i < b.i ? a : b;
+    const bool a_wins = an ? (!bn || a.i < b.i)
+                           : (!bn && (a.v > b.v || (a.v == b.v && a.i < b.i)));
+    return {a_wins ? a.v : b.v, a_wins ? a.i : b.i};
   }
   template <class F> __device__ __forceinline__ static ArgP map(const ArgP& a, F f) {
     return {f(a.v), __float_as_int(f(__int_as_float(a.i)))};
@@ -65,11 +63,23 @@ __device__ __forceinline__ typename AccOf<OP>::type identity() {
   else return ArgP{-INFINITY, 0x7fffffff};
 }
 
+// One step of an accumulator that sees its columns in increasing order.
+// Argmax keeps the first of equal values and the first NaN: it moves only to
+// a strictly larger value, or to a NaN while it holds none (`first` takes the
+// accumulator's first element whatever it is, -inf and NaN included).  Max
+// propagates NaN (v_maximum3_f32 on gfx950).
 template <int OP>
-__device__ __forceinline__ void accumulate(typename AccOf<OP>::type& acc, float v, int col) {
-  if constexpr (OP == kOpSum) acc.s += v;
-  else if constexpr (OP == kOpMax) acc = MaxP::combine(acc, MaxP{v});
-  else acc = ArgP::combine(acc, ArgP{v, col});
+__device__ __forceinline__ void accumulate(typename AccOf<OP>::type& acc, float v, int col,
+                                           bool first) {
+  if constexpr (OP == kOpSum) {
+    acc.s += v;
+  } else if constexpr (OP == kOpMax) {
+    acc.m = __builtin_elementwise_maximum(acc.m, v);
+  } else {
+    const bool upd = first || (!(v <= acc.v) && acc.v == acc.v);
+    acc.v = upd ? v : acc.v;
+    acc.i = upd ? col : acc.i;
+  }
 }
 
 template <typename T, int OP, int W, int G, bool VEC>
@@ -92,7 +102,13 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
 
   for (int64_t row = int64_t(blockIdx.x) * G + g; row < rows; row += int64_t(gridDim.x) * G) {
     const T* xr = x + row * ld_x;
-    P acc = identity<OP>();
+    // V independent accumulators, one per slot of a vector: each sees its
+    // columns in increasing order, and their chains run side by side (one
+    // chain through all of a lane's elements made max and argmax
+    // latency-bound, ten times slower than the sum)
+    P acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = identity<OP>();
     for (int t = 0; t < trips; ++t) {
       Raw<T, V> rv[U];
 #pragma unroll
@@ -104,15 +120,21 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int c0 = ((t * U + u) * kThreads + tid) * V;
+        // the lane's first vector holds its lowest columns; if it lies past
+        // the row end, so do all the lane's vectors
+        const bool first = t == 0 && u == 0;
         float v[V];
         rv[u].unpack(v);
         if (c0 < cols) {   // the whole vector is in the row (cols % V == 0 on this path)
 #pragma unroll
-          for (int i = 0; i < V; ++i) accumulate<OP>(acc, v[i], c0 + i);
+          for (int i = 0; i < V; ++i) accumulate<OP>(acc[i], v[i], c0 + i, first);
         }
       }
     }
-    const P tot = group_allreduce<W>(acc, lds[parity], wave, lane);
+    P lane_acc = acc[0];
+#pragma unroll
+    for (int i = 1; i < V; ++i) lane_acc = P::combine(lane_acc, acc[i]);
+    const P tot = group_allreduce<W>(lane_acc, lds[parity], wave, lane);
     parity ^= 1;
     if (tid == 0) {
       if constexpr (OP == kOpArg) out_i[row] = tot.i;
