@@ -424,15 +424,23 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   FS_LN(1, 8, 4, 8)
   FS_LN(1, 16, 4, 8)
   FS_LN(1, 32, 4, 8)
-  FS_LN(1, 64, 4, 8)
-  FS_LN(2, 32, 1, 16)
-  FS_LN(2, 64, 1, 16)
-  FS_LN(4, 16, 1, 8)
-  FS_LN(4, 32, 1, 8)
-  FS_LN(4, 64, 1, 8)
-  FS_LN(8, 8, 1, 4)
-  FS_LN(8, 16, 1, 4)
-  FS_LN(8, 32, 1, 4)
+  if constexpr (VEC) {
+    FS_LN(1, 64, 4, 8)
+    FS_LN(2, 32, 1, 16)
+    FS_LN(2, 64, 1, 16)
+    FS_LN(4, 16, 1, 8)
+    FS_LN(4, 32, 1, 8)
+    FS_LN(4, 64, 1, 8)
+    FS_LN(8, 8, 1, 4)
+    FS_LN(8, 16, 1, 4)
+    FS_LN(8, 32, 1, 4)
+  } else {
+    // element-wise loads: 64 elements per thread (or 32 at 8 waves with a
+    // residual) exceed the registers and spill, so wider rows take more
+    // waves and, past 8192 columns, the streamed kernel
+    FS_LN(2, 32, 1, 16)
+    FS_LN(4, 32, 1, 8)
+  }
 #undef FS_LN
   // longer rows: streamed, one 8-wave block per row
   {

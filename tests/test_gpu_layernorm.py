@@ -57,7 +57,10 @@ def test_cfg3_full_size_sampled(seed):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("cols", [1, 2, 7, 64, 100, 1024, 4096, 4099, 8192, 20000, 65536])
+# odd widths take the element-wise path: 4099 and 6001 the 2- and 4-wave
+# register rungs, 8195 and 12347 the streamed kernel
+@pytest.mark.parametrize("cols", [1, 2, 7, 64, 100, 1024, 4096, 4099, 6001, 8192, 8195, 12347,
+                                  20000, 65536])
 def test_widths(dtype, cols):
     rows = 9 if cols <= 8192 else 3
     d = fd.layernorm_inputs(cols, rows, cols, dtype)
@@ -168,7 +171,7 @@ def test_rmsnorm_five_seeds(seed):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("cols", [1, 7, 64, 1024, 4099, 8192, 20000])
+@pytest.mark.parametrize("cols", [1, 7, 64, 1024, 4099, 6001, 8192, 8195, 20000])
 def test_rmsnorm_widths(dtype, cols):
     d = fd.layernorm_inputs(cols + 1, 9 if cols <= 8192 else 3, cols, dtype)
     announce("rmsnorm width", cols, dtype)
