@@ -17,7 +17,7 @@
 #define FS_STRIDED_UNROLL 4
 #endif
 #ifndef FS_STRIDED_TILE_UNITS
-#define FS_STRIDED_TILE_UNITS 4096
+#define FS_STRIDED_TILE_UNITS 1024   // at most 256 * kMaxItems
 #endif
 #ifndef FS_STRIDED_BLOCKS_PER_CU
 #define FS_STRIDED_BLOCKS_PER_CU 8
@@ -25,6 +25,9 @@
 
 namespace fs {
 namespace {
+
+constexpr int kMaxItems = 8;   // items per thread per tile of the strided copy
+static_assert(FS_STRIDED_TILE_UNITS <= 256 * kMaxItems, "tile larger than a block's items");
 
 // Each wave copies whole chunks of 64 * C vectors (C 16-byte accesses per
 // lane, all loads issued before the stores) and strides over the chunks; the
@@ -60,38 +63,70 @@ __global__ __launch_bounds__(256) void copy8_kernel(const uint8_t* __restrict__ 
 
 
 // Batched strided 2-D copy (a layout transform such as a head split or
-// merge): dst[b, r, c] = src[b, r, c].  Work items are ordered (row, batch,
-// unit) with the unit (16 bytes, or one element) fastest, so the items of one
-// row of a head split read one contiguous source row and write whole 128-byte
-// segments.  A block walks tiles of kRB rows; its loads for FS_STRIDED_UNROLL
-// items are issued before their stores (indices past the tile are clamped
-// onto its last item and not stored).
-template <typename U>
+// merge): dst[b, r, c] = src[b, r, c].  A block copies tiles of rb rows; the
+// items of a tile are ordered (row, batch, unit) with the unit (16 bytes, or
+// one element) fastest, so the items of one row of a head split read one
+// contiguous source row and write whole 128-byte segments.  Every tile has
+// the same shape, so each thread splits its K items of a tile into (row,
+// batch, unit) once, before the tile loop, and keeps their offsets relative
+// to the tile's first row; the loop itself has no division.  All K loads of
+// a tile are issued before its stores (items past the last row re-read the
+// tile's first item and are not stored).
+template <typename U, int K>
 __global__ __launch_bounds__(256) void copy_strided_kernel(
     const U* __restrict__ src, int64_t ld_s, int64_t st_s, U* __restrict__ dst, int64_t ld_d,
     int64_t st_d, int64_t rows, int upr, int per_row, int rb) {
-  constexpr int UN = FS_STRIDED_UNROLL;
+  const int items = rb * per_row;
+  int64_t rel_s[K], rel_d[K];
+  int row_of[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int i0 = int(threadIdx.x) + k * 256;
+    const int i = i0 < items ? i0 : items - 1;
+    const int rr = i / per_row;
+    const int rem = i - rr * per_row;
+    const int bb = rem / upr;
+    const int c = rem - bb * upr;
+    rel_s[k] = bb * st_s + rr * ld_s + c;
+    rel_d[k] = bb * st_d + rr * ld_d + c;
+    row_of[k] = i0 < items ? rr : rb;     // rb: never stored
+  }
   for (int64_t r0 = int64_t(blockIdx.x) * rb; r0 < rows; r0 += int64_t(gridDim.x) * rb) {
-    const int nr = int(rows - r0 < rb ? rows - r0 : rb);
-    const int n = nr * per_row;
-    for (int j0 = threadIdx.x; j0 < n; j0 += 256 * UN) {
+    const U* s0 = src + r0 * ld_s;
+    U* d0 = dst + r0 * ld_d;
+    const int live_rows = int(rows - r0 < rb ? rows - r0 : rb);
+    U v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = s0[row_of[k] < live_rows ? rel_s[k] : 0];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      if (row_of[k] < live_rows) d0[rel_d[k]] = v[k];
+  }
+}
+
+// Rows of more than 256 * kMaxItems units: one row per block, the items of
+// the row in a loop.
+template <typename U>
+__global__ __launch_bounds__(256) void copy_strided_rows_kernel(
+    const U* __restrict__ src, int64_t ld_s, int64_t st_s, U* __restrict__ dst, int64_t ld_d,
+    int64_t st_d, int64_t rows, int upr, int per_row) {
+  constexpr int UN = FS_STRIDED_UNROLL;
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    for (int j0 = threadIdx.x; j0 < per_row; j0 += 256 * UN) {
       U v[UN];
       int64_t di[UN];
 #pragma unroll
       for (int u = 0; u < UN; ++u) {
         int j = j0 + u * 256;
-        j = j < n ? j : n - 1;
-        const int rr = j / per_row;
-        const int rem = j - rr * per_row;
-        const int b = rem / upr;
-        const int c = rem - b * upr;
-        const int64_t r = r0 + rr;
-        v[u] = src[b * st_s + r * ld_s + c];
-        di[u] = b * st_d + r * ld_d + c;
+        j = j < per_row ? j : per_row - 1;
+        const int bb = j / upr;
+        const int c = j - bb * upr;
+        v[u] = src[bb * st_s + r * ld_s + c];
+        di[u] = bb * st_d + r * ld_d + c;
       }
 #pragma unroll
       for (int u = 0; u < UN; ++u)
-        if (j0 + u * 256 < n) dst[di[u]] = v[u];
+        if (j0 + u * 256 < per_row) dst[di[u]] = v[u];
     }
   }
 }
@@ -126,19 +161,36 @@ hipError_t launch_copy_strided(const CopyStridedArgs& a, int cus, hipStream_t s)
   const int ue = vec ? 16 : es;                      // bytes per unit
   const int upr = int(a.cols * es / ue);
   const int per_row = int(a.batch) * upr;
-  int rb = FS_STRIDED_TILE_UNITS / per_row;
-  if (rb < 1) rb = 1;
-  int64_t grid = (a.rows + rb - 1) / rb;
   const int64_t cap = int64_t(cus) * FS_STRIDED_BLOCKS_PER_CU;
-  if (grid > cap) grid = cap;
   auto go = [&](auto* tag) {
     using U = std::remove_pointer_t<decltype(tag)>;
     const int64_t k = ue / es;                       // elements per unit
-    hipLaunchKernelGGL(copy_strided_kernel<U>, dim3(unsigned(grid)), dim3(256), 0, s,
-                       static_cast<const U*>(a.src), a.ld_src / k, a.stride_src / k,
-                       static_cast<U*>(a.dst), a.ld_dst / k, a.stride_dst / k, a.rows, upr,
-                       per_row, rb);
-    return hipGetLastError();
+    const U* sp = static_cast<const U*>(a.src);
+    U* dp = static_cast<U*>(a.dst);
+    if (per_row > 256 * kMaxItems) {
+      const int64_t grid = a.rows < cap ? a.rows : cap;
+      hipLaunchKernelGGL(copy_strided_rows_kernel<U>, dim3(unsigned(grid)), dim3(256), 0, s, sp,
+                         a.ld_src / k, a.stride_src / k, dp, a.ld_dst / k, a.stride_dst / k,
+                         a.rows, upr, per_row);
+      return hipGetLastError();
+    }
+    // rows per tile: as many as fill the tile's 256 * kMaxItems items
+    int rb = FS_STRIDED_TILE_UNITS / per_row;
+    if (rb < 1) rb = 1;
+    if (int64_t(rb) > a.rows) rb = int(a.rows);
+    const int items = rb * per_row;
+    int64_t grid = (a.rows + rb - 1) / rb;
+    if (grid > cap) grid = cap;
+    auto launch = [&](auto kern) {
+      hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(256), 0, s, sp, a.ld_src / k,
+                         a.stride_src / k, dp, a.ld_dst / k, a.stride_dst / k, a.rows, upr,
+                         per_row, rb);
+      return hipGetLastError();
+    };
+    if (items <= 256) return launch(copy_strided_kernel<U, 1>);
+    if (items <= 512) return launch(copy_strided_kernel<U, 2>);
+    if (items <= 1024) return launch(copy_strided_kernel<U, 4>);
+    return launch(copy_strided_kernel<U, kMaxItems>);
   };
   if (vec) return go(static_cast<u32x4*>(nullptr));
   if (es == 4) return go(static_cast<uint32_t*>(nullptr));
