@@ -1,0 +1,101 @@
+"""Host tests of bench.py's profile tooling: the kernel-name patterns that tell
+the bench kernels apart in rocprofv3 output, the compulsory-byte formulas, the
+traffic.json writer and the duration report."""
+import importlib.util
+import json
+import os
+
+import pytest
+
+from paper_2609_30059_amd import tiers as T
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+_spec = importlib.util.spec_from_file_location("bench", os.path.join(ROOT, "bench.py"))
+bench = importlib.util.module_from_spec(_spec)
+_spec.loader.exec_module(bench)
+
+# kernel names as rocprofv3 prints them (anonymous namespace removed), one per
+# bench kernel, plus library and runtime kernels that must match nothing
+NAMES = {
+    "pw_cfg1": "void fs::pointwise_kernel<float, 1, true, true, 1>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
+    "sm_cfg2": "void fs::softmax_kernel<unsigned short, unsigned short, true, 2, 32, true, 1, 1>(unsigned short const*, long)",
+    "ln_cfg3": "void fs::layernorm_kernel<unsigned short, true, false, 2, 32, true, 1, 1>(unsigned short const*, long)",
+    "ep_cfg4": "void fs::epilogue_lds_kernel<unsigned short, unsigned short, 2, 16, 2, 16, true>(unsigned short const*, long)",
+    "blk_ln1": "void fs::layernorm_kernel<unsigned short, false, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
+    "blk_sm": "void fs::softmax_kernel<unsigned short, unsigned short, false, 1, 8, true, 4, 2>(unsigned short const*, long)",
+    "blk_ln2": "void fs::layernorm_kernel<unsigned short, true, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
+    "blk_gelu": "void fs::pointwise_kernel<unsigned short, 1, false, true, 4>(unsigned short const*, long)",
+    "blk_res": "void fs::pointwise_kernel<unsigned short, 0, true, true, 4>(unsigned short const*, long)",
+    "copy_1GiB": "void fs::copy128_kernel<4>(unsigned int __vector(4) const*, unsigned int __vector(4)*, long)",
+}
+OTHERS = [
+    "void fs::copy_strided_kernel<unsigned int __vector(4), 4>(unsigned int __vector(4) const*, long)",
+    "Cijk_Ailk_Bljk_BBS_BH_Bias_HA_S_SAV_UserArgs_MT256x256x64_MI16x16x1_SN_LDSB1",
+    "__amd_rocclr_copyBuffer",
+]
+
+
+def test_every_bench_kernel_matches_exactly_one_name():
+    names = list(NAMES.values()) + OTHERS
+    for label in bench.KERNEL_PATTERNS:
+        assert bench._match(names, label) == NAMES[label], label
+    assert set(bench.KERNEL_PATTERNS) == set(NAMES)
+    with pytest.raises(ValueError):       # two candidates for one label
+        bench._match([NAMES["blk_ln1"], NAMES["blk_ln1"] + " "], "blk_ln1")
+
+
+def test_compulsory_bytes():
+    T_, H, F = 32 * 512, 1024, 4096
+    live = sum(p + 1 for p in range(512))                       # lower triangle with diagonal
+    assert live == 512 * 513 // 2
+    assert bench.STEP_BYTES["blk_sm"] == 32 * 16 * (live * 2 + 512 * 512 * 2)
+    assert bench.STEP_BYTES["blk_ln2"] == T_ * H * 2 * 4 + 2 * H * 2   # x, res in; y, res out
+    assert bench.STEP_BYTES["blk_gelu"] == T_ * F * 2 * 2 + F * 2
+    assert bench.STEP_BYTES["ep_cfg4"] == 8192 * 8192 * 2 + 8192 * 2 + 8192 * 4 + 8192 * 4
+    assert bench.STEP_BYTES["copy_1GiB"] == 2 << 30
+    assert set(bench.KIND) == set(bench.STEP_BYTES) - {"copy_1GiB"}
+
+
+def _counters(path, counter, per_label):
+    with open(path, "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value\n")
+        for i, (label, v) in enumerate(per_label.items()):
+            f.write(f'{i},"{NAMES[label]}",{counter},{v}\n')
+
+
+def test_write_traffic_scales_by_the_copy(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic.json"))
+    # the copy moves 1 GiB each way; FETCH_SIZE reads half of it, WRITE_SIZE all
+    fetch = {"copy_1GiB": 524288, "ln_cfg3": 131072, "ep_cfg4": 65536}
+    write = {"copy_1GiB": 1048576, "ln_cfg3": 262144, "ep_cfg4": 32}
+    _counters(tmp_path / "f.csv", "FETCH_SIZE", fetch)
+    _counters(tmp_path / "w.csv", "WRITE_SIZE", write)
+    out = bench.write_traffic(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "abc", "F", "W")
+    assert out["fetch_scale"] == 2.0 and out["write_scale"] == 1.0
+    assert out["ln_cfg3"]["bytes_per_launch"] == (2 * 131072 + 262144) * 1024
+    assert out["ep_cfg4"]["bytes_per_launch"] == (2 * 65536 + 32) * 1024
+    assert out["ln_cfg3"]["source_hash"] == bench.source_hash("ln")
+    assert "pw_cfg1" not in out and "copy_1GiB" not in out
+    assert json.load(open(tmp_path / "traffic.json"))["measured_at"] == "abc"
+
+
+def test_report_trace(tmp_path, capsys):
+    p = tmp_path / "s.csv"
+    p.write_text('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs"\n'
+                 f'"{NAMES["ln_cfg3"]}",4,352000,88000,80,87000,89000\n'
+                 f'"{OTHERS[1]}",1,88000,88000,20,88000,88000\n')
+    bench.report_trace(str(p))
+    rows = [l for l in capsys.readouterr().out.splitlines() if l.startswith("| ln_cfg3")]
+    gbs = bench.STEP_BYTES["ln_cfg3"] / 88000
+    assert rows == [f"| ln_cfg3 | 4 | 88.00 | 87.00 | 89.00 | 80.0 | {gbs:.0f} | "
+                    f"{100 * gbs / 8000:.1f} |"]
+
+
+def test_tier_labels():
+    assert T.label("void fs::layernorm_kernel<unsigned short, true, false>(unsigned short const*, long)") \
+        == "layernorm_kernel<unsigned short, true, false>"
+    assert T.label("void fs::copy_strided_kernel<unsigned int __vector(4), 4>(int)") \
+        == "copy_strided_kernel<unsigned int __vector(4), 4>"
+    long_name = "Cijk_" + "A" * 100
+    assert T.label(long_name) == long_name[:64] + "..."
+    assert T.label("__amd_rocclr_copyBuffer") == "__amd_rocclr_copyBuffer"
