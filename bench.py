@@ -58,7 +58,8 @@ KERNEL_SOURCES = {
 # Each bench kernel by its (demangled, anonymous-namespace-free) kernel name in
 # rocprofv3 output: the template arguments tell the launches apart.
 KERNEL_PATTERNS = {
-    "pw_cfg1": r"pointwise_kernel<float, 1, true,",
+    "pw_cfg1": r"pointwise_kernel<float, 1, true, true, 1>",       # one row per trip
+    "pw_cfg1_bw": r"pointwise_kernel<float, 1, true, true, 4>",    # four rows per trip
     "sm_cfg2": r"softmax_kernel<unsigned short, unsigned short, true,",
     "ln_cfg3": r"layernorm_kernel<unsigned short, true, false, 2,",
     "ep_cfg4": r"epilogue_lds_kernel<unsigned short, unsigned short, 2,",
@@ -69,12 +70,13 @@ KERNEL_PATTERNS = {
     "blk_res": r"pointwise_kernel<unsigned short, 0, true,",
     "copy_1GiB": r"copy128_kernel",
 }
-KIND = {"pw_cfg1": "pw", "sm_cfg2": "sm", "ln_cfg3": "ln", "ep_cfg4": "ep", "blk_ln1": "ln",
+KIND = {"pw_cfg1": "pw", "pw_cfg1_bw": "pw", "sm_cfg2": "sm", "ln_cfg3": "ln", "ep_cfg4": "ep", "blk_ln1": "ln",
         "blk_sm": "sm", "blk_ln2": "ln", "blk_gelu": "pw", "blk_res": "pw"}
 # compulsory bytes per launch (block: batch 32, seq 512, hidden 1024, 16 heads, MLP 4096)
 _T, _H, _F, _NH, _S = 32 * 512, 1024, 4096, 16, 512
 STEP_BYTES = {
     "pw_cfg1": 256 * 1024 * 4 * 3 + 1024 * 4,
+    "pw_cfg1_bw": 262144 * 1024 * 4 * 3 + 1024 * 4,    # context, not in the step
     "sm_cfg2": 8192 * 4096 * 2 * 3,
     "ln_cfg3": 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
     "ep_cfg4": 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
@@ -204,6 +206,11 @@ class Workload:
         self.host["cfg1"] = h1
         self.pw = dict(x=d(h1["x"]), b=d(h1["bias"]), r=d(h1["residual"]), s=h1["scale"])
         self.pw["y"] = torch.empty_like(self.pw["x"])
+        # the same chain at bandwidth scale, [262144, 1024] (the [256, 1024]
+        # draws repeated), measured as context outside the step
+        reps = 262144 // 256
+        self.pwbw = dict(x=self.pw["x"].repeat(reps, 1), r=self.pw["r"].repeat(reps, 1))
+        self.pwbw["y"] = torch.empty_like(self.pwbw["x"])
         # cfg2
         h2 = fd.make_inputs("cfg2", seed)
         self.host["cfg2"] = h2
@@ -312,6 +319,25 @@ class Workload:
         ms = e0.elapsed_time(e1) / iters
         del src, dst
         return 2 * nbytes / (ms * 1e-3) / 1e9
+
+    def pointwise_bandwidth_scale(self, reps):
+        """Median launch interval of the fp32 chain at [262144, 1024] (3 GiB
+        moved): the 3 MiB workload is latency-bound, this one carries the
+        chain's bandwidth.  Each launch is bracketed by its own two events."""
+        torch, fs, p = self.torch, self.fs, self.pwbw
+        fn = lambda: fs.pointwise_chain(p["x"], self.pw["b"], p["r"], self.pw["s"], "gelu_erf",
+                                        out=p["y"])
+        fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) for a, b in evs)
+        return ts[reps // 2]
 
     def same_size_copies(self, sizes, reps):
         """Median interval of a calibration copy moving the same number of
@@ -522,6 +548,9 @@ def main():
     copies = ([float("nan")] * nk if args.no_copy_reference
               else wl.same_size_copies([k[2] for k in wl.kernels], max(args.steps, 5)))
 
+    bw_ms = wl.pointwise_bandwidth_scale(max(args.steps // 5, 5))
+    bw_bytes = STEP_BYTES["pw_cfg1_bw"]
+
     traffic = load_traffic()
     per_kernel = {}
     for (name, kind, nbytes, _), ms, cms in zip(wl.kernels, per, copies):
@@ -568,7 +597,12 @@ def main():
                            "same_size_copy_us: the calibration copy moving the same bytes "
                            "(half read, half written), timed the same way",
         "copy_calibration_GBs": round(copy_gbs, 1),
-        "context": {"block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
+        "context": {"pointwise_bandwidth_scale": {
+                        "shape": [262144, 1024], "dtype": "f32", "bytes": bw_bytes,
+                        "us": round(bw_ms * 1e3, 2),
+                        "GB/s": round(bw_bytes / (bw_ms * 1e-3) / 1e9, 1),
+                        "frac": round(bw_bytes / (bw_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+                    "block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
                     "gemm_cfg4_ms": round(wl.gemm_cfg4_ms, 3),
                     "wall_s_timed_region": round(wall_s, 4), "setup_s": round(setup_s, 1),
                     "paper_geomean_speedups_vs_torch_compile_H200":

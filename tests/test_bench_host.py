@@ -18,6 +18,7 @@ _spec.loader.exec_module(bench)
 # bench kernel, plus library and runtime kernels that must match nothing
 NAMES = {
     "pw_cfg1": "void fs::pointwise_kernel<float, 1, true, true, 1>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
+    "pw_cfg1_bw": "void fs::pointwise_kernel<float, 1, true, true, 4>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
     "sm_cfg2": "void fs::softmax_kernel<unsigned short, unsigned short, true, 2, 32, true, 1, 1>(unsigned short const*, long)",
     "ln_cfg3": "void fs::layernorm_kernel<unsigned short, true, false, 2, 32, true, 1, 1>(unsigned short const*, long)",
     "ep_cfg4": "void fs::epilogue_lds_kernel<unsigned short, unsigned short, 2, 16, 2, 16, true>(unsigned short const*, long)",
@@ -53,6 +54,7 @@ def test_compulsory_bytes():
     assert bench.STEP_BYTES["blk_gelu"] == T_ * F * 2 * 2 + F * 2
     assert bench.STEP_BYTES["ep_cfg4"] == 8192 * 8192 * 2 + 8192 * 2 + 8192 * 4 + 8192 * 4
     assert bench.STEP_BYTES["copy_1GiB"] == 2 << 30
+    assert bench.STEP_BYTES["pw_cfg1_bw"] == 3 * (1 << 30) + 4096
     assert set(bench.KIND) == set(bench.STEP_BYTES) - {"copy_1GiB"}
 
 
