@@ -101,3 +101,12 @@ def test_tier_labels():
     long_name = "Cijk_" + "A" * 100
     assert T.label(long_name) == long_name[:64] + "..."
     assert T.label("__amd_rocclr_copyBuffer") == "__amd_rocclr_copyBuffer"
+
+
+def test_more_than_one_gpu_exits_with_the_reason():
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
