@@ -2,15 +2,15 @@
 """Benchmark of the fused sub-kernels on one MI355X.
 
 One step = one launch of every fused sub-kernel at its workload shape:
-  pw_cfg1    pointwise GELU_erf(x*s + b) + r, fp32 [256, 1024]
-  sm_cfg2    row softmax, scale + bf16 additive mask, bf16 [8192, 4096]
-  ln_cfg3    LayerNorm + residual, bf16 [16384, 4096]
-  ep_cfg4    GEMM epilogue (+bias, *scale, sigmoid, row sum) on C bf16 [8192, 8192]
-  blk_ln1    block LayerNorm 1, bf16 [16384, 1024]
-  blk_sm     block causal softmax, bf16 [32, 16, 512, 512], scale 1/8
-  blk_ln2    block LayerNorm 2 + residual, bf16 [16384, 1024]
-  blk_gelu   block bias + GELU_erf, bf16 [16384, 4096]
-  blk_res    block residual add, bf16 [16384, 1024]
+  pw_256x1024     pointwise GELU_erf(x*s + b) + r, fp32 [256, 1024]
+  sm_8192x4096    row softmax, scale + bf16 additive mask, bf16 [8192, 4096]
+  ln_16384x4096   LayerNorm + residual, bf16 [16384, 4096]
+  ep_8192x8192    GEMM epilogue (+bias, *scale, sigmoid, row sum) on C bf16 [8192, 8192]
+  blk_ln1         block LayerNorm 1, bf16 [16384, 1024]
+  blk_sm          block causal softmax, bf16 [32, 16, 512, 512], scale 1/8
+  blk_ln2         block LayerNorm 2 + residual, bf16 [16384, 1024]
+  blk_gelu        block bias + GELU_erf, bf16 [16384, 4096]
+  blk_res         block residual add, bf16 [16384, 1024]
 The GEMMs (the fixed library calls) run once before timing to produce the
 resident inputs of the epilogue and block sub-kernels; they are reported
 separately as context, never inside `value`.
@@ -19,7 +19,7 @@ separately as context, never inside `value`.
 written once; the causal upper triangle is not read) / step time, in GB/s.
 Inputs are resident in HBM when timing starts.  Every kernel in a step is
 separated from its previous launch by more than the 256 MB Infinity Cache of
-other traffic, so inputs come from HBM (pw_cfg1, 3 MiB, stays cache
+other traffic, so inputs come from HBM (pw_256x1024, 3 MiB, stays cache
 resident and is latency-bound).
 
 Timing: the K timed steps are bracketed by two events; inside them only the
@@ -58,11 +58,11 @@ KERNEL_SOURCES = {
 # Each bench kernel by its (demangled, anonymous-namespace-free) kernel name in
 # rocprofv3 output: the template arguments tell the launches apart.
 KERNEL_PATTERNS = {
-    "pw_cfg1": r"pointwise_kernel<float, 1, true, true, 1>",       # one row per trip
-    "pw_cfg1_bw": r"pointwise_kernel<float, 1, true, true, 4>",    # four rows per trip
-    "sm_cfg2": r"softmax_kernel<unsigned short, unsigned short, true,",
-    "ln_cfg3": r"layernorm_kernel<unsigned short, true, false, 2,",
-    "ep_cfg4": r"epilogue_lds_kernel<unsigned short, unsigned short, 2,",
+    "pw_256x1024": r"pointwise_kernel<float, 1, true, true, 1>",       # one row per trip
+    "pw_262144x1024": r"pointwise_kernel<float, 1, true, true, 4>",    # four rows per trip
+    "sm_8192x4096": r"softmax_kernel<unsigned short, unsigned short, true,",
+    "ln_16384x4096": r"layernorm_kernel<unsigned short, true, false, 2,",
+    "ep_8192x8192": r"epilogue_lds_kernel<unsigned short, unsigned short, 2,",
     "blk_ln1": r"layernorm_kernel<unsigned short, false, false, 1,",
     "blk_sm": r"softmax_kernel<unsigned short, unsigned short, false,",
     "blk_ln2": r"layernorm_kernel<unsigned short, true, false, 1,",
@@ -70,16 +70,17 @@ KERNEL_PATTERNS = {
     "blk_res": r"pointwise_kernel<unsigned short, 0, true,",
     "copy_1GiB": r"copy128_kernel",
 }
-KIND = {"pw_cfg1": "pw", "pw_cfg1_bw": "pw", "sm_cfg2": "sm", "ln_cfg3": "ln", "ep_cfg4": "ep", "blk_ln1": "ln",
-        "blk_sm": "sm", "blk_ln2": "ln", "blk_gelu": "pw", "blk_res": "pw"}
+KIND = {"pw_256x1024": "pw", "pw_262144x1024": "pw", "sm_8192x4096": "sm",
+        "ln_16384x4096": "ln", "ep_8192x8192": "ep", "blk_ln1": "ln", "blk_sm": "sm",
+        "blk_ln2": "ln", "blk_gelu": "pw", "blk_res": "pw"}
 # compulsory bytes per launch (block: batch 32, seq 512, hidden 1024, 16 heads, MLP 4096)
 _T, _H, _F, _NH, _S = 32 * 512, 1024, 4096, 16, 512
 STEP_BYTES = {
-    "pw_cfg1": 256 * 1024 * 4 * 3 + 1024 * 4,
-    "pw_cfg1_bw": 262144 * 1024 * 4 * 3 + 1024 * 4,    # context, not in the step
-    "sm_cfg2": 8192 * 4096 * 2 * 3,
-    "ln_cfg3": 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
-    "ep_cfg4": 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
+    "pw_256x1024": 256 * 1024 * 4 * 3 + 1024 * 4,
+    "pw_262144x1024": 262144 * 1024 * 4 * 3 + 1024 * 4,    # context, not in the step
+    "sm_8192x4096": 8192 * 4096 * 2 * 3,
+    "ln_16384x4096": 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
+    "ep_8192x8192": 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
     "blk_ln1": _T * _H * 2 * 2 + _H * 2 * 2,
     "blk_sm": 32 * _NH * (_S * (_S + 1) // 2) * 2 + 32 * _NH * _S * _S * 2,
     "blk_ln2": _T * _H * 2 * 4 + _H * 2 * 2,
@@ -201,9 +202,9 @@ class Workload:
                 return torch.from_numpy(t.data).to(dev)
             return torch.from_numpy(t.data.view(np.int16)).view(torch.bfloat16).to(dev)
 
-        # cfg1
-        h1 = fd.make_inputs("cfg1", seed)
-        self.host["cfg1"] = h1
+        # pointwise_256x1024
+        h1 = fd.make_inputs("pointwise_256x1024", seed)
+        self.host["pointwise_256x1024"] = h1
         self.pw = dict(x=d(h1["x"]), b=d(h1["bias"]), r=d(h1["residual"]), s=h1["scale"])
         self.pw["y"] = torch.empty_like(self.pw["x"])
         # the same chain at bandwidth scale, [262144, 1024] (the [256, 1024]
@@ -211,21 +212,21 @@ class Workload:
         reps = 262144 // 256
         self.pwbw = dict(x=self.pw["x"].repeat(reps, 1), r=self.pw["r"].repeat(reps, 1))
         self.pwbw["y"] = torch.empty_like(self.pwbw["x"])
-        # cfg2
-        h2 = fd.make_inputs("cfg2", seed)
-        self.host["cfg2"] = h2
+        # softmax_8192x4096
+        h2 = fd.make_inputs("softmax_8192x4096", seed)
+        self.host["softmax_8192x4096"] = h2
         self.sm = dict(x=d(h2["x"]), m=d(h2["mask"]), s=h2["scale"])
         self.sm["y"] = torch.empty_like(self.sm["x"])
-        # cfg3
-        h3 = fd.make_inputs("cfg3", seed)
-        self.host["cfg3"] = h3
+        # layernorm_16384x4096
+        h3 = fd.make_inputs("layernorm_16384x4096", seed)
+        self.host["layernorm_16384x4096"] = h3
         self.ln = dict(x=d(h3["x"]), r=d(h3["residual"]), g=d(h3["gamma"]), b=d(h3["beta"]),
                        eps=h3["eps"])
         self.ln["y"] = torch.empty_like(self.ln["x"])
         self.ln["ro"] = torch.empty_like(self.ln["x"])
-        # cfg4: GEMM once (library call), then the epilogue on its output
-        h4 = fd.make_inputs("cfg4", seed)
-        self.host["cfg4"] = h4
+        # GEMM [8192, 4096] x [4096, 8192] once (library call), then the epilogue on its output
+        h4 = fd.make_inputs("gemm_epilogue_8192x8192x4096", seed)
+        self.host["gemm_epilogue_8192x8192x4096"] = h4
         a, b = d(h4["a"]), d(h4["b"])
         self.ep = dict(bias=d(h4["bias"]), scale=d(h4["col_scale"]))
         self.ep["c"] = fs.gemm(a, b)
@@ -235,11 +236,11 @@ class Workload:
         for _ in range(3):
             fs.gemm(a, b, out=self.ep["c"])
         torch.cuda.synchronize()
-        self.gemm_cfg4_ms = (time.perf_counter() - t0) / 3 * 1e3
+        self.gemm_8192x8192x4096_ms = (time.perf_counter() - t0) / 3 * 1e3
         del a, b
-        # cfg5: one full forward pass makes every block sub-kernel input resident
-        h5 = fd.make_inputs("cfg5", seed)
-        self.host["cfg5"] = {k: h5[k] for k in ("x", "eps", "heads")}
+        # block_32x512x1024: one full forward pass makes every block sub-kernel input resident
+        h5 = fd.make_inputs("block_32x512x1024", seed)
+        self.host["block_32x512x1024"] = {k: h5[k] for k in ("x", "eps", "heads")}
         params = {k: d(h5[k]) for k in fs.block.PARAM_NAMES}
         self.blk = fs.TransformerBlock(params, heads=h5["heads"], eps=h5["eps"])
         self.bx = d(h5["x"])
@@ -261,16 +262,16 @@ class Workload:
         x2 = self.bx.view(T, H)
         buf = self.buf
         self.kernels = [
-            ("pw_cfg1", "pw", 256 * 1024 * 4 * 3 + 1024 * 4,
+            ("pw_256x1024", "pw", 256 * 1024 * 4 * 3 + 1024 * 4,
              lambda: fs.pointwise_chain(self.pw["x"], self.pw["b"], self.pw["r"], self.pw["s"],
                                         "gelu_erf", out=self.pw["y"])),
-            ("sm_cfg2", "sm", 8192 * 4096 * 2 * 3,
+            ("sm_8192x4096", "sm", 8192 * 4096 * 2 * 3,
              lambda: fs.row_softmax(self.sm["x"], self.sm["m"], self.sm["s"], out=self.sm["y"])),
-            ("ln_cfg3", "ln", 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
+            ("ln_16384x4096", "ln", 16384 * 4096 * 2 * 4 + 4096 * 2 * 2,
              lambda: fs.layernorm_residual(self.ln["x"], self.ln["r"], self.ln["g"], self.ln["b"],
                                            self.ln["eps"], out=self.ln["y"],
                                            residual_out=self.ln["ro"])),
-            ("ep_cfg4", "ep", 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
+            ("ep_8192x8192", "ep", 8192 * 8192 * 2 + 8192 * (2 + 4) + 8192 * 4,
              lambda: fs.gemm_epilogue_reduce(self.ep["c"], self.ep["bias"], self.ep["scale"],
                                              "sigmoid", "sum", out=self.ep["out"])),
             ("blk_ln1", "ln", T * H * 2 * 2 + H * 2 * 2,
@@ -392,13 +393,13 @@ def cpu_baseline(wl: Workload, frac: float):
     seed = 7
     g64 = {k: v.float().cpu().numpy().astype(np.float64) for k, v in blk.p.items()}
     # host stand-ins for the resident block activations (same shapes and dtypes)
-    blk_x = h["cfg5"]["x"].f64().reshape(T, H)
+    blk_x = h["block_32x512x1024"]["x"].f64().reshape(T, H)
     scores = fd.softmax_inputs(seed, B * blk.heads * S, S, "bf16", sigma=1.0, mask_dtype=None)
     att = fd.layernorm_inputs(seed, T, H, "bf16")
     u = fd.pointwise_inputs(seed, T, F, "bf16", with_residual=False)
     dres = fd.pointwise_inputs(seed + 1, T, H, "bf16", with_bias=False)
     epi = fd.epilogue_inputs(seed, 8192, 8192)
-    c1, c2, c3 = h["cfg1"], h["cfg2"], h["cfg3"]
+    c1, c2, c3 = h["pointwise_256x1024"], h["softmax_8192x4096"], h["layernorm_16384x4096"]
 
     def n(rows):
         return max(1, int(rows * frac))
@@ -406,20 +407,20 @@ def cpu_baseline(wl: Workload, frac: float):
     # (name, rows, chunk, bytes per row, fn(lo, hi)) -- f64 conversion of the
     # inputs is part of the oracle's work and is timed
     jobs = [
-        ("pw_cfg1", 256, 256, 1024 * 12,
+        ("pw_256x1024", 256, 256, 1024 * 12,
          lambda lo, hi: oracle.pointwise_chain(c1["x"].rows(slice(lo, hi)).f64(), c1["bias"].f64(),
                                                c1["residual"].rows(slice(lo, hi)).f64(),
                                                c1["scale"], "gelu_erf")),
-        ("sm_cfg2", n(8192), 1024, 4096 * 6,
+        ("sm_8192x4096", n(8192), 1024, 4096 * 6,
          lambda lo, hi: oracle.row_softmax(c2["x"].rows(slice(lo, hi)).f64(),
                                            c2["mask"].rows(slice(lo, hi)).f64(), c2["scale"])),
-        ("ln_cfg3", n(16384), 1024, 4096 * 8,
+        ("ln_16384x4096", n(16384), 1024, 4096 * 8,
          lambda lo, hi: (oracle.layernorm_residual(c3["x"].rows(slice(lo, hi)).f64(),
                                                    c3["residual"].rows(slice(lo, hi)).f64(),
                                                    c3["gamma"].f64(), c3["beta"].f64(), c3["eps"]),
                          oracle.residual_store_bf16(c3["x"].rows(slice(lo, hi)).f64(),
                                                     c3["residual"].rows(slice(lo, hi)).f64()))),
-        ("ep_cfg4", n(8192), 512, 8192 * 2 + 4,
+        ("ep_8192x8192", n(8192), 512, 8192 * 2 + 4,
          lambda lo, hi: oracle.gemm_epilogue_reduce(epi["c"].rows(slice(lo, hi)).f64(),
                                                     epi["bias"].f64(), epi["col_scale"].f64(),
                                                     "sigmoid", "sum")),
@@ -549,7 +550,7 @@ def main():
               else wl.same_size_copies([k[2] for k in wl.kernels], max(args.steps, 5)))
 
     bw_ms = wl.pointwise_bandwidth_scale(max(args.steps // 5, 5))
-    bw_bytes = STEP_BYTES["pw_cfg1_bw"]
+    bw_bytes = STEP_BYTES["pw_262144x1024"]
 
     traffic = load_traffic()
     per_kernel = {}
@@ -603,7 +604,7 @@ def main():
                         "GB/s": round(bw_bytes / (bw_ms * 1e-3) / 1e9, 1),
                         "frac": round(bw_bytes / (bw_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
                     "block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
-                    "gemm_cfg4_ms": round(wl.gemm_cfg4_ms, 3),
+                    "gemm_8192x8192x4096_ms": round(wl.gemm_8192x8192x4096_ms, 3),
                     "wall_s_timed_region": round(wall_s, 4), "setup_s": round(setup_s, 1),
                     "paper_geomean_speedups_vs_torch_compile_H200":
                         {"L1": 1.40, "L2": 1.15, "L3": 1.07}},

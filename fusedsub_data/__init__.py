@@ -11,8 +11,9 @@ I/O dtype.  fp32 storage uses numpy's float64->float32 cast (IEEE round to
 nearest even); bf16 storage rounds that float32 value to bf16 (round to
 nearest even on the upper 16 bits).
 
-The five named workloads (``cfg1`` .. ``cfg5``) are the paper-style shapes
-the kernels are measured on.  The paper evaluates on KernelBench problems,
+The named workloads (``CONFIGS``: a pointwise chain, a softmax, a LayerNorm, a
+GEMM epilogue and a transformer block, each named by its kind and shape) are
+the paper-style shapes the kernels are measured on.  The paper evaluates on KernelBench problems,
 which are not reproduced here; these seeded draws stand in for them with the
 shapes and distributions of the workloads this library targets.
 """
@@ -251,20 +252,21 @@ def block_inputs(seed: int, batch: int = 32, seq: int = 512, hidden: int = 1024,
 
 
 # ----------------------------------------------------------------------------
-# the five named workloads
+# the named workloads
 # ----------------------------------------------------------------------------
 CONFIGS = {
-    "cfg1": dict(kind="pointwise", rows=256, cols=1024, dtype="f32", scale=0.7,
-                 act="gelu_erf"),
+    "pointwise_256x1024": dict(kind="pointwise", rows=256, cols=1024, dtype="f32", scale=0.7,
+                               act="gelu_erf"),
     # same chain and draws at a bandwidth-scale shape (3 GiB moved)
-    "cfg1_bw": dict(kind="pointwise", rows=262144, cols=1024, dtype="f32", scale=0.7,
-                    act="gelu_erf"),
-    "cfg2": dict(kind="softmax", rows=8192, cols=4096, dtype="bf16", sigma=3.0,
-                 mask_dtype="bf16", p_masked=0.1, scale=0.125),
-    "cfg3": dict(kind="layernorm", rows=16384, cols=4096, dtype="bf16", eps=1e-5),
-    "cfg4": dict(kind="gemm_epilogue", m=8192, n=8192, k=4096, act="sigmoid",
-                 reduce="sum"),
-    "cfg5": dict(kind="block", **BLOCK_DIMS),
+    "pointwise_262144x1024": dict(kind="pointwise", rows=262144, cols=1024, dtype="f32",
+                                  scale=0.7, act="gelu_erf"),
+    "softmax_8192x4096": dict(kind="softmax", rows=8192, cols=4096, dtype="bf16", sigma=3.0,
+                              mask_dtype="bf16", p_masked=0.1, scale=0.125),
+    "layernorm_16384x4096": dict(kind="layernorm", rows=16384, cols=4096, dtype="bf16",
+                                 eps=1e-5),
+    "gemm_epilogue_8192x8192x4096": dict(kind="gemm_epilogue", m=8192, n=8192, k=4096,
+                                         act="sigmoid", reduce="sum"),
+    "block_32x512x1024": dict(kind="block", **BLOCK_DIMS),
 }
 
 

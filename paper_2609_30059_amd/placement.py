@@ -167,7 +167,7 @@ def mlp_study(seed: int = 0, reps: int = 30) -> Dict[str, object]:
 
     import fusedsub_data as fd
     from .block import PARAM_NAMES
-    h = fd.make_inputs("cfg5", seed)
+    h = fd.make_inputs("block_32x512x1024", seed)
 
     def dev(t):
         return torch.from_numpy(t.data.view(np.int16)).view(torch.bfloat16).cuda()

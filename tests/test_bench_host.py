@@ -17,11 +17,11 @@ _spec.loader.exec_module(bench)
 # kernel names as rocprofv3 prints them (anonymous namespace removed), one per
 # bench kernel, plus library and runtime kernels that must match nothing
 NAMES = {
-    "pw_cfg1": "void fs::pointwise_kernel<float, 1, true, true, 1>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
-    "pw_cfg1_bw": "void fs::pointwise_kernel<float, 1, true, true, 4>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
-    "sm_cfg2": "void fs::softmax_kernel<unsigned short, unsigned short, true, 2, 32, true, 1, 1>(unsigned short const*, long)",
-    "ln_cfg3": "void fs::layernorm_kernel<unsigned short, true, false, 2, 32, true, 1, 1>(unsigned short const*, long)",
-    "ep_cfg4": "void fs::epilogue_lds_kernel<unsigned short, unsigned short, 2, 16, 2, 16, true>(unsigned short const*, long)",
+    "pw_256x1024": "void fs::pointwise_kernel<float, 1, true, true, 1>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
+    "pw_262144x1024": "void fs::pointwise_kernel<float, 1, true, true, 4>(float const*, long, float const*, float const*, long, float*, long, long, int, float, int)",
+    "sm_8192x4096": "void fs::softmax_kernel<unsigned short, unsigned short, true, 2, 32, true, 1, 1>(unsigned short const*, long)",
+    "ln_16384x4096": "void fs::layernorm_kernel<unsigned short, true, false, 2, 32, true, 1, 1>(unsigned short const*, long)",
+    "ep_8192x8192": "void fs::epilogue_lds_kernel<unsigned short, unsigned short, 2, 16, 2, 16, true>(unsigned short const*, long)",
     "blk_ln1": "void fs::layernorm_kernel<unsigned short, false, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
     "blk_sm": "void fs::softmax_kernel<unsigned short, unsigned short, false, 1, 8, true, 4, 2>(unsigned short const*, long)",
     "blk_ln2": "void fs::layernorm_kernel<unsigned short, true, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
@@ -52,9 +52,9 @@ def test_compulsory_bytes():
     assert bench.STEP_BYTES["blk_sm"] == 32 * 16 * (live * 2 + 512 * 512 * 2)
     assert bench.STEP_BYTES["blk_ln2"] == T_ * H * 2 * 4 + 2 * H * 2   # x, res in; y, res out
     assert bench.STEP_BYTES["blk_gelu"] == T_ * F * 2 * 2 + F * 2
-    assert bench.STEP_BYTES["ep_cfg4"] == 8192 * 8192 * 2 + 8192 * 2 + 8192 * 4 + 8192 * 4
+    assert bench.STEP_BYTES["ep_8192x8192"] == 8192 * 8192 * 2 + 8192 * 2 + 8192 * 4 + 8192 * 4
     assert bench.STEP_BYTES["copy_1GiB"] == 2 << 30
-    assert bench.STEP_BYTES["pw_cfg1_bw"] == 3 * (1 << 30) + 4096
+    assert bench.STEP_BYTES["pw_262144x1024"] == 3 * (1 << 30) + 4096
     assert set(bench.KIND) == set(bench.STEP_BYTES) - {"copy_1GiB"}
 
 
@@ -68,28 +68,28 @@ def _counters(path, counter, per_label):
 def test_write_traffic_scales_by_the_copy(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic.json"))
     # the copy moves 1 GiB each way; FETCH_SIZE reads half of it, WRITE_SIZE all
-    fetch = {"copy_1GiB": 524288, "ln_cfg3": 131072, "ep_cfg4": 65536}
-    write = {"copy_1GiB": 1048576, "ln_cfg3": 262144, "ep_cfg4": 32}
+    fetch = {"copy_1GiB": 524288, "ln_16384x4096": 131072, "ep_8192x8192": 65536}
+    write = {"copy_1GiB": 1048576, "ln_16384x4096": 262144, "ep_8192x8192": 32}
     _counters(tmp_path / "f.csv", "FETCH_SIZE", fetch)
     _counters(tmp_path / "w.csv", "WRITE_SIZE", write)
     out = bench.write_traffic(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "abc", "F", "W")
     assert out["fetch_scale"] == 2.0 and out["write_scale"] == 1.0
-    assert out["ln_cfg3"]["bytes_per_launch"] == (2 * 131072 + 262144) * 1024
-    assert out["ep_cfg4"]["bytes_per_launch"] == (2 * 65536 + 32) * 1024
-    assert out["ln_cfg3"]["source_hash"] == bench.source_hash("ln")
-    assert "pw_cfg1" not in out and "copy_1GiB" not in out
+    assert out["ln_16384x4096"]["bytes_per_launch"] == (2 * 131072 + 262144) * 1024
+    assert out["ep_8192x8192"]["bytes_per_launch"] == (2 * 65536 + 32) * 1024
+    assert out["ln_16384x4096"]["source_hash"] == bench.source_hash("ln")
+    assert "pw_256x1024" not in out and "copy_1GiB" not in out
     assert json.load(open(tmp_path / "traffic.json"))["measured_at"] == "abc"
 
 
 def test_report_trace(tmp_path, capsys):
     p = tmp_path / "s.csv"
     p.write_text('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs"\n'
-                 f'"{NAMES["ln_cfg3"]}",4,352000,88000,80,87000,89000\n'
+                 f'"{NAMES["ln_16384x4096"]}",4,352000,88000,80,87000,89000\n'
                  f'"{OTHERS[1]}",1,88000,88000,20,88000,88000\n')
     bench.report_trace(str(p))
-    rows = [l for l in capsys.readouterr().out.splitlines() if l.startswith("| ln_cfg3")]
-    gbs = bench.STEP_BYTES["ln_cfg3"] / 88000
-    assert rows == [f"| ln_cfg3 | 4 | 88.00 | 87.00 | 89.00 | 80.0 | {gbs:.0f} | "
+    rows = [l for l in capsys.readouterr().out.splitlines() if l.startswith("| ln_16384x4096")]
+    gbs = bench.STEP_BYTES["ln_16384x4096"] / 88000
+    assert rows == [f"| ln_16384x4096 | 4 | 88.00 | 87.00 | 89.00 | 80.0 | {gbs:.0f} | "
                     f"{100 * gbs / 8000:.1f} |"]
 
 

@@ -73,13 +73,13 @@ def test_small_block_causal_row_blocks(attn_block):
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg5_full_block_sampled_sequences(seed):
-    c = fd.CONFIGS["cfg5"]
-    d = fd.make_inputs("cfg5", seed)
+def test_full_block_sampled_sequences(seed):
+    c = fd.CONFIGS["block_32x512x1024"]
+    d = fd.make_inputs("block_32x512x1024", seed)
     seqs = [0, c["batch"] - 1] if seed else [0, 13, c["batch"] - 1]
-    announce("block cfg5", seed, seqs)
+    announce("block 32x512x1024", seed, seqs)
     buf, ref = run_block(d, c["heads"], seqs)
-    compare(buf, ref, seqs, c["batch"], c["seq"], f"cfg5 seed {seed}", d["x"].f64()[seqs])
+    compare(buf, ref, seqs, c["batch"], c["seq"], f"block seed {seed}", d["x"].f64()[seqs])
     # causal softmax structure at full size: row 0 of every head is one-hot
     p0 = buf["probs"][:, :, 0, :].float()
     assert torch.all(p0[..., 0] == 1.0) and torch.all(p0[..., 1:] == 0.0)

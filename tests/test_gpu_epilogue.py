@@ -18,7 +18,7 @@ SUM_ATOL = 5e-3
 @pytest.mark.parametrize("seed", SEEDS)
 def test_epilogue_only_five_seeds(seed):
     d = fd.epilogue_inputs(seed, 128, 8192)
-    announce("epilogue cfg4-width", seed)
+    announce("epilogue 8192 columns", seed)
     o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]), "sigmoid", "sum")
     ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
                                       "sigmoid", "sum")
@@ -29,11 +29,11 @@ def test_epilogue_only_five_seeds(seed):
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg4_end_to_end_sampled(seed):
-    c = fd.CONFIGS["cfg4"]
+def test_gemm_epilogue_end_to_end_sampled(seed):
+    c = fd.CONFIGS["gemm_epilogue_8192x8192x4096"]
     m, n, k = c["m"], c["n"], c["k"]
     d = fd.gemm_epilogue_inputs(seed, m, n, k)
-    announce("cfg4 gemm + epilogue", seed)
+    announce("gemm 8192x8192x4096 + epilogue", seed)
     a, b = dev(d["a"]), dev(d["b"])
     cmat = fs.gemm(a, b)
     o = fs.gemm_epilogue_reduce(cmat, dev(d["bias"]), dev(d["col_scale"]), "sigmoid", "sum")

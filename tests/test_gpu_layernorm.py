@@ -31,26 +31,26 @@ def check(name, d, y, ro, dtype, has_res=True, affine=True):
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg3_rows_five_seeds(seed):
+def test_4096_column_rows_five_seeds(seed):
     d = fd.layernorm_inputs(seed, 80, 4096)
-    announce("layernorm cfg3-width", seed)
+    announce("layernorm 4096 columns", seed)
     y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
                                   dev(d["beta"]), d["eps"])
     check(f"seed {seed}", d, y, ro, "bf16")
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg3_full_size_sampled(seed):
-    d = fd.make_inputs("cfg3", seed)
-    rows = fd.CONFIGS["cfg3"]["rows"]
-    announce("layernorm cfg3 full", seed)
+def test_16384x4096_sampled_rows(seed):
+    d = fd.make_inputs("layernorm_16384x4096", seed)
+    rows = fd.CONFIGS["layernorm_16384x4096"]["rows"]
+    announce("layernorm 16384x4096 full", seed)
     y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
                                   dev(d["beta"]), d["eps"])
     idx = np.unique(np.concatenate([[0, rows - 1], np.random.default_rng(seed).integers(0, rows, 62)]))
     ti = torch.from_numpy(idx).cuda()
     sub = {k: d[k].rows(idx) for k in ("x", "residual")}
     sub.update(gamma=d["gamma"], beta=d["beta"], eps=d["eps"])
-    check(f"cfg3 seed {seed}", sub, y[ti], ro[ti], "bf16")
+    check(f"layernorm_16384x4096 seed {seed}", sub, y[ti], ro[ti], "bf16")
     # every row: residual_out is bit-exactly the rounded fp32 sum
     want = (dev(d["x"]).float() + dev(d["residual"]).float()).to(torch.bfloat16)
     assert torch.equal(ro.view(torch.int16), want.view(torch.int16))

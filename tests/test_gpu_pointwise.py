@@ -23,9 +23,9 @@ def run_case(rows, cols, dtype, act, seed=0, bias=True, residual=True, scale=0.7
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg1_fp32_gelu_five_seeds(seed):
+def test_256x1024_fp32_gelu_five_seeds(seed):
     d, got, ref = run_case(256, 1024, "f32", "gelu_erf", seed)
-    assert_close(f"cfg1 seed {seed}", got, ref, *TOL["f32"])
+    assert_close(f"pointwise_256x1024 seed {seed}", got, ref, *TOL["f32"])
     # Gate-3 style diagnostic: an unfused torch fp32 evaluation as r32
     x, b, r = (torch.from_numpy(d[k].data) for k in ("x", "bias", "residual"))
     r32 = torch.nn.functional.gelu(x * d["scale"] + b) + r
@@ -94,16 +94,17 @@ def test_empty():
 
 @pytest.mark.slow
 def test_bandwidth_scale_sampled_rows():
-    rows, cols = fd.CONFIGS["cfg1_bw"]["rows"], fd.CONFIGS["cfg1_bw"]["cols"]
+    c = fd.CONFIGS["pointwise_262144x1024"]
+    rows, cols = c["rows"], c["cols"]
     d = fd.pointwise_inputs(0, rows, cols, "f32")
-    announce("pointwise cfg1_bw", rows, cols)
+    announce("pointwise 262144x1024", rows, cols)
     y = fs.pointwise_chain(dev(d["x"]), dev(d["bias"]), dev(d["residual"]), d["scale"], "gelu_erf")
     idx = np.unique(np.concatenate([[0, 1, rows - 1], np.random.default_rng(0).integers(0, rows, 256)]))
     got = host64(y[torch.from_numpy(idx).cuda()])
     ref = oracle.pointwise_chain(d["x"].rows(idx).f64(),
                                  d["bias"].f64(), d["residual"].rows(idx).f64(), d["scale"],
                                  "gelu_erf")
-    assert_close("cfg1_bw sampled", got, ref, *TOL["f32"])
+    assert_close("pointwise_262144x1024 sampled", got, ref, *TOL["f32"])
 
 
 @pytest.mark.slow

@@ -24,9 +24,9 @@ def supplementary_bf16(name, got, ref, masked):
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg2_rows_five_seeds(seed):
+def test_4096_column_rows_five_seeds(seed):
     d = fd.softmax_inputs(seed, 96, 4096)
-    announce("softmax cfg2-width", seed)
+    announce("softmax 4096 columns", seed)
     y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
     got = host64(y)
     ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
@@ -35,18 +35,18 @@ def test_cfg2_rows_five_seeds(seed):
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-def test_cfg2_full_size_sampled(seed):
-    c = fd.CONFIGS["cfg2"]
-    d = fd.make_inputs("cfg2", seed)
-    announce("softmax cfg2 full", seed)
+def test_8192x4096_sampled_rows(seed):
+    c = fd.CONFIGS["softmax_8192x4096"]
+    d = fd.make_inputs("softmax_8192x4096", seed)
+    announce("softmax 8192x4096 full", seed)
     y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
     rows = c["rows"]
     idx = np.unique(np.concatenate([[0, 1, rows - 1],
                                     np.random.default_rng(seed).integers(0, rows, 61)]))
     got = host64(y[torch.from_numpy(idx).cuda()])
     ref = oracle.row_softmax(d["x"].rows(idx).f64(), d["mask"].rows(idx).f64(), d["scale"])
-    assert_close(f"cfg2 seed {seed}", got, ref, *TOL["bf16"])
-    supplementary_bf16(f"cfg2 seed {seed}", got, ref, np.isinf(d["mask"].rows(idx).f64()))
+    assert_close(f"softmax_8192x4096 seed {seed}", got, ref, *TOL["bf16"])
+    supplementary_bf16(f"softmax_8192x4096 seed {seed}", got, ref, np.isinf(d["mask"].rows(idx).f64()))
     # property at every row: sums of the whole output
     s = y.float().sum(dim=1)
     assert torch.all((s - 1).abs() < 2e-2), "a row sum is off"
