@@ -109,37 +109,49 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   // rows without a causal rule that fill every slot of every lane have no
   // column to mask (uniform)
   const bool whole = FS_SM_FULL_PATH && q_len == 0 && cols == kThreads * EPT;
+  // every slot of every lane is stored: rows written whole (no trimming)
+  // that fill every slot (uniform; causal rows included)
+  const bool store_all = trim_shift < 0 && cols == kThreads * EPT;
 
   // causal position of row0 (row0 mod q_len), advanced by the loop step
-  // without a division per row
+  // without a division per row.  The host sends q_len >= 2^30 to the
+  // streamed kernel, so positions and column limits fit in 32 bits here and
+  // stay in scalar registers with native scalar compares (64-bit compares
+  // run on the vector unit).
   const int64_t step = int64_t(gridDim.x) * G * R;
   int64_t row0 = (int64_t(blockIdx.x) * G + g) * R;
-  int64_t pos0 = 0, step_mod = 0;
-  if (q_len > 0) {
-    pos0 = row0 % q_len;
-    step_mod = step % q_len;
+  const int q = int(q_len);
+  const int coff = cols - q;                 // cols - q_len
+  int pos0 = 0, step_mod = 0;
+  if (q > 0) {
+    pos0 = int(row0 % q_len);
+    step_mod = int(step % q_len);
   }
   for (; row0 < rows; row0 += step) {
     Raw<T, V> rx[R][NV];
     Raw<MT, V> rm[R][HAS_MASK ? NV : 1];
     int lim[R], wend[R];
+    // one 64-bit row offset per trip; only the last trip can run past the
+    // end, and its missing rows re-read the last row (in bounds, not stored)
+    const bool full_trip = row0 + R <= rows;
+    const T* xb = x + row0 * ld_x;
+    const MT* mb = HAS_MASK ? mask + row0 * ld_m : nullptr;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      // rows past the end re-read the last row (in bounds) and are not stored
-      const int64_t row = row0 + r < rows ? row0 + r : rows - 1;
-      const T* xr = x + row * ld_x;
-      const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
+      const bool in = full_trip || row0 + r < rows;
+      const T* xr = in ? xb + r * ld_x : x + (rows - 1) * ld_x;
+      const MT* mr = HAS_MASK ? (in ? mb + r * ld_m : mask + (rows - 1) * ld_m) : nullptr;
       // last live column (inclusive) under the causal rule; -1 if none; and
       // the end of the written columns
-      int64_t limit = int64_t(cols) - 1, we = cols;
-      if (q_len > 0) {
-        int64_t pos = pos0 + r;
-        if (pos >= q_len) pos = q_len >= R ? pos - q_len : pos % q_len;
-        limit = pos + (cols - q_len);
-        if (trim_shift >= 0) we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
+      int limit = cols - 1, we = cols;
+      if (q > 0) {
+        int pos = pos0 + r;
+        if (pos >= q) pos = q >= R ? pos - q : pos % q;
+        limit = pos + coff;
+        if (trim_shift >= 0) we = (((pos >> trim_shift) + 1) << trim_shift) + coff;
       }
-      lim[r] = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
-      wend[r] = int(we < cols ? (we < 0 ? 0 : we) : cols);
+      lim[r] = limit < cols - 1 ? (limit < -1 ? -1 : limit) : cols - 1;
+      wend[r] = we < cols ? (we < 0 ? 0 : we) : cols;
       // vectors past lim are not read: their address is clamped onto the
       // vector holding column lim (fetched by a live lane), then masked
       const int limv = lim[r] < 0 ? 0 : (lim[r] / V) * V;
@@ -151,9 +163,9 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         if constexpr (HAS_MASK) rm[r][k].load(mr + cl);
       }
     }
-    if (q_len > 0) {
+    if (q > 0) {
       pos0 += step_mod;
-      if (pos0 >= q_len) pos0 -= q_len;
+      if (pos0 >= q) pos0 -= q;
     }
     // keep every load of the trip ahead of the first use (one HBM round trip)
     __builtin_amdgcn_sched_barrier(0);
@@ -254,17 +266,19 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       }
     }
 
+    T* yb = y + row0 * ld_y;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      if (row0 + r < rows) {
-        T* yr = y + (row0 + r) * ld_y;
+      if (full_trip || row0 + r < rows) {
+        T* yr = yb + r * ld_y;
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
           const int c0 = (k * kThreads + tid) * V;
           float o[V];
 #pragma unroll
           for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f[r];
-          store_until(yr, c0, wend[r], o);
+          if (store_all) stv<T, V>(yr + c0, o);
+          else store_until(yr, c0, wend[r], o);
         }
       }
     }
@@ -396,8 +410,10 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   // Variant ladder, in order: the first rung with at least min_w waves per row
   // and a row capacity 64 * W * EPT >= cols is launched.
   const int min_w = c >= FS_SM_SPLIT_COLS ? FS_SM_MIN_WAVES : 1;
+  // the register-resident kernel keeps causal positions in 32 bits
+  const bool small_q = a.causal_q_len < (int64_t(1) << 30);
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
-  if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                   \
+  if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E)                       \
     return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }

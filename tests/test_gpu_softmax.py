@@ -179,3 +179,16 @@ def test_beyond_2_31_elements():
                              d["scale"])
     assert_close("beyond 2^31", got, ref, *TOL["bf16"])
     bf16_ulp_close("beyond 2^31", got, ref, atol=1e-7)
+
+
+@pytest.mark.parametrize("q_len", [(1 << 30) - 1, 1 << 30, (1 << 40) + 5])
+def test_huge_causal_q_len(q_len):
+    # q_len at or above 2^30 takes the streamed kernel (64-bit positions);
+    # with q_len > cols every row here lies wholly above the diagonal shift,
+    # so the oracle's rule masks it completely: all outputs are +0
+    d = fd.softmax_inputs(5, 6, 64, "bf16", mask_dtype=None)
+    announce("softmax huge causal q_len", q_len)
+    got = host64(fs.row_softmax(dev(d["x"]), None, 0.5, causal_q_len=q_len))
+    ref = oracle.row_softmax(d["x"].f64(), None, 0.5, causal_q_len=q_len)
+    np.testing.assert_array_equal(ref, 0.0)
+    np.testing.assert_array_equal(got, ref)
