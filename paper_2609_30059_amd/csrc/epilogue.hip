@@ -13,7 +13,10 @@
 // in the row loop.  A wave reads its row in chunks of CH 16-byte vectors per
 // lane and software-pipelines them: the loads of the next chunk (of this row
 // or of its next row) are in flight while the current chunk is evaluated, so
-// HBM traffic and the transcendental work overlap inside every wave.
+// HBM traffic and the transcendental work overlap inside every wave.  Row r
+// starts at chunk r mod (chunks per row), so waves running side by side read
+// different offsets of their rows; blocks of 16 waves at 8 waves per SIMD
+// keep 32 waves per CU.
 //
 // LDS layout: vector v = k*64 + lane of a row holds V columns; its V scale
 // factors are H = V/4 float4s at index (k*H + h)*64 + lane, so each
