@@ -12,6 +12,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 // Build-time tuning parameters (defaults measured on MI355X).  Streaming
 // loads and stores use the non-temporal hint unless these are set to 0.
 #ifndef FS_NT_LOAD
@@ -27,6 +29,7 @@ constexpr bool kNtLoad = FS_NT_LOAD != 0;
 constexpr bool kNtStore = FS_NT_STORE != 0;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;

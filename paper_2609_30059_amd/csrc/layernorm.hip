@@ -33,6 +33,24 @@
 #ifndef FS_LN_BATCH_ELEMS
 #define FS_LN_BATCH_ELEMS 16
 #endif
+#ifndef FS_LN_CACHE_REGS
+#define FS_LN_CACHE_REGS 32   // row-cache elements per lane held in registers
+#endif
+#ifndef FS_LN_CACHE_GB_AHEAD
+#define FS_LN_CACHE_GB_AHEAD 1   // slots of gamma/beta loads in flight ahead in the row cache's pass 2
+#endif
+#ifndef FS_LN_CACHE_AHEAD
+#define FS_LN_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
+#endif
+#ifndef FS_LN_CACHE_GROUP_WORDS
+#define FS_LN_CACHE_GROUP_WORDS 8   // raw load registers per slot group of the row cache
+#endif
+#ifndef FS_LN_STREAM_WAVES
+#define FS_LN_STREAM_WAVES 8   // waves per row of the streamed kernel
+#endif
+#ifndef FS_LN_STREAM_BPC
+#define FS_LN_STREAM_BPC 4     // its blocks per compute unit
+#endif
 #ifndef FS_LN_GRID_SCALE
 #define FS_LN_GRID_SCALE 16
 #endif
@@ -389,6 +407,249 @@ __global__ __launch_bounds__(64 * W) void layernorm_stream_kernel(
   }
 }
 
+// Rows longer than the register-resident capacity, with a row cache: one
+// block of 16 waves per row keeps h = x + residual (fp32) of its first
+// 64*16*CL columns in LDS (CL per lane) and of the next 64*16*CR columns in
+// registers, so those columns are read from HBM once; with TAIL, the `tail`
+// vector slots per lane past both are read twice as in
+// layernorm_stream_kernel.  Pass 1 writes residual_out of the cached columns
+// (they are never read again, so in-place outputs stay correct) and merges
+// each slot group's exact two-pass (count, mean, M2) into one running triple
+// per lane (RMSNorm: a running sum of squares), combined once across the
+// block; pass 2 writes y from the registers, from LDS and from the re-read
+// tail, with the tail's residual_out.  Each lane reads back only the LDS
+// words it wrote, so the cache needs no barrier.  One block per compute unit
+// holds one row at a time, so the loads of the next row's first slot groups
+// are issued before the block-wide combine: they are in flight while this
+// row's outputs are written.
+template <typename T, bool HAS_RES, bool RMS, int CL, int CR, bool TAIL>
+__global__ __launch_bounds__(1024) void layernorm_cached_kernel(
+    const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
+    const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
+    int64_t ld_ro, int64_t rows, int cols, float eps, int tail) {
+  constexpr int W = 16, kThreads = 64 * W;
+  constexpr int V = Elem<T>::kVec;
+  constexpr int NL = CL / V, NR = CR / V, NS = NL + NR;   // vector slots per lane
+  static_assert(CL % V == 0 && CR % V == 0 && CL % 4 == 0, "cache parts are whole vectors");
+  // cached slots go in groups of G (about FS_LN_CACHE_GROUP_WORDS raw
+  // registers each) with the loads of the next AH groups in flight
+  constexpr int kWords = Raw<T, V>::kWords * (HAS_RES ? 2 : 1);
+  constexpr int G = kWords >= FS_LN_CACHE_GROUP_WORDS ? 1 : FS_LN_CACHE_GROUP_WORDS / kWords;
+  constexpr int NG = NS / G, AH = FS_LN_CACHE_AHEAD, R = AH + 1;
+  static_assert(NL % G == 0 && NR % G == 0, "slot groups split the cache parts");
+  using P = MeanM2P;
+  __shared__ f32x4 cache[CL / 4][kThreads];
+  __shared__ P lds[2][W];
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+  const int clast = cols - V;
+  const int nslots = (cols + kThreads * V - 1) / (kThreads * V);   // slots the row uses
+  int parity = 0;
+
+  // loads of a slot of row `row`, clamped in bounds past the row end
+  auto load = [&](int64_t row, int lt, int slot, Raw<T, V>& rx, Raw<T, V>& rres) {
+    const int c0 = (slot * kThreads + lt) * V;
+    const int cl = c0 < cols ? c0 : clast;
+    rx.load(x + row * ld_x + cl);
+    if constexpr (HAS_RES) rres.load(res + row * ld_r + cl);
+  };
+  Raw<T, V> rx[R][G], rres[R][G];
+  // the first AH slot groups of a row
+  auto prime = [&](int64_t row, int lt) {
+#pragma unroll
+    for (int g = 0; g < AH && g < NG; ++g) {
+      if (g * G < nslots) {
+#pragma unroll
+        for (int k = 0; k < G; ++k) load(row, lt, g * G + k, rx[g][k], rres[g][k]);
+      }
+    }
+  };
+  if (int64_t(blockIdx.x) < rows) prime(blockIdx.x, tid);
+
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+    T* yr = y + row * ld_y;
+    T* ro = res_out ? res_out + row * ld_ro : nullptr;
+    // the lane index is re-read per row (an empty asm) so that per-lane
+    // offsets and column tests are recomputed, not kept in registers
+    // across rows
+    int lt = tid;
+    asm volatile("" : "+v"(lt));
+    auto col_of = [&](int slot) { return (slot * kThreads + lt) * V; };
+    auto hval = [&](const Raw<T, V>& rxs, const Raw<T, V>& rrs, float* h) {
+      rxs.unpack(h);
+      if constexpr (HAS_RES) {
+        float rv[V];
+        rrs.unpack(rv);
+#pragma unroll
+        for (int i = 0; i < V; ++i) h[i] += rv[i];
+      }
+    };
+    // merge the statistics of K slots from s0 on into the lane's running triple
+    P run{0.f, 0.f, 0.f};
+    auto absorb = [&](auto kslots, int s0, const float* h) {
+      constexpr int K = decltype(kslots)::value;
+      float n = 0.f, sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const bool in = col_of(s0 + k) < cols;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          const float v = in ? h[k * V + i] : 0.f;
+          sum = RMS ? fmaf(v, v, sum) : sum + v;
+        }
+        n += in ? float(V) : 0.f;
+      }
+      if constexpr (RMS) {
+        run.m2 += sum;                        // running sum of squares
+      } else {
+        const float mt = n > 0.f ? sum / n : 0.f;
+        float m2 = 0.f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const bool in = col_of(s0 + k) < cols;
+#pragma unroll
+          for (int i = 0; i < V; ++i) {
+            const float d = in ? h[k * V + i] - mt : 0.f;
+            m2 = fmaf(d, d, m2);
+          }
+        }
+        run = P::combine(run, P{n, mt, m2});
+      }
+    };
+    auto store_res = [&](int slot, const float* h) {
+      const int c0 = col_of(slot);
+      if (ro && c0 < cols) stv<T, V>(ro + c0, h);
+    };
+    // the tail slots NS ... NS + tail - 1, one ahead: a slot's loads are in
+    // flight while the previous slot is used.  Loads of slots past the row
+    // are clamped in bounds (they count nothing and store nothing).
+    auto over_tail = [&](auto use) {
+      Raw<T, V> tx[2], tr[2];
+      load(row, lt, NS, tx[0], tr[0]);
+      for (int j = 0; j < tail; j += 2) {
+        load(row, lt, NS + j + 1, tx[1], tr[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        use(NS + j, tx[0], tr[0]);
+        load(row, lt, NS + j + 2, tx[0], tr[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 1 < tail) use(NS + j + 1, tx[1], tr[1]);
+      }
+    };
+
+    // pass 1: LDS part, register part (the first AH groups were issued
+    // before), tail
+    float hr[CR];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (g + AH < NG && (g + AH) * G < nslots) {
+#pragma unroll
+        for (int k = 0; k < G; ++k)
+          load(row, lt, (g + AH) * G + k, rx[(g + AH) % R][k], rres[(g + AH) % R][k]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (g * G < nslots) {
+        float h[G * V];
+#pragma unroll
+        for (int k = 0; k < G; ++k) hval(rx[g % R][k], rres[g % R][k], h + k * V);
+        absorb(std::integral_constant<int, G>{}, g * G, h);
+#pragma unroll
+        for (int k = 0; k < G; ++k) store_res(g * G + k, h + k * V);
+        if (g * G < NL) {
+#pragma unroll
+          for (int k = 0; k < G * V / 4; ++k)
+            cache[g * G * V / 4 + k][lt] = f32x4{h[4 * k], h[4 * k + 1], h[4 * k + 2], h[4 * k + 3]};
+        } else {
+#pragma unroll
+          for (int i = 0; i < G * V; ++i) hr[g * G * V - CL + i] = h[i];
+        }
+      }
+    }
+    if constexpr (TAIL) {
+      over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<T, V>& rrs) {
+        float h[V];
+        hval(rxs, rrs, h);
+        absorb(std::integral_constant<int, 1>{}, slot, h);
+      });
+    }
+
+    // gamma and beta of the cached slots are loaded D slots ahead of their
+    // use in pass 2, the first D before the next row's loads and the
+    // block-wide combine
+    constexpr int D = FS_LN_CACHE_GB_AHEAD;
+    auto slot_at = [](int i) { return i < NR ? NL + i : i - NR; };   // pass-2 order
+    auto load_gb = [&](int slot, Raw<T, V>& rg, Raw<T, V>& rb) {
+      const int c0 = col_of(slot);
+      const int cl = c0 < cols ? c0 : clast;
+      if (gamma) rg.template load<false>(gamma + cl);
+      if (!RMS && beta) rb.template load<false>(beta + cl);
+    };
+    Raw<T, V> rg[D + 1], rb[D + 1];
+#pragma unroll
+    for (int i = 0; i < D && i < NS; ++i)
+      if (slot_at(i) < nslots) load_gb(slot_at(i), rg[i], rb[i]);
+    // the next row's first slot groups, in flight from here on
+    const int64_t next = row + gridDim.x;
+    if (next < rows) prime(next, lt);
+
+    if constexpr (RMS) run.n = 1.f;          // keep the fold from skipping lanes
+    const P st = group_allreduce<W>(run, lds[parity], wave, lane);
+    parity ^= 1;
+    const float mean = RMS ? 0.f : st.mean;
+    // RMS: every lane carried mean 0, so the fold added the sums of squares
+    const float rstd = rsqrtf(st.m2 * (1.f / float(cols)) + eps);
+
+    asm volatile("" : "+v"(lt));   // pass 2 recomputes its column tests too
+    // pass 2: y, register part first (which frees its registers), then LDS
+    auto emit = [&](int slot, const float* h, const Raw<T, V>& g, const Raw<T, V>& b) {
+      const int c0 = col_of(slot);
+      if (c0 >= cols) return;
+      float gv[V], bv[V], o[V];
+      if (gamma) g.unpack(gv);
+      else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) gv[i] = 1.f;
+      }
+      if (!RMS && beta) b.unpack(bv);
+      else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) bv[i] = 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < V; ++i) o[i] = fmaf((h[i] - mean) * rstd, gv[i], bv[i]);
+      stv<T, V>(yr + c0, o);
+    };
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      if (i + D < NS && slot_at(i + D) < nslots)
+        load_gb(slot_at(i + D), rg[(i + D) % (D + 1)], rb[(i + D) % (D + 1)]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (slot_at(i) >= nslots) continue;
+      float h[V];
+      if (i < NR) {
+#pragma unroll
+        for (int k = 0; k < V; ++k) h[k] = hr[i * V + k];
+      } else {
+#pragma unroll
+        for (int k = 0; k < V / 4; ++k) {
+          const f32x4 v = cache[(i - NR) * (V / 4) + k][lt];
+          h[4 * k] = v.x; h[4 * k + 1] = v.y; h[4 * k + 2] = v.z; h[4 * k + 3] = v.w;
+        }
+      }
+      emit(slot_at(i), h, rg[i % (D + 1)], rb[i % (D + 1)]);
+    }
+    if constexpr (TAIL) {
+      over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<T, V>& rrs) {
+        float h[V];
+        hval(rxs, rrs, h);
+        store_res(slot, h);
+        Raw<T, V> g1, b1;
+        load_gb(slot, g1, b1);
+        emit(slot, h, g1, b1);
+      });
+    }
+  }
+}
+
 // rows batched per group: enough that a one-wave group handles about
 // FS_LN_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
@@ -434,6 +695,8 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
     FS_LN(8, 8, 1, 4)
     FS_LN(8, 16, 1, 4)
     FS_LN(8, 32, 1, 4)
+    // fp32 rows at 16 waves x 32 elements spill; bf16 rows fit
+    if constexpr (sizeof(T) == 2) { FS_LN(16, 32, 1, 1) }
   } else {
     // element-wise loads: 64 elements per thread (or 32 at 8 waves with a
     // residual) exceed the registers and spill, so wider rows take more
@@ -442,11 +705,32 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
     FS_LN(4, 32, 1, 8)
   }
 #undef FS_LN
-  // longer rows: streamed, one 8-wave block per row
+  // longer rows on the 16-byte path: row cache in LDS and registers, the
+  // columns past it streamed; one 16-wave block per compute unit
+  if constexpr (VEC) {
+    constexpr int CL = 32, CR = FS_LN_CACHE_REGS;
+    constexpr int64_t kCached = int64_t(1024) * (CL + CR);
+    auto go = [&](auto kern, int tail) {
+      const int64_t grid = a.rows < cus ? a.rows : cus;
+      hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(1024), 0, s, static_cast<const T*>(a.x),
+                         a.ld_x, static_cast<const T*>(a.res), a.ld_r,
+                         static_cast<const T*>(a.gamma), static_cast<const T*>(a.beta),
+                         static_cast<T*>(a.y), a.ld_y, static_cast<T*>(a.res_out), a.ld_ro, a.rows,
+                         int(a.cols), a.eps, tail);
+      return hipGetLastError();
+    };
+    if (c <= kCached) return go(layernorm_cached_kernel<T, HAS_RES, RMS, CL, CR, false>, 0);
+    constexpr int64_t kSlot = int64_t(1024) * V;
+    return go(layernorm_cached_kernel<T, HAS_RES, RMS, CL, CR, true>,
+              int((c - kCached + kSlot - 1) / kSlot));
+  }
+  // longer rows, element-wise path: streamed, one block of FS_LN_STREAM_WAVES
+  // waves per row
   {
-    constexpr int W = 8, U = 4;
+    constexpr int W = FS_LN_STREAM_WAVES, U = 4;
     const int trips = int((c + int64_t(64) * W * V * U - 1) / (int64_t(64) * W * V * U));
-    int64_t grid = a.rows < int64_t(cus) * 4 ? a.rows : int64_t(cus) * 4;
+    const int64_t cap = int64_t(cus) * FS_LN_STREAM_BPC;
+    int64_t grid = a.rows < cap ? a.rows : cap;
     hipLaunchKernelGGL((layernorm_stream_kernel<T, HAS_RES, RMS, W, VEC>), dim3(unsigned(grid)),
                        dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
                        static_cast<const T*>(a.res), a.ld_r, static_cast<const T*>(a.gamma),

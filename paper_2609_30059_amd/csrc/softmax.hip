@@ -32,6 +32,18 @@
 #ifndef FS_SM_BATCH_ELEMS
 #define FS_SM_BATCH_ELEMS 16
 #endif
+#ifndef FS_SM_STREAM_WAVES
+#define FS_SM_STREAM_WAVES 8   // waves per row of the streamed kernel
+#endif
+#ifndef FS_SM_STREAM_BPC
+#define FS_SM_STREAM_BPC 4     // its blocks per compute unit
+#endif
+#ifndef FS_SM_CACHE_AHEAD
+#define FS_SM_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
+#endif
+#ifndef FS_SM_CACHE_GROUP_WORDS
+#define FS_SM_CACHE_GROUP_WORDS 8   // raw load registers per slot group of the row cache
+#endif
 #ifndef FS_SM_GRID_SCALE
 #define FS_SM_GRID_SCALE 64
 #endif
@@ -384,6 +396,221 @@ __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
   }
 }
 
+// Rows longer than the register-resident capacity, with a row cache: one
+// block of 16 waves per row keeps the logits of its first 64*16*CL columns in
+// LDS (fp32, CL per lane) and of the next 64*16*CR columns in registers, so
+// those columns are read from HBM once; with TAIL, the `tail` vector slots
+// per lane past both are streamed as in softmax_stream_kernel (read twice).
+// Pass 1 runs one online (m', d) per lane over the LDS part, the register
+// part and the tail, combined once across the block; pass 2 writes
+// 2^(a*log2e - M) / D from the registers, from LDS and from the re-read tail.
+// Each lane reads back only the LDS words it wrote, so the cache needs no
+// barrier.  One block per compute unit holds one row at a time, so the loads
+// of the next row's first slot groups are issued before the block-wide
+// combine: they are in flight while this row's outputs are written.
+template <typename T, typename MT, bool HAS_MASK, int CL, int CR, bool TAIL>
+__global__ __launch_bounds__(1024) void softmax_cached_kernel(
+    const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
+    int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift, int tail) {
+  constexpr int W = 16, kThreads = 64 * W;
+  constexpr int V = Elem<T>::kVec;
+  constexpr int NL = CL / V, NR = CR / V, NS = NL + NR;   // vector slots per lane
+  static_assert(CL % V == 0 && CR % V == 0 && CL % 4 == 0, "cache parts are whole vectors");
+  // cached slots go in groups of G (about FS_SM_CACHE_GROUP_WORDS raw
+  // registers each) with the loads of the next AH groups in flight
+  constexpr int kWords = Raw<T, V>::kWords + (HAS_MASK ? Raw<MT, V>::kWords : 0);
+  constexpr int G = kWords >= FS_SM_CACHE_GROUP_WORDS ? 1 : FS_SM_CACHE_GROUP_WORDS / kWords;
+  constexpr int NG = NS / G, AH = FS_SM_CACHE_AHEAD, R = AH + 1;
+  static_assert(NL % G == 0 && NR % G == 0, "slot groups split the cache parts");
+  __shared__ f32x4 cache[CL / 4][kThreads];
+  __shared__ MaxSumP lds[2][W];
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+  const int nslots = (cols + kThreads * V - 1) / (kThreads * V);   // slots the row uses
+  int parity = 0;
+
+  // per-row context: row pointers, last live column (causal rule), end of
+  // the written columns (trimmed causal rows)
+  struct Row {
+    const T* xr;
+    const MT* mr;
+    int lim, limv, wend;
+  };
+  auto row_ctx = [&](int64_t row, int64_t pos) {
+    Row c;
+    c.xr = x + row * ld_x;
+    c.mr = HAS_MASK ? mask + row * ld_m : nullptr;
+    const int64_t limit = q_len > 0 ? pos + (cols - q_len) : int64_t(cols) - 1;
+    c.lim = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+    c.limv = c.lim < 0 ? 0 : (c.lim / V) * V;
+    int64_t we = cols;
+    if (q_len > 0 && trim_shift >= 0)
+      we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
+    c.wend = int(we < cols ? (we < 0 ? 0 : we) : cols);
+    return c;
+  };
+  // loads of a slot, clamped in bounds past the row's last live column
+  auto load = [&](const Row& c, int lt, int slot, Raw<T, V>& rx, Raw<MT, V>& rm) {
+    const int c0 = (slot * kThreads + lt) * V;
+    const int cl = c0 <= c.lim ? c0 : c.limv;
+    rx.load(c.xr + cl);
+    if constexpr (HAS_MASK) rm.load(c.mr + cl);
+  };
+  Raw<T, V> rx[R][G];
+  Raw<MT, V> rm[R][G];
+  // the first AH slot groups of a row
+  auto prime = [&](const Row& c, int lt) {
+#pragma unroll
+    for (int g = 0; g < AH && g < NG; ++g) {
+      if (g * G < nslots) {
+#pragma unroll
+        for (int k = 0; k < G; ++k) load(c, lt, g * G + k, rx[g][k], rm[g][k]);
+      }
+    }
+  };
+
+  // causal position row mod q_len, advanced by the grid stride
+  const int64_t step_mod = q_len > 0 ? int64_t(gridDim.x) % q_len : 0;
+  int64_t pos = q_len > 0 ? int64_t(blockIdx.x) % q_len : 0;
+  Row cur = row_ctx(blockIdx.x, pos);
+  if (int64_t(blockIdx.x) < rows) prime(cur, tid);
+
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+    // the lane index is re-read per row (an empty asm) so that per-lane
+    // offsets and column tests are recomputed, not kept in registers
+    // across rows
+    int lt = tid;
+    asm volatile("" : "+v"(lt));
+    auto col_of = [&](int slot) { return (slot * kThreads + lt) * V; };
+    auto logit = [&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms, float* a) {
+      const int c0 = col_of(slot);
+      float xv[V];
+      rxs.unpack(xv);
+      if constexpr (HAS_MASK) {
+        float mv[V];
+        rms.unpack(mv);
+#pragma unroll
+        for (int i = 0; i < V; ++i) xv[i] = fmaf(xv[i], scale, mv[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) xv[i] *= scale;
+      }
+#pragma unroll
+      for (int i = 0; i < V; ++i) a[i] = (c0 + i <= cur.lim) ? xv[i] : -INFINITY;
+    };
+    // merge N logits into the lane's running (m', d)
+    float mrun = -INFINITY, drun = 0.f;
+    auto absorb = [&](auto kn, const float* a) {
+      constexpr int N = decltype(kn)::value;
+      float tm = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < N; ++i) tm = fmaxf(tm, a[i]);
+      const float mnew = fmaxf(mrun, tm == -INFINITY ? -INFINITY : tm * kLog2e);
+      const float msafe = mnew == -INFINITY ? 0.f : mnew;
+      float dt = 0.f;
+#pragma unroll
+      for (int i = 0; i < N; ++i) dt += __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
+      drun = fmaf(drun, __builtin_amdgcn_exp2f(mrun - msafe), dt);   // 2^-inf = 0
+      mrun = mnew;
+    };
+    // the tail slots NS ... NS + tail - 1, one ahead: a slot's loads are in
+    // flight while the previous slot is used.  Loads of slots past the row
+    // are clamped in bounds (their logits are -inf and they store nothing).
+    auto over_tail = [&](auto use) {
+      Raw<T, V> tx[2];
+      Raw<MT, V> tm[2];
+      load(cur, lt, NS, tx[0], tm[0]);
+      for (int j = 0; j < tail; j += 2) {
+        load(cur, lt, NS + j + 1, tx[1], tm[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        use(NS + j, tx[0], tm[0]);
+        load(cur, lt, NS + j + 2, tx[0], tm[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 1 < tail) use(NS + j + 1, tx[1], tm[1]);
+      }
+    };
+
+    // pass 1: LDS part, register part (the first AH groups were issued
+    // before), tail
+    float ar[CR];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (g + AH < NG && (g + AH) * G < nslots) {
+#pragma unroll
+        for (int k = 0; k < G; ++k) load(cur, lt, (g + AH) * G + k, rx[(g + AH) % R][k], rm[(g + AH) % R][k]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (g * G < nslots) {
+        float a[G * V];
+#pragma unroll
+        for (int k = 0; k < G; ++k) logit(g * G + k, rx[g % R][k], rm[g % R][k], a + k * V);
+        absorb(std::integral_constant<int, G * V>{}, a);
+        if (g * G < NL) {
+#pragma unroll
+          for (int k = 0; k < G * V / 4; ++k)
+            cache[g * G * V / 4 + k][lt] = f32x4{a[4 * k], a[4 * k + 1], a[4 * k + 2], a[4 * k + 3]};
+        } else {
+#pragma unroll
+          for (int i = 0; i < G * V; ++i) ar[g * G * V - CL + i] = a[i];
+        }
+      }
+    }
+    if constexpr (TAIL) {
+      over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms) {
+        float a[V];
+        logit(slot, rxs, rms, a);
+        absorb(std::integral_constant<int, V>{}, a);
+      });
+    }
+
+    // the next row's first slot groups, in flight from here on
+    const int64_t next = row + gridDim.x;
+    int64_t npos = pos + step_mod;
+    if (npos >= q_len) npos -= q_len;
+    const Row nxt = row_ctx(next, npos);
+    if (next < rows) prime(nxt, lt);
+
+    const MaxSumP p = group_allreduce<W>(MaxSumP{mrun, drun}, lds[parity], wave, lane);
+    parity ^= 1;
+    const bool empty = p.m == -INFINITY;
+    const float M = empty ? 0.f : p.m;
+    const float inv_d = empty ? 0.f : 1.f / p.d;
+
+    asm volatile("" : "+v"(lt));   // pass 2 recomputes its column tests too
+    // pass 2: outputs (register part first, which frees its registers)
+    T* yr = y + row * ld_y;
+    auto emit = [&](int slot, const float* a) {
+      float o[V];
+#pragma unroll
+      for (int i = 0; i < V; ++i) o[i] = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -M)) * inv_d;
+      store_until(yr, col_of(slot), cur.wend, o);
+    };
+#pragma unroll
+    for (int s = 0; s < NR; ++s)
+      if (NL + s < nslots) emit(NL + s, ar + s * V);
+#pragma unroll
+    for (int s = 0; s < NL; ++s) {
+      if (s >= nslots) continue;
+      float a[V];
+#pragma unroll
+      for (int k = 0; k < V / 4; ++k) {
+        const f32x4 v = cache[s * (V / 4) + k][lt];
+        a[4 * k] = v.x; a[4 * k + 1] = v.y; a[4 * k + 2] = v.z; a[4 * k + 3] = v.w;
+      }
+      emit(s, a);
+    }
+    if constexpr (TAIL) {
+      over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms) {
+        float a[V];
+        logit(slot, rxs, rms, a);
+        emit(slot, a);
+      });
+    }
+    cur = nxt;
+    pos = npos;
+  }
+}
+
 // rows batched per group: enough that a one-wave group handles about
 // FS_SM_BATCH_ELEMS elements per lane per trip
 template <int W, int EPT>
@@ -431,12 +658,32 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   FS_SM(8, 8, 1, 4)
   FS_SM(8, 16, 1, 4)
   FS_SM(8, 32, 1, 4)
+  FS_SM(16, 32, 1, 1)
 #undef FS_SM
-  // longer rows: streamed, one 8-wave block per row
+  // longer rows on the 16-byte path: row cache in LDS and registers, the
+  // columns past it streamed; one 16-wave block per compute unit
+  if constexpr (VEC) {
+    constexpr int CL = 32, CR = 32;
+    constexpr int64_t kCached = int64_t(1024) * (CL + CR);
+    auto go = [&](auto kern, int tail) {
+      const int64_t grid = a.rows < cus ? a.rows : cus;
+      hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(1024), 0, s, static_cast<const T*>(a.x),
+                         a.ld_x, static_cast<const MT*>(a.mask), a.ld_mask, static_cast<T*>(a.y),
+                         a.ld_y, a.rows, int(a.cols), a.scale, a.causal_q_len, a.trim_shift, tail);
+      return hipGetLastError();
+    };
+    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, false>, 0);
+    constexpr int64_t kSlot = int64_t(1024) * V;
+    return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, true>,
+              int((c - kCached + kSlot - 1) / kSlot));
+  }
+  // longer rows, element-wise path: streamed, one block of FS_SM_STREAM_WAVES
+  // waves per row
   {
-    constexpr int W = 8, U = 4;
+    constexpr int W = FS_SM_STREAM_WAVES, U = 4;
     const int trips = int((c + int64_t(64) * W * V * U - 1) / (int64_t(64) * W * V * U));
-    int64_t grid = a.rows < int64_t(cus) * 4 ? a.rows : int64_t(cus) * 4;
+    const int64_t cap = int64_t(cus) * FS_SM_STREAM_BPC;
+    int64_t grid = a.rows < cap ? a.rows : cap;
     hipLaunchKernelGGL((softmax_stream_kernel<T, MT, HAS_MASK, W, VEC>), dim3(unsigned(grid)),
                        dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
                        static_cast<const MT*>(a.mask), a.ld_mask, static_cast<T*>(a.y), a.ld_y,

@@ -1,7 +1,10 @@
-"""GPU parity of the streamed (long-row) softmax and LayerNorm/RMSNorm
-kernels against the float64 oracle: rows longer than the register-resident
-capacity (16384 columns), ragged tails, causal offsets, in-place outputs and
-rows whose running statistics must be rescaled from one chunk to the next."""
+"""GPU parity of the long-row softmax and LayerNorm/RMSNorm kernels against
+the float64 oracle: rows past the 8-wave register rungs (16384 columns), the
+16-wave rung (to 32768), the row cache in LDS and registers (to 65536) and its
+streamed tail, and the element-wise streamed kernel (widths that are not a
+whole number of 16-byte vectors); ragged tails, causal offsets, in-place
+outputs and rows whose running statistics must be rescaled from one chunk to
+the next."""
 import numpy as np
 import pytest
 import torch
@@ -13,7 +16,11 @@ from gpu_util import (TOL, Guarded, announce, assert_close, bf16_ulp_close, dev,
 
 pytestmark = pytest.mark.gpu
 
-LONG = [16384 + 8, 20000, 65536, 65536 + 24, 100003, 262144]
+# 16-wave register rung: 16392, 20000, 32768; row cache without a tail:
+# 32776, 49160, 65536; with a tail: 65560, 131112, 262144; element-wise
+# streamed kernel: 100003
+LONG = [16384 + 8, 20000, 32768, 32768 + 8, 49160, 65536, 65536 + 24, 100003, 131072 + 40,
+        262144]
 
 
 # ---- softmax -----------------------------------------------------------------
@@ -36,11 +43,12 @@ def test_softmax_streamed_widths(dtype, mask_dtype, cols):
         assert np.all(got[np.isinf(m)] == 0.0)
 
 
+@pytest.mark.parametrize("cols", [50000, 100000])
 @pytest.mark.parametrize("order", ["rising", "falling", "spike_last"])
-def test_softmax_streamed_running_max_moves(order):
+def test_softmax_streamed_running_max_moves(order, cols):
     # the running max changes in every chunk (rising), only in the first
-    # (falling), or only in the last element of the row (spike_last)
-    cols = 50000
+    # (falling), or only in the last element of the row (spike_last); 50000
+    # columns are all in the row cache, 100000 have a streamed tail
     base = np.linspace(-40.0, 40.0, cols)
     if order == "falling":
         base = base[::-1].copy()
@@ -48,7 +56,7 @@ def test_softmax_streamed_running_max_moves(order):
         base = np.zeros(cols)
         base[-1] = 30.0
     x = np.stack([base, base * 0.5, -base]).astype(np.float32)
-    announce("softmax streamed order", order)
+    announce("softmax streamed order", order, cols)
     y = host64(fs.row_softmax(torch.from_numpy(x).cuda(), None, 1.0))
     ref = oracle.row_softmax(x.astype(np.float64), None, 1.0)
     assert_close(order, y, ref, *TOL["f32"])
@@ -69,13 +77,13 @@ def test_softmax_streamed_causal(q_len, cols, rows):
     assert np.all(got[masked] == 0.0) and not np.any(np.signbit(got[masked]))
 
 
-def test_softmax_streamed_fully_masked_and_single_live():
-    cols = 30000
+@pytest.mark.parametrize("cols", [30000, 50000, 70000, 30001])
+def test_softmax_streamed_fully_masked_and_single_live(cols):
     x = torch.randn(3, cols, device="cuda")
     m = torch.full((3, cols), float("-inf"), device="cuda")
     m[1, cols - 1] = 0.0                         # only the last element is live
     m[2, 0] = 0.0                                # only the first
-    announce("softmax streamed masked")
+    announce("softmax streamed masked", cols)
     y = host64(fs.row_softmax(x, m, 1.0))
     assert np.all(y[0] == 0.0) and not np.any(np.signbit(y[0]))
     want1 = np.zeros(cols)
@@ -86,14 +94,17 @@ def test_softmax_streamed_fully_masked_and_single_live():
     np.testing.assert_array_equal(y[2], want2)
 
 
+@pytest.mark.parametrize("cols,ld", [(33333, 33400), (40000, 40016), (70000, 70064)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_softmax_streamed_strided_in_place(dtype):
+def test_softmax_streamed_strided_in_place(dtype, cols, ld):
+    # offset 0 with 16-byte rows takes the row cache, offset 1 the
+    # element-wise streamed kernel
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
-    rows, cols, ld = 4, 33333, 33400
+    rows = 4
     d = fd.softmax_inputs(41, rows, cols, dtype, mask_dtype=dtype)
     ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
     for offset in (0, 1):
-        announce("softmax streamed guard", dtype, offset)
+        announce("softmax streamed guard", dtype, cols, offset)
         xg = Guarded(rows, cols, ld, tdt, offset=offset)
         xg.view.copy_(dev(d["x"]))
         mg = Guarded(rows, cols, ld + 8, tdt, offset=offset)
@@ -147,13 +158,13 @@ def test_norm_streamed_widths(rms, dtype, cols):
     check_ln(f"cols {cols}", d, y, ro, dtype, rms)
 
 
-def test_layernorm_streamed_statistics_properties():
+@pytest.mark.parametrize("cols", [70001, 70000, 50000])
+def test_layernorm_streamed_statistics_properties(cols):
     # gamma = 1, beta = 0, rows with an offset mean: mean 0 and variance
     # var/(var+eps) after normalisation, whatever the chunking
     rng = np.random.default_rng(12)
-    cols = 70001
     x = (rng.standard_normal((4, cols)) + np.array([[0.0], [3.0], [-5.0], [0.5]])).astype(np.float32)
-    announce("layernorm streamed properties")
+    announce("layernorm streamed properties", cols)
     y, _ = fs.layernorm_residual(torch.from_numpy(x).cuda(), None, None, None, 0.25)
     y = host64(y)
     var = x.astype(np.float64).var(axis=1)
@@ -163,8 +174,8 @@ def test_layernorm_streamed_statistics_properties():
     assert_close("offset rows", y, ref, *TOL["f32"])
 
 
-def test_layernorm_streamed_constant_rows_give_beta():
-    cols = 40000
+@pytest.mark.parametrize("cols", [40000, 90000])
+def test_layernorm_streamed_constant_rows_give_beta(cols):
     x = torch.full((2, cols), -7.0, device="cuda")
     beta = torch.linspace(-1, 1, cols, device="cuda")
     gamma = torch.ones(cols, device="cuda")
@@ -172,12 +183,12 @@ def test_layernorm_streamed_constant_rows_give_beta():
     assert_close("constant rows", host64(y), np.broadcast_to(host64(beta), (2, cols)), 1e-6, 0)
 
 
+@pytest.mark.parametrize("cols", [50000, 70000])
 @pytest.mark.parametrize("rms", [False, True])
-def test_norm_streamed_in_place(rms):
-    cols = 50000
+def test_norm_streamed_in_place(rms, cols):
     d = fd.layernorm_inputs(7, 3, cols, "bf16")
     x, r = dev(d["x"]), dev(d["residual"])
-    announce("norm streamed in place", rms)
+    announce("norm streamed in place", rms, cols)
     if rms:
         fs.rmsnorm_residual(x, r, dev(d["gamma"]), d["eps"], out=x, residual_out=r)
     else:
@@ -187,13 +198,14 @@ def test_norm_streamed_in_place(rms):
     check_ln("in place", d, x, r, "bf16", rms)
 
 
+@pytest.mark.parametrize("cols,ld", [(24999, 25100), (40000, 40064), (70000, 70032)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_norm_streamed_strided_guards(dtype):
+def test_norm_streamed_strided_guards(dtype, cols, ld):
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
-    rows, cols, ld = 3, 24999, 25100
+    rows = 3
     d = fd.layernorm_inputs(19, rows, cols, dtype)
     for offset in (0, 1):
-        announce("norm streamed guard", dtype, offset)
+        announce("norm streamed guard", dtype, cols, offset)
         xg = Guarded(rows, cols, ld, tdt, offset=offset)
         xg.view.copy_(dev(d["x"]))
         yg = Guarded(rows, cols, ld + 16, tdt, offset=offset)
@@ -206,10 +218,10 @@ def test_norm_streamed_strided_guards(dtype):
         og.check_untouched("layernorm residual_out")
 
 
-def test_norm_optional_operands_streamed():
-    cols = 30000
+@pytest.mark.parametrize("cols", [30000, 50000, 70000])
+def test_norm_optional_operands_streamed(cols):
     d = fd.layernorm_inputs(23, 2, cols, "bf16")
-    announce("norm streamed optional")
+    announce("norm streamed optional", cols)
     y, ro = fs.layernorm_residual(dev(d["x"]), None, None, None, d["eps"])
     assert ro is None
     ref, _ = oracle.layernorm_residual(d["x"].f64(), None, None, None, d["eps"])
