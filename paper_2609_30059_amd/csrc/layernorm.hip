@@ -454,17 +454,21 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
     if constexpr (HAS_RES) rres.load(res + row * ld_r + cl);
   };
   Raw<T, V> rx[R][G], rres[R][G];
-  // the first AH slot groups of a row
+  // the first AH slot groups of a row.  Every load of the kernel is issued
+  // unconditionally (addresses past the row are clamped in bounds, and the
+  // row after the last is replaced by the last): with no branch around a
+  // load, the waits for each group count exactly the loads issued after it
   auto prime = [&](int64_t row, int lt) {
 #pragma unroll
     for (int g = 0; g < AH && g < NG; ++g) {
-      if (g * G < nslots) {
 #pragma unroll
-        for (int k = 0; k < G; ++k) load(row, lt, g * G + k, rx[g][k], rres[g][k]);
-      }
+      for (int k = 0; k < G; ++k) load(row, lt, g * G + k, rx[g][k], rres[g][k]);
     }
   };
-  if (int64_t(blockIdx.x) < rows) prime(blockIdx.x, tid);
+  // gamma and beta, or any valid address when absent (their values unused)
+  const T* gsrc = gamma ? gamma : x;
+  const T* bsrc = beta ? beta : x;
+  prime(blockIdx.x, tid);
 
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     T* yr = y + row * ld_y;
@@ -541,7 +545,7 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
     float hr[CR];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      if (g + AH < NG && (g + AH) * G < nslots) {
+      if (g + AH < NG) {
 #pragma unroll
         for (int k = 0; k < G; ++k)
           load(row, lt, (g + AH) * G + k, rx[(g + AH) % R][k], rres[(g + AH) % R][k]);
@@ -580,16 +584,15 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
     auto load_gb = [&](int slot, Raw<T, V>& rg, Raw<T, V>& rb) {
       const int c0 = col_of(slot);
       const int cl = c0 < cols ? c0 : clast;
-      if (gamma) rg.template load<false>(gamma + cl);
-      if (!RMS && beta) rb.template load<false>(beta + cl);
+      rg.template load<false>(gsrc + cl);
+      if constexpr (!RMS) rb.template load<false>(bsrc + cl);
     };
     Raw<T, V> rg[D + 1], rb[D + 1];
 #pragma unroll
-    for (int i = 0; i < D && i < NS; ++i)
-      if (slot_at(i) < nslots) load_gb(slot_at(i), rg[i], rb[i]);
+    for (int i = 0; i < D && i < NS; ++i) load_gb(slot_at(i), rg[i], rb[i]);
     // the next row's first slot groups, in flight from here on
     const int64_t next = row + gridDim.x;
-    if (next < rows) prime(next, lt);
+    prime(next < rows ? next : rows - 1, lt);
 
     if constexpr (RMS) run.n = 1.f;          // keep the fold from skipping lanes
     const P st = group_allreduce<W>(run, lds[parity], wave, lane);
@@ -620,8 +623,7 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
     };
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
-      if (i + D < NS && slot_at(i + D) < nslots)
-        load_gb(slot_at(i + D), rg[(i + D) % (D + 1)], rb[(i + D) % (D + 1)]);
+      if (i + D < NS) load_gb(slot_at(i + D), rg[(i + D) % (D + 1)], rb[(i + D) % (D + 1)]);
       __builtin_amdgcn_sched_barrier(0);
       if (slot_at(i) >= nslots) continue;
       float h[V];

@@ -397,13 +397,16 @@ __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
 }
 
 // Rows longer than the register-resident capacity, with a row cache: one
-// block of 16 waves per row keeps the logits of its first 64*16*CL columns in
-// LDS (fp32, CL per lane) and of the next 64*16*CR columns in registers, so
-// those columns are read from HBM once; with TAIL, the `tail` vector slots
-// per lane past both are streamed as in softmax_stream_kernel (read twice).
-// Pass 1 runs one online (m', d) per lane over the LDS part, the register
-// part and the tail, combined once across the block; pass 2 writes
-// 2^(a*log2e - M) / D from the registers, from LDS and from the re-read tail.
+// block of 16 waves per row keeps the exponentials of its first 64*16*CL
+// columns in LDS (fp32, CL per lane) and of the next 64*16*CR columns in
+// registers, so those columns are read from HBM once; with TAIL, the `tail`
+// vector slots per lane past both are streamed as in softmax_stream_kernel
+// (read twice).  Pass 1 runs one online (m', d) per lane over the LDS part,
+// the register part and the tail, combined once across the block; each
+// cached slot group keeps 2^(a*log2e - mg), mg the lane's running max after
+// the group.  Pass 2 writes 2^(a*log2e - M) / D as e * 2^(mg - M) / D from
+// the registers and from LDS (one product per element), and recomputes it
+// for the re-read tail.
 // Each lane reads back only the LDS words it wrote, so the cache needs no
 // barrier.  One block per compute unit holds one row at a time, so the loads
 // of the next row's first slot groups are issued before the block-wide
@@ -458,14 +461,16 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
   };
   Raw<T, V> rx[R][G];
   Raw<MT, V> rm[R][G];
-  // the first AH slot groups of a row
+  // the first AH slot groups of a row.  Every load of the kernel is issued
+  // unconditionally (addresses past the live columns are clamped in bounds,
+  // and the row after the last is replaced by the last): with no branch
+  // around a load, the waits for each group count exactly the loads issued
+  // after it
   auto prime = [&](const Row& c, int lt) {
 #pragma unroll
     for (int g = 0; g < AH && g < NG; ++g) {
-      if (g * G < nslots) {
 #pragma unroll
-        for (int k = 0; k < G; ++k) load(c, lt, g * G + k, rx[g][k], rm[g][k]);
-      }
+      for (int k = 0; k < G; ++k) load(c, lt, g * G + k, rx[g][k], rm[g][k]);
     }
   };
 
@@ -473,7 +478,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
   const int64_t step_mod = q_len > 0 ? int64_t(gridDim.x) % q_len : 0;
   int64_t pos = q_len > 0 ? int64_t(blockIdx.x) % q_len : 0;
   Row cur = row_ctx(blockIdx.x, pos);
-  if (int64_t(blockIdx.x) < rows) prime(cur, tid);
+  prime(cur, tid);
 
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     // the lane index is re-read per row (an empty asm) so that per-lane
@@ -498,9 +503,11 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
 #pragma unroll
       for (int i = 0; i < V; ++i) a[i] = (c0 + i <= cur.lim) ? xv[i] : -INFINITY;
     };
-    // merge N logits into the lane's running (m', d)
+    // merge N logits into the lane's running (m', d); with KEEP the logits
+    // are replaced by their exponentials 2^(a*log2e - m'), m' the running max
+    // after this merge (returned), so pass 2 needs one product per element
     float mrun = -INFINITY, drun = 0.f;
-    auto absorb = [&](auto kn, const float* a) {
+    auto absorb = [&](auto kn, auto keep, float* a) {
       constexpr int N = decltype(kn)::value;
       float tm = -INFINITY;
 #pragma unroll
@@ -509,10 +516,17 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
       const float msafe = mnew == -INFINITY ? 0.f : mnew;
       float dt = 0.f;
 #pragma unroll
-      for (int i = 0; i < N; ++i) dt += __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
+      for (int i = 0; i < N; ++i) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
+        dt += e;
+        if constexpr (decltype(keep)::value) a[i] = e;
+      }
       drun = fmaf(drun, __builtin_amdgcn_exp2f(mrun - msafe), dt);   // 2^-inf = 0
       mrun = mnew;
+      return msafe;
     };
+    using Keep = std::true_type;
+    using Drop = std::false_type;
     // the tail slots NS ... NS + tail - 1, one ahead: a slot's loads are in
     // flight while the previous slot is used.  Loads of slots past the row
     // are clamped in bounds (their logits are -inf and they store nothing).
@@ -531,11 +545,12 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     };
 
     // pass 1: LDS part, register part (the first AH groups were issued
-    // before), tail
-    float ar[CR];
+    // before), tail.  The cached parts keep exponentials, each group's
+    // relative to its own running max mg
+    float ar[CR], mg[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      if (g + AH < NG && (g + AH) * G < nslots) {
+      if (g + AH < NG) {
 #pragma unroll
         for (int k = 0; k < G; ++k) load(cur, lt, (g + AH) * G + k, rx[(g + AH) % R][k], rm[(g + AH) % R][k]);
       }
@@ -544,7 +559,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
         float a[G * V];
 #pragma unroll
         for (int k = 0; k < G; ++k) logit(g * G + k, rx[g % R][k], rm[g % R][k], a + k * V);
-        absorb(std::integral_constant<int, G * V>{}, a);
+        mg[g] = absorb(std::integral_constant<int, G * V>{}, Keep{}, a);
         if (g * G < NL) {
 #pragma unroll
           for (int k = 0; k < G * V / 4; ++k)
@@ -559,7 +574,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
       over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms) {
         float a[V];
         logit(slot, rxs, rms, a);
-        absorb(std::integral_constant<int, V>{}, a);
+        absorb(std::integral_constant<int, V>{}, Drop{}, a);
       });
     }
 
@@ -567,8 +582,8 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     const int64_t next = row + gridDim.x;
     int64_t npos = pos + step_mod;
     if (npos >= q_len) npos -= q_len;
-    const Row nxt = row_ctx(next, npos);
-    if (next < rows) prime(nxt, lt);
+    const Row nxt = row_ctx(next < rows ? next : rows - 1, npos);
+    prime(nxt, lt);
 
     const MaxSumP p = group_allreduce<W>(MaxSumP{mrun, drun}, lds[parity], wave, lane);
     parity ^= 1;
@@ -585,19 +600,27 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
       for (int i = 0; i < V; ++i) o[i] = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -M)) * inv_d;
       store_until(yr, col_of(slot), cur.wend, o);
     };
+    // a cached slot: its exponentials times 2^(mg - M) / D (at most 1 / D)
+    auto emit_e = [&](int slot, const float* e) {
+      const float f = __builtin_amdgcn_exp2f(mg[slot / G] - M) * inv_d;
+      float o[V];
+#pragma unroll
+      for (int i = 0; i < V; ++i) o[i] = e[i] * f;
+      store_until(yr, col_of(slot), cur.wend, o);
+    };
 #pragma unroll
     for (int s = 0; s < NR; ++s)
-      if (NL + s < nslots) emit(NL + s, ar + s * V);
+      if (NL + s < nslots) emit_e(NL + s, ar + s * V);
 #pragma unroll
     for (int s = 0; s < NL; ++s) {
       if (s >= nslots) continue;
-      float a[V];
+      float e[V];
 #pragma unroll
       for (int k = 0; k < V / 4; ++k) {
         const f32x4 v = cache[s * (V / 4) + k][lt];
-        a[4 * k] = v.x; a[4 * k + 1] = v.y; a[4 * k + 2] = v.z; a[4 * k + 3] = v.w;
+        e[4 * k] = v.x; e[4 * k + 1] = v.y; e[4 * k + 2] = v.z; e[4 * k + 3] = v.w;
       }
-      emit(s, a);
+      emit_e(s, e);
     }
     if constexpr (TAIL) {
       over_tail([&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms) {
@@ -672,8 +695,8 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
                          a.ld_y, a.rows, int(a.cols), a.scale, a.causal_q_len, a.trim_shift, tail);
       return hipGetLastError();
     };
-    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, false>, 0);
     constexpr int64_t kSlot = int64_t(1024) * V;
+    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, false>, 0);
     return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, true>,
               int((c - kCached + kSlot - 1) / kSlot));
   }
