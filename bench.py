@@ -33,6 +33,9 @@ script into the summaries under profiles/:
   --report-trace STATS_CSV          per-kernel durations (Markdown table)
   --write-traffic FETCH_CSV WRITE_CSV
                                     HBM bytes per launch -> profiles/traffic.json
+A third GPU mode, --long-rows, times softmax and LayerNorm/RMSNorm rows past
+the register-resident widths (16392 ... 262144 columns) and prints a Markdown
+table (not part of the step).
 """
 from __future__ import annotations
 
@@ -178,6 +181,8 @@ def parse():
     ap.add_argument("--measured-at", default="", help="commit the counter runs measured")
     ap.add_argument("--commands", nargs=2, default=("", ""), metavar=("FETCH_CMD", "WRITE_CMD"),
                     help="the rocprofv3 commands of the two counter runs (recorded)")
+    ap.add_argument("--long-rows", action="store_true",
+                    help="time long-row softmax and LayerNorm/RMSNorm and print a Markdown table")
     return ap.parse_args()
 
 
@@ -471,8 +476,84 @@ def load_traffic():
         return {}
 
 
+# widths of the long-row table: the 16-wave register rung (16392, 32768), the
+# row cache (49152, 65536), the row cache with a streamed tail (98304 and up)
+LONG_ROW_WIDTHS = (16392, 32768, 49152, 65536, 98304, 131072, 262144)
+# (name, dtype, bytes per element of one launch): compulsory reads + writes
+LONG_ROW_CASES = (
+    ("softmax bf16 + bf16 mask", "bf16", 6),
+    ("softmax bf16", "bf16", 4),
+    ("softmax fp32", "f32", 8),
+    ("LayerNorm + residual bf16", "bf16", 8),
+    ("RMSNorm + residual bf16", "bf16", 8),
+    ("LayerNorm + residual fp32", "f32", 16),
+)
+
+
+def long_rows(reps: int = 9) -> None:
+    """Median launch time of each long-row case: 256 MiB per bf16 input
+    (128 MiB of rows for fp32), a 512 MiB scrub between launches so that every
+    launch reads HBM, one event pair per launch."""
+    import torch
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    g = torch.Generator(device=dev)
+    results = {}
+    for cols in LONG_ROW_WIDTHS:
+        for name, dt, bpe in LONG_ROW_CASES:
+            tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+            rows = (128 << 20) // cols if dt == "bf16" else (32 << 20) // cols
+            g.manual_seed(cols)
+            x = (torch.randn(rows, cols, device=dev, generator=g) * 3).to(tdt)
+            y = torch.empty_like(x)
+            if name.startswith("softmax"):
+                m = None
+                if "mask" in name:
+                    m = torch.where(torch.rand(rows, cols, device=dev, generator=g) < 0.1,
+                                    float("-inf"), 0.0).to(tdt)
+                fn = lambda: fs.row_softmax(x, m, 0.125, out=y)
+            else:
+                r = torch.randn(rows, cols, device=dev, generator=g).to(tdt)
+                ro = torch.empty_like(x)
+                gam = (torch.randn(cols, device=dev, generator=g) * 0.1 + 1).to(tdt)
+                bet = (torch.randn(cols, device=dev, generator=g) * 0.1).to(tdt)
+                if name.startswith("RMS"):
+                    fn = lambda: fs.rmsnorm_residual(x, r, gam, 1e-5, out=y, residual_out=ro)
+                else:
+                    fn = lambda: fs.layernorm_residual(x, r, gam, bet, 1e-5, out=y,
+                                                       residual_out=ro)
+            fn()
+            torch.cuda.synchronize()
+            ts = []
+            for i in range(reps):
+                scrub.fill_(i & 0xFF)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            us = sorted(ts)[reps // 2]
+            results[(cols, name)] = (us, bpe * x.numel() / us / 1e3)
+            print(f"  {cols:>6} {name:<28} {us:8.1f} us {results[(cols, name)][1]:6.0f} GB/s",
+                  file=sys.stderr, flush=True)
+            del x, y
+    names = [c[0] for c in LONG_ROW_CASES]
+    print("| columns | " + " | ".join(names) + " |")
+    print("|---" * (len(names) + 1) + "|")
+    for cols in LONG_ROW_WIDTHS:
+        cells = [f"{results[(cols, n)][1]:.0f}" for n in names]
+        print(f"| {cols} | " + " | ".join(cells) + " |")
+
+
 def main():
     args = parse()
+    if args.long_rows:
+        long_rows()
+        return
     if args.report_trace:
         report_trace(args.report_trace)
         return

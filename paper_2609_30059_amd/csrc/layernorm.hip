@@ -697,6 +697,7 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
     FS_LN(8, 8, 1, 4)
     FS_LN(8, 16, 1, 4)
     FS_LN(8, 32, 1, 4)
+    FS_LN(16, 24, 1, 1)
     // fp32 rows at 16 waves x 32 elements spill; bf16 rows fit
     if constexpr (sizeof(T) == 2) { FS_LN(16, 32, 1, 1) }
   } else {

@@ -681,6 +681,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   FS_SM(8, 8, 1, 4)
   FS_SM(8, 16, 1, 4)
   FS_SM(8, 32, 1, 4)
+  FS_SM(16, 24, 1, 1)
   FS_SM(16, 32, 1, 1)
 #undef FS_SM
   // longer rows on the 16-byte path: row cache in LDS and registers, the
