@@ -101,14 +101,26 @@ def _match(names, label):
     return hits[0] if hits else None
 
 
-def report_trace(stats_csv: str) -> None:
-    """Markdown table of the bench kernels' rocprofv3 durations."""
+def report_trace(stats_csv: str, every: bool = False) -> None:
+    """Markdown table of the bench kernels' rocprofv3 durations; with `every`,
+    of every kernel of this library in the stats file (by name, without byte
+    counts)."""
     import csv
     rows = {}
     with open(stats_csv, newline="") as f:
         for r in csv.DictReader(f):
             rows[r["Name"].replace("(anonymous namespace)::", "")] = r
     total = sum(float(r["TotalDurationNs"]) for r in rows.values())
+    if every:
+        print("| kernel | calls | avg us | min us | max us | % of GPU time |")
+        print("|---|---|---|---|---|---|")
+        ours = {n: r for n, r in rows.items() if "fs::" in n}
+        for n, r in sorted(ours.items(), key=lambda kv: -float(kv[1]["TotalDurationNs"])):
+            short = n.split("(")[0].replace("void ", "").replace("fs::", "")
+            print(f"| `{short}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                  f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                  f"{100 * float(r['TotalDurationNs']) / total:.1f} |")
+        return
     print("| kernel | calls | avg us | min us | max us | % of GPU time | GB/s (avg) | % of 8 TB/s |")
     print("|---|---|---|---|---|---|---|---|")
     for label in KERNEL_PATTERNS:
@@ -176,6 +188,8 @@ def parse():
                     help="fraction of each sub-kernel's rows the CPU oracle baseline runs over")
     ap.add_argument("--report-trace", metavar="STATS_CSV",
                     help="print the bench kernels' durations from a rocprofv3 kernel-stats CSV")
+    ap.add_argument("--all-kernels", action="store_true",
+                    help="with --report-trace: list every kernel of the stats file")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from FETCH_SIZE and WRITE_SIZE runs")
     ap.add_argument("--measured-at", default="", help="commit the counter runs measured")
@@ -555,7 +569,7 @@ def main():
         long_rows()
         return
     if args.report_trace:
-        report_trace(args.report_trace)
+        report_trace(args.report_trace, args.all_kernels)
         return
     if args.write_traffic:
         out = write_traffic(*args.write_traffic, args.measured_at, *args.commands)

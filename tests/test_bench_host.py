@@ -93,6 +93,27 @@ def test_report_trace(tmp_path, capsys):
                     f"{100 * gbs / 8000:.1f} |"]
 
 
+def test_report_trace_every_library_kernel(tmp_path, capsys):
+    p = tmp_path / "s.csv"
+    p.write_text('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs"\n'
+                 '"void fs::(anonymous namespace)::softmax_cached_kernel<unsigned short, true>'
+                 '(unsigned short const*, long)",3,300000,100000,60,90000,110000\n'
+                 '"void at::native::fill_kernel<float>(float*)",2,200000,100000,40,100000,100000\n')
+    bench.report_trace(str(p), every=True)
+    out = capsys.readouterr().out.splitlines()
+    assert out[2] == "| `softmax_cached_kernel<unsigned short, true>` | 3 | 100.00 | 90.00 | 110.00 | 60.0 |"
+    assert len(out) == 3                      # torch's own kernels are not listed
+
+
+def test_long_row_widths_span_every_long_row_path():
+    # the 16-wave register rungs, the row cache with and without a tail
+    w = bench.LONG_ROW_WIDTHS
+    assert any(16384 < c <= 32768 for c in w)
+    assert any(32768 < c <= 65536 for c in w)
+    assert any(c > 65536 for c in w)
+    assert all(c % 8 == 0 for c in w)         # whole 16-byte bf16 vectors
+
+
 def test_tier_labels():
     assert T.label("void fs::layernorm_kernel<unsigned short, true, false>(unsigned short const*, long)") \
         == "layernorm_kernel<unsigned short, true, false>"
