@@ -39,6 +39,15 @@
 #ifndef FS_LN_CACHE_GB_AHEAD
 #define FS_LN_CACHE_GB_AHEAD 1   // slots of gamma/beta loads in flight ahead in the row cache's pass 2
 #endif
+#ifndef FS_LN_ELEMENTWISE_REG_COLS
+#define FS_LN_ELEMENTWISE_REG_COLS 8192   // widest element-wise row on the register rungs
+#endif
+#ifndef FS_LN_ELEMENTWISE_CACHE_COLS
+#define FS_LN_ELEMENTWISE_CACHE_COLS 32768   // element-wise rows take the row cache past this
+#endif
+#ifndef FS_LN_CACHE_ELEMENTWISE
+#define FS_LN_CACHE_ELEMENTWISE 1   // row cache also for rows of element-wise loads
+#endif
 #ifndef FS_LN_CACHE_AHEAD
 #define FS_LN_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
 #endif
@@ -69,9 +78,11 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   constexpr int kThreads = 64 * W;
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;
-  // gamma and beta stay in registers for the whole kernel when they fit;
-  // wider rows re-read them (cache-resident) after each trip's statistics
-  constexpr bool kAffineResident = EPT <= 32;
+  // gamma and beta stay in registers for the whole kernel when they fit
+  // (element-wise loads hold one value per register, so only small rungs
+  // keep them); wider rows re-read them (cache-resident) after each trip's
+  // statistics
+  constexpr bool kAffineResident = VEC ? EPT <= 32 : EPT <= 8;
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
   // one LDS fold area and one barrier sequence per block: rows wider than a
   // wave take the whole block (the row loop is then uniform across it)
@@ -422,19 +433,20 @@ __global__ __launch_bounds__(64 * W) void layernorm_stream_kernel(
 // holds one row at a time, so the loads of the next row's first slot groups
 // are issued before the block-wide combine: they are in flight while this
 // row's outputs are written.
-template <typename T, bool HAS_RES, bool RMS, int CL, int CR, bool TAIL>
+template <typename T, bool HAS_RES, bool RMS, bool VEC, int CL, int CR, bool TAIL>
 __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
     const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
     const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
     int64_t ld_ro, int64_t rows, int cols, float eps, int tail) {
   constexpr int W = 16, kThreads = 64 * W;
-  constexpr int V = Elem<T>::kVec;
+  constexpr int V = VEC ? Elem<T>::kVec : 1;   // elements per slot and lane
   constexpr int NL = CL / V, NR = CR / V, NS = NL + NR;   // vector slots per lane
   static_assert(CL % V == 0 && CR % V == 0 && CL % 4 == 0, "cache parts are whole vectors");
   // cached slots go in groups of G (about FS_LN_CACHE_GROUP_WORDS raw
   // registers each) with the loads of the next AH groups in flight
   constexpr int kWords = Raw<T, V>::kWords * (HAS_RES ? 2 : 1);
-  constexpr int G = kWords >= FS_LN_CACHE_GROUP_WORDS ? 1 : FS_LN_CACHE_GROUP_WORDS / kWords;
+  constexpr int G0 = kWords >= FS_LN_CACHE_GROUP_WORDS ? 1 : FS_LN_CACHE_GROUP_WORDS / kWords;
+  constexpr int G = VEC || G0 < 4 ? G0 : 4;   // element-wise slots: groups of 4
   constexpr int NG = NS / G, AH = FS_LN_CACHE_AHEAD, R = AH + 1;
   static_assert(NL % G == 0 && NR % G == 0, "slot groups split the cache parts");
   using P = MeanM2P;
@@ -630,12 +642,15 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
       if (i < NR) {
 #pragma unroll
         for (int k = 0; k < V; ++k) h[k] = hr[i * V + k];
-      } else {
+      } else if constexpr (V >= 4) {
 #pragma unroll
         for (int k = 0; k < V / 4; ++k) {
           const f32x4 v = cache[(i - NR) * (V / 4) + k][lt];
           h[4 * k] = v.x; h[4 * k + 1] = v.y; h[4 * k + 2] = v.z; h[4 * k + 3] = v.w;
         }
+      } else {
+#pragma unroll
+        for (int k = 0; k < V; ++k) h[k] = cache[((i - NR) * V + k) / 4][lt][((i - NR) * V + k) % 4];
       }
       emit(slot_at(i), h, rg[i % (D + 1)], rb[i % (D + 1)]);
     }
@@ -678,16 +693,17 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
   // and a row capacity 64 * W * EPT >= cols is launched.
   const int min_w = c >= FS_LN_SPLIT_COLS ? FS_LN_MIN_WAVES : 1;
 #define FS_LN(Wv, E, Gv, BPC)                                                       \
-  if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                   \
+  if (Wv >= min_w && c <= int64_t(64) * Wv * E &&                                 \
+      (VEC || c <= FS_LN_ELEMENTWISE_REG_COLS))                                  \
     return launch(layernorm_kernel<T, HAS_RES, RMS, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_LN(1, 1, 4, 8) }
   if constexpr (V <= 2) { FS_LN(1, 2, 4, 8) }
   if constexpr (V <= 4) { FS_LN(1, 4, 4, 8) }
   FS_LN(1, 8, 4, 8)
-  FS_LN(1, 16, 4, 8)
-  FS_LN(1, 32, 4, 8)
   if constexpr (VEC) {
+    FS_LN(1, 16, 4, 8)
+    FS_LN(1, 32, 4, 8)
     FS_LN(1, 64, 4, 8)
     FS_LN(2, 32, 1, 16)
     FS_LN(2, 64, 1, 16)
@@ -701,16 +717,20 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
     // fp32 rows at 16 waves x 32 elements spill; bf16 rows fit
     if constexpr (sizeof(T) == 2) { FS_LN(16, 32, 1, 1) }
   } else {
-    // element-wise loads: 64 elements per thread (or 32 at 8 waves with a
-    // residual) exceed the registers and spill, so wider rows take more
-    // waves and, past 8192 columns, the streamed kernel
-    FS_LN(2, 32, 1, 16)
-    FS_LN(4, 32, 1, 8)
+    // element-wise loads take one register per value and one address per
+    // element: wider rows take more waves at 8 elements per thread (16 and
+    // more left 1-2 waves per SIMD), and past 8192 columns the row cache
+    FS_LN(2, 8, 1, 16)
+    FS_LN(4, 8, 1, 8)
+    FS_LN(8, 8, 1, 4)
+    FS_LN(16, 8, 1, 1)
   }
 #undef FS_LN
-  // longer rows on the 16-byte path: row cache in LDS and registers, the
-  // columns past it streamed; one 16-wave block per compute unit
-  if constexpr (VEC) {
+  // longer rows: row cache in LDS and registers, the columns past it
+  // streamed; one 16-wave block per compute unit
+  // (element-wise rows only past FS_LN_ELEMENTWISE_CACHE_COLS: below it the
+  // row cache's single-element slots cost more than the streamed re-read)
+  if constexpr (VEC || FS_LN_CACHE_ELEMENTWISE) if (VEC || c > FS_LN_ELEMENTWISE_CACHE_COLS) {
     constexpr int CL = 32, CR = FS_LN_CACHE_REGS;
     constexpr int64_t kCached = int64_t(1024) * (CL + CR);
     auto go = [&](auto kern, int tail) {
@@ -722,9 +742,9 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
                          int(a.cols), a.eps, tail);
       return hipGetLastError();
     };
-    if (c <= kCached) return go(layernorm_cached_kernel<T, HAS_RES, RMS, CL, CR, false>, 0);
+    if (c <= kCached) return go(layernorm_cached_kernel<T, HAS_RES, RMS, VEC, CL, CR, false>, 0);
     constexpr int64_t kSlot = int64_t(1024) * V;
-    return go(layernorm_cached_kernel<T, HAS_RES, RMS, CL, CR, true>,
+    return go(layernorm_cached_kernel<T, HAS_RES, RMS, VEC, CL, CR, true>,
               int((c - kCached + kSlot - 1) / kSlot));
   }
   // longer rows, element-wise path: streamed, one block of FS_LN_STREAM_WAVES

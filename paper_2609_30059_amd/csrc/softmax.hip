@@ -38,6 +38,12 @@
 #ifndef FS_SM_STREAM_BPC
 #define FS_SM_STREAM_BPC 4     // its blocks per compute unit
 #endif
+#ifndef FS_SM_ELEMENTWISE_REG_COLS
+#define FS_SM_ELEMENTWISE_REG_COLS 32768   // widest element-wise row on the register rungs
+#endif
+#ifndef FS_SM_CACHE_ELEMENTWISE
+#define FS_SM_CACHE_ELEMENTWISE 1   // row cache also for rows of element-wise loads
+#endif
 #ifndef FS_SM_CACHE_AHEAD
 #define FS_SM_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
 #endif
@@ -411,18 +417,19 @@ __global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
 // barrier.  One block per compute unit holds one row at a time, so the loads
 // of the next row's first slot groups are issued before the block-wide
 // combine: they are in flight while this row's outputs are written.
-template <typename T, typename MT, bool HAS_MASK, int CL, int CR, bool TAIL>
+template <typename T, typename MT, bool HAS_MASK, bool VEC, int CL, int CR, bool TAIL>
 __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
     int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift, int tail) {
   constexpr int W = 16, kThreads = 64 * W;
-  constexpr int V = Elem<T>::kVec;
+  constexpr int V = VEC ? Elem<T>::kVec : 1;   // elements per slot and lane
   constexpr int NL = CL / V, NR = CR / V, NS = NL + NR;   // vector slots per lane
   static_assert(CL % V == 0 && CR % V == 0 && CL % 4 == 0, "cache parts are whole vectors");
   // cached slots go in groups of G (about FS_SM_CACHE_GROUP_WORDS raw
   // registers each) with the loads of the next AH groups in flight
   constexpr int kWords = Raw<T, V>::kWords + (HAS_MASK ? Raw<MT, V>::kWords : 0);
-  constexpr int G = kWords >= FS_SM_CACHE_GROUP_WORDS ? 1 : FS_SM_CACHE_GROUP_WORDS / kWords;
+  constexpr int G0 = kWords >= FS_SM_CACHE_GROUP_WORDS ? 1 : FS_SM_CACHE_GROUP_WORDS / kWords;
+  constexpr int G = VEC || G0 < 4 ? G0 : 4;   // element-wise slots: groups of 4
   constexpr int NG = NS / G, AH = FS_SM_CACHE_AHEAD, R = AH + 1;
   static_assert(NL % G == 0 && NR % G == 0, "slot groups split the cache parts");
   __shared__ f32x4 cache[CL / 4][kThreads];
@@ -615,10 +622,15 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     for (int s = 0; s < NL; ++s) {
       if (s >= nslots) continue;
       float e[V];
+      if constexpr (V >= 4) {
 #pragma unroll
-      for (int k = 0; k < V / 4; ++k) {
-        const f32x4 v = cache[s * (V / 4) + k][lt];
-        e[4 * k] = v.x; e[4 * k + 1] = v.y; e[4 * k + 2] = v.z; e[4 * k + 3] = v.w;
+        for (int k = 0; k < V / 4; ++k) {
+          const f32x4 v = cache[s * (V / 4) + k][lt];
+          e[4 * k] = v.x; e[4 * k + 1] = v.y; e[4 * k + 2] = v.z; e[4 * k + 3] = v.w;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) e[i] = cache[(s * V + i) / 4][lt][(s * V + i) % 4];
       }
       emit_e(s, e);
     }
@@ -663,7 +675,8 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   // the register-resident kernel keeps causal positions in 32 bits
   const bool small_q = a.causal_q_len < (int64_t(1) << 30);
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
-  if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E)                       \
+  if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E &&                     \
+      (VEC || c <= FS_SM_ELEMENTWISE_REG_COLS))                                  \
     return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }
@@ -684,9 +697,9 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   FS_SM(16, 24, 1, 1)
   FS_SM(16, 32, 1, 1)
 #undef FS_SM
-  // longer rows on the 16-byte path: row cache in LDS and registers, the
-  // columns past it streamed; one 16-wave block per compute unit
-  if constexpr (VEC) {
+  // longer rows: row cache in LDS and registers, the columns past it
+  // streamed; one 16-wave block per compute unit
+  if constexpr (VEC || FS_SM_CACHE_ELEMENTWISE) {
     constexpr int CL = 32, CR = 32;
     constexpr int64_t kCached = int64_t(1024) * (CL + CR);
     auto go = [&](auto kern, int tail) {
@@ -697,8 +710,8 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
       return hipGetLastError();
     };
     constexpr int64_t kSlot = int64_t(1024) * V;
-    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, false>, 0);
-    return go(softmax_cached_kernel<T, MT, HAS_MASK, CL, CR, true>,
+    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, false>, 0);
+    return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, true>,
               int((c - kCached + kSlot - 1) / kSlot));
   }
   // longer rows, element-wise path: streamed, one block of FS_SM_STREAM_WAVES

@@ -16,11 +16,12 @@ from gpu_util import (TOL, Guarded, announce, assert_close, bf16_ulp_close, dev,
 
 pytestmark = pytest.mark.gpu
 
-# 16-wave register rung: 16392, 20000, 32768; row cache without a tail:
-# 32776, 49160, 65536; with a tail: 65560, 131112, 262144; element-wise
-# streamed kernel: 100003
-LONG = [16384 + 8, 20000, 32768, 32768 + 8, 49160, 65536, 65536 + 24, 100003, 131072 + 40,
-        262144]
+# 16-wave register rungs: 16392, 20000, 32768; row cache without a tail:
+# 32776, 49160, 65536; with a tail: 65560, 131112, 262144; widths that are not
+# whole 16-byte vectors take element-wise loads: the row cache without a tail
+# (50001) and with one (100003)
+LONG = [16384 + 8, 20000, 32768, 32768 + 8, 49160, 50001, 65536, 65536 + 24, 100003,
+        131072 + 40, 262144]
 
 
 # ---- softmax -----------------------------------------------------------------
