@@ -490,9 +490,10 @@ def load_traffic():
         return {}
 
 
-# widths of the long-row table: the 16-wave register rung (16392, 32768), the
-# row cache (49152, 65536), the row cache with a streamed tail (98304 and up)
-LONG_ROW_WIDTHS = (16392, 32768, 49152, 65536, 98304, 131072, 262144)
+# widths of the long-row table: the 16-wave register rungs (16392, 32768), the
+# row cache (49152, 65536), the row cache with a streamed tail (98304 and up);
+# 50257 columns are not a whole number of 16-byte vectors (element-wise loads)
+LONG_ROW_WIDTHS = (16392, 32768, 49152, 50257, 65536, 98304, 131072, 262144)
 # (name, dtype, bytes per element of one launch): compulsory reads + writes
 LONG_ROW_CASES = (
     ("softmax bf16 + bf16 mask", "bf16", 6),

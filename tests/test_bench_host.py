@@ -111,7 +111,8 @@ def test_long_row_widths_span_every_long_row_path():
     assert any(16384 < c <= 32768 for c in w)
     assert any(32768 < c <= 65536 for c in w)
     assert any(c > 65536 for c in w)
-    assert all(c % 8 == 0 for c in w)         # whole 16-byte bf16 vectors
+    assert any(c % 8 for c in w)              # element-wise loads (not whole 16-byte vectors)
+    assert sum(c % 8 == 0 for c in w) >= 6    # the 16-byte path at every other width
 
 
 def test_tier_labels():
