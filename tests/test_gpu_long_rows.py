@@ -65,9 +65,11 @@ def test_softmax_streamed_running_max_moves(order, cols):
 
 
 @pytest.mark.parametrize("q_len,cols,rows", [(5, 40000, 11), (64, 70000, 9), (3, 16400, 7),
-                                             (25000, 40000, 3), (39990, 40000, 12)])
+                                             (25000, 40000, 3), (39990, 40000, 12),
+                                             (7, 40001, 9), (4, 70001, 5)])
 def test_softmax_streamed_causal(q_len, cols, rows):
-    # the causal limit falls near the row end, mid-row and within the first chunk
+    # the causal limit falls near the row end, mid-row and within the first
+    # chunk; 40001 and 70001 columns take element-wise loads
     d = fd.softmax_inputs(q_len * cols, rows, cols, "f32", mask_dtype="f32", p_masked=0.2)
     announce("softmax streamed causal", q_len, cols)
     y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"], causal_q_len=q_len)

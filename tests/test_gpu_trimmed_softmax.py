@@ -56,16 +56,21 @@ def test_square_attention_rows(dtype, block):
     check(f"block {block}", d["x"].f64(), y, d["scale"], q, block, dtype)
 
 
-@pytest.mark.parametrize("rows,cols,q,block", [(37, 40, 10, 4), (20, 3000, 2900, 256),
-                                              (16, 20000, 20000, 4096), (9, 33333, 9, 1024)])
-def test_rectangular_ragged_and_streamed(rows, cols, q, block):
-    d = fd.softmax_inputs(rows + cols, rows, cols, "f32", mask_dtype=None, sigma=2.0)
-    announce("trimmed softmax rect", rows, cols, q, block)
+# register rows, the 16-wave rung (20000), the row cache with element-wise
+# loads (33333, 100001 with a streamed tail) and with 16-byte loads (50000,
+# 70000 with a tail)
+@pytest.mark.parametrize("rows,cols,q,block,dtype", [
+    (37, 40, 10, 4, "f32"), (20, 3000, 2900, 256, "f32"), (16, 20000, 20000, 4096, "f32"),
+    (9, 33333, 9, 1024, "f32"), (6, 50000, 40000, 2048, "bf16"), (6, 70000, 70000, 8192, "f32"),
+    (5, 100001, 3, 16384, "f32")])
+def test_rectangular_ragged_and_streamed(rows, cols, q, block, dtype):
+    d = fd.softmax_inputs(rows + cols, rows, cols, dtype, mask_dtype=None, sigma=2.0)
+    announce("trimmed softmax rect", rows, cols, q, block, dtype)
     x = dev(d["x"])
     y = guard_like(x)
     fs.causal_softmax_trimmed(x, d["scale"], q, block, out=y)
     torch.cuda.synchronize()
-    check(f"{rows}x{cols} q{q} b{block}", d["x"].f64(), y, d["scale"], q, block, "f32")
+    check(f"{rows}x{cols} q{q} b{block}", d["x"].f64(), y, d["scale"], q, block, dtype)
 
 
 def test_in_place_keeps_the_unwritten_logits():
