@@ -115,12 +115,12 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  *          elements are not read and are written as +0.  0 = off.
  * Entries whose logit is -inf come out exactly +0; a fully masked row comes
  * out all +0.  Rows up to 32768 columns are held in registers and read from
- * HBM once, with a single (max, sum) online combine per row.  Longer rows of
- * whole 16-byte vectors keep their first 65536 logits on chip (LDS and
+ * HBM once, with a single (max, sum) online combine per row.  Longer rows
+ * keep the exponentials of their first 65536 columns on chip (LDS and
  * registers, one row per compute unit) and read those columns once; the
- * columns past them, and every column of rows that are not whole 16-byte
- * vectors, are streamed: one pass keeps a running (max, sum) and a second
- * re-reads x (and mask) to write y (2 reads + 1 write per element).  Rows
+ * columns past them are streamed: one pass keeps a running (max, sum) and a
+ * second re-reads x (and mask) to write y (2 reads + 1 write per element).
+ * Rows that are not whole 16-byte vectors load one element per lane.  Rows
  * may be up to FS_SOFTMAX_MAX_COLS columns.
  * scale must be finite; mask values may be any float or -inf.
  */
@@ -173,13 +173,14 @@ FS_API fs_status fs_causal_softmax_trimmed(const void* x, int64_t ld_x, void* y,
  * each other.  eps must be finite and >= 0.  Rows of whole 16-byte vectors up
  * to 16384 columns (32768 for bf16), and other rows up to 8192 columns, are
  * held in registers: x and residual are read once and the statistics take
- * two exact passes over the registers.  Longer rows of whole
- * 16-byte vectors keep h of their first 65536 columns on chip (LDS and
- * registers, one row per compute unit) and read those columns once, merging
- * per-chunk (count, mean, M2) statistics; the columns past them, and every
- * column of rows that are not whole 16-byte vectors, are streamed: a first
- * pass merges the statistics, a second re-reads x and residual and writes
- * residual_out and y.  Rows may be up to FS_LAYERNORM_MAX_COLS columns.
+ * two exact passes over the registers.  Longer rows (for rows that are not
+ * whole 16-byte vectors: past 32768 columns) keep h of their first 65536
+ * columns on chip (LDS and registers, one row per compute unit) and read
+ * those columns once, merging per-chunk (count, mean, M2) statistics; the
+ * columns past them, and the other rows that are not whole 16-byte vectors,
+ * are streamed: a first pass merges the statistics, a second re-reads x and
+ * residual and writes residual_out and y.  Rows may be up to
+ * FS_LAYERNORM_MAX_COLS columns.
  */
 #define FS_LAYERNORM_MAX_COLS 16777216
 FS_API fs_status fs_layernorm_residual(const void* x, int64_t ld_x, const void* residual,

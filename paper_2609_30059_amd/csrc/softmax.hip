@@ -32,17 +32,8 @@
 #ifndef FS_SM_BATCH_ELEMS
 #define FS_SM_BATCH_ELEMS 16
 #endif
-#ifndef FS_SM_STREAM_WAVES
-#define FS_SM_STREAM_WAVES 8   // waves per row of the streamed kernel
-#endif
-#ifndef FS_SM_STREAM_BPC
-#define FS_SM_STREAM_BPC 4     // its blocks per compute unit
-#endif
 #ifndef FS_SM_ELEMENTWISE_REG_COLS
 #define FS_SM_ELEMENTWISE_REG_COLS 32768   // widest element-wise row on the register rungs
-#endif
-#ifndef FS_SM_CACHE_ELEMENTWISE
-#define FS_SM_CACHE_ELEMENTWISE 1   // row cache also for rows of element-wise loads
 #endif
 #ifndef FS_SM_CACHE_AHEAD
 #define FS_SM_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
@@ -132,8 +123,8 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   const bool store_all = trim_shift < 0 && cols == kThreads * EPT;
 
   // causal position of row0 (row0 mod q_len), advanced by the loop step
-  // without a division per row.  The host sends q_len >= 2^30 to the
-  // streamed kernel, so positions and column limits fit in 32 bits here and
+  // without a division per row.  The host sends q_len >= 2^30 to the row
+  // cache, so positions and column limits fit in 32 bits here and
   // stay in scalar registers with native scalar compares (64-bit compares
   // run on the vector unit).
   const int64_t step = int64_t(gridDim.x) * G * R;
@@ -303,111 +294,12 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   }
 }
 
-// Rows longer than the register-resident capacity: one block of W waves per
-// row streams the row twice.  Pass 1 keeps a running online (m', d) per lane
-// (one rescale exp2 per trip of U vectors) and combines the lanes once; pass 2
-// re-reads the row and writes 2^(a*log2e - M) / D.  Two HBM reads of x (the
-// second is often served from L2 or the Infinity Cache) and one write.
-template <typename T, typename MT, bool HAS_MASK, int W, bool VEC>
-__global__ __launch_bounds__(64 * W) void softmax_stream_kernel(
-    const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
-    int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift, int trips) {
-  constexpr int kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<T>::kVec : 1;
-  constexpr int U = 4;
-  __shared__ MaxSumP lds[2][W];
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
-  int parity = 0;
-
-  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
-    const T* xr = x + row * ld_x;
-    const MT* mr = HAS_MASK ? mask + row * ld_m : nullptr;
-    const int64_t pos = q_len > 0 ? row % q_len : 0;   // one division per (long) row
-    const int64_t limit = q_len > 0 ? pos + (cols - q_len) : int64_t(cols) - 1;
-    const int lim = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
-    int64_t we = cols;
-    if (q_len > 0 && trim_shift >= 0)
-      we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
-    const int wend = int(we < cols ? (we < 0 ? 0 : we) : cols);
-    const int limv = lim < 0 ? 0 : (lim / V) * V;
-
-    // logits of one trip: U vectors per lane, -inf past lim
-    auto trip_logits = [&](int t, float (&a)[U * V]) {
-      Raw<T, V> rx[U];
-      Raw<MT, V> rm[HAS_MASK ? U : 1];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int c0 = ((t * U + u) * kThreads + tid) * V;
-        const int cl = c0 <= lim ? c0 : limv;
-        rx[u].load(xr + cl);
-        if constexpr (HAS_MASK) rm[u].load(mr + cl);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int c0 = ((t * U + u) * kThreads + tid) * V;
-        float xv[V];
-        rx[u].unpack(xv);
-        if constexpr (HAS_MASK) {
-          float mv[V];
-          rm[u].unpack(mv);
-#pragma unroll
-          for (int i = 0; i < V; ++i) xv[i] = fmaf(xv[i], scale, mv[i]);
-        } else {
-#pragma unroll
-          for (int i = 0; i < V; ++i) xv[i] *= scale;
-        }
-#pragma unroll
-        for (int i = 0; i < V; ++i) a[u * V + i] = (c0 + i <= lim) ? xv[i] : -INFINITY;
-      }
-    };
-
-    // pass 1: running (m', d) per lane
-    float mrun = -INFINITY, drun = 0.f;
-    for (int t = 0; t < trips; ++t) {
-      float a[U * V];
-      trip_logits(t, a);
-      float tm = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < U * V; ++i) tm = fmaxf(tm, a[i]);
-      const float mnew = fmaxf(mrun, tm == -INFINITY ? -INFINITY : tm * kLog2e);
-      const float msafe = mnew == -INFINITY ? 0.f : mnew;
-      float dt = 0.f;
-#pragma unroll
-      for (int i = 0; i < U * V; ++i) dt += __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
-      drun = fmaf(drun, __builtin_amdgcn_exp2f(mrun - msafe), dt);   // 2^-inf = 0
-      mrun = mnew;
-    }
-    const MaxSumP p = group_allreduce<W>(MaxSumP{mrun, drun}, lds[parity], wave, lane);
-    parity ^= 1;
-    const bool empty = p.m == -INFINITY;
-    const float M = empty ? 0.f : p.m;
-    const float inv_d = empty ? 0.f : 1.f / p.d;
-
-    // pass 2: outputs
-    T* yr = y + row * ld_y;
-    for (int t = 0; t < trips; ++t) {
-      float a[U * V];
-      trip_logits(t, a);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int c0 = ((t * U + u) * kThreads + tid) * V;
-        float o[V];
-#pragma unroll
-        for (int i = 0; i < V; ++i)
-          o[i] = __builtin_amdgcn_exp2f(fmaf(a[u * V + i], kLog2e, -M)) * inv_d;
-        store_until(yr, c0, wend, o);
-      }
-    }
-  }
-}
-
 // Rows longer than the register-resident capacity, with a row cache: one
 // block of 16 waves per row keeps the exponentials of its first 64*16*CL
 // columns in LDS (fp32, CL per lane) and of the next 64*16*CR columns in
 // registers, so those columns are read from HBM once; with TAIL, the `tail`
-// vector slots per lane past both are streamed as in softmax_stream_kernel
-// (read twice).  Pass 1 runs one online (m', d) per lane over the LDS part,
+// slots per lane past both are streamed: read once for the running (m', d)
+// and again for the outputs.  Pass 1 runs one online (m', d) per lane over the LDS part,
 // the register part and the tail, combined once across the block; each
 // cached slot group keeps 2^(a*log2e - mg), mg the lane's running max after
 // the group.  Pass 2 writes 2^(a*log2e - M) / D as e * 2^(mg - M) / D from
@@ -697,9 +589,10 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   FS_SM(16, 24, 1, 1)
   FS_SM(16, 32, 1, 1)
 #undef FS_SM
-  // longer rows: row cache in LDS and registers, the columns past it
-  // streamed; one 16-wave block per compute unit
-  if constexpr (VEC || FS_SM_CACHE_ELEMENTWISE) {
+  // longer rows (and causal rows with q_len >= 2^30): row cache in LDS and
+  // registers, the columns past it streamed; one 16-wave block per compute
+  // unit, 16-byte or element-wise slots
+  {
     constexpr int CL = 32, CR = 32;
     constexpr int64_t kCached = int64_t(1024) * (CL + CR);
     auto go = [&](auto kern, int tail) {
@@ -713,19 +606,6 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
     if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, false>, 0);
     return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, true>,
               int((c - kCached + kSlot - 1) / kSlot));
-  }
-  // longer rows, element-wise path: streamed, one block of FS_SM_STREAM_WAVES
-  // waves per row
-  {
-    constexpr int W = FS_SM_STREAM_WAVES, U = 4;
-    const int trips = int((c + int64_t(64) * W * V * U - 1) / (int64_t(64) * W * V * U));
-    const int64_t cap = int64_t(cus) * FS_SM_STREAM_BPC;
-    int64_t grid = a.rows < cap ? a.rows : cap;
-    hipLaunchKernelGGL((softmax_stream_kernel<T, MT, HAS_MASK, W, VEC>), dim3(unsigned(grid)),
-                       dim3(64 * W), 0, s, static_cast<const T*>(a.x), a.ld_x,
-                       static_cast<const MT*>(a.mask), a.ld_mask, static_cast<T*>(a.y), a.ld_y,
-                       a.rows, int(a.cols), a.scale, a.causal_q_len, a.trim_shift, trips);
-    return hipGetLastError();
   }
 }
 
