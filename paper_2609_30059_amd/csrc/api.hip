@@ -109,6 +109,11 @@ bool vec_ok(const void* p, int64_t ld, int es) {
   return p == nullptr || (aligned(p, 16) && (ld * es) % 16 == 0);
 }
 
+// q (or NULL) starts every row at the same offset within a 16-byte unit as p
+bool same_phase(const void* p, int64_t ld, const void* q, int64_t ldq, int es) {
+  return q == nullptr || ((addr(p) - addr(q)) % 16 == 0 && ((ld - ldq) * es) % 16 == 0);
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +200,8 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
                     causal_q_len, dtype, false};
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(mask, ld_mask, ms);
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && (mask == nullptr || ms == es) &&
+              same_phase(x, ld_x, y, ld_y, es) && same_phase(x, ld_x, mask, ld_mask, es);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_softmax(a, cus, stream);
@@ -228,6 +235,7 @@ fs_status fs_causal_softmax_trimmed(const void* x, int64_t ld_x, void* y, int64_
   fs::SoftmaxArgs a{x, ld_x, nullptr, 0, dtype, y, ld_y, rows, cols, scale,
                     causal_q_len, dtype, false};
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es);
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && same_phase(x, ld_x, y, ld_y, es);
   int shift = 0;
   while ((int64_t(1) << shift) < block) ++shift;
   a.trim_shift = shift;

@@ -31,6 +31,10 @@ struct SoftmaxArgs {
   fs_dtype dtype;
   bool vec;
   int trim_shift = -1;   // causal block trimming: log2(block), or -1 (write whole rows)
+  // not vec, but x, mask and y start every row at one offset within a
+  // 16-byte unit: the row cache loads the aligned span of each row 16 bytes
+  // at a time and its few head and tail elements one at a time
+  bool shifted = false;
 };
 
 struct LayerNormArgs {

@@ -35,6 +35,9 @@
 #ifndef FS_SM_ELEMENTWISE_REG_COLS
 #define FS_SM_ELEMENTWISE_REG_COLS 32768   // widest element-wise row on the register rungs
 #endif
+#ifndef FS_SM_SHIFT_REG_COLS
+#define FS_SM_SHIFT_REG_COLS 16384  // widest row of a shared 16-byte phase on the register rungs
+#endif
 #ifndef FS_SM_CACHE_AHEAD
 #define FS_SM_CACHE_AHEAD 3   // slot groups of loads in flight ahead in the row cache's pass 1
 #endif
@@ -309,19 +312,19 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 // barrier.  One block per compute unit holds one row at a time, so the loads
 // of the next row's first slot groups are issued before the block-wide
 // combine: they are in flight while this row's outputs are written.
-template <typename T, typename MT, bool HAS_MASK, bool VEC, int CL, int CR, bool TAIL>
+template <typename T, typename MT, bool HAS_MASK, bool VEC, bool SHIFT, int CL, int CR, bool TAIL>
 __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m, T* y,
     int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift, int tail) {
   constexpr int W = 16, kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<T>::kVec : 1;   // elements per slot and lane
+  constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;   // elements per slot and lane
   constexpr int NL = CL / V, NR = CR / V, NS = NL + NR;   // vector slots per lane
   static_assert(CL % V == 0 && CR % V == 0 && CL % 4 == 0, "cache parts are whole vectors");
   // cached slots go in groups of G (about FS_SM_CACHE_GROUP_WORDS raw
   // registers each) with the loads of the next AH groups in flight
   constexpr int kWords = Raw<T, V>::kWords + (HAS_MASK ? Raw<MT, V>::kWords : 0);
   constexpr int G0 = kWords >= FS_SM_CACHE_GROUP_WORDS ? 1 : FS_SM_CACHE_GROUP_WORDS / kWords;
-  constexpr int G = VEC || G0 < 4 ? G0 : 4;   // element-wise slots: groups of 4
+  constexpr int G = V > 1 || G0 < 4 ? G0 : 4;   // element-wise slots: groups of 4
   constexpr int NG = NS / G, AH = FS_SM_CACHE_AHEAD, R = AH + 1;
   static_assert(NL % G == 0 && NR % G == 0, "slot groups split the cache parts");
   __shared__ f32x4 cache[CL / 4][kThreads];
@@ -332,28 +335,40 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
   int parity = 0;
 
   // per-row context: row pointers, last live column (causal rule), end of
-  // the written columns (trimmed causal rows)
+  // the written columns (trimmed causal rows).  With SHIFT the slots cover
+  // the row's aligned body [h, bend), whole 16-byte units, and its h head
+  // and cols - bend tail elements (at most 2 V - 2) are extra elements of
+  // the first lanes; lim, limv and wendb then refer to the body
   struct Row {
     const T* xr;
     const MT* mr;
-    int lim, limv, wend;
+    int lim, limv, wend, wendb, h, bend, lime;
   };
   auto row_ctx = [&](int64_t row, int64_t pos) {
     Row c;
     c.xr = x + row * ld_x;
     c.mr = HAS_MASK ? mask + row * ld_m : nullptr;
+    c.h = 0;
+    c.bend = cols;
+    if constexpr (SHIFT) {
+      const int phase = int(reinterpret_cast<uintptr_t>(c.xr) & 15) / int(sizeof(T));
+      c.h = (V - phase) % V;
+      c.bend = c.h + ((cols - c.h) / V) * V;
+    }
     const int64_t limit = q_len > 0 ? pos + (cols - q_len) : int64_t(cols) - 1;
-    c.lim = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
-    c.limv = c.lim < 0 ? 0 : (c.lim / V) * V;
+    c.lime = int(limit < int64_t(cols) - 1 ? (limit < -1 ? -1 : limit) : int64_t(cols) - 1);
+    c.lim = c.lime < c.bend - 1 ? c.lime : c.bend - 1;
+    c.limv = c.lim < c.h ? c.h : c.h + ((c.lim - c.h) / V) * V;
     int64_t we = cols;
     if (q_len > 0 && trim_shift >= 0)
       we = (((pos >> trim_shift) + 1) << trim_shift) + (cols - q_len);
     c.wend = int(we < cols ? (we < 0 ? 0 : we) : cols);
+    c.wendb = c.wend < c.bend ? c.wend : c.bend;
     return c;
   };
   // loads of a slot, clamped in bounds past the row's last live column
   auto load = [&](const Row& c, int lt, int slot, Raw<T, V>& rx, Raw<MT, V>& rm) {
-    const int c0 = (slot * kThreads + lt) * V;
+    const int c0 = c.h + (slot * kThreads + lt) * V;
     const int cl = c0 <= c.lim ? c0 : c.limv;
     rx.load(c.xr + cl);
     if constexpr (HAS_MASK) rm.load(c.mr + cl);
@@ -385,7 +400,17 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     // across rows
     int lt = tid;
     asm volatile("" : "+v"(lt));
-    auto col_of = [&](int slot) { return (slot * kThreads + lt) * V; };
+    auto col_of = [&](int slot) { return cur.h + (slot * kThreads + lt) * V; };
+    // SHIFT: the lane's extra element (head or tail), loaded first
+    const int nx = cur.h + (cols - cur.bend);
+    const bool has_x = SHIFT && lt < nx;
+    const int ce = has_x ? (lt < cur.h ? lt : cur.bend + (lt - cur.h)) : 0;
+    Raw<T, 1> ex;
+    Raw<MT, 1> em;
+    if constexpr (SHIFT) {
+      ex.load(cur.xr + ce);
+      if constexpr (HAS_MASK) em.load(cur.mr + ce);
+    }
     auto logit = [&](int slot, const Raw<T, V>& rxs, const Raw<MT, V>& rms, float* a) {
       const int c0 = col_of(slot);
       float xv[V];
@@ -476,6 +501,15 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
         absorb(std::integral_constant<int, V>{}, Drop{}, a);
       });
     }
+    float ax = -INFINITY;   // the extra element's logit
+    if constexpr (SHIFT) {
+      float xv, mv = 0.f;
+      ex.unpack(&xv);
+      if constexpr (HAS_MASK) em.unpack(&mv);
+      const float v = HAS_MASK ? fmaf(xv, scale, mv) : xv * scale;
+      ax = has_x && ce <= cur.lime ? v : -INFINITY;
+      absorb(std::integral_constant<int, 1>{}, Drop{}, &ax);
+    }
 
     // the next row's first slot groups, in flight from here on
     const int64_t next = row + gridDim.x;
@@ -497,7 +531,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
       float o[V];
 #pragma unroll
       for (int i = 0; i < V; ++i) o[i] = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -M)) * inv_d;
-      store_until(yr, col_of(slot), cur.wend, o);
+      store_until(yr, col_of(slot), cur.wendb, o);
     };
     // a cached slot: its exponentials times 2^(mg - M) / D (at most 1 / D)
     auto emit_e = [&](int slot, const float* e) {
@@ -505,7 +539,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
       float o[V];
 #pragma unroll
       for (int i = 0; i < V; ++i) o[i] = e[i] * f;
-      store_until(yr, col_of(slot), cur.wend, o);
+      store_until(yr, col_of(slot), cur.wendb, o);
     };
 #pragma unroll
     for (int s = 0; s < NR; ++s)
@@ -532,6 +566,12 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
         logit(slot, rxs, rms, a);
         emit(slot, a);
       });
+    }
+    if constexpr (SHIFT) {
+      if (has_x && ce < cur.wend) {
+        const float o = __builtin_amdgcn_exp2f(fmaf(ax, kLog2e, -M)) * inv_d;
+        stv<T, 1>(yr + ce, &o);
+      }
     }
     cur = nxt;
     pos = npos;
@@ -568,7 +608,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   const bool small_q = a.causal_q_len < (int64_t(1) << 30);
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
   if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E &&                     \
-      (VEC || c <= FS_SM_ELEMENTWISE_REG_COLS))                                  \
+      (VEC || c <= (a.shifted ? FS_SM_SHIFT_REG_COLS : FS_SM_ELEMENTWISE_REG_COLS)))  \
     return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }
@@ -603,8 +643,17 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
       return hipGetLastError();
     };
     constexpr int64_t kSlot = int64_t(1024) * V;
-    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, false>, 0);
-    return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, CL, CR, true>,
+    if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T))) {
+      if (a.shifted) {
+        // 16-byte slots over each row's aligned body
+        constexpr int64_t kVSlot = int64_t(1024) * Elem<T>::kVec;
+        if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, false, true, CL, CR, false>, 0);
+        return go(softmax_cached_kernel<T, MT, HAS_MASK, false, true, CL, CR, true>,
+                  int((c - kCached + kVSlot - 1) / kVSlot));
+      }
+    }
+    if (c <= kCached) return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, false, CL, CR, false>, 0);
+    return go(softmax_cached_kernel<T, MT, HAS_MASK, VEC, false, CL, CR, true>,
               int((c - kCached + kSlot - 1) / kSlot));
   }
 }

@@ -119,6 +119,41 @@ def test_softmax_streamed_strided_in_place(dtype, cols, ld):
         mg.check_untouched("softmax mask")
 
 
+@pytest.mark.parametrize("dtype,mask_dtype", [("bf16", "bf16"), ("bf16", None), ("f32", "f32")])
+@pytest.mark.parametrize("cols", [8193, 12001, 24999, 32001, 65537])
+def test_softmax_rows_sharing_a_16_byte_phase(dtype, mask_dtype, cols):
+    # contiguous rows of a width that is not a whole number of 16-byte
+    # vectors start at varying offsets, the same for x, mask and y: the row
+    # cache loads each row's aligned body 16 bytes at a time and its head
+    # and tail elements one at a time
+    rows = 7
+    d = fd.softmax_inputs(cols + 11, rows, cols, dtype, mask_dtype=mask_dtype)
+    announce("softmax shared phase", cols, dtype, mask_dtype)
+    m = d["mask"].f64() if mask_dtype else None
+    ref = oracle.row_softmax(d["x"].f64(), m, d["scale"])
+    got = host64(fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"]))
+    assert_close(f"cols {cols}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"cols {cols}", got, ref, ulps=1.0, atol=1e-9)
+    x = dev(d["x"])                                       # in place
+    fs.row_softmax(x, dev(d["mask"]), d["scale"], out=x)
+    assert_close(f"cols {cols} in place", host64(x), ref, *TOL[dtype])
+
+
+def test_softmax_rows_of_different_phases():
+    # y at a row stride one element longer than x: the phases differ from row
+    # to row, so the rows take element-wise loads; same result
+    rows, cols = 5, 40001
+    d = fd.softmax_inputs(5, rows, cols, "bf16", mask_dtype="bf16")
+    ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
+    yg = Guarded(rows, cols, cols + 1, torch.bfloat16)
+    announce("softmax different phases")
+    fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"], out=yg.view)
+    torch.cuda.synchronize()
+    assert_close("different phases", host64(yg.view), ref, *TOL["bf16"])
+    yg.check_untouched("softmax y")
+
+
 def test_softmax_at_maximum_width():
     cols = fs.FS_SOFTMAX_MAX_COLS
     d = fd.softmax_inputs(17, 1, cols, "bf16", mask_dtype=None)
