@@ -209,25 +209,77 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
   }
 }
 
-// Any width, any alignment: one block per row, coefficients through the cache.
-template <typename CT, typename BT, int ACT>
+// Rows the staged kernel does not take (wider than 16384 columns, or not
+// whole 16-byte vectors): one block of 4 waves per row, coefficients through
+// the cache.  Each thread keeps U vectors of the row in flight per trip
+// (clamped loads, issued together) with one accumulator per vector slot;
+// with VEC and coef_vec the coefficients are read as vectors too.
+template <typename CT, typename BT, int ACT, bool VEC>
 __global__ __launch_bounds__(256) void epilogue_wide_kernel(
     const CT* __restrict__ c, int64_t ld_c, const BT* __restrict__ bias,
     const float* __restrict__ col_scale, float* __restrict__ out, int64_t rows, int64_t cols,
-    int mean) {
+    int mean, int coef_vec) {
+  constexpr int V = VEC ? Elem<CT>::kVec : 1;
+  constexpr int U = VEC ? 4 : 8;
   __shared__ SumP lds[2][4];
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const float sgn = coef_sign<ACT>();
+  const int64_t nv = (cols + V - 1) / V;   // VEC rows are whole vectors
   int parity = 0;
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const CT* cr = c + row * ld_c;
-    float acc = 0.f;
-    for (int64_t j = tid; j < cols; j += 256) {
-      const float s = (col_scale ? col_scale[j] : 1.f) * sgn;
-      const float b = bias ? Elem<BT>::load1(bias + j) : 0.f;
-      acc += epi_act<ACT>(fmaf(Elem<CT>::load1(cr + j), s, b * s));
+    float acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc[u] = 0.f;
+    for (int64_t v0 = tid; v0 < nv; v0 += 256 * U) {
+      Raw<CT, V> rc[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t v = v0 + u * 256;
+        rc[u].load(cr + (v < nv ? v : nv - 1) * V);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t v = v0 + u * 256;
+        const int64_t j0 = (v < nv ? v : nv - 1) * V;
+        float cv[V], sv[V], bv[V];
+        rc[u].unpack(cv);
+        if (col_scale) {
+          if (VEC && coef_vec) {
+            ldv<float, V, false>(col_scale + j0, sv);
+          } else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) sv[i] = col_scale[j0 + i];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < V; ++i) sv[i] = 1.f;
+        }
+        if (bias) {
+          if (VEC && coef_vec) {
+            ldv<BT, V, false>(bias + j0, bv);
+          } else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) bv[i] = Elem<BT>::load1(bias + j0 + i);
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < V; ++i) bv[i] = 0.f;
+        }
+        float part = 0.f;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          const float s = sv[i] * sgn;
+          part += epi_act<ACT>(fmaf(cv[i], s, bv[i] * s));
+        }
+        acc[u] += v < nv ? part : 0.f;
+      }
     }
-    const SumP t = group_allreduce<4>(SumP{acc}, lds[parity], wave, lane);
+    float tot = 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) tot += acc[u];
+    const SumP t = group_allreduce<4>(SumP{tot}, lds[parity], wave, lane);
     parity ^= 1;
     if (tid == 0) out[row] = mean ? t.s / float(cols) : t.s;
   }
@@ -253,7 +305,8 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
   auto staged = [&](auto kern, int nvec) {
     const size_t lds = size_t(2) * nvec * (V / 4) * 64 * 16;
     int64_t want = (a.rows + kLdsW - 1) / kLdsW;
-    int64_t cap = int64_t(cus) * FS_EPI_BLOCKS_PER_CU;
+    // tables above 80 KiB leave room for one block per compute unit
+    int64_t cap = int64_t(cus) * (lds > 80 * 1024 ? 1 : FS_EPI_BLOCKS_PER_CU);
     int grid = int(want < cap ? want : cap);
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kLdsW), lds, s, static_cast<const CT*>(a.c),
@@ -271,17 +324,20 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
     FS_EPI_RUNG(4)
     FS_EPI_RUNG(8)
     FS_EPI_RUNG(16)
-    if constexpr (V == 4) {   // fp32 C: 64 KiB of coefficients cover 8192 columns
-      FS_EPI_RUNG(32)
-    }
+    FS_EPI_RUNG(32)
+    if constexpr (V == 4) { FS_EPI_RUNG(64) }
 #undef FS_EPI_RUNG
   }
   int64_t grid = a.rows < int64_t(cus) * 8 ? a.rows : int64_t(cus) * 8;
   if (grid < 1) grid = 1;
-  hipLaunchKernelGGL((epilogue_wide_kernel<CT, BT, ACT>), dim3(unsigned(grid)), dim3(256), 0, s,
-                     static_cast<const CT*>(a.c), a.ld_c, static_cast<const BT*>(a.bias),
-                     a.col_scale, a.out, a.rows, a.cols, mean);
-  return hipGetLastError();
+  auto wide = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(256), 0, s, static_cast<const CT*>(a.c),
+                       a.ld_c, static_cast<const BT*>(a.bias), a.col_scale, a.out, a.rows, a.cols,
+                       mean, int(a.coef_vec));
+    return hipGetLastError();
+  };
+  return a.vec && a.cols > 0 ? wide(epilogue_wide_kernel<CT, BT, ACT, true>)
+                             : wide(epilogue_wide_kernel<CT, BT, ACT, false>);
 }
 
 template <typename CT, typename BT>

@@ -58,6 +58,7 @@ struct EpilogueArgs {
   float* out;
   int64_t rows, cols;
   bool vec;
+  bool coef_vec = false;   // bias and col_scale (when given) are 16-byte aligned
 };
 
 // `cus` is the compute-unit count of the current device.

@@ -66,7 +66,10 @@ def test_sign_flip_symmetry():
 
 @pytest.mark.parametrize("c_dtype,b_dtype", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
                                              ("f32", "bf16")])
-@pytest.mark.parametrize("cols", [1, 7, 8, 100, 512, 1000, 4096, 8192, 8200, 16384, 40000])
+# staged rungs up to 16384 columns; the wide kernel with 16-byte loads
+# (24000, 40000) and with element loads (7, 100, 24001)
+@pytest.mark.parametrize("cols", [1, 7, 8, 100, 512, 1000, 4096, 8192, 8200, 16384, 24000, 24001,
+                                  40000])
 def test_widths_and_dtypes(c_dtype, b_dtype, cols):
     rows = 11 if cols <= 16384 else 3
     d = fd.epilogue_inputs(cols, rows, cols, c_dtype, bias_dtype=b_dtype)
@@ -90,6 +93,37 @@ def test_acts_reductions_optionals(act, reduce, with_bias, with_scale):
     ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64() if with_bias else None,
                                       d["col_scale"].f64() if with_scale else None, act, reduce)
     assert_close(f"{act} {reduce}", host64(o), ref, 2e-3 if reduce == "sum" else 1e-6, 1e-5)
+
+
+@pytest.mark.parametrize("cols", [24000, 24001])
+@pytest.mark.parametrize("act,reduce,with_bias,with_scale", [
+    ("sigmoid", "sum", True, True), ("gelu_erf", "mean", False, True),
+    ("relu", "sum", True, False), ("none", "mean", False, False)])
+def test_wide_rows_options(cols, act, reduce, with_bias, with_scale):
+    d = fd.epilogue_inputs(cols + 1, 5, cols, "bf16", c_std=1.0, bias_dtype="f32")
+    announce("epilogue wide options", cols, act, reduce, with_bias, with_scale)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]) if with_bias else None,
+                                dev(d["col_scale"]) if with_scale else None, act, reduce)
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64() if with_bias else None,
+                                      d["col_scale"].f64() if with_scale else None, act, reduce)
+    assert_close(f"{act} {reduce}", host64(o), ref, 2e-2 if reduce == "sum" else 1e-6, 1e-5)
+
+
+def test_wide_rows_misaligned_coefficients():
+    # bias and column scale one element off a 16-byte boundary: element loads
+    # of the coefficients next to 16-byte loads of C
+    cols = 24000
+    d = fd.epilogue_inputs(8, 4, cols, "bf16", bias_dtype="bf16")
+    bb = torch.empty(cols + 1, dtype=torch.bfloat16, device="cuda")
+    sb = torch.empty(cols + 1, dtype=torch.float32, device="cuda")
+    b, s = bb[1:], sb[1:]
+    b.copy_(dev(d["bias"]))
+    s.copy_(dev(d["col_scale"]))
+    announce("epilogue misaligned coefficients")
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), b, s)
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                      "sigmoid", "sum")
+    assert_close("misaligned coefficients", host64(o), ref, SUM_ATOL * 3, 1e-6)
 
 
 def test_strided_and_misaligned_c():
