@@ -315,6 +315,7 @@ fs_status row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op, 
   if (overlap(eo, ex)) return fail(FS_ERR_ALIASING, "out overlaps x");
   fs::ReduceArgs a{x, ld_x, dtype, op, out_f, out_i, rows, cols, false};
   a.vec = cols > 0 && cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es);
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_reduce(a, cus, stream);

@@ -83,6 +83,7 @@ struct ReduceArgs {
   int64_t* out_i;    // argmax
   int64_t rows, cols;
   bool vec;
+  bool shifted = false;   // not vec, element-aligned rows of at least two vectors
 };
 hipError_t launch_reduce(const ReduceArgs& a, int cus, hipStream_t s);
 

@@ -82,12 +82,16 @@ __device__ __forceinline__ void accumulate(typename AccOf<OP>::type& acc, float 
   }
 }
 
-template <typename T, int OP, int W, int G, bool VEC>
+// SHIFT (element-aligned rows that are not whole 16-byte vectors): 16-byte
+// loads over each row's aligned body [h, bend) and one extra element per
+// lane for the first h + (cols - bend) lanes (the head and the tail, at most
+// 2 V - 2), merged with the symmetric combine, which keeps argmax exact.
+template <typename T, int OP, int W, int G, bool VEC, bool SHIFT>
 __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
     const T* __restrict__ x, int64_t ld_x, float* __restrict__ out_f,
     int64_t* __restrict__ out_i, int64_t rows, int cols, int trips, float post_scale) {
   constexpr int kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;
   constexpr int U = FS_RED_UNROLL;
   // one LDS fold area and one barrier sequence per block: rows wider than a
   // wave take the whole block (the row loop is then uniform across it)
@@ -102,6 +106,13 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
 
   for (int64_t row = int64_t(blockIdx.x) * G + g; row < rows; row += int64_t(gridDim.x) * G) {
     const T* xr = x + row * ld_x;
+    int h = 0, bend = cols;   // the row's 16-byte-aligned body (SHIFT)
+    if constexpr (SHIFT) {
+      const int phase = int(reinterpret_cast<uintptr_t>(xr) & 15) / int(sizeof(T));
+      h = (V - phase) % V;
+      bend = h + ((cols - h) / V) * V;
+    }
+    const int blast = bend - V;   // start of the body's last vector
     // V independent accumulators, one per slot of a vector: each sees its
     // columns in increasing order, and their chains run side by side (one
     // chain through all of a lane's elements made max and argmax
@@ -113,19 +124,19 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
       Raw<T, V> rv[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int c0 = ((t * U + u) * kThreads + tid) * V;
-        rv[u].load(xr + (c0 < cols ? c0 : clast));
+        const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+        rv[u].load(xr + (c0 < bend ? c0 : (SHIFT ? blast : clast)));
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int c0 = ((t * U + u) * kThreads + tid) * V;
+        const int c0 = h + ((t * U + u) * kThreads + tid) * V;
         // the lane's first vector holds its lowest columns; if it lies past
         // the row end, so do all the lane's vectors
         const bool first = t == 0 && u == 0;
         float v[V];
         rv[u].unpack(v);
-        if (c0 < cols) {   // the whole vector is in the row (cols % V == 0 on this path)
+        if (c0 < bend) {   // the whole vector is in the row (or body)
 #pragma unroll
           for (int i = 0; i < V; ++i) accumulate<OP>(acc[i], v[i], c0 + i, first);
         }
@@ -134,6 +145,15 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
     P lane_acc = acc[0];
 #pragma unroll
     for (int i = 1; i < V; ++i) lane_acc = P::combine(lane_acc, acc[i]);
+    if constexpr (SHIFT) {
+      const int nx = h + (cols - bend);
+      const bool has = tid < nx;
+      const int ce = has ? (tid < h ? tid : bend + (tid - h)) : 0;
+      P ax = identity<OP>();
+      const float v = Elem<T>::load1(xr + ce);
+      if (has) accumulate<OP>(ax, v, ce, true);
+      lane_acc = P::combine(lane_acc, ax);
+    }
     const P tot = group_allreduce<W>(lane_acc, lds[parity], wave, lane);
     parity ^= 1;
     if (tid == 0) {
@@ -144,9 +164,9 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
   }
 }
 
-template <typename T, int OP, bool VEC>
+template <typename T, int OP, bool VEC, bool SHIFT>
 hipError_t dispatch(const ReduceArgs& a, int cus, hipStream_t s) {
-  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;
   constexpr int U = FS_RED_UNROLL;
   // waves per row: enough that a trip covers about half the row, at most 8
   const int64_t per_wave_trip = int64_t(64) * V * U;
@@ -162,18 +182,24 @@ hipError_t dispatch(const ReduceArgs& a, int cus, hipStream_t s) {
                        a.ld_x, a.out_f, a.out_i, a.rows, int(a.cols), trips, post);
     return hipGetLastError();
   };
-  if (want_w <= 1) return launch(reduce_kernel<T, OP, 1, 4, VEC>, 1, 4);
-  if (want_w <= 2) return launch(reduce_kernel<T, OP, 2, 1, VEC>, 2, 1);
-  if (want_w <= 4) return launch(reduce_kernel<T, OP, 4, 1, VEC>, 4, 1);
-  return launch(reduce_kernel<T, OP, 8, 1, VEC>, 8, 1);
+  if (want_w <= 1) return launch(reduce_kernel<T, OP, 1, 4, VEC, SHIFT>, 1, 4);
+  if (want_w <= 2) return launch(reduce_kernel<T, OP, 2, 1, VEC, SHIFT>, 2, 1);
+  if (want_w <= 4) return launch(reduce_kernel<T, OP, 4, 1, VEC, SHIFT>, 4, 1);
+  return launch(reduce_kernel<T, OP, 8, 1, VEC, SHIFT>, 8, 1);
+}
+
+template <typename T, int OP>
+hipError_t by_path(const ReduceArgs& a, int cus, hipStream_t s) {
+  if (a.vec) return dispatch<T, OP, true, false>(a, cus, s);
+  if (a.shifted) return dispatch<T, OP, false, true>(a, cus, s);
+  return dispatch<T, OP, false, false>(a, cus, s);
 }
 
 template <typename T>
 hipError_t by_op(const ReduceArgs& a, bool argmax, int cus, hipStream_t s) {
-  if (argmax) return a.vec ? dispatch<T, kOpArg, true>(a, cus, s) : dispatch<T, kOpArg, false>(a, cus, s);
-  if (a.op == FS_ROW_MAX)
-    return a.vec ? dispatch<T, kOpMax, true>(a, cus, s) : dispatch<T, kOpMax, false>(a, cus, s);
-  return a.vec ? dispatch<T, kOpSum, true>(a, cus, s) : dispatch<T, kOpSum, false>(a, cus, s);
+  if (argmax) return by_path<T, kOpArg>(a, cus, s);
+  if (a.op == FS_ROW_MAX) return by_path<T, kOpMax>(a, cus, s);
+  return by_path<T, kOpSum>(a, cus, s);
 }
 
 }  // namespace

@@ -48,7 +48,7 @@ def test_widths(dtype, rows, cols):
 
 @pytest.mark.parametrize("seed", SEEDS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("cols", [64, 1000, 4096, 70000])
+@pytest.mark.parametrize("cols", [64, 1000, 1001, 4096, 70000, 70001])
 def test_argmax_bit_exact_with_ties(seed, dtype, cols):
     # small integers: every row is full of exact ties, so only the
     # lowest-index rule picks the right answer
@@ -76,6 +76,39 @@ def test_argmax_nan_inf_and_constant_rows():
     np.testing.assert_array_equal(got, [0, 123, 0, 299, 17, 0])
     mx = host64(fs.row_reduce(t, "max"))
     assert np.isnan(mx[1]) and mx[2] == -np.inf and mx[4] == np.inf
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_head_and_tail_elements_of_odd_rows(dtype):
+    # contiguous rows of 4099 columns start at every offset within a 16-byte
+    # unit; their first and last few columns are loaded one at a time next
+    # to the 16-byte body: put the maximum, NaNs and ties there
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols = 8, 4099
+    x = np.zeros((rows, cols), dtype=np.float32)
+    x[0, 0] = 5.0                                # first column (head)
+    x[1, cols - 1] = 5.0                         # last column (tail)
+    x[2, 1] = np.nan
+    x[2, cols - 2] = np.nan                      # first NaN wins
+    x[3, 2] = 7.0
+    x[3, cols - 1] = 7.0                         # tie: head beats tail
+    x[4, cols - 3] = 7.0
+    x[4, 3000] = 7.0                             # tie: body beats tail
+    x[5, 6] = -1.0
+    x[5, :] = -2.0                               # constant row
+    x[6, 3] = np.inf
+    x[7, :] = np.arange(cols, dtype=np.float32)  # increasing: the last column
+    t = torch.from_numpy(x).to(tdt).cuda()
+    xr = t.float().cpu().numpy().astype(np.float64)
+    announce("row_argmax head and tail", dtype)
+    got = fs.row_argmax(t).cpu().numpy()
+    np.testing.assert_array_equal(got, oracle.row_argmax(xr))
+    np.testing.assert_array_equal(got[:5], [0, cols - 1, 1, 2, 3000])
+    np.testing.assert_array_equal(host64(fs.row_reduce(t, "max")), oracle.row_reduce(xr, "max"))
+    sums = host64(fs.row_reduce(t, "sum"))
+    fin = [0, 1, 3, 4, 5, 7]
+    assert_close("sum", sums[fin], oracle.row_reduce(xr[fin], "sum"), sum_tol(xr[fin]), 0)
+    assert np.isnan(sums[2]) and sums[6] == np.inf
 
 
 def test_zero_columns_sum_and_empty_rows():
