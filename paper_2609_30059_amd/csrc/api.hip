@@ -393,6 +393,7 @@ fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype,
                      rows, cols, false};
   a.vec = cols > 0 && cols % vec_width(c_dtype) == 0 && vec_ok(c, ld_c, es);
   a.coef_vec = aligned(bias, 16) && aligned(col_scale, 16);
+  a.shifted = !a.vec && cols >= 2 * vec_width(c_dtype);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_epilogue(a, cus, stream);

@@ -209,6 +209,166 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
   }
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// (s, b*s) pairs of every column into V planes: column j at plane j % V,
+// index j / V (Q pairs per plane, zeros past the row).
+template <typename BT, int V, int Q, int W, bool HB, bool HS>
+__device__ __forceinline__ void fill_planes(f32x2* pl, const BT* __restrict__ bias,
+                                            const float* __restrict__ col_scale, int cols,
+                                            float sgn) {
+  for (int i = threadIdx.x; i < V * Q; i += 64 * W) {
+    const int r = i / Q, q = i % Q;
+    const int j = q * V + r;
+    const bool live = j < cols;
+    const int jc = live ? j : cols - 1;            // clamped: always in bounds
+    const float sv = HS ? col_scale[jc] : 1.f;
+    const float bv = HB ? Elem<BT>::load1(bias + jc) : 0.f;
+    const float sc = sv * sgn;
+    f32x2 pr;
+    pr[0] = live ? sc : 0.f;
+    pr[1] = live ? bv * sc : 0.f;
+    pl[i] = pr;
+  }
+}
+
+// Rows that are not whole 16-byte vectors (odd widths, odd row offsets) but
+// span at least two, up to the staged widths: each row's aligned body, from
+// its first 16-byte boundary to its last, is read 16 bytes at a time with the
+// pipelining of epilogue_lds_kernel; its head and tail (at most V-1 elements
+// each) go one per lane to the first lanes.  The body of a row starting h
+// columns before a 16-byte boundary holds columns h + v*V + e, so element e
+// of every lane's vector v lies in coefficient plane (h+e) % V at index
+// v + (h+e) / V: 64 lanes read 64 consecutive pairs, whatever the row's h.
+// WPE: waves per SIMD the register budget is sized for: 4 (one block per
+// compute unit) where 8 would spill, i.e. from 16 bf16 vectors per lane.
+template <typename CT, typename BT, int ACT, int NVEC, int CHMAX, int W, int WPE>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void
+epilogue_shift_kernel(
+    const CT* __restrict__ c, int64_t ld_c, const BT* __restrict__ bias,
+    const float* __restrict__ col_scale, float* __restrict__ out, int64_t rows, int cols,
+    int mean) {
+  constexpr int V = Elem<CT>::kVec;
+  constexpr int Q = NVEC * 64 + 1;       // body vectors of a row, plus the carry
+  constexpr int CH = CHMAX < NVEC ? CHMAX : NVEC;
+  constexpr int NCH = NVEC / CH;
+  static_assert(NVEC % CH == 0, "NVEC must be a multiple of CH");
+  static_assert((NCH & (NCH - 1)) == 0, "the chunk count must be a power of two");
+  extern __shared__ f32x2 lds_pl[];      // [V][Q]
+
+  const float sgn = coef_sign<ACT>();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const int lane = threadIdx.x % 64;
+  const int64_t stride = int64_t(gridDim.x) * W;
+  int64_t row = int64_t(blockIdx.x) * W + wave;
+
+  // h: columns before the row's first 16-byte boundary; nb: whole vectors
+  // after it (>= 1 since cols >= 2V); the rest, cols - nb*V, are extras
+  auto head_of = [&](int64_t r) {
+    const int phase = int(reinterpret_cast<uintptr_t>(c + r * ld_c) & 15) / int(sizeof(CT));
+    return (V - phase) & (V - 1);
+  };
+  u32x4 buf[2][CH];
+  // ln: the lane index (per row, a copy the compiler cannot see through, so
+  // that no per-lane offset is hoisted out of the row loop and kept live)
+  auto load_chunk = [&](u32x4 (&dst)[CH], int64_t r, int hh, int nbb, int j, int ln) {
+    const CT* cb = c + r * ld_c + hh;
+#pragma unroll
+    for (int q = 0; q < CH; ++q) {
+      const int vi = (j * CH + q) * 64 + ln;
+      dst[q] = ld128<true>(cb + (vi < nbb ? vi : nbb - 1) * V);
+    }
+  };
+  // a lane's extra column: lanes below h take the head, the next ones the
+  // tail (column nb*V + lane); lanes past the extras re-read column 0
+  auto extra_col = [&](int hh, int nbb, int ln) {
+    const int nx = cols - nbb * V;
+    return ln < nx ? (ln < hh ? ln : nbb * V + ln) : 0;
+  };
+  auto rot_of = [&](int64_t r) { return FS_EPI_ROTATE ? int(r & (NCH - 1)) : 0; };
+
+  const int64_t first = row < rows ? row : rows - 1;
+  int h = head_of(first);
+  int nb = (cols - h) / V;
+  int rot = rot_of(row);
+  load_chunk(buf[0], first, h, nb, rot, lane);
+  CT xraw = c[first * ld_c + extra_col(h, nb, lane)];
+
+  if (bias) {
+    if (col_scale) fill_planes<BT, V, Q, W, true, true>(lds_pl, bias, col_scale, cols, sgn);
+    else fill_planes<BT, V, Q, W, true, false>(lds_pl, bias, col_scale, cols, sgn);
+  } else {
+    if (col_scale) fill_planes<BT, V, Q, W, false, true>(lds_pl, bias, col_scale, cols, sgn);
+    else fill_planes<BT, V, Q, W, false, false>(lds_pl, bias, col_scale, cols, sgn);
+  }
+  __syncthreads();
+  if (row >= rows) return;            // no barrier after this point
+
+  while (true) {
+    float acc = 0.f;
+    const int64_t next = row + stride;
+    int li = lane;
+    asm volatile("" : "+v"(li));
+    // element e of this row's vectors: plane (h+e) % V, index + (h+e) / V
+    // (uniform offsets; the lane's addresses are formed again in every chunk
+    // rather than kept live through the row)
+    int off[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) off[e] = ((h + e) & (V - 1)) * Q + ((h + e) >= V ? 1 : 0);
+    const int64_t pre_row = next < rows ? next : 0;
+    const int ph = head_of(pre_row);
+    const int pnb = (cols - ph) / V;
+    const int pre_chunk = next < rows ? rot_of(next) : 0;
+    CT xnext;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      if (j + 1 < NCH) {
+        load_chunk(buf[(j + 1) & 1], row, h, nb, (j + 1 + rot) & (NCH - 1), li);
+      } else {
+        load_chunk(buf[(j + 1) & 1], pre_row, ph, pnb, pre_chunk, li);
+        xnext = c[pre_row * ld_c + extra_col(ph, pnb, li)];
+      }
+      const int pj = (j + rot) & (NCH - 1);
+      int lj = li;
+      asm volatile("" : "+v"(lj));
+#pragma unroll
+      for (int q = 0; q < CH; ++q) {
+        const int kq = (pj * CH + q) * 64;
+        float v[V];
+        Elem<CT>::unpack(buf[j & 1][q], v);
+        float part = 0.f;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          const f32x2 pr = lds_pl[off[e] + lj + kq];
+          part += epi_act<ACT>(fmaf(v[e], pr[0], pr[1]));
+        }
+        acc += kq + li < nb ? part : 0.f;
+      }
+    }
+    {
+      const int ce = extra_col(h, nb, li);
+      const f32x2 pr = lds_pl[(ce & (V - 1)) * Q + ce / V];
+      float xv;
+      if constexpr (std::is_same<CT, float>::value) xv = xraw;
+      else xv = bf16_to_f32(xraw);
+      const float part = epi_act<ACT>(fmaf(xv, pr[0], pr[1]));
+      acc += li < cols - nb * V ? part : 0.f;
+    }
+    const SumP t = wave_allreduce(SumP{acc});
+    if (lane == 0) out[row] = mean ? t.s / float(cols) : t.s;
+    if (next >= rows) break;
+    row = next;
+    rot = rot_of(row);
+    h = ph;
+    nb = pnb;
+    xraw = xnext;
+    if constexpr (NCH % 2 == 1) {
+#pragma unroll
+      for (int q = 0; q < CH; ++q) buf[0][q] = buf[1][q];
+    }
+  }
+}
+
 // Rows the staged kernel does not take (wider than 16384 columns, or not
 // whole 16-byte vectors): one block of 4 waves per row, coefficients through
 // the cache.  Each thread keeps U vectors of the row in flight per trip
@@ -327,6 +487,31 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
     FS_EPI_RUNG(32)
     if constexpr (V == 4) { FS_EPI_RUNG(64) }
 #undef FS_EPI_RUNG
+  }
+  if (a.shifted) {
+    const int64_t body = a.cols / V;   // at most this many vectors in a row's body
+    auto shift = [&](auto kern, int nvec, int wpe) {
+      const size_t lds = size_t(V) * (nvec * 64 + 1) * 8;
+      int64_t want = (a.rows + kLdsW - 1) / kLdsW;
+      int64_t cap = int64_t(cus) * (wpe == 4 ? 1 : FS_EPI_BLOCKS_PER_CU);
+      int grid = int(want < cap ? want : cap);
+      if (grid < 1) grid = 1;
+      hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kLdsW), lds, s, static_cast<const CT*>(a.c),
+                         a.ld_c, static_cast<const BT*>(a.bias), a.col_scale, a.out, a.rows,
+                         int(a.cols), mean);
+      return hipGetLastError();
+    };
+#define FS_EPI_SHIFT_RUNG(NV)                                                                   \
+  if (body <= int64_t(NV) * 64) {                                                          \
+    constexpr int wpe = V * NV >= 128 ? 4 : 8;                                             \
+    return shift(epilogue_shift_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, wpe>, NV, wpe);     \
+  }
+    FS_EPI_SHIFT_RUNG(4)
+    FS_EPI_SHIFT_RUNG(8)
+    FS_EPI_SHIFT_RUNG(16)
+    FS_EPI_SHIFT_RUNG(32)
+    if constexpr (V == 4) { FS_EPI_SHIFT_RUNG(64) }
+#undef FS_EPI_SHIFT_RUNG
   }
   int64_t grid = a.rows < int64_t(cus) * 8 ? a.rows : int64_t(cus) * 8;
   if (grid < 1) grid = 1;

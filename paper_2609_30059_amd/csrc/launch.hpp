@@ -59,6 +59,7 @@ struct EpilogueArgs {
   int64_t rows, cols;
   bool vec;
   bool coef_vec = false;   // bias and col_scale (when given) are 16-byte aligned
+  bool shifted = false;    // not vec, rows of at least two 16-byte vectors
 };
 
 // `cus` is the compute-unit count of the current device.

@@ -66,10 +66,12 @@ def test_sign_flip_symmetry():
 
 @pytest.mark.parametrize("c_dtype,b_dtype", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
                                              ("f32", "bf16")])
-# staged rungs up to 16384 columns; the wide kernel with 16-byte loads
-# (24000, 40000) and with element loads (7, 100, 24001)
-@pytest.mark.parametrize("cols", [1, 7, 8, 100, 512, 1000, 4096, 8192, 8200, 16384, 24000, 24001,
-                                  40000])
+# staged rungs up to 16384 columns; rows that are not whole vectors, from two
+# vectors up (15, 17, 100, 1001, 4095, 16383, 16391: every rung, its edges and
+# each row at another offset within a 16-byte unit); the wide kernel with
+# 16-byte loads (24000, 40000) and with element loads (1, 7, 16399, 24001)
+@pytest.mark.parametrize("cols", [1, 7, 8, 15, 17, 100, 512, 1000, 1001, 4095, 4096, 8192, 8200,
+                                  16383, 16384, 16391, 16399, 24000, 24001, 40000])
 def test_widths_and_dtypes(c_dtype, b_dtype, cols):
     rows = 11 if cols <= 16384 else 3
     d = fd.epilogue_inputs(cols, rows, cols, c_dtype, bias_dtype=b_dtype)
@@ -109,6 +111,38 @@ def test_wide_rows_options(cols, act, reduce, with_bias, with_scale):
     assert_close(f"{act} {reduce}", host64(o), ref, 2e-2 if reduce == "sum" else 1e-6, 1e-5)
 
 
+@pytest.mark.parametrize("c_dtype,cols", [("bf16", 2051), ("f32", 2051), ("bf16", 9001)])
+@pytest.mark.parametrize("act,reduce,with_bias,with_scale", [
+    ("sigmoid", "sum", True, True), ("gelu_erf", "mean", False, True),
+    ("relu", "sum", True, False), ("none", "mean", False, False)])
+def test_odd_rows_options(c_dtype, cols, act, reduce, with_bias, with_scale):
+    # rows of an odd width start at every offset within a 16-byte unit
+    d = fd.epilogue_inputs(cols + 2, 13, cols, c_dtype, c_std=1.0, bias_dtype="bf16")
+    announce("epilogue odd rows options", c_dtype, cols, act, reduce, with_bias, with_scale)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]) if with_bias else None,
+                                dev(d["col_scale"]) if with_scale else None, act, reduce)
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64() if with_bias else None,
+                                      d["col_scale"].f64() if with_scale else None, act, reduce)
+    assert_close(f"{act} {reduce}", host64(o), ref, 1e-2 if reduce == "sum" else 1e-6, 1e-5)
+
+
+def test_odd_rows_head_and_tail_columns():
+    # one large value in the first or the last columns of each row: the head
+    # and tail elements, read one per lane, must each count once
+    rows, cols = 16, 4099
+    c = torch.zeros(rows, cols, dtype=torch.bfloat16, device="cuda")
+    for i, j in enumerate([0, 1, 6, 7, cols - 1, cols - 2, cols - 7, cols - 8]):
+        c[2 * i, j] = 64.0
+        c[2 * i + 1, j] = -64.0
+    b = torch.zeros(cols, dtype=torch.float32, device="cuda")
+    s = torch.ones(cols, dtype=torch.float32, device="cuda")
+    announce("epilogue odd rows head and tail")
+    got = host64(fs.gemm_epilogue_reduce(c, b, s, "relu", "sum"))
+    np.testing.assert_array_equal(got, np.tile([64.0, 0.0], rows // 2))
+    got = host64(fs.gemm_epilogue_reduce(c, b, s, "none", "sum"))
+    np.testing.assert_array_equal(got, np.tile([64.0, -64.0], rows // 2))
+
+
 def test_wide_rows_misaligned_coefficients():
     # bias and column scale one element off a 16-byte boundary: element loads
     # of the coefficients next to 16-byte loads of C
@@ -129,7 +163,7 @@ def test_wide_rows_misaligned_coefficients():
 def test_strided_and_misaligned_c():
     d = fd.epilogue_inputs(4, 17, 3000, "bf16")
     base = torch.empty(17 * 3072 + 8, dtype=torch.bfloat16, device="cuda")
-    for offset in (0, 1):
+    for offset in (0, 1, 3):
         announce("epilogue strided", offset)
         view = base[offset:offset + 17 * 3072].view(17, 3072)[:, :3000]
         view.copy_(dev(d["c"]))
