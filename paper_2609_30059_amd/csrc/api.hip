@@ -164,6 +164,8 @@ fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bias, cons
   fs::PointwiseArgs a{x, ld_x, bias, residual, ld_r, y, ld_y, rows, cols, scale, act, dtype, false};
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(residual, ld_r, es) && (bias == nullptr || aligned(bias, 16));
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && same_phase(x, ld_x, y, ld_y, es) &&
+              same_phase(x, ld_x, residual, ld_r, es);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_pointwise(a, cus, stream);

@@ -71,27 +71,38 @@ template <typename BT, int V, int H, int NVEC, int W, bool HB, bool HS>
 __device__ __forceinline__ void fill_coef(f32x4* sc, f32x4* bs, const BT* __restrict__ bias,
                                           const float* __restrict__ col_scale, int nvec,
                                           float sgn) {
-  for (int i = threadIdx.x; i < NVEC * 64 * H; i += 64 * W) {
-    // i enumerates (vector, half): vector vi = i / H, half h = i % H
+  // i enumerates (vector, half): vector vi = i / H, half h = i % H.  Every
+  // load is issued before the first is used.
+  constexpr int N = NVEC * 64 * H, NS = (N + 64 * W - 1) / (64 * W);
+  float sv[NS][4], bv[NS][4];
+#pragma unroll
+  for (int t = 0; t < NS; ++t) {
+    const int i = threadIdx.x + t * 64 * W;
+    const int vi = i / H, h = i % H;
+    const int c0 = (i < N && vi < nvec ? vi : nvec - 1) * V + h * 4;   // clamped: in bounds
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sv[t][e] = HS ? col_scale[c0 + e] : 1.f;
+      bv[t][e] = HB ? Elem<BT>::load1(bias + c0 + e) : 0.f;
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NS; ++t) {
+    const int i = threadIdx.x + t * 64 * W;
     const int vi = i / H, h = i % H;
     const int k = vi / 64, ln = vi % 64;
     const bool live = vi < nvec;
-    const int c0 = (live ? vi : nvec - 1) * V + h * 4;   // clamped: always in bounds
-    float sv[4], bv[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      sv[e] = HS ? col_scale[c0 + e] : 1.f;
-      bv[e] = HB ? Elem<BT>::load1(bias + c0 + e) : 0.f;
-    }
     f32x4 s4, b4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float s = sv[e] * sgn;
+      const float s = sv[t][e] * sgn;
       s4[e] = live ? s : 0.f;
-      b4[e] = live ? bv[e] * s : 0.f;
+      b4[e] = live ? bv[t][e] * s : 0.f;
     }
-    sc[(k * H + h) * 64 + ln] = s4;
-    bs[(k * H + h) * 64 + ln] = b4;
+    if (i < N) {
+      sc[(k * H + h) * 64 + ln] = s4;
+      bs[(k * H + h) * 64 + ln] = b4;
+    }
   }
 }
 
@@ -217,18 +228,26 @@ template <typename BT, int V, int Q, int W, bool HB, bool HS>
 __device__ __forceinline__ void fill_planes(f32x2* pl, const BT* __restrict__ bias,
                                             const float* __restrict__ col_scale, int cols,
                                             float sgn) {
-  for (int i = threadIdx.x; i < V * Q; i += 64 * W) {
-    const int r = i / Q, q = i % Q;
+  // every load is issued before the first is used
+  constexpr int NS = (V * Q + 64 * W - 1) / (64 * W);
+  float sv[NS], bv[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const int i = threadIdx.x + k * 64 * W, r = i / Q, q = i % Q;
     const int j = q * V + r;
-    const bool live = j < cols;
-    const int jc = live ? j : cols - 1;            // clamped: always in bounds
-    const float sv = HS ? col_scale[jc] : 1.f;
-    const float bv = HB ? Elem<BT>::load1(bias + jc) : 0.f;
-    const float sc = sv * sgn;
+    const int jc = i < V * Q && j < cols ? j : cols - 1;   // clamped: always in bounds
+    sv[k] = HS ? col_scale[jc] : 1.f;
+    bv[k] = HB ? Elem<BT>::load1(bias + jc) : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const int i = threadIdx.x + k * 64 * W, r = i / Q, q = i % Q;
+    const bool live = q * V + r < cols;
+    const float sc = sv[k] * sgn;
     f32x2 pr;
     pr[0] = live ? sc : 0.f;
-    pr[1] = live ? bv * sc : 0.f;
-    pl[i] = pr;
+    pr[1] = live ? bv[k] * sc : 0.f;
+    if (i < V * Q) pl[i] = pr;
   }
 }
 

@@ -19,6 +19,9 @@ struct PointwiseArgs {
   fs_act act;
   fs_dtype dtype;
   bool vec;
+  // not vec, rows of at least two 16-byte vectors, and x, res and y start
+  // every row at one offset within a 16-byte unit
+  bool shifted = false;
 };
 
 struct SoftmaxArgs {

@@ -88,6 +88,123 @@ __global__ __launch_bounds__(kBlock) void pointwise_kernel(
   }
 }
 
+// a loaded element as fp32 (bf16 bit patterns are widened when used, so the
+// conversion does not wait on the load where it is issued)
+template <typename T>
+__device__ __forceinline__ float raw_to_f32(T v) {
+  if constexpr (std::is_same<T, float>::value) return v;
+  else return bf16_to_f32(v);
+}
+
+// Rows that are not whole 16-byte vectors (odd widths, odd row offsets) but
+// whose x, residual and y start every row at one offset within a 16-byte
+// unit: each row's aligned body, from its first 16-byte boundary to its last,
+// is read and written 16 bytes at a time; thread t of column block cb owns
+// body vector cb*kBlock + t of every row.  A row starting h columns before a
+// 16-byte boundary puts element e of body vector v at column h + v*V + e, so
+// the block stages the bias of its columns in LDS in V planes (column j at
+// plane j % V, index j / V): element e reads plane (h+e) % V at index
+// t + (h+e) / V, consecutive across the lanes whatever h is.  The head and
+// tail of each row (at most V-1 elements each) go one per lane to wave 0 of
+// column block 0, whose loads are issued with the body's.
+template <typename T, int ACT, bool HAS_RES, int U>
+__global__ __launch_bounds__(kBlock) void pointwise_shift_kernel(
+    const T* x, int64_t ld_x, const T* __restrict__ bias, const T* res, int64_t ld_r, T* y,
+    int64_t ld_y, int64_t rows, int cols, float scale, int col_blocks) {
+  constexpr int V = Elem<T>::kVec;
+  constexpr int Q = kBlock + 1;          // the block's vectors, plus the carry
+  __shared__ float bpl[V * Q];
+  const int cb = blockIdx.x % col_blocks;
+  const int64_t rg = blockIdx.x / col_blocks;
+  const int64_t nrg = gridDim.x / col_blocks;
+  const int tid = threadIdx.x;
+  const int v = cb * kBlock + tid;       // the thread's body vector
+  // every staging load is issued before the first is used (a stand-in
+  // pointer when there is no bias keeps them unconditional)
+  constexpr int NS = (V * Q + kBlock - 1) / kBlock;
+  const T* bsrc = bias != nullptr ? bias : x;
+  float bst[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const int i = tid + k * kBlock, pl = i / Q, q = i % Q;
+    const int j = (cb * kBlock + q) * V + pl;
+    bst[k] = Elem<T>::load1(bsrc + (i < V * Q && j < cols ? j : 0));
+  }
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const int i = tid + k * kBlock, pl = i / Q, q = i % Q;
+    const int j = (cb * kBlock + q) * V + pl;
+    if (i < V * Q) bpl[i] = bias != nullptr && j < cols ? bst[k] : 0.f;
+  }
+  __syncthreads();
+  const bool edge = cb == 0 && tid < 64;   // uniform per wave
+  if (v >= cols / V && !edge) return;      // no barriers below
+
+  auto head_of = [&](int64_t r) {
+    const int phase = int(reinterpret_cast<uintptr_t>(x + r * ld_x) & 15) / int(sizeof(T));
+    return (V - phase) & (V - 1);
+  };
+  for (int64_t r0 = rg * U; r0 < rows; r0 += nrg * U) {
+    Raw<T, V> rx[U], rr[HAS_RES ? U : 1];
+    int hh[U], nb[U];
+    T ex[U], er[U];
+    float eb[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t r = r0 + u < rows ? r0 + u : rows - 1;
+      hh[u] = head_of(r);
+      nb[u] = (cols - hh[u]) / V;          // >= 1: rows span at least two vectors
+      const int vc = v < nb[u] ? v : nb[u] - 1;
+      rx[u].load(x + r * ld_x + hh[u] + vc * V);
+      if constexpr (HAS_RES) rr[u].load(res + r * ld_r + hh[u] + vc * V);
+    }
+    if (edge) {
+      // lanes below h take the head, the next ones the tail (column
+      // nb*V + lane); lanes past them re-read column 0 and store nothing
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t r = r0 + u < rows ? r0 + u : rows - 1;
+        const int nx = cols - nb[u] * V;
+        const int ce = tid < nx ? (tid < hh[u] ? tid : nb[u] * V + tid) : 0;
+        ex[u] = x[r * ld_x + ce];
+        if constexpr (HAS_RES) er[u] = res[r * ld_r + ce];
+        eb[u] = Elem<T>::load1(bsrc + ce);   // zeroed at use when there is no bias
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float xv[V], o[V];
+      rx[u].unpack(xv);
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const int he = hh[u] + e;
+        const float b = bpl[(he & (V - 1)) * Q + (he >= V ? 1 : 0) + tid];
+        o[e] = act_fn<ACT>(fmaf(xv[e], scale, b));
+      }
+      if constexpr (HAS_RES) {
+        float rv[V];
+        rr[u].unpack(rv);
+#pragma unroll
+        for (int e = 0; e < V; ++e) o[e] += rv[e];
+      }
+      if (r0 + u < rows && v < nb[u]) stv<T, V>(y + (r0 + u) * ld_y + hh[u] + v * V, o);
+    }
+    if (edge) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int nx = cols - nb[u] * V;
+        if (r0 + u < rows && tid < nx) {
+          const int ce = tid < hh[u] ? tid : nb[u] * V + tid;
+          float o = act_fn<ACT>(fmaf(raw_to_f32(ex[u]), scale, bias != nullptr ? eb[u] : 0.f));
+          if constexpr (HAS_RES) o += raw_to_f32(er[u]);
+          Elem<T>::store1(y + (r0 + u) * ld_y + ce, o);
+        }
+      }
+    }
+  }
+}
+
 template <typename T, int ACT, bool HAS_RES, bool VEC>
 hipError_t dispatch(const PointwiseArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
@@ -128,8 +245,45 @@ hipError_t by_act(const PointwiseArgs& a, int cus, hipStream_t s) {
   }
 }
 
+template <typename T, int ACT, bool HAS_RES>
+hipError_t dispatch_shift(const PointwiseArgs& a, int cus, hipStream_t s) {
+  constexpr int V = Elem<T>::kVec;
+  const int64_t vecs = a.cols / V;     // the most body vectors a row can hold
+  const int col_blocks = int((vecs + kBlock - 1) / kBlock);
+  constexpr int U = FS_PW_ROWS_PER_TRIP;
+  const int64_t row_groups_needed = (a.rows + U - 1) / U;
+  const int64_t target_blocks = int64_t(cus) * FS_PW_BLOCKS_PER_CU;
+  auto go = [&](auto kern, int64_t grid) {
+    hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(kBlock), 0, s,
+                       static_cast<const T*>(a.x), a.ld_x, static_cast<const T*>(a.bias),
+                       static_cast<const T*>(a.res), a.ld_r, static_cast<T*>(a.y), a.ld_y,
+                       a.rows, int(a.cols), a.scale, col_blocks);
+    return hipGetLastError();
+  };
+  if (row_groups_needed < int64_t(cus) * 2) {
+    const int64_t r1 = a.rows < target_blocks ? a.rows : target_blocks;
+    return go(pointwise_shift_kernel<T, ACT, HAS_RES, 1>, r1 * col_blocks);
+  }
+  int64_t rg = target_blocks / col_blocks;
+  if (rg < 1) rg = 1;
+  if (rg > row_groups_needed) rg = row_groups_needed;
+  return go(pointwise_shift_kernel<T, ACT, HAS_RES, U>, rg * col_blocks);
+}
+
+template <typename T, bool HAS_RES>
+hipError_t by_act_shift(const PointwiseArgs& a, int cus, hipStream_t s) {
+  switch (a.act) {
+    case FS_ACT_GELU_ERF: return dispatch_shift<T, FS_ACT_GELU_ERF, HAS_RES>(a, cus, s);
+    case FS_ACT_SIGMOID: return dispatch_shift<T, FS_ACT_SIGMOID, HAS_RES>(a, cus, s);
+    case FS_ACT_RELU: return dispatch_shift<T, FS_ACT_RELU, HAS_RES>(a, cus, s);
+    default: return dispatch_shift<T, FS_ACT_NONE, HAS_RES>(a, cus, s);
+  }
+}
+
 template <typename T>
 hipError_t by_res(const PointwiseArgs& a, int cus, hipStream_t s) {
+  if (a.shifted)
+    return a.res == nullptr ? by_act_shift<T, false>(a, cus, s) : by_act_shift<T, true>(a, cus, s);
   if (a.res == nullptr)
     return a.vec ? by_act<T, false, true>(a, cus, s) : by_act<T, false, false>(a, cus, s);
   return a.vec ? by_act<T, true, true>(a, cus, s) : by_act<T, true, false>(a, cus, s);

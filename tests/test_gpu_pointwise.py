@@ -42,6 +42,26 @@ def test_shapes_and_acts(dtype, act, shape):
         bf16_ulp_close(f"{shape} {act}", got, ref)
 
 
+# rows that are not whole 16-byte vectors: odd widths around the column
+# blocks' edges (2048 bf16 / 1024 fp32 columns) and below two vectors (15);
+# 2100 rows take several rows per trip
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(9, 15), (9, 17), (6, 1025), (5, 2047), (4, 2055), (4, 2063),
+                                   (3, 4097), (2100, 1001)])
+def test_odd_rows(dtype, shape):
+    _, got, ref = run_case(*shape, dtype, "gelu_erf", seed=shape[1] + 1)
+    assert_close(f"{shape} {dtype}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"{shape}", got, ref)
+
+
+@pytest.mark.parametrize("bias,residual", [(False, True), (True, False), (False, False)])
+@pytest.mark.parametrize("rows,cols", [(33, 1024), (2100, 1001)])
+def test_optional_operands_odd_rows(bias, residual, rows, cols):
+    _, got, ref = run_case(rows, cols, "bf16", "sigmoid", 6, bias, residual)
+    assert_close("optional odd rows", got, ref, *TOL["bf16"])
+
+
 @pytest.mark.parametrize("bias,residual", [(False, True), (True, False), (False, False)])
 def test_optional_operands(bias, residual):
     _, got, ref = run_case(33, 1024, "f32", "gelu_erf", 5, bias, residual)
@@ -73,6 +93,38 @@ def test_strided_misaligned_and_guard_bands(dtype):
         torch.cuda.synchronize()
         assert_close(f"strided offset {offset}", host64(yg.view), ref, *TOL[dtype])
         yg.check_untouched("pointwise y")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_same_phase_rows(dtype):
+    # x, residual and y share one odd row stride and offset: every row starts
+    # at the same offset within a 16-byte unit in all three, and at a
+    # different one from row to row
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 23, 3001, 3013
+    d = fd.pointwise_inputs(12, rows, cols, dtype)
+    ref = oracle.pointwise_chain(d["x"].f64(), d["bias"].f64(), d["residual"].f64(), d["scale"],
+                                 "relu")
+    for offset in (1, 3):
+        announce("pointwise same-phase strided", dtype, offset)
+        xg = Guarded(rows, cols, ld, tdt, offset=offset)
+        rg = Guarded(rows, cols, ld, tdt, offset=offset)
+        yg = Guarded(rows, cols, ld, tdt, offset=offset)
+        xg.view.copy_(dev(d["x"]))
+        rg.view.copy_(dev(d["residual"]))
+        fs.pointwise_chain(xg.view, dev(d["bias"]), rg.view, d["scale"], "relu", out=yg.view)
+        torch.cuda.synchronize()
+        assert_close(f"same-phase offset {offset}", host64(yg.view), ref, *TOL[dtype])
+        yg.check_untouched("pointwise y")
+
+
+def test_in_place_odd_rows():
+    d = fd.pointwise_inputs(8, 41, 2047, "bf16")
+    ref = oracle.pointwise_chain(d["x"].f64(), d["bias"].f64(), d["residual"].f64(), d["scale"],
+                                 "gelu_erf")
+    x, b, r = dev(d["x"]), dev(d["bias"]), dev(d["residual"])
+    fs.pointwise_chain(x, b, r, d["scale"], "gelu_erf", out=x)
+    assert_close("in place on x, odd rows", host64(x), ref, *TOL["bf16"])
 
 
 def test_in_place():
