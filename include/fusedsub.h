@@ -121,10 +121,10 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  * columns past them are streamed: one pass keeps a running (max, sum) and a
  * second re-reads x (and mask) to write y (2 reads + 1 write per element).
  * Rows that are not whole 16-byte vectors load one element per lane, except
- * rows past 16384 columns whose x, mask (of x's dtype) and y start each row at
- * the same offset within a 16-byte unit (contiguous tensors, for instance):
- * there the aligned body of every row is loaded 16 bytes at a time.  Rows
- * may be up to FS_SOFTMAX_MAX_COLS columns.
+ * rows of at least two vectors whose x, mask (of x's dtype) and y start each
+ * row at the same offset within a 16-byte unit (contiguous tensors, for
+ * instance): there the aligned body of every row is loaded 16 bytes at a
+ * time.  Rows may be up to FS_SOFTMAX_MAX_COLS columns.
  * scale must be finite; mask values may be any float or -inf.
  */
 #define FS_SOFTMAX_MAX_COLS 16777216

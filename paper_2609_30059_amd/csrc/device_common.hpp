@@ -88,6 +88,11 @@ template <> struct Elem<uint16_t> {   // bf16 bit patterns
   }
 };
 
+// A loaded element as fp32.  Loading the raw value and widening it where it
+// is used keeps the wait for the load at the use, not at the load.
+__device__ __forceinline__ float raw_f32(float v) { return v; }
+__device__ __forceinline__ float raw_f32(uint16_t v) { return bf16_to_f32(v); }
+
 // 128-bit loads/stores.  Streaming data is touched once, so it is loaded and
 // stored non-temporally (it should not displace reused data from the caches);
 // NT = true means "streaming", subject to the build-time switches above.

@@ -367,10 +367,7 @@ epilogue_shift_kernel(
     {
       const int ce = extra_col(h, nb, li);
       const f32x2 pr = lds_pl[(ce & (V - 1)) * Q + ce / V];
-      float xv;
-      if constexpr (std::is_same<CT, float>::value) xv = xraw;
-      else xv = bf16_to_f32(xraw);
-      const float part = epi_act<ACT>(fmaf(xv, pr[0], pr[1]));
+      const float part = epi_act<ACT>(fmaf(raw_f32(xraw), pr[0], pr[1]));
       acc += li < cols - nb * V ? part : 0.f;
     }
     const SumP t = wave_allreduce(SumP{acc});

@@ -88,14 +88,6 @@ __global__ __launch_bounds__(kBlock) void pointwise_kernel(
   }
 }
 
-// a loaded element as fp32 (bf16 bit patterns are widened when used, so the
-// conversion does not wait on the load where it is issued)
-template <typename T>
-__device__ __forceinline__ float raw_to_f32(T v) {
-  if constexpr (std::is_same<T, float>::value) return v;
-  else return bf16_to_f32(v);
-}
-
 // Rows that are not whole 16-byte vectors (odd widths, odd row offsets) but
 // whose x, residual and y start every row at one offset within a 16-byte
 // unit: each row's aligned body, from its first 16-byte boundary to its last,
@@ -196,8 +188,8 @@ __global__ __launch_bounds__(kBlock) void pointwise_shift_kernel(
         const int nx = cols - nb[u] * V;
         if (r0 + u < rows && tid < nx) {
           const int ce = tid < hh[u] ? tid : nb[u] * V + tid;
-          float o = act_fn<ACT>(fmaf(raw_to_f32(ex[u]), scale, bias != nullptr ? eb[u] : 0.f));
-          if constexpr (HAS_RES) o += raw_to_f32(er[u]);
+          float o = act_fn<ACT>(fmaf(raw_f32(ex[u]), scale, bias != nullptr ? eb[u] : 0.f));
+          if constexpr (HAS_RES) o += raw_f32(er[u]);
           Elem<T>::store1(y + (r0 + u) * ld_y + ce, o);
         }
       }

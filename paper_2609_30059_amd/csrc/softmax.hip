@@ -99,12 +99,19 @@ __device__ __forceinline__ void store_until(T* row, int c0, int end, const float
 // path; G row groups per block (W == 1 only); R rows per group per trip --
 // narrow rows are batched so that a wave keeps R rows of loads in flight and
 // reduces them with one shuffle sequence.
-template <typename T, typename MT, bool HAS_MASK, int W, int EPT, bool VEC, int G, int R>
+// SHIFT: rows that are not whole 16-byte vectors but whose x, mask and y
+// start every row at one offset within a 16-byte unit.  The thread's vectors
+// tile the row's aligned body, from its first 16-byte boundary (h columns
+// in) to its last; the head and tail (at most V-1 columns each) are one
+// extra element for each of the group's first lanes: lanes below h take
+// the head, the next ones the tail.
+template <typename T, typename MT, bool HAS_MASK, int W, int EPT, bool VEC, bool SHIFT, int G,
+          int R>
 __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m,
     T* y, int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift) {
   constexpr int kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;                       // vectors per thread
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
   // one LDS fold area and one barrier sequence per block: rows wider than a
@@ -120,10 +127,10 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   int parity = 0;
   // rows without a causal rule that fill every slot of every lane have no
   // column to mask (uniform)
-  const bool whole = FS_SM_FULL_PATH && q_len == 0 && cols == kThreads * EPT;
+  const bool whole = !SHIFT && FS_SM_FULL_PATH && q_len == 0 && cols == kThreads * EPT;
   // every slot of every lane is stored: rows written whole (no trimming)
   // that fill every slot (uniform; causal rows included)
-  const bool store_all = trim_shift < 0 && cols == kThreads * EPT;
+  const bool store_all = !SHIFT && trim_shift < 0 && cols == kThreads * EPT;
 
   // causal position of row0 (row0 mod q_len), advanced by the loop step
   // without a division per row.  The host sends q_len >= 2^30 to the row
@@ -143,6 +150,10 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     Raw<T, V> rx[R][NV];
     Raw<MT, V> rm[R][HAS_MASK ? NV : 1];
     int lim[R], wend[R];
+    // SHIFT: the body [hh, bend) and each lane's extra element (raw)
+    int hh[R], bend[R];
+    T ex[R];
+    MT em[R];
     // one 64-bit row offset per trip; only the last trip can run past the
     // end, and its missing rows re-read the last row (in bounds, not stored)
     const bool full_trip = row0 + R <= rows;
@@ -164,15 +175,31 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       }
       lim[r] = limit < cols - 1 ? (limit < -1 ? -1 : limit) : cols - 1;
       wend[r] = we < cols ? (we < 0 ? 0 : we) : cols;
-      // vectors past lim are not read: their address is clamped onto the
-      // vector holding column lim (fetched by a live lane), then masked
-      const int limv = lim[r] < 0 ? 0 : (lim[r] / V) * V;
+      int h = 0, be = cols;
+      if constexpr (SHIFT) {
+        const int phase = int(reinterpret_cast<uintptr_t>(xr) & 15) / int(sizeof(T));
+        h = (V - phase) & (V - 1);
+        be = h + ((cols - h) / V) * V;
+      }
+      hh[r] = h;
+      bend[r] = be;
+      // vectors past lim (or past the body) are not read: their address is
+      // clamped onto the vector holding the last body column to read
+      // (fetched by a live lane), then masked
+      const int lc = SHIFT && be - 1 < lim[r] ? be - 1 : lim[r];
+      const int limv = SHIFT ? (lc < h ? h : h + ((lc - h) / V) * V) : (lc < 0 ? 0 : (lc / V) * V);
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
-        const int cl = c0 <= lim[r] ? c0 : limv;
+        const int c0 = h + (k * kThreads + tid) * V;
+        const int cl = c0 <= lc ? c0 : limv;
         rx[r][k].load(xr + cl);
         if constexpr (HAS_MASK) rm[r][k].load(mr + cl);
+      }
+      if constexpr (SHIFT) {
+        const int nx = cols - (be - h);
+        const int ce = tid < nx ? (tid < h ? tid : be - h + tid) : 0;
+        ex[r] = xr[ce];
+        if constexpr (HAS_MASK) em[r] = mr[ce];
       }
     }
     if (q > 0) {
@@ -182,13 +209,21 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     // keep every load of the trip ahead of the first use (one HBM round trip)
     __builtin_amdgcn_sched_barrier(0);
 
-    // logits a = x * scale + mask (-inf past lim)
-    float a[R][EPT];
+    // logits a = x * scale + mask (-inf past lim, and past the body); ae:
+    // the extra element's (SHIFT)
+    float a[R][EPT], ae[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
+      if constexpr (SHIFT) {
+        const int nx = cols - (bend[r] - hh[r]);
+        const int ce = tid < hh[r] ? tid : bend[r] - hh[r] + tid;
+        float xv = raw_f32(ex[r]) * scale;
+        if constexpr (HAS_MASK) xv += raw_f32(em[r]);
+        ae[r] = tid < nx && ce <= lim[r] ? xv : -INFINITY;
+      }
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
+        const int c0 = hh[r] + (k * kThreads + tid) * V;
         float xv[V];
         rx[r][k].unpack(xv);
         if constexpr (HAS_MASK) {
@@ -205,7 +240,8 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
           for (int i = 0; i < V; ++i) a[r][k * V + i] = xv[i];
         } else {
 #pragma unroll
-          for (int i = 0; i < V; ++i) a[r][k * V + i] = (c0 + i <= lim[r]) ? xv[i] : -INFINITY;
+          for (int i = 0; i < V; ++i)
+            a[r][k * V + i] = (c0 + i <= lim[r] && (!SHIFT || c0 < bend[r])) ? xv[i] : -INFINITY;
         }
       }
     }
@@ -220,7 +256,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       Multi<MaxF, R> mx;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        float m = -INFINITY;
+        float m = SHIFT ? ae[r] : -INFINITY;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
         mx.p[r].m = m;
@@ -238,6 +274,10 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
           a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2));
           d += a[r][i];
         }
+        if constexpr (SHIFT) {
+          ae[r] = __builtin_amdgcn_exp2f(fmaf(ae[r], kLog2e, -ml2));
+          d += ae[r];
+        }
         sm.p[r].s = d;
       }
       sm = wave_allreduce(sm);
@@ -253,7 +293,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       float ml2[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        float m = -INFINITY;
+        float m = SHIFT ? ae[r] : -INFINITY;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
         empty[r] = (m == -INFINITY);
@@ -263,6 +303,10 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         for (int i = 0; i < EPT; ++i) {
           a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2[r]));   // exp2(-inf) = 0
           d += a[r][i];
+        }
+        if constexpr (SHIFT) {
+          ae[r] = __builtin_amdgcn_exp2f(fmaf(ae[r], kLog2e, -ml2[r]));
+          d += ae[r];
         }
         part.p[r] = MaxSumP{empty[r] ? -INFINITY : ml2[r], d};
       }
@@ -283,14 +327,23 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     for (int r = 0; r < R; ++r) {
       if (full_trip || row0 + r < rows) {
         T* yr = yb + r * ld_y;
+        const int send = SHIFT && bend[r] < wend[r] ? bend[r] : wend[r];
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
-          const int c0 = (k * kThreads + tid) * V;
+          const int c0 = hh[r] + (k * kThreads + tid) * V;
           float o[V];
 #pragma unroll
           for (int i = 0; i < V; ++i) o[i] = a[r][k * V + i] * f[r];
           if (store_all) stv<T, V>(yr + c0, o);
-          else store_until(yr, c0, wend[r], o);
+          else store_until(yr, c0, send, o);
+        }
+        if constexpr (SHIFT) {
+          const int nx = cols - (bend[r] - hh[r]);
+          const int ce = tid < hh[r] ? tid : bend[r] - hh[r] + tid;
+          if (tid < nx && ce < wend[r]) {
+            const float o = ae[r] * f[r];
+            stv<T, 1>(yr + ce, &o);
+          }
         }
       }
     }
@@ -606,10 +659,37 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   const int min_w = c >= FS_SM_SPLIT_COLS ? FS_SM_MIN_WAVES : 1;
   // the register-resident kernel keeps causal positions in 32 bits
   const bool small_q = a.causal_q_len < (int64_t(1) << 30);
+  // rows that share a 16-byte phase: the vector ladder over each row's
+  // aligned body (a row of c columns has at most c / V whole vectors in it)
+  if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T))) {
+    if (a.shifted && c <= FS_SM_SHIFT_REG_COLS) {
+      constexpr int VS = Elem<T>::kVec;
+#define FS_SMS(Wv, E, Gv, BPC)                                                                  \
+  if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E)                                      \
+    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, false, true, Gv, RowsPerGroup<Wv, E>::value>, \
+                  64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
+      if constexpr (VS <= 4) { FS_SMS(1, 4, 4, 8) }
+      FS_SMS(1, 8, 4, 8)
+      FS_SMS(1, 16, 4, 8)
+      FS_SMS(1, 32, 4, 8)
+      FS_SMS(1, 64, 4, 8)
+      FS_SMS(2, 32, 1, 16)
+      FS_SMS(2, 64, 1, 16)
+      FS_SMS(4, 16, 1, 8)
+      FS_SMS(4, 32, 1, 8)
+      FS_SMS(4, 64, 1, 8)
+      FS_SMS(8, 8, 1, 4)
+      FS_SMS(8, 16, 1, 4)
+      FS_SMS(8, 32, 1, 4)
+      FS_SMS(16, 24, 1, 1)
+      FS_SMS(16, 32, 1, 1)
+#undef FS_SMS
+    }
+  }
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
   if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E &&                     \
       (VEC || c <= (a.shifted ? FS_SM_SHIFT_REG_COLS : FS_SM_ELEMENTWISE_REG_COLS)))  \
-    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
+    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, false, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }
   if constexpr (V <= 2) { FS_SM(1, 2, 4, 8) }

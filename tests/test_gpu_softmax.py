@@ -71,6 +71,44 @@ def test_widths(dtype, mask_dtype, cols):
         assert np.all(got[np.isinf(m)] == 0.0)
 
 
+# rows that are not whole 16-byte vectors, with x, mask and y at one offset
+# within a 16-byte unit per row (contiguous rows: a different one each row):
+# every register rung's edges, one-wave rows batched several per trip
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [17, 63, 65, 1001, 2047, 4097, 8191, 12289, 16383])
+def test_odd_rows_sharing_a_phase(dtype, cols):
+    rows = 45 if cols <= 4097 else 9
+    d = fd.softmax_inputs(cols + 3, rows, cols, dtype, mask_dtype=dtype, p_masked=0.3)
+    announce("softmax odd rows", cols, dtype)
+    got = host64(fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"]))
+    m = d["mask"].f64()
+    ref = oracle.row_softmax(d["x"].f64(), m, d["scale"])
+    assert_close(f"odd rows {cols}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"odd rows {cols}", got, ref, ulps=1.0, atol=1e-7)
+    assert np.all(got[np.isinf(m)] == 0.0)
+
+
+def test_odd_rows_head_and_tail_extremes():
+    # the row maximum in the first or the last columns (read one per lane
+    # next to the 16-byte body), masked heads and tails, an all-masked row
+    rows, cols = 24, 2051
+    x = torch.zeros(rows, cols, dtype=torch.bfloat16, device="cuda")
+    m = torch.zeros(rows, cols, dtype=torch.bfloat16, device="cuda")
+    for i, j in enumerate([0, 1, 6, 7, cols - 1, cols - 2, cols - 7, cols - 8]):
+        x[i, j] = 30.0
+        x[8 + i, j] = 30.0
+        m[8 + i, j] = float("-inf")
+        m[16 + i, :] = float("-inf")
+        m[16 + i, j] = 0.0
+    announce("softmax odd rows head and tail")
+    got = host64(fs.row_softmax(x, m, 1.0))
+    ref = oracle.row_softmax(host64(x), host64(m), 1.0)
+    assert_close("head and tail", got, ref, *TOL["bf16"])
+    for i, j in enumerate([0, 1, 6, 7, cols - 1, cols - 2, cols - 7, cols - 8]):
+        assert got[i, j] > 0.99 and got[8 + i, j] == 0.0 and got[16 + i, j] == 1.0
+
+
 @pytest.mark.parametrize("seed", SEEDS)
 def test_causal_attention_scores(seed):
     # [2, 16, 512, 512] scores, causal, scale 1/8: the block's softmax shape
@@ -89,7 +127,8 @@ def test_causal_attention_scores(seed):
         np.testing.assert_array_equal(got[r], one_hot)
 
 
-@pytest.mark.parametrize("q_len,cols", [(3, 10), (64, 512), (100, 4096), (512, 512)])
+@pytest.mark.parametrize("q_len,cols", [(3, 10), (64, 512), (100, 4096), (512, 512), (37, 1001),
+                                        (64, 4095), (9, 12289)])
 def test_causal_offsets_and_widths(q_len, cols):
     rows = 3 * q_len
     d = fd.softmax_inputs(q_len + cols, rows, cols, "f32", mask_dtype="f32", p_masked=0.2)

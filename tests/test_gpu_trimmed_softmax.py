@@ -62,7 +62,8 @@ def test_square_attention_rows(dtype, block):
 @pytest.mark.parametrize("rows,cols,q,block,dtype", [
     (37, 40, 10, 4, "f32"), (20, 3000, 2900, 256, "f32"), (16, 20000, 20000, 4096, "f32"),
     (9, 33333, 9, 1024, "f32"), (6, 50000, 40000, 2048, "bf16"), (6, 70000, 70000, 8192, "f32"),
-    (5, 100001, 3, 16384, "f32")])
+    (5, 100001, 3, 16384, "f32"), (37, 1001, 1001, 64, "bf16"), (19, 4095, 300, 128, "bf16"),
+    (11, 12289, 12289, 1024, "bf16"), (13, 2051, 2051, 16, "f32")])
 def test_rectangular_ragged_and_streamed(rows, cols, q, block, dtype):
     d = fd.softmax_inputs(rows + cols, rows, cols, dtype, mask_dtype=None, sigma=2.0)
     announce("trimmed softmax rect", rows, cols, q, block, dtype)
