@@ -174,9 +174,12 @@ FS_API fs_status fs_causal_softmax_trimmed(const void* x, int64_t ld_x, void* y,
  * gamma, beta  : [cols] of `dtype`, or NULL (1 and 0).
  * y and residual_out may each be x or residual exactly; they may not overlap
  * each other.  eps must be finite and >= 0.  Rows of whole 16-byte vectors up
- * to 16384 columns (32768 for bf16), and other rows up to 8192 columns, are
- * held in registers: x and residual are read once and the statistics take
- * two exact passes over the registers.  Longer rows (for rows that are not
+ * to 16384 columns (32768 for bf16), rows up to 16384 columns whose x,
+ * residual, y and residual_out start each row at one offset within a 16-byte
+ * unit (the aligned body of each row loaded 16 bytes at a time, gamma and
+ * beta staged on chip), and other rows up to 8192 columns, are held in
+ * registers: x and residual are read once and the statistics take two exact
+ * passes over the registers.  Longer rows (for rows that are not
  * whole 16-byte vectors: past 32768 columns) keep h of their first 65536
  * columns on chip (LDS and registers, one row per compute unit) and read
  * those columns once, merging per-chunk (count, mean, M2) statistics; the

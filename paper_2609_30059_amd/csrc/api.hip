@@ -288,6 +288,8 @@ fs_status norm_residual(const void* x, int64_t ld_x, const void* residual, int64
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(residual, ld_r, es) && vec_ok(residual_out, ld_ro, es) &&
           (gamma == nullptr || aligned(gamma, 16)) && (beta == nullptr || aligned(beta, 16));
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && same_phase(x, ld_x, y, ld_y, es) &&
+              same_phase(x, ld_x, residual, ld_r, es) && same_phase(x, ld_x, residual_out, ld_ro, es);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_layernorm(a, cus, stream);

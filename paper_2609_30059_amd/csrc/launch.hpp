@@ -51,6 +51,9 @@ struct LayerNormArgs {
   fs_dtype dtype;
   bool vec;
   bool rms;        // RMSNorm: no mean, no beta
+  // not vec, rows of at least two 16-byte vectors, and x, res, y and res_out
+  // start every row at one offset within a 16-byte unit
+  bool shifted = false;
 };
 
 struct EpilogueArgs {

@@ -64,25 +64,59 @@
 #define FS_LN_GRID_SCALE 16
 #endif
 
+// rows that share a 16-byte phase take the register rungs up to this many
+// columns (their LDS table of (gamma, beta) pairs grows with the rung)
+#ifndef FS_LN_SHIFT_REG_COLS
+#define FS_LN_SHIFT_REG_COLS 16384
+#endif
+
 namespace fs {
 namespace {
+
+// (gamma, beta) of one column as staged in LDS: two bf16 bit patterns in one
+// dword (exact), or two floats
+template <typename T> struct AffinePair;
+template <> struct AffinePair<uint16_t> {
+  using type = uint32_t;
+  __device__ __forceinline__ static type make(uint16_t g, uint16_t b) { return uint32_t(g) | (uint32_t(b) << 16); }
+  __device__ __forceinline__ static float gamma(type p) { return __uint_as_float(p << 16); }
+  __device__ __forceinline__ static float beta(type p) { return __uint_as_float(p & 0xffff0000u); }
+};
+template <> struct AffinePair<float> {
+  typedef float type __attribute__((ext_vector_type(2)));
+  __device__ __forceinline__ static type make(float g, float b) { type p; p[0] = g; p[1] = b; return p; }
+  __device__ __forceinline__ static float gamma(type p) { return p[0]; }
+  __device__ __forceinline__ static float beta(type p) { return p[1]; }
+};
 
 // W waves per row, EPT elements per thread, G row groups per block (W == 1
 // only), R rows per group per trip: narrow rows are batched so that a wave
 // keeps R rows of loads in flight and reduces them with one shuffle sequence.
-template <typename T, bool HAS_RES, bool RMS, int W, int EPT, bool VEC, int G, int R>
+// SHIFT: rows that are not whole 16-byte vectors but whose x, residual, y and
+// residual_out start every row at one offset within a 16-byte unit.  The
+// threads' vectors tile each row's aligned body, from its first 16-byte
+// boundary (h columns in) to its last; the head and tail (at most V-1 columns
+// each) are one extra element for each of the group's first lanes.  gamma and
+// beta are staged once per block in LDS as (gamma, beta) pairs in V planes,
+// column j at plane j % V, index j / V: element e of body vector v (column
+// h + v*V + e) reads plane (h+e) % V at index v + (h+e) / V, consecutive
+// across the lanes whatever h is.
+template <typename T, bool HAS_RES, bool RMS, int W, int EPT, bool VEC, bool SHIFT, int G, int R>
 __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
     const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
     const T* __restrict__ gamma, const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out,
     int64_t ld_ro, int64_t rows, int cols, float eps) {
   constexpr int kThreads = 64 * W;
-  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;
+  using AP = AffinePair<T>;
+  using Pair = typename AP::type;
+  constexpr int Q = NV * kThreads + 1;     // SHIFT: pairs per plane
   // gamma and beta stay in registers for the whole kernel when they fit
   // (element-wise loads hold one value per register, so only small rungs
   // keep them); wider rows re-read them (cache-resident) after each trip's
   // statistics
-  constexpr bool kAffineResident = VEC ? EPT <= 32 : EPT <= 8;
+  constexpr bool kAffineResident = !SHIFT && (VEC ? EPT <= 32 : EPT <= 8);
   static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
   // one LDS fold area and one barrier sequence per block: rows wider than a
   // wave take the whole block (the row loop is then uniform across it)
@@ -100,7 +134,7 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   const int clast = cols - V;
   const float inv_cols = 1.f / float(cols);
   // rows that fill every slot of every lane need no masking (uniform)
-  const bool full = FS_LN_FULL_PATH && cols == kThreads * EPT;
+  const bool full = !SHIFT && FS_LN_FULL_PATH && cols == kThreads * EPT;
   const bool affine = FS_LN_FULL_PATH && gamma != nullptr && (RMS || beta != nullptr);
 
   Raw<T, V> rg[NV], rb[NV];
@@ -115,28 +149,82 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
   };
 
   if constexpr (kAffineResident) load_affine();
+  extern __shared__ unsigned char ln_dyn[];
+  Pair* pl = reinterpret_cast<Pair*>(ln_dyn);   // SHIFT: [V][Q]
+  if constexpr (SHIFT) {
+    // every staging load is issued before the first is used; stand-in
+    // pointers keep them unconditional (1 and 0 replace what is absent)
+    constexpr int kAll = 64 * W * G, NS = (V * Q + kAll - 1) / kAll;
+    const T* gs = gamma ? gamma : x;
+    const T* bs = beta ? beta : x;
+    T gv[NS], bv[NS];
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      const int i = int(threadIdx.x) + t * kAll, q = i % Q;
+      const int j = q * V + i / Q;
+      const int jc = i < V * Q && j < cols ? j : 0;
+      gv[t] = gs[jc];
+      bv[t] = bs[jc];
+    }
+    const T one = std::is_same<T, float>::value ? T(1.f) : T(0x3F80), zero = T(0);
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      const int i = int(threadIdx.x) + t * kAll, q = i % Q;
+      const bool live = q * V + i / Q < cols;
+      const T gg = !live ? zero : gamma ? gv[t] : one;
+      const T bb = !live || RMS || !beta ? zero : bv[t];
+      if (i < V * Q) pl[i] = AP::make(gg, bb);
+    }
+    __syncthreads();
+  }
 
   for (int64_t row0 = (int64_t(blockIdx.x) * G + g) * R; row0 < rows;
        row0 += int64_t(gridDim.x) * G * R) {
     Raw<T, V> rx[R][NV], rres[R][HAS_RES ? NV : 1];
+    // SHIFT: the body [hh, bend) of each row and the lanes' extra elements
+    int hh[R], bend[R];
+    T ex[R], er[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       // rows past the end re-read the last row (in bounds) and are not stored
       const int64_t row = row0 + r < rows ? row0 + r : rows - 1;
+      int h0 = 0, be = cols;
+      if constexpr (SHIFT) {
+        const int phase = int(reinterpret_cast<uintptr_t>(x + row * ld_x) & 15) / int(sizeof(T));
+        h0 = (V - phase) & (V - 1);
+        be = h0 + ((cols - h0) / V) * V;
+      }
+      hh[r] = h0;
+      bend[r] = be;
+      const int last = SHIFT ? be - V : clast;
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
-        const int c0 = (k * kThreads + tid) * V;
-        const int cl = c0 < cols ? c0 : clast;
+        const int c0 = h0 + (k * kThreads + tid) * V;
+        const int cl = c0 < be ? c0 : last;
         rx[r][k].load(x + row * ld_x + cl);
         if constexpr (HAS_RES) rres[r][k].load(res + row * ld_r + cl);
+      }
+      if constexpr (SHIFT) {
+        const int nx = cols - (be - h0);
+        const int ce = tid < nx ? (tid < h0 ? tid : be - h0 + tid) : 0;
+        ex[r] = x[row * ld_x + ce];
+        if constexpr (HAS_RES) er[r] = res[row * ld_r + ce];
       }
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    float h[R][EPT];
+    float h[R][EPT], he[R];
     P part;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
+      // SHIFT: the extra element (0 for lanes without one)
+      const int nx = cols - (bend[r] - hh[r]);
+      const int ce = tid < hh[r] ? tid : bend[r] - hh[r] + tid;
+      if constexpr (SHIFT) {
+        float v = raw_f32(ex[r]);
+        if constexpr (HAS_RES) v += raw_f32(er[r]);
+        he[r] = tid < nx ? v : 0.f;
+      }
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
         float xv[V];
@@ -154,7 +242,7 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
         // slots past the row end hold 0 (they re-read the row's last vector)
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
-          const bool in = (k * kThreads + tid) * V < cols;
+          const bool in = hh[r] + (k * kThreads + tid) * V < bend[r];
 #pragma unroll
           for (int i = 0; i < V; ++i) h[r][k * V + i] = in ? h[r][k * V + i] : 0.f;
         }
@@ -163,13 +251,17 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
         T* ro = res_out + (row0 + r) * ld_ro;
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
-          const int c0 = (k * kThreads + tid) * V;
-          if (c0 < cols) stv<T, V>(ro + c0, h[r] + k * V);
+          const int c0 = hh[r] + (k * kThreads + tid) * V;
+          if (c0 < bend[r]) stv<T, V>(ro + c0, h[r] + k * V);
+        }
+        if constexpr (SHIFT) {
+          if (tid < nx) stv<T, 1>(ro + ce, &he[r]);
         }
       }
       float sum = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) sum = RMS ? fmaf(h[r][i], h[r][i], sum) : sum + h[r][i];
+      if constexpr (SHIFT) sum = RMS ? fmaf(he[r], he[r], sum) : sum + he[r];
       part.p[r] = SumP{sum};      // out-of-row slots hold 0
     }
     float mean[R];
@@ -195,12 +287,16 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
         } else {
 #pragma unroll
           for (int k = 0; k < NV; ++k) {
-            const bool in = (k * kThreads + tid) * V < cols;
+            const bool in = hh[r] + (k * kThreads + tid) * V < bend[r];
 #pragma unroll
             for (int i = 0; i < V; ++i) {
               const float d = in ? h[r][k * V + i] - mean[r] : 0.f;
               m2 = fmaf(d, d, m2);
             }
+          }
+          if constexpr (SHIFT) {
+            const float d = tid < cols - (bend[r] - hh[r]) ? he[r] - mean[r] : 0.f;
+            m2 = fmaf(d, d, m2);
           }
         }
         part.p[r] = SumP{m2};
@@ -208,12 +304,36 @@ __global__ __launch_bounds__(64 * W * G) void layernorm_kernel(
     }
     const P sq = group_allreduce<W>(part, lds[parity], wave, lane);
     parity ^= 1;
-    if constexpr (!kAffineResident) load_affine();
+    if constexpr (!kAffineResident && !SHIFT) load_affine();
 
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const float rstd = rsqrtf(sq.p[r].s * inv_cols + eps);
-      if (row0 + r < rows) {
+      if (SHIFT && row0 + r < rows) {
+        T* yr = y + (row0 + r) * ld_y;
+        int off[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+          off[i] = ((hh[r] + i) & (V - 1)) * Q + (hh[r] + i >= V ? 1 : 0) + tid;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const int c0 = hh[r] + (k * kThreads + tid) * V;
+          float o[V];
+#pragma unroll
+          for (int i = 0; i < V; ++i) {
+            const Pair pr = pl[off[i] + k * kThreads];
+            o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, AP::gamma(pr), AP::beta(pr));
+          }
+          if (c0 < bend[r]) stv<T, V>(yr + c0, o);
+        }
+        const int nx = cols - (bend[r] - hh[r]);
+        if (tid < nx) {
+          const int ce = tid < hh[r] ? tid : bend[r] - hh[r] + tid;
+          const Pair pr = pl[(ce & (V - 1)) * Q + ce / V];
+          const float o = fmaf((he[r] - mean[r]) * rstd, AP::gamma(pr), AP::beta(pr));
+          stv<T, 1>(yr + ce, &o);
+        }
+      } else if (row0 + r < rows) {
         T* yr = y + (row0 + r) * ld_y;
         // the affine form is uniform: one loop for gamma and beta both given
         // (no per-element choice of 1 / 0), one for the other cases
@@ -692,10 +812,51 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
 // Variant ladder, in order: the first rung with at least min_w waves per row
   // and a row capacity 64 * W * EPT >= cols is launched.
   const int min_w = c >= FS_LN_SPLIT_COLS ? FS_LN_MIN_WAVES : 1;
+  // rows that share a 16-byte phase: the vector ladder over each row's
+  // aligned body, gamma and beta staged in LDS (a row of c columns has at
+  // most c / V whole vectors in it)
+  if constexpr (!VEC) {
+    if (a.shifted && c <= FS_LN_SHIFT_REG_COLS) {
+      constexpr int VS = Elem<T>::kVec;
+      constexpr int kPair = sizeof(typename AffinePair<T>::type);
+      auto shift = [&](auto kern, int threads, int rows_per_block, int wt) {
+        const size_t lds = size_t(VS) * (wt + 1) * kPair;   // wt: vectors per row group
+        int64_t want = (a.rows + rows_per_block - 1) / rows_per_block;
+        const int per_cu = int((160 * 1024) / (lds + 1024));
+        int64_t cap = int64_t(cus) * (per_cu < 1 ? 1 : per_cu) * FS_LN_GRID_SCALE / 4;
+        int grid = int(want < cap ? want : cap);
+        if (grid < 1) grid = 1;
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), lds, s, static_cast<const T*>(a.x),
+                           a.ld_x, static_cast<const T*>(a.res), a.ld_r,
+                           static_cast<const T*>(a.gamma), static_cast<const T*>(a.beta),
+                           static_cast<T*>(a.y), a.ld_y, static_cast<T*>(a.res_out), a.ld_ro,
+                           a.rows, int(a.cols), a.eps);
+        return hipGetLastError();
+      };
+#define FS_LNS(Wv, E, Gv)                                                                       \
+  if (Wv >= min_w && c <= int64_t(64) * Wv * E)                                                 \
+    return shift(layernorm_kernel<T, HAS_RES, RMS, Wv, E, false, true, Gv, RowsPerGroup<Wv, E>::value>, \
+                 64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, 64 * Wv * (E / VS));
+      if constexpr (VS <= 4) { FS_LNS(1, 4, 4) }
+      FS_LNS(1, 8, 4)
+      FS_LNS(1, 16, 4)
+      FS_LNS(1, 32, 4)
+      FS_LNS(1, 64, 4)
+      FS_LNS(2, 32, 1)
+      FS_LNS(2, 64, 1)
+      FS_LNS(4, 16, 1)
+      FS_LNS(4, 32, 1)
+      FS_LNS(4, 64, 1)
+      FS_LNS(8, 8, 1)
+      FS_LNS(8, 16, 1)
+      FS_LNS(8, 32, 1)
+#undef FS_LNS
+    }
+  }
 #define FS_LN(Wv, E, Gv, BPC)                                                       \
   if (Wv >= min_w && c <= int64_t(64) * Wv * E &&                                 \
       (VEC || c <= FS_LN_ELEMENTWISE_REG_COLS))                                  \
-    return launch(layernorm_kernel<T, HAS_RES, RMS, Wv, E, VEC, Gv, RowsPerGroup<Wv, E>::value>, \
+    return launch(layernorm_kernel<T, HAS_RES, RMS, Wv, E, VEC, false, Gv, RowsPerGroup<Wv, E>::value>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_LN(1, 1, 4, 8) }
   if constexpr (V <= 2) { FS_LN(1, 2, 4, 8) }

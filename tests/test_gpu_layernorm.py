@@ -70,6 +70,79 @@ def test_widths(dtype, cols):
     check(f"cols {cols}", d, y, ro, dtype)
 
 
+# rows that are not whole 16-byte vectors, with x, residual, y and
+# residual_out at one offset within a 16-byte unit per row (contiguous rows: a
+# different one each row): the register rungs with gamma and beta staged in
+# LDS, across the rungs and their edges
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [17, 100, 1001, 2047, 4097, 8191, 12289, 16383])
+def test_odd_rows_sharing_a_phase(dtype, cols):
+    rows = 37 if cols <= 4097 else 7
+    d = fd.layernorm_inputs(cols + 5, rows, cols, dtype)
+    announce("layernorm odd rows", cols, dtype)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                  dev(d["beta"]), d["eps"])
+    check(f"odd rows {cols}", d, y, ro, dtype)
+
+
+@pytest.mark.parametrize("has_res,affine,store", [(False, True, False), (True, False, True),
+                                                  (False, False, False)])
+def test_optional_operands_odd_rows(has_res, affine, store):
+    d = fd.layernorm_inputs(6, 29, 3001, "bf16")
+    announce("layernorm optional odd rows", has_res, affine, store)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]) if has_res else None,
+                                  dev(d["gamma"]) if affine else None,
+                                  dev(d["beta"]) if affine else None, d["eps"],
+                                  store_residual=store)
+    check("optional odd rows", d, y, ro, "bf16", has_res, affine)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_misaligned_gamma_beta(dtype):
+    # whole-vector rows with gamma and beta one element off a 16-byte boundary
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    cols = 4096
+    d = fd.layernorm_inputs(14, 11, cols, dtype)
+    gb = torch.empty(2 * cols + 2, dtype=tdt, device="cuda")
+    g, b = gb[1:cols + 1], gb[cols + 2:]
+    g.copy_(dev(d["gamma"]))
+    b.copy_(dev(d["beta"]))
+    announce("layernorm misaligned gamma beta", dtype)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), g, b, d["eps"])
+    check("misaligned gamma beta", d, y, ro, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_same_phase_rows_and_guards(dtype):
+    # x, residual, y and residual_out share one odd row stride and offset
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 17, 2501, 2519
+    d = fd.layernorm_inputs(15, rows, cols, dtype)
+    for offset in (1, 5):
+        announce("layernorm same-phase strided", dtype, offset)
+        xg = Guarded(rows, cols, ld, tdt, offset=offset)
+        rg = Guarded(rows, cols, ld, tdt, offset=offset)
+        yg = Guarded(rows, cols, ld, tdt, offset=offset)
+        og = Guarded(rows, cols, ld, tdt, offset=offset)
+        xg.view.copy_(dev(d["x"]))
+        rg.view.copy_(dev(d["residual"]))
+        fs.layernorm_residual(xg.view, rg.view, dev(d["gamma"]), dev(d["beta"]), d["eps"],
+                              out=yg.view, residual_out=og.view)
+        torch.cuda.synchronize()
+        check(f"same-phase offset {offset}", d, yg.view, og.view, dtype)
+        yg.check_untouched("layernorm y")
+        og.check_untouched("layernorm residual_out")
+
+
+def test_in_place_odd_rows():
+    d = fd.layernorm_inputs(16, 23, 4093, "bf16")
+    x, r = dev(d["x"]), dev(d["residual"])
+    fs.layernorm_residual(x, r, dev(d["gamma"]), dev(d["beta"]), d["eps"], out=x,
+                          residual_out=r)
+    torch.cuda.synchronize()
+    check("in place odd rows", d, x, r, "bf16")
+
+
 @pytest.mark.parametrize("has_res,affine,store", [(False, True, False), (True, False, True),
                                                   (True, True, False), (False, False, False)])
 def test_optional_operands(has_res, affine, store):
@@ -178,6 +251,16 @@ def test_rmsnorm_widths(dtype, cols):
     eps = float(np.float32(1e-6))
     y, ro = fs.rmsnorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]), eps)
     check_rms(f"cols {cols}", d, y, ro, dtype, eps=eps)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols", [1001, 12289])
+def test_rmsnorm_odd_rows(dtype, cols):
+    d = fd.layernorm_inputs(cols + 2, 9, cols, dtype)
+    announce("rmsnorm odd rows", cols, dtype)
+    eps = float(np.float32(1e-6))
+    y, ro = fs.rmsnorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]), eps)
+    check_rms(f"odd rows {cols}", d, y, ro, dtype, eps=eps)
 
 
 def test_rmsnorm_without_residual_or_gamma():
