@@ -822,8 +822,10 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
       auto shift = [&](auto kern, int threads, int rows_per_block, int wt) {
         const size_t lds = size_t(VS) * (wt + 1) * kPair;   // wt: vectors per row group
         int64_t want = (a.rows + rows_per_block - 1) / rows_per_block;
+        // no more blocks than fit at once: every block stages the whole
+        // table, so each should normalise many rows with it
         const int per_cu = int((160 * 1024) / (lds + 1024));
-        int64_t cap = int64_t(cus) * (per_cu < 1 ? 1 : per_cu) * FS_LN_GRID_SCALE / 4;
+        int64_t cap = int64_t(cus) * (per_cu < 1 ? 1 : per_cu);
         int grid = int(want < cap ? want : cap);
         if (grid < 1) grid = 1;
         hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), lds, s, static_cast<const T*>(a.x),
