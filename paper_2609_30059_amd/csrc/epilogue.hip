@@ -497,6 +497,7 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
     return nvec == int64_t(NV) * 64                                                      \
                ? staged(epilogue_lds_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, true>, NV)   \
                : staged(epilogue_lds_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, false>, NV);
+    FS_EPI_RUNG(2)
     FS_EPI_RUNG(4)
     FS_EPI_RUNG(8)
     FS_EPI_RUNG(16)
@@ -522,6 +523,7 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
     constexpr int wpe = V * NV >= 128 ? 4 : 8;                                             \
     return shift(epilogue_shift_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, wpe>, NV, wpe);     \
   }
+    FS_EPI_SHIFT_RUNG(2)
     FS_EPI_SHIFT_RUNG(4)
     FS_EPI_SHIFT_RUNG(8)
     FS_EPI_SHIFT_RUNG(16)
