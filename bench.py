@@ -476,7 +476,8 @@ def cpu_baseline(wl: Workload, frac: float):
             total_s += dt
     return {"value": round(total_bytes / total_s / 1e9, 4), "unit": "GB/s", "cores": 1,
             "kind": "oracle", "seconds": round(total_s, 2),
-            "sample": f"float64 oracle, one thread, over {frac:g} of the rows of every "
+            "sample": f"float64 oracle, one thread, over "
+                      f"{'all' if frac >= 1 else f'a fraction {frac:g}'} of the rows of every "
                       f"sub-kernel of one step ({total_bytes} compulsory bytes), on host "
                       f"inputs of the same shapes from the seeded generators",
             "per_kernel": per}
