@@ -68,10 +68,11 @@ def test_sign_flip_symmetry():
                                              ("f32", "bf16")])
 # staged rungs up to 16384 columns; rows that are not whole vectors, from two
 # vectors up (15, 17, 100, 1001, 4095, 16383, 16391: every rung, its edges and
-# each row at another offset within a 16-byte unit); the wide kernel with
+# each row at another offset within a 16-byte unit); 512 (fp32) and 1024
+# (bf16) fill the 2-vector rung exactly; the wide kernel with
 # 16-byte loads (24000, 40000) and with element loads (1, 7, 16399, 24001)
-@pytest.mark.parametrize("cols", [1, 7, 8, 15, 17, 100, 512, 1000, 1001, 4095, 4096, 8192, 8200,
-                                  16383, 16384, 16391, 16399, 24000, 24001, 40000])
+@pytest.mark.parametrize("cols", [1, 7, 8, 15, 17, 100, 512, 1000, 1001, 1024, 4095, 4096, 8192,
+                                  8200, 16383, 16384, 16391, 16399, 24000, 24001, 40000])
 def test_widths_and_dtypes(c_dtype, b_dtype, cols):
     rows = 11 if cols <= 16384 else 3
     d = fd.epilogue_inputs(cols, rows, cols, c_dtype, bias_dtype=b_dtype)
