@@ -29,8 +29,10 @@ def fs_dtype(t: torch.Tensor) -> int:
 def as_rows(t: torch.Tensor) -> Tuple[int, int, int]:
     """(rows, cols, ld) of a tensor viewed as [prod(leading dims), last dim].
 
-    The last dim must have unit stride and the leading dims must collapse
-    onto one row stride (a contiguous batch of rows)."""
+    The last dim must have unit stride, the leading dims must collapse onto
+    one row stride (a batch of rows), and distinct rows must not overlap:
+    broadcast (stride-0) and overlapping views are refused, since a kernel
+    would read or write past the memory they cover."""
     nd = t.dim()
     if nd >= 2 and t.is_contiguous():
         cols = t.shape[-1]
@@ -38,21 +40,29 @@ def as_rows(t: torch.Tensor) -> Tuple[int, int, int]:
             return t.numel() // cols, cols, cols
     if nd == 0:
         raise ValueError("scalar tensors are not supported")
-    if nd == 1:
-        return 1, t.shape[0], max(t.shape[0], 1)
-    if t.shape[-1] > 1 and t.stride(-1) != 1:
+    cols = t.shape[-1]
+    if cols > 1 and t.stride(-1) != 1:
         raise ValueError("the last dimension must be contiguous")
-    ld = t.stride(-2)
-    for i in range(t.dim() - 2):
-        if t.shape[i] > 1 and t.stride(i) != t.stride(i + 1) * t.shape[i + 1]:
-            raise ValueError("leading dimensions do not collapse onto one row stride")
+    if nd == 1:
+        return 1, cols, max(cols, 1)
+    # leading dims of extent > 1, innermost first: the innermost gives the
+    # row stride, each outer one must step over whole inner blocks
+    lead = [(t.shape[i], t.stride(i)) for i in range(nd - 2, -1, -1) if t.shape[i] > 1]
     rows = 1
     for s in t.shape[:-1]:
         rows *= s
-    cols = t.shape[-1]
-    if rows <= 1:
-        ld = max(cols, 1)
-    return rows, cols, max(ld, cols)
+    if rows <= 1 or not lead:
+        return rows, cols, max(cols, 1)
+    ld = lead[0][1]
+    for (n_in, s_in), (_, s_out) in zip(lead, lead[1:]):
+        if s_out != s_in * n_in:
+            raise ValueError("leading dimensions do not collapse onto one row stride")
+    if cols == 0:
+        return rows, 0, max(ld, 1)
+    if ld < cols:
+        raise ValueError(f"rows overlap or are broadcast (row stride {ld} < {cols} columns); "
+                         "make the tensor contiguous")
+    return rows, cols, ld
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

@@ -72,22 +72,6 @@ def test_small_block_causal_row_blocks(attn_block):
             block=attn_block)
 
 
-@pytest.mark.parametrize("seed", SEEDS)
-def test_full_block_sampled_sequences(seed):
-    c = fd.CONFIGS["block_32x512x1024"]
-    d = fd.make_inputs("block_32x512x1024", seed)
-    seqs = [0, c["batch"] - 1] if seed else [0, 13, c["batch"] - 1]
-    announce("block 32x512x1024", seed, seqs)
-    buf, ref = run_block(d, c["heads"], seqs)
-    compare(buf, ref, seqs, c["batch"], c["seq"], f"block seed {seed}", d["x"].f64()[seqs])
-    # causal softmax structure at full size: row 0 of every head is one-hot
-    p0 = buf["probs"][:, :, 0, :].float()
-    assert torch.all(p0[..., 0] == 1.0) and torch.all(p0[..., 1:] == 0.0)
-    # the attention branch carries signal: out - x differs from the MLP-only value
-    delta = host64(buf["att"].view(c["batch"], c["seq"], -1)[seqs])
-    assert np.abs(delta).mean() > 1e-3
-
-
 def test_block_causality_on_gpu():
     d = fd.block_inputs(1, batch=2, seq=128, hidden=256, heads=4, mlp=512)
     params = {k: dev(d[k]) for k in fs.block.PARAM_NAMES}

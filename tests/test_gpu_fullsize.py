@@ -1,0 +1,250 @@
+"""Whole-output parity at the full workload shapes, on seeds 0-4.
+
+Every row of every output is compared with the float64 oracle, mirroring the
+multi-seed correctness gates of Section 4.4 (Gates 2-3), at the shapes the
+benchmark times:
+  * the pointwise chain at its bandwidth scale, fp32 [262144, 1024];
+  * the masked softmax, bf16 [8192, 4096];
+  * LayerNorm + residual, bf16 [16384, 4096];
+  * the GEMM epilogue on the GPU's own hipBLASLt output C [8192, 8192];
+  * the stitched block [32, 512, 1024], all 32 sequences, every stage.
+
+Each case also reports the Gate-3 error ratio rho = d_opt / d_ref (Eq. 4):
+d_opt and d_ref are the largest deviations from the float64 oracle of the
+fused output and of an unfused PyTorch eager evaluation in the same I/O
+precision.  Comparisons run over row chunks so host memory stays bounded.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import (SEEDS, TOL, announce, assert_close, bf16_ulp_close, dev, f64_rows, host64,
+                      max_abs_dev, record_rho, softmax_supplementary)
+
+pytestmark = pytest.mark.gpu
+
+# fp32 tree sum of 8192 terms below 1: |error| <= log2(8192) * ulp(4096) ~ 5e-3
+SUM_ATOL = 5e-3
+
+
+class Deviation:
+    """Running maxima over chunks: |fused - f64|, |eager - f64|, |eager|."""
+
+    def __init__(self):
+        self.opt = self.ref = self.scale = 0.0
+
+    def add(self, got, eager, ref):
+        self.opt = max(self.opt, max_abs_dev(got, ref))
+        self.ref = max(self.ref, max_abs_dev(eager, ref))
+        self.scale = max(self.scale, float(np.max(np.abs(eager), initial=0.0)))
+
+    def record(self, case):
+        return record_rho(case, self.opt, self.ref, self.scale)
+
+
+def chunks(rows, n):
+    for r0 in range(0, rows, n):
+        yield r0, min(rows, r0 + n)
+
+
+# ---- a1: pointwise chain at the bandwidth scale --------------------------------
+@pytest.mark.parametrize("seed", SEEDS)
+def test_pointwise_262144x1024_every_row(seed):
+    name = "pointwise_262144x1024"
+    c = fd.CONFIGS[name]
+    d = fd.make_inputs(name, seed)
+    announce(name, "every row", seed)
+    x, b, r = dev(d["x"]), dev(d["bias"]), dev(d["residual"])
+    y = fs.pointwise_chain(x, b, r, d["scale"], "gelu_erf")
+    b64 = d["bias"].f64()
+    dv = Deviation()
+    for r0, r1 in chunks(c["rows"], 16384):
+        ref = oracle.pointwise_chain(f64_rows(d["x"], r0, r1), b64, f64_rows(d["residual"], r0, r1),
+                                     d["scale"], "gelu_erf")
+        got = host64(y[r0:r1])
+        assert_close(f"{name} seed {seed} rows {r0}:{r1}", got, ref, *TOL["f32"])
+        eager = host64(F.gelu(x[r0:r1] * d["scale"] + b) + r[r0:r1])
+        dv.add(got, eager, ref)
+    dv.record(f"{name} seed {seed}")
+
+
+# ---- a2: masked softmax ------------------------------------------------------
+@pytest.mark.parametrize("seed", SEEDS)
+def test_softmax_8192x4096_every_row(seed):
+    name = "softmax_8192x4096"
+    c = fd.CONFIGS[name]
+    d = fd.make_inputs(name, seed)
+    announce(name, "every row", seed)
+    x, m = dev(d["x"]), dev(d["mask"])
+    y = fs.row_softmax(x, m, d["scale"])
+    dv = Deviation()
+    for r0, r1 in chunks(c["rows"], 2048):
+        m64 = f64_rows(d["mask"], r0, r1)
+        ref = oracle.row_softmax(f64_rows(d["x"], r0, r1), m64, d["scale"])
+        got = host64(y[r0:r1])
+        case = f"{name} seed {seed} rows {r0}:{r1}"
+        assert_close(case, got, ref, *TOL["bf16"])
+        softmax_supplementary(case, got, ref, np.isinf(m64))
+        eager = host64(torch.softmax(x[r0:r1] * d["scale"] + m[r0:r1], dim=-1))
+        dv.add(got, eager, ref)
+    dv.record(f"{name} seed {seed}")
+
+
+# ---- a3: LayerNorm + residual ------------------------------------------------
+@pytest.mark.parametrize("seed", SEEDS)
+def test_layernorm_16384x4096_every_row(seed):
+    name = "layernorm_16384x4096"
+    c = fd.CONFIGS[name]
+    d = fd.make_inputs(name, seed)
+    announce(name, "every row", seed)
+    x, res, g, b = (dev(d[k]) for k in ("x", "residual", "gamma", "beta"))
+    y, ro = fs.layernorm_residual(x, res, g, b, d["eps"])
+    g64, b64 = d["gamma"].f64(), d["beta"].f64()
+    dv = Deviation()
+    for r0, r1 in chunks(c["rows"], 2048):
+        x64, r64 = f64_rows(d["x"], r0, r1), f64_rows(d["residual"], r0, r1)
+        ref, _ = oracle.layernorm_residual(x64, r64, g64, b64, d["eps"])
+        got = host64(y[r0:r1])
+        case = f"{name} seed {seed} rows {r0}:{r1}"
+        assert_close(case, got, ref, *TOL["bf16"])
+        # fp32 statistics keep y within one bf16 rounding of exact (+ fp32 noise)
+        bf16_ulp_close(case, got, ref, ulps=1.0, atol=2e-5)
+        np.testing.assert_array_equal(host64(ro[r0:r1]), oracle.residual_store_bf16(x64, r64),
+                                      err_msg=case + " residual_out")
+        eager = host64(F.layer_norm(x[r0:r1] + res[r0:r1], (c["cols"],), g, b, d["eps"]))
+        dv.add(got, eager, ref)
+    dv.record(f"{name} seed {seed}")
+
+
+# ---- a4: GEMM epilogue on the library GEMM's own output ----------------------
+@pytest.mark.parametrize("seed", SEEDS)
+def test_gemm_epilogue_8192x8192_every_row_on_gpu_c(seed):
+    name = "gemm_epilogue_8192x8192x4096"
+    c = fd.CONFIGS[name]
+    m, n, k = c["m"], c["n"], c["k"]
+    d = fd.gemm_epilogue_inputs(seed, m, n, k)
+    announce(name, "every row", seed)
+    cmat = fs.gemm(dev(d["a"]), dev(d["b"]))
+    bias, s = dev(d["bias"]), dev(d["col_scale"])
+    o = fs.gemm_epilogue_reduce(cmat, bias, s, "sigmoid", "sum")
+    got = host64(o)
+    b64, s64 = d["bias"].f64(), d["col_scale"].f64()
+    # the measured kernel alone: the oracle on the C the GPU computed
+    ref = np.empty(m)
+    for r0, r1 in chunks(m, 1024):
+        ref[r0:r1] = oracle.gemm_epilogue_reduce(host64(cmat[r0:r1]), b64, s64, "sigmoid", "sum")
+    assert_close(f"{name} seed {seed}", got, ref, *TOL["bf16"])
+    # the contract tolerance (~82 at 4096) cannot see a kernel that ignores C
+    assert_close(f"{name} seed {seed} supplementary", got, ref, SUM_ATOL, 0.0)
+    eager = host64(torch.sigmoid((cmat + bias) * s).sum(dim=1))
+    dv = Deviation()
+    dv.add(got, eager, ref)
+    dv.record(f"{name} seed {seed}")
+    # the library call itself against the f64 product, on sampled rows
+    idx = np.unique(np.concatenate([[0, m - 1], np.random.default_rng(seed).integers(0, m, 30)]))
+    c64 = d["a"].rows(idx).f64() @ d["b"].f64()
+    assert_close(f"{name} seed {seed} library C", host64(cmat[torch.from_numpy(idx).cuda()]),
+                 c64, *TOL["bf16"])
+
+
+# ---- a5: the stitched block, every sequence and every stage -------------------
+BLOCK_STAGES = ("a", "qkv", "probs", "o", "att", "h1", "m", "u", "g", "d", "out")
+# residual adds whose exact result can be far smaller than its operands also
+# allow one bf16 rounding (2^-8 relative) of each operand
+RESIDUAL_OPERANDS = {"h1": ("x", "att"), "out": ("h1", "d")}
+# mean |delta_gpu - delta_f64| / mean |delta_f64| of a residual branch: about
+# 0.05 from bf16 rounding of the stream; a dropped branch gives 1
+BRANCH_MEAN_LIMIT = 0.2
+
+
+def _host_stage(buf, st, batch, seq):
+    """A GPU stage on the host, per sequence: probs [batch, heads, seq, seq],
+    the raw scores likewise, token-major stages [batch, seq, width]."""
+    if st in ("probs", "scores"):
+        return buf[st].transpose(0, 1).cpu()          # bf16 on the host
+    return buf[st].view(batch, seq, -1).cpu()
+
+
+def _f64(t):
+    return t.float().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_block_32x512x1024_every_sequence(seed):
+    from paper_2609_30059_amd.gate import _baseline_block_class
+
+    name = "block_32x512x1024"
+    c = fd.CONFIGS[name]
+    B, S, H, NH = c["batch"], c["seq"], c["hidden"], c["heads"]
+    d = fd.make_inputs(name, seed)
+    announce(name, "every sequence", seed)
+    params = {k: dev(d[k]) for k in fs.block.PARAM_NAMES}
+    x = dev(d["x"])
+    buf = fs.TransformerBlock(params, heads=NH, eps=d["eps"]).forward(x)
+    # the same GEMM calls with PyTorch eager sub-kernels: the unfused
+    # reference of the Gate-3 ratio
+    eager_out = _baseline_block_class()(params, heads=NH, eps=d["eps"]).forward(x)["out"]
+    eager_out = eager_out.view(B, S, H).cpu()
+    torch.cuda.synchronize()
+    # GPU-side structure: row 0 of every (head, sequence) is exactly one-hot
+    p0 = buf["probs"][:, :, 0, :].float()
+    assert torch.all(p0[..., 0] == 1.0) and torch.all(p0[..., 1:] == 0.0)
+    host = {st: _host_stage(buf, st, B, S) for st in BLOCK_STAGES + ("scores",)}
+    p64 = {k: d[k].f64() for k in fs.block.PARAM_NAMES}
+    x64_all = d["x"].f64()
+    atol, rtol = TOL["bf16"]
+    dv = Deviation()
+    branch = {"att": [0.0, 0.0], "d": [0.0, 0.0]}
+    scale = 1.0 / math.sqrt(H // NH)
+    for b in range(B):
+        case = f"{name} seed {seed} sequence {b}"
+        x64 = x64_all[b]
+        ref = oracle.block_forward_sequence(x64, p64, NH, d["eps"], keep=BLOCK_STAGES)
+        got = {st: _f64(host[st][b]) for st in host}
+        # 1. end to end: every stage against the float64 block
+        for st in BLOCK_STAGES:
+            a = atol
+            if st in RESIDUAL_OPERANDS:
+                ops = [x64 if o == "x" else ref[o] for o in RESIDUAL_OPERANDS[st]]
+                a = atol + 2.0 ** -8 * (np.abs(ops[0]) + np.abs(ops[1]))
+            assert_close(f"{case} stage {st}", got[st], ref[st], a, rtol)
+        # 2. each fused stage on the GPU's own inputs, at one bf16 rounding
+        a_ref, _ = oracle.layernorm_residual(x64, None, p64["ln1_gamma"], p64["ln1_beta"],
+                                             d["eps"])
+        bf16_ulp_close(f"{case} LN1", got["a"], a_ref, ulps=1.0, atol=2e-5)
+        pr = oracle.row_softmax(got["scores"].reshape(-1, S), None, scale, causal_q_len=S)
+        bf16_ulp_close(f"{case} causal softmax", got["probs"].reshape(-1, S), pr, ulps=1.0,
+                       atol=1e-7)
+        masked = oracle.causal_mask(NH * S, S, S)
+        pg = got["probs"].reshape(-1, S)
+        assert np.all(pg[masked] == 0.0) and not np.any(np.signbit(pg[masked])), case
+        m_ref, _ = oracle.layernorm_residual(got["att"], x64, p64["ln2_gamma"], p64["ln2_beta"],
+                                             d["eps"])
+        bf16_ulp_close(f"{case} LN2", got["m"], m_ref, ulps=1.0, atol=2e-5)
+        np.testing.assert_array_equal(got["h1"], oracle.residual_store_bf16(got["att"], x64),
+                                      err_msg=f"{case} h1")
+        g_ref = oracle.pointwise_chain(got["u"], p64["b_1"], None, 1.0, "gelu_erf")
+        bf16_ulp_close(f"{case} bias+GELU", got["g"], g_ref)
+        np.testing.assert_array_equal(got["out"], oracle.residual_store_bf16(got["d"], got["h1"]),
+                                      err_msg=f"{case} residual add")
+        # 3. the residual branches: h1 - x against att, out - h1 against d
+        for key, delta, total in (("att", got["h1"] - x64, ref["h1"]),
+                                  ("d", got["out"] - got["h1"], ref["out"])):
+            want = ref[key]
+            assert_close(f"{case} branch {key}", delta, want,
+                         atol + 2.0 ** -8 * np.abs(total), rtol)
+            branch[key][0] += float(np.abs(delta - want).sum())
+            branch[key][1] += float(np.abs(want).sum())
+        dv.add(got["out"], _f64(eager_out[b]), ref["out"])
+    for key, (err, mag) in branch.items():
+        ratio = err / mag
+        print(f"[branch] {name} seed {seed} {key}: mean |error| / mean |branch| = {ratio:.4f}",
+              flush=True)
+        assert ratio <= BRANCH_MEAN_LIMIT, f"branch {key}: {ratio:.3f}"
+    dv.record(f"{name} seed {seed}")

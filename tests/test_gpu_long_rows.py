@@ -1,10 +1,12 @@
 """GPU parity of the long-row softmax and LayerNorm/RMSNorm kernels against
 the float64 oracle: rows past the 8-wave register rungs (16384 columns), the
 16-wave rung (to 32768), the row cache in LDS and registers (to 65536) and its
-streamed tail, and the element-wise streamed kernel (widths that are not a
-whole number of 16-byte vectors); ragged tails, causal offsets, in-place
-outputs and rows whose running statistics must be rescaled from one chunk to
-the next."""
+streamed tail (columns past the cache, read twice), the row cache with
+element-wise slots (softmax widths that are not a whole number of 16-byte
+vectors) and LayerNorm's element-wise streamed kernel; ragged tails, causal
+offsets, in-place outputs, rows whose running statistics must be rescaled
+from one chunk to the next, and grids that loop over more rows than they
+hold blocks."""
 import numpy as np
 import pytest
 import torch
@@ -28,9 +30,9 @@ LONG = [16384 + 8, 20000, 32768, 32768 + 8, 49160, 50001, 65536, 65536 + 24, 100
 @pytest.mark.parametrize("dtype,mask_dtype", [("f32", "f32"), ("bf16", "bf16"), ("bf16", None),
                                               ("f32", None), ("bf16", "f32")])
 @pytest.mark.parametrize("cols", LONG)
-def test_softmax_streamed_widths(dtype, mask_dtype, cols):
+def test_softmax_long_rows_widths(dtype, mask_dtype, cols):
     d = fd.softmax_inputs(cols + 7, 3, cols, dtype, mask_dtype=mask_dtype)
-    announce("softmax streamed", cols, dtype, mask_dtype)
+    announce("softmax long rows", cols, dtype, mask_dtype)
     y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
     got = host64(y)
     m = d["mask"].f64() if mask_dtype else None
@@ -46,7 +48,7 @@ def test_softmax_streamed_widths(dtype, mask_dtype, cols):
 
 @pytest.mark.parametrize("cols", [50000, 100000])
 @pytest.mark.parametrize("order", ["rising", "falling", "spike_last"])
-def test_softmax_streamed_running_max_moves(order, cols):
+def test_softmax_long_rows_running_max_moves(order, cols):
     # the running max changes in every chunk (rising), only in the first
     # (falling), or only in the last element of the row (spike_last); 50000
     # columns are all in the row cache, 100000 have a streamed tail
@@ -57,7 +59,7 @@ def test_softmax_streamed_running_max_moves(order, cols):
         base = np.zeros(cols)
         base[-1] = 30.0
     x = np.stack([base, base * 0.5, -base]).astype(np.float32)
-    announce("softmax streamed order", order, cols)
+    announce("softmax long rows order", order, cols)
     y = host64(fs.row_softmax(torch.from_numpy(x).cuda(), None, 1.0))
     ref = oracle.row_softmax(x.astype(np.float64), None, 1.0)
     assert_close(order, y, ref, *TOL["f32"])
@@ -67,26 +69,26 @@ def test_softmax_streamed_running_max_moves(order, cols):
 @pytest.mark.parametrize("q_len,cols,rows", [(5, 40000, 11), (64, 70000, 9), (3, 16400, 7),
                                              (25000, 40000, 3), (39990, 40000, 12),
                                              (7, 40001, 9), (4, 70001, 5)])
-def test_softmax_streamed_causal(q_len, cols, rows):
+def test_softmax_long_rows_causal(q_len, cols, rows):
     # the causal limit falls near the row end, mid-row and within the first
     # chunk; 40001 and 70001 columns take element-wise loads
     d = fd.softmax_inputs(q_len * cols, rows, cols, "f32", mask_dtype="f32", p_masked=0.2)
-    announce("softmax streamed causal", q_len, cols)
+    announce("softmax long rows causal", q_len, cols)
     y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"], causal_q_len=q_len)
     ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"], causal_q_len=q_len)
     got = host64(y)
-    assert_close("streamed causal", got, ref, *TOL["f32"])
+    assert_close("long-row causal", got, ref, *TOL["f32"])
     masked = oracle.causal_mask(rows, cols, q_len)
     assert np.all(got[masked] == 0.0) and not np.any(np.signbit(got[masked]))
 
 
 @pytest.mark.parametrize("cols", [30000, 50000, 70000, 30001])
-def test_softmax_streamed_fully_masked_and_single_live(cols):
+def test_softmax_long_rows_fully_masked_and_single_live(cols):
     x = torch.randn(3, cols, device="cuda")
     m = torch.full((3, cols), float("-inf"), device="cuda")
     m[1, cols - 1] = 0.0                         # only the last element is live
     m[2, 0] = 0.0                                # only the first
-    announce("softmax streamed masked", cols)
+    announce("softmax long rows masked", cols)
     y = host64(fs.row_softmax(x, m, 1.0))
     assert np.all(y[0] == 0.0) and not np.any(np.signbit(y[0]))
     want1 = np.zeros(cols)
@@ -99,22 +101,22 @@ def test_softmax_streamed_fully_masked_and_single_live(cols):
 
 @pytest.mark.parametrize("cols,ld", [(33333, 33400), (40000, 40016), (70000, 70064)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_softmax_streamed_strided_in_place(dtype, cols, ld):
-    # offset 0 with 16-byte rows takes the row cache, offset 1 the
-    # element-wise streamed kernel
+def test_softmax_long_rows_strided_in_place(dtype, cols, ld):
+    # offset 0 with 16-byte rows takes the row cache with 16-byte slots,
+    # offset 1 (rows not on a 16-byte boundary) its element-wise slots
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     rows = 4
     d = fd.softmax_inputs(41, rows, cols, dtype, mask_dtype=dtype)
     ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
     for offset in (0, 1):
-        announce("softmax streamed guard", dtype, cols, offset)
+        announce("softmax long rows guard", dtype, cols, offset)
         xg = Guarded(rows, cols, ld, tdt, offset=offset)
         xg.view.copy_(dev(d["x"]))
         mg = Guarded(rows, cols, ld + 8, tdt, offset=offset)
         mg.view.copy_(dev(d["mask"]))
         fs.row_softmax(xg.view, mg.view, d["scale"], out=xg.view)
         torch.cuda.synchronize()
-        assert_close(f"streamed in place offset {offset}", host64(xg.view), ref, *TOL[dtype])
+        assert_close(f"row cache in place offset {offset}", host64(xg.view), ref, *TOL[dtype])
         xg.check_untouched("softmax y")
         mg.check_untouched("softmax mask")
 
@@ -276,3 +278,51 @@ def test_norm_at_maximum_width():
     y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
                                   dev(d["beta"]), d["eps"])
     check_ln("max width", d, y, ro, "bf16")
+
+
+# ---- grids that loop: more rows than the row caches launch blocks -------------
+def _cus():
+    return torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+
+
+# one 16-wave block per compute unit: 2 * cus + 3 rows give every block two or
+# three rows, so the next row's prefetch, the carried causal position and the
+# last block's partial trip all run; 40000 / 70000 take 16-byte slots (without
+# and with a streamed tail), 40001 / 70001 element-wise slots, 50257 bf16 with
+# a bf16 mask the 16-byte slots over each row's aligned body; q_len 37 does
+# not divide the grid, so the causal position advances unevenly between trips
+@pytest.mark.parametrize("dtype,mask_dtype,cols,q_len", [
+    ("bf16", "bf16", 40000, 0), ("f32", "f32", 40001, 0), ("bf16", None, 70000, 0),
+    ("f32", None, 70001, 0), ("bf16", "bf16", 50257, 0), ("f32", None, 40000, 37),
+    ("bf16", "bf16", 70001, 37), ("bf16", "bf16", 50257, 37)])
+def test_softmax_row_cache_loops_over_rows(dtype, mask_dtype, cols, q_len):
+    rows = 2 * _cus() + 3
+    d = fd.softmax_inputs(cols + q_len, rows, cols, dtype, mask_dtype=mask_dtype, p_masked=0.2)
+    announce("softmax row cache looping", rows, cols, dtype, mask_dtype, q_len)
+    y = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"], causal_q_len=q_len)
+    m = d["mask"].f64() if mask_dtype else None
+    ref = oracle.row_softmax(d["x"].f64(), m, d["scale"], causal_q_len=q_len)
+    got = host64(y)
+    assert_close(f"looping cols {cols}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"looping cols {cols}", got, ref, ulps=1.0, atol=1e-9)
+    if q_len:
+        masked = oracle.causal_mask(rows, cols, q_len)
+        assert np.all(got[masked] == 0.0) and not np.any(np.signbit(got[masked]))
+
+
+# LayerNorm's row cache: 40000 its 16-per-lane register part, 60000 the full
+# cache, 70000 a streamed tail, 40001 element-wise slots
+@pytest.mark.parametrize("rms", [False, True])
+@pytest.mark.parametrize("dtype,cols", [("bf16", 40000), ("f32", 60000), ("bf16", 70000),
+                                        ("f32", 40001)])
+def test_norm_row_cache_loops_over_rows(rms, dtype, cols):
+    rows = 2 * _cus() + 3
+    d = fd.layernorm_inputs(cols + 9, rows, cols, dtype)
+    announce("norm row cache looping", "rms" if rms else "ln", rows, cols, dtype)
+    if rms:
+        y, ro = fs.rmsnorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]), d["eps"])
+    else:
+        y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                      dev(d["beta"]), d["eps"])
+    check_ln(f"looping cols {cols}", d, y, ro, dtype, rms)

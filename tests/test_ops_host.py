@@ -34,3 +34,21 @@ def test_layouts_that_are_refused():
         as_rows(torch.empty(4, 6).t())                        # last dim not contiguous
     with pytest.raises(ValueError):
         as_rows(torch.empty(4, 6, 8)[:, :3, :])               # rows 8 apart, batches 48 apart
+
+
+def test_size_one_leading_dims_do_not_set_the_row_stride():
+    # a size-1 dim between the rows and the columns may carry any stride
+    t = torch.empty(3, 10).as_strided((3, 1, 5), (10, 999, 1))
+    assert as_rows(t) == (3, 5, 10)
+
+
+@pytest.mark.parametrize("make", [
+    lambda: torch.randn(1, 5).expand(3, 5),                   # broadcast rows (stride 0)
+    lambda: torch.empty(20).as_strided((3, 5), (2, 1)),       # overlapping rows
+    lambda: torch.empty(10)[::2],                             # 1-D with stride 2
+    lambda: torch.randn(1).expand(5),                         # 1-D broadcast
+    lambda: torch.randn(1, 3, 5).expand(2, 3, 5),             # broadcast batch
+])
+def test_broadcast_and_overlapping_views_are_refused(make):
+    with pytest.raises(ValueError):
+        as_rows(make())

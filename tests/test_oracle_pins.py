@@ -409,6 +409,30 @@ class TestBlock:
         np.testing.assert_allclose(r["out"], x + r["att"], atol=1e-14)
         np.testing.assert_array_equal(r["out"], r["h1"])
 
+    def test_sequence_selection_of_a_batch(self):
+        # block_forward(sequences=[3, 0]) stacks sequence 3, then sequence 0,
+        # each as computed alone; attention never crosses sequences, so
+        # changing sequence 1 changes nothing of them; the default is every
+        # sequence in order
+        rng = np.random.default_rng(17)
+        p = _tiny_params(rng, self.H, self.F)
+        x = rng.standard_normal((4, self.S, self.H))
+        keep = ("a", "probs", "att", "out")
+        sel = oracle.block_forward(x, p, self.NH, 1e-5, sequences=[3, 0], keep=keep)
+        for k in keep:
+            assert sel[k].shape[0] == 2
+            for i, b in enumerate((3, 0)):
+                alone = oracle.block_forward_sequence(x[b], p, self.NH, 1e-5, keep=(k,))[k]
+                np.testing.assert_array_equal(sel[k][i], alone)
+        x2 = x.copy()
+        x2[1] = rng.standard_normal((self.S, self.H)) * 3
+        sel2 = oracle.block_forward(x2, p, self.NH, 1e-5, sequences=[3, 0], keep=("out",))
+        np.testing.assert_array_equal(sel2["out"], sel["out"])
+        full = oracle.block_forward(x, p, self.NH, 1e-5)["out"]
+        assert full.shape == (4, self.S, self.H)
+        np.testing.assert_array_equal(full[[3, 0]], sel["out"])
+        assert not np.allclose(full[1], full[2])
+
 
 # ---------------------------------------------------------------------------
 # RMSNorm + residual
