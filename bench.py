@@ -66,11 +66,11 @@ KERNEL_PATTERNS = {
     "sm_8192x4096": r"softmax_kernel<unsigned short, unsigned short, true,",
     "ln_16384x4096": r"layernorm_kernel<unsigned short, true, false, 2,",
     "ep_8192x8192": r"epilogue_lds_kernel<unsigned short, unsigned short, 2,",
-    "blk_ln1": r"layernorm_kernel<unsigned short, false, false, 1,",
+    "blk_ln1": r"layernorm_wave_kernel<unsigned short, false, false, 16,",
     "blk_sm": r"softmax_kernel<unsigned short, unsigned short, false,",
-    "blk_ln2": r"layernorm_kernel<unsigned short, true, false, 1,",
+    "blk_ln2": r"layernorm_wave_kernel<unsigned short, true, false, 16,",
     "blk_gelu": r"pointwise_kernel<unsigned short, 1, false,",
-    "blk_res": r"pointwise_kernel<unsigned short, 0, true,",
+    "blk_res": r"pointwise_flat_kernel<unsigned short, 0, true,",
     "copy_1GiB": r"copy128_kernel",
 }
 KIND = {"pw_256x1024": "pw", "pw_262144x1024": "pw", "sm_8192x4096": "sm",

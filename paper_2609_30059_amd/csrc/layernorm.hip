@@ -21,6 +21,9 @@
 // FS_LN_MIN_WAVES waves per row; one-wave rows are batched to about
 // FS_LN_BATCH_ELEMS elements per lane per trip; the grid holds at most
 // FS_LN_GRID_SCALE/4 times the per-variant blocks-per-CU figure.
+#ifndef FS_LN_WAVE_PATH
+#define FS_LN_WAVE_PATH 1   // lean one-wave kernel for rows that fill a wave's slots exactly
+#endif
 #ifndef FS_LN_FULL_PATH
 #define FS_LN_FULL_PATH 1   // mask-free code for rows that fill every lane's slots
 #endif
@@ -789,9 +792,144 @@ __global__ __launch_bounds__(1024) void layernorm_cached_kernel(
 
 // rows batched per group: enough that a one-wave group handles about
 // FS_LN_BATCH_ELEMS elements per lane per trip
+// Rows that fill one wave's 16-byte slots exactly (cols == 64 * EPT, every
+// operand on 16-byte rows) with the affine parameters given: the one-wave
+// rung of layernorm_kernel without its general cases.  A short kernel (the
+// block's 64 MiB LN1) is bound by how soon its waves put their loads in
+// flight, so each wave issues its row loads first -- before gamma and beta,
+// before any other kernel argument is needed -- and the host passes 1/cols;
+// there is no masking, no staging and no LDS.  R rows per wave share one
+// shuffle sequence per statistic; rows past the end re-read the last row and
+// are not stored.  LOOP: the grid is capped and waves loop over the rows;
+// otherwise one trip covers them all.  Same arithmetic, in the same order, as
+// layernorm_kernel.
+// The arguments a wave needs before its first row loads (x, residual, rows,
+// eps, gamma, beta) fill the first 64 bytes of the argument block, so one
+// scalar-cache line serves them; the outputs' follow.
+template <typename T, bool HAS_RES, bool RMS, int EPT, int R, bool LOOP>
+__global__ __launch_bounds__(256) void layernorm_wave_kernel(
+    const T* __restrict__ x, int64_t ld_x, const T* __restrict__ res, int64_t ld_r,
+    int64_t rows, float eps, float inv_cols, const T* __restrict__ gamma,
+    const T* __restrict__ beta, T* y, int64_t ld_y, T* res_out, int64_t ld_ro) {
+  constexpr int V = Elem<T>::kVec;
+  constexpr int NV = EPT / V;
+  static_assert(EPT % V == 0, "EPT must be a multiple of the vector width");
+  const int lane = threadIdx.x % 64;
+  const int64_t wave = __builtin_amdgcn_readfirstlane(int(blockIdx.x) * 4 + int(threadIdx.x / 64));
+  const int64_t step = int64_t(gridDim.x) * 4 * R;
+  int64_t row0 = wave * R;
+  // eps is tested with rows (the host guarantees eps >= 0) so that both come
+  // in the wave's first scalar load instead of a load after the reductions
+  if (row0 >= rows || !(eps >= 0.f)) return;
+  Raw<T, V> rx[R][NV], rr[R][HAS_RES ? NV : 1], rg[NV], rb[NV];
+  auto load_rows = [&](int64_t r0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t row = r0 + r < rows ? r0 + r : rows - 1;
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        rx[r][k].load(x + row * ld_x + (k * 64 + lane) * V);
+        if constexpr (HAS_RES) rr[r][k].load(res + row * ld_r + (k * 64 + lane) * V);
+      }
+    }
+  };
+  // the first trip's rows go out before gamma and beta (loaded once, kept
+  // in registers); later trips load their rows at the end of the previous
+  // one
+  load_rows(row0);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    rg[k].template load<false>(gamma + (k * 64 + lane) * V);
+    if constexpr (!RMS) rb[k].template load<false>(beta + (k * 64 + lane) * V);
+  }
+  for (;;) {
+    float h[R][EPT];
+    Multi<SumP, R> part;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        float xv[V];
+        rx[r][k].unpack(xv);
+        if constexpr (HAS_RES) {
+          float rv[V];
+          rr[r][k].unpack(rv);
+#pragma unroll
+          for (int i = 0; i < V; ++i) xv[i] += rv[i];
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) h[r][k * V + i] = xv[i];
+      }
+      if (res_out && row0 + r < rows) {
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+          stv<T, V>(res_out + (row0 + r) * ld_ro + (k * 64 + lane) * V, h[r] + k * V);
+      }
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) sum = RMS ? fmaf(h[r][i], h[r][i], sum) : sum + h[r][i];
+      part.p[r] = SumP{sum};
+    }
+    float mean[R];
+    if constexpr (RMS) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) mean[r] = 0.f;
+    } else {
+      const Multi<SumP, R> tot = wave_allreduce(part);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        mean[r] = tot.p[r].s * inv_cols;
+        float m2 = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const float d = h[r][i] - mean[r];
+          m2 = fmaf(d, d, m2);
+        }
+        part.p[r] = SumP{m2};
+      }
+    }
+    const Multi<SumP, R> sq = wave_allreduce(part);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (row0 + r >= rows) break;
+      const float rstd = rsqrtf(sq.p[r].s * inv_cols + eps);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        float gv[V], bv[V], o[V];
+        rg[k].unpack(gv);
+        if constexpr (RMS) {
+#pragma unroll
+          for (int i = 0; i < V; ++i) bv[i] = 0.f;
+        } else {
+          rb[k].unpack(bv);
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) o[i] = fmaf((h[r][k * V + i] - mean[r]) * rstd, gv[i], bv[i]);
+        stv<T, V>(y + (row0 + r) * ld_y + (k * 64 + lane) * V, o);
+      }
+    }
+    // one trip covers every row when the grid does (straight-line code: the
+    // compiler then keeps gamma and beta packed until the outputs)
+    if constexpr (!LOOP) break;
+    row0 += step;
+    if (row0 >= rows) break;
+    load_rows(row0);
+  }
+}
+
 template <int W, int EPT>
 struct RowsPerGroup {
   static constexpr int value = (W == 1 && EPT < FS_LN_BATCH_ELEMS) ? FS_LN_BATCH_ELEMS / EPT : 1;
+};
+
+// the one-trip and the looping form of one layernorm_wave_kernel variant
+template <typename T, bool HAS_RES, bool RMS, int EPT, int R>
+struct WaveKernels {
+  decltype(&layernorm_wave_kernel<T, HAS_RES, RMS, EPT, R, false>) one =
+      layernorm_wave_kernel<T, HAS_RES, RMS, EPT, R, false>;
+  decltype(&layernorm_wave_kernel<T, HAS_RES, RMS, EPT, R, true>) loop =
+      layernorm_wave_kernel<T, HAS_RES, RMS, EPT, R, true>;
 };
 
 template <typename T, bool HAS_RES, bool RMS, bool VEC>
@@ -809,6 +947,31 @@ hipError_t dispatch(const LayerNormArgs& a, int cus, hipStream_t s) {
                        static_cast<T*>(a.res_out), a.ld_ro, a.rows, int(a.cols), a.eps);
     return hipGetLastError();
   };
+  // one-wave rows that fill every lane's slots, affine parameters given
+  if constexpr (VEC) {
+    if (FS_LN_WAVE_PATH && a.gamma != nullptr && (RMS || a.beta != nullptr) &&
+        c < FS_LN_SPLIT_COLS) {
+      auto wave = [&](auto kern, int r) {
+        const int64_t want = (a.rows + 4 * r - 1) / (4 * r);
+        const int64_t cap = int64_t(cus) * 8 * FS_LN_GRID_SCALE / 4;
+        const int grid = int(want < cap ? (want < 1 ? 1 : want) : cap);
+        hipLaunchKernelGGL(want <= cap ? kern.one : kern.loop, dim3(grid), dim3(256), 0, s,
+                           static_cast<const T*>(a.x), a.ld_x, static_cast<const T*>(a.res),
+                           a.ld_r, a.rows, a.eps, 1.f / float(a.cols),
+                           static_cast<const T*>(a.gamma), static_cast<const T*>(a.beta),
+                           static_cast<T*>(a.y), a.ld_y, static_cast<T*>(a.res_out), a.ld_ro);
+        return hipGetLastError();
+      };
+#define FS_LNW(E)                                                                        \
+  if (c == int64_t(64) * E)                                                             \
+    return wave(WaveKernels<T, HAS_RES, RMS, E, RowsPerGroup<1, E>::value>{},           \
+                RowsPerGroup<1, E>::value);
+      FS_LNW(V)
+      FS_LNW(2 * V)
+      FS_LNW(4 * V)
+#undef FS_LNW
+    }
+  }
 // Variant ladder, in order: the first rung with at least min_w waves per row
   // and a row capacity 64 * W * EPT >= cols is launched.
   const int min_w = c >= FS_LN_SPLIT_COLS ? FS_LN_MIN_WAVES : 1;

@@ -20,6 +20,15 @@
 #ifndef FS_PW_BLOCKS_PER_CU
 #define FS_PW_BLOCKS_PER_CU 16
 #endif
+#ifndef FS_PW_FLAT
+#define FS_PW_FLAT 1            // dense rows without a bias walk one flat run of vectors
+#endif
+#ifndef FS_PW_FLAT_CHUNK
+#define FS_PW_FLAT_CHUNK 4      // vectors per lane per wave chunk of the flat walk
+#endif
+#ifndef FS_PW_FLAT_BPC
+#define FS_PW_FLAT_BPC 4        // its 256-thread blocks per compute unit
+#endif
 
 namespace fs {
 namespace {
@@ -85,6 +94,60 @@ __global__ __launch_bounds__(kBlock) void pointwise_kernel(
       }
       if (r0 + u < rows) stv<T, V>(y + (r0 + u) * ld_y + c0, o);
     }
+  }
+}
+
+// Dense rows without a bias (x, residual and y all with row stride == cols):
+// the tensor is one contiguous run of n vectors, walked in chunks of 64 U
+// vectors per wave (4 KiB of bf16 or fp32 for U = 4) with a grid stride.
+// The U loads of a wave cover one contiguous span of every input, where the
+// row-slab kernel reads U rows' 1 KiB slices; a short launch (the block's
+// 96 MiB residual add) starts streaming sooner.  Vectors past the last whole
+// chunk go one per thread.  Same arithmetic as pointwise_kernel.
+template <typename T, int ACT, bool HAS_RES, int U>
+__global__ __launch_bounds__(kBlock) void pointwise_flat_kernel(const T* x, const T* res, T* y,
+                                                                int64_t n, float scale) {
+  constexpr int V = Elem<T>::kVec;
+  const int lane = threadIdx.x % 64;
+  const int64_t wave = int64_t(blockIdx.x) * (kBlock / 64) + threadIdx.x / 64;
+  const int64_t waves = int64_t(gridDim.x) * (kBlock / 64);
+  const int64_t nch = n / (64 * U);
+  auto chain = [](const Raw<T, V>& rx, const Raw<T, V>& rr, float scale, float* o) {
+    float xv[V];
+    rx.unpack(xv);
+#pragma unroll
+    for (int i = 0; i < V; ++i) o[i] = act_fn<ACT>(fmaf(xv[i], scale, 0.f));
+    if constexpr (HAS_RES) {
+      float rv[V];
+      rr.unpack(rv);
+#pragma unroll
+      for (int i = 0; i < V; ++i) o[i] += rv[i];
+    }
+  };
+  for (int64_t c = wave; c < nch; c += waves) {
+    const int64_t base = (c * 64 * U + lane) * V;
+    Raw<T, V> rx[U], rr[HAS_RES ? U : 1];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      rx[k].load(x + base + k * 64 * V);
+      if constexpr (HAS_RES) rr[k].load(res + base + k * 64 * V);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      float o[V];
+      chain(rx[k], rr[HAS_RES ? k : 0], scale, o);
+      stv<T, V>(y + base + k * 64 * V, o);
+    }
+  }
+  for (int64_t v = nch * 64 * U + int64_t(blockIdx.x) * kBlock + threadIdx.x; v < n;
+       v += int64_t(gridDim.x) * kBlock) {
+    Raw<T, V> rx, rr;
+    rx.load(x + v * V);
+    if constexpr (HAS_RES) rr.load(res + v * V);
+    float o[V];
+    chain(rx, rr, scale, o);
+    stv<T, V>(y + v * V, o);
   }
 }
 
@@ -200,6 +263,21 @@ __global__ __launch_bounds__(kBlock) void pointwise_shift_kernel(
 template <typename T, int ACT, bool HAS_RES, bool VEC>
 hipError_t dispatch(const PointwiseArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
+  if constexpr (VEC) {
+    // dense rows without a bias, large enough that every wave of the flat
+    // grid gets at least one chunk
+    constexpr int UF = FS_PW_FLAT_CHUNK;
+    const bool dense = a.rows == 1 || (a.ld_x == a.cols && a.ld_y == a.cols &&
+                                       (a.res == nullptr || a.ld_r == a.cols));
+    const int64_t n = a.rows * (a.cols / V);
+    const int64_t grid = int64_t(cus) * FS_PW_FLAT_BPC;
+    if (FS_PW_FLAT && a.bias == nullptr && dense && n / (64 * UF) >= grid * (kBlock / 64)) {
+      hipLaunchKernelGGL((pointwise_flat_kernel<T, ACT, HAS_RES, UF>), dim3(unsigned(grid)),
+                         dim3(kBlock), 0, s, static_cast<const T*>(a.x),
+                         static_cast<const T*>(a.res), static_cast<T*>(a.y), n, a.scale);
+      return hipGetLastError();
+    }
+  }
   const int64_t vecs = (a.cols + V - 1) / V;
   const int col_blocks = int((vecs + kBlock - 1) / kBlock);
   // U rows per trip; fewer when the problem is too small to fill the chip

@@ -22,14 +22,16 @@ NAMES = {
     "sm_8192x4096": "void fs::softmax_kernel<unsigned short, unsigned short, true, 2, 32, true, 1, 1>(unsigned short const*, long)",
     "ln_16384x4096": "void fs::layernorm_kernel<unsigned short, true, false, 2, 32, true, 1, 1>(unsigned short const*, long)",
     "ep_8192x8192": "void fs::epilogue_lds_kernel<unsigned short, unsigned short, 2, 16, 2, 16, true>(unsigned short const*, long)",
-    "blk_ln1": "void fs::layernorm_kernel<unsigned short, false, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
+    "blk_ln1": "void fs::layernorm_wave_kernel<unsigned short, false, false, 16, 1>(unsigned short const*, long)",
     "blk_sm": "void fs::softmax_kernel<unsigned short, unsigned short, false, 1, 8, true, 4, 2>(unsigned short const*, long)",
-    "blk_ln2": "void fs::layernorm_kernel<unsigned short, true, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
+    "blk_ln2": "void fs::layernorm_wave_kernel<unsigned short, true, false, 16, 1>(unsigned short const*, long)",
     "blk_gelu": "void fs::pointwise_kernel<unsigned short, 1, false, true, 4>(unsigned short const*, long)",
-    "blk_res": "void fs::pointwise_kernel<unsigned short, 0, true, true, 4>(unsigned short const*, long)",
+    "blk_res": "void fs::pointwise_flat_kernel<unsigned short, 0, true, 4>(unsigned short const*, long)",
     "copy_1GiB": "void fs::copy128_kernel<4>(unsigned int __vector(4) const*, unsigned int __vector(4)*, long)",
 }
 OTHERS = [
+    "void fs::layernorm_kernel<unsigned short, false, false, 1, 16, true, 4, 1>(unsigned short const*, long)",
+    "void fs::pointwise_kernel<unsigned short, 0, true, true, 4>(unsigned short const*, long)",
     "void fs::copy_strided_kernel<unsigned int __vector(4), 4>(unsigned int __vector(4) const*, long)",
     "Cijk_Ailk_Bljk_BBS_BH_Bias_HA_S_SAV_UserArgs_MT256x256x64_MI16x16x1_SN_LDSB1",
     "__amd_rocclr_copyBuffer",

@@ -252,3 +252,64 @@ def test_rmsnorm_without_residual_or_gamma():
     y, ro = fs.rmsnorm_residual(dev(d["x"]), None, None, eps)
     assert ro is None
     check_rms("plain", d, y, None, "bf16", has_res=False, affine=False, eps=eps)
+
+
+# rows that fill one wave's 16-byte slots exactly (fp32 256 / 512 / 1024,
+# bf16 512 / 1024 columns) with gamma and beta take the one-wave kernel:
+# LayerNorm and RMSNorm, with and without a residual (stored or not); row
+# counts that leave the last wave partly empty, and one large enough that the
+# grid loops
+@pytest.mark.parametrize("dtype,cols", [("f32", 256), ("f32", 512), ("f32", 1024),
+                                        ("bf16", 512), ("bf16", 1024)])
+@pytest.mark.parametrize("rms", [False, True])
+@pytest.mark.parametrize("has_res,store", [(False, False), (True, True), (True, False)])
+def test_one_wave_rows(dtype, cols, rms, has_res, store):
+    rows = 4099
+    d = fd.layernorm_inputs(cols + 31, rows, cols, dtype)
+    announce("one-wave rows", dtype, cols, rms, has_res, store)
+    r = dev(d["residual"]) if has_res else None
+    if rms:
+        y, ro = fs.rmsnorm_residual(dev(d["x"]), r, dev(d["gamma"]), d["eps"],
+                                    store_residual=store)
+        check_rms(f"rms {cols}", d, y, ro, dtype, has_res, eps=d["eps"])
+    else:
+        y, ro = fs.layernorm_residual(dev(d["x"]), r, dev(d["gamma"]), dev(d["beta"]), d["eps"],
+                                      store_residual=store)
+        check(f"ln {cols}", d, y, ro, dtype, has_res)
+    assert (ro is None) == (not (has_res and store))
+
+
+@pytest.mark.parametrize("dtype,cols,rows_per_wave", [("bf16", 512, 2), ("f32", 256, 4)])
+def test_one_wave_rows_grid_loops(dtype, cols, rows_per_wave):
+    # twice the rows that the capped grid (8 * 16 / 4 four-wave blocks per
+    # compute unit) covers in one trip: every wave loops
+    cus = torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+    rows = 2 * (cus * 8 * 16 // 4) * 4 * rows_per_wave + 5
+    d = fd.layernorm_inputs(cols + 41, rows, cols, dtype)
+    announce("one-wave rows looping", dtype, cols, rows)
+    y, ro = fs.layernorm_residual(dev(d["x"]), dev(d["residual"]), dev(d["gamma"]),
+                                  dev(d["beta"]), d["eps"])
+    check(f"looping {cols}", d, y, ro, dtype)
+
+
+def test_one_wave_rows_in_place_and_strided():
+    # y == x and residual_out == residual; then rows 16-byte aligned with a
+    # row stride above the width, guard bands around every output
+    d = fd.layernorm_inputs(77, 301, 1024, "bf16")
+    x, r = dev(d["x"]), dev(d["residual"])
+    announce("one-wave rows in place")
+    fs.layernorm_residual(x, r, dev(d["gamma"]), dev(d["beta"]), d["eps"], out=x, residual_out=r)
+    torch.cuda.synchronize()
+    check("one-wave in place", d, x, r, "bf16")
+    rows, cols, ld = 301, 1024, 1032
+    xg = Guarded(rows, cols, ld, torch.bfloat16)
+    xg.view.copy_(dev(d["x"]))
+    yg = Guarded(rows, cols, ld + 8, torch.bfloat16)
+    og = Guarded(rows, cols, ld + 16, torch.bfloat16)
+    announce("one-wave rows strided")
+    fs.layernorm_residual(xg.view, dev(d["residual"]), dev(d["gamma"]), dev(d["beta"]), d["eps"],
+                          out=yg.view, residual_out=og.view)
+    torch.cuda.synchronize()
+    check("one-wave strided", d, yg.view, og.view, "bf16")
+    yg.check_untouched("y")
+    og.check_untouched("residual_out")

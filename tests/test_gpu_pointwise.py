@@ -160,3 +160,30 @@ def test_beyond_2_31_elements():
     ref = oracle.pointwise_chain(d["x"].rows(idx % 64).f64(), d["bias"].f64(),
                                  d["residual"].rows(idx % 64).f64(), d["scale"], "gelu_erf")
     assert_close("beyond 2^31", got, ref, *TOL["bf16"])
+
+
+# dense rows without a bias walk one flat run of 16-byte vectors (large
+# tensors only): acts, scale, with and without a residual, a vector count that
+# leaves a tail past the last whole chunk, and in place
+@pytest.mark.parametrize("dtype,rows,cols", [("bf16", 16387, 1000), ("f32", 4201, 1000),
+                                             ("bf16", 2048, 8192)])
+@pytest.mark.parametrize("act", ["none", "gelu_erf", "sigmoid", "relu"])
+@pytest.mark.parametrize("residual", [True, False])
+def test_flat_dense_rows(dtype, rows, cols, act, residual):
+    d, got, ref = run_case(rows, cols, dtype, act, seed=rows + cols, bias=False, residual=residual,
+                           scale=0.8)
+    assert_close(f"flat {rows}x{cols} {dtype} {act}", got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(f"flat {rows}x{cols} {act}", got, ref)
+
+
+def test_flat_dense_rows_in_place():
+    d = fd.pointwise_inputs(91, 16385, 1024, "bf16", with_bias=False)
+    ref = oracle.pointwise_chain(d["x"].f64(), None, d["residual"].f64(), d["scale"], "none")
+    x, r = dev(d["x"]), dev(d["residual"])
+    announce("flat in place")
+    fs.pointwise_chain(x, None, r, d["scale"], "none", out=r)          # y == residual
+    assert_close("flat in place on residual", host64(r), ref, *TOL["bf16"])
+    x2, r2 = dev(d["x"]), dev(d["residual"])
+    fs.pointwise_chain(x2, None, r2, d["scale"], "none", out=x2)        # y == x
+    assert_close("flat in place on x", host64(x2), ref, *TOL["bf16"])
