@@ -197,6 +197,16 @@ def parse():
                     help="the rocprofv3 commands of the two counter runs (recorded)")
     ap.add_argument("--long-rows", action="store_true",
                     help="time long-row softmax and LayerNorm/RMSNorm and print a Markdown table")
+    ap.add_argument("--odd-rows", action="store_true",
+                    help="time rows that are not whole 16-byte vectors (the aligned-body "
+                         "variants) and print a Markdown table")
+    ap.add_argument("--report-counters", nargs="+", metavar="COUNTER_CSV",
+                    help="LDS and occupancy table from rocprofv3 --pmc counter-collection CSVs")
+    ap.add_argument("--copy-floor", action="store_true",
+                    help="time the short block kernels next to copies moving the same bytes, "
+                         "each after a read-only 1 GiB pass (run under a kernel trace)")
+    ap.add_argument("--report-floor", metavar="TRACE_CSV",
+                    help="the --copy-floor table from a rocprofv3 kernel-trace CSV")
     return ap.parse_args()
 
 
@@ -480,7 +490,56 @@ def cpu_baseline(wl: Workload, frac: float):
                       f"{'all' if frac >= 1 else f'a fraction {frac:g}'} of the rows of every "
                       f"sub-kernel of one step ({total_bytes} compulsory bytes), on host "
                       f"inputs of the same shapes from the seeded generators",
-            "per_kernel": per}
+            "cpu_model": cpu_model(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "per_kernel": per, "blas_legs": blas_legs(wl)}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def blas_legs(wl: "Workload", gemm_rows: int = 512, block_seqs: int = 2):
+    """The float64 legs that run through BLAS, each on a bounded sample, with
+    the BLAS thread count set to the process's affinity cores: the product
+    A.B of the GEMM-epilogue workload (its first rows) and the whole-block
+    oracle (its first sequences).  Each reports its time on the sample and
+    the time the whole workload would take at that rate."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    h4 = wl.host["gemm_epilogue_8192x8192x4096"]
+    m, k = h4["a"].shape
+    n = h4["b"].shape[1]
+    blk = wl.blk
+    p64 = {k_: v.float().cpu().numpy().astype(np.float64) for k_, v in blk.p.items()}
+    x64 = wl.host["block_32x512x1024"]["x"].f64()
+    out = {"threads": threads}
+    with threadpool_limits(limits=threads, user_api="blas"):
+        a = h4["a"].rows(slice(0, gemm_rows)).f64()
+        b = h4["b"].f64()
+        t0 = time.perf_counter()
+        a @ b
+        dt = time.perf_counter() - t0
+        flop = 2.0 * gemm_rows * k * n
+        out["gemm_f64"] = {"shape": [m, k, n], "rows_sampled": gemm_rows, "s": round(dt, 3),
+                           "GFLOP/s": round(flop / dt / 1e9, 1),
+                           "full_s_at_this_rate": round(dt * m / gemm_rows, 2)}
+        t0 = time.perf_counter()
+        oracle.block_forward(x64[:block_seqs], p64, blk.heads, blk.eps)
+        dt = time.perf_counter() - t0
+        out["block_forward_f64"] = {"sequences_sampled": block_seqs, "s": round(dt, 3),
+                                    "s_per_sequence": round(dt / block_seqs, 3),
+                                    "full_s_at_this_rate": round(dt * x64.shape[0] / block_seqs, 2)}
+    return out
 
 
 def load_traffic():
@@ -565,10 +624,258 @@ def long_rows(reps: int = 9) -> None:
         print(f"| {cols} | " + " | ".join(cells) + " |")
 
 
+# widths of the odd-row table: rows that are not whole 16-byte vectors, whose
+# operands share one 16-byte phase per row (contiguous tensors), so each row's
+# aligned body is read 16 bytes at a time
+ODD_ROW_WIDTHS = (1001, 4095, 16383)
+ODD_ROW_CASES = (
+    ("softmax bf16 + bf16 mask", 6),
+    ("LayerNorm + residual bf16", 8),
+    ("bias + GELU bf16", 4),
+    ("GEMM epilogue bf16 (sigmoid, row sum)", 2),
+    ("row sum bf16", 2),
+)
+
+
+def odd_rows(reps: int = 9) -> None:
+    """Median launch time of each odd-row case: 64 MiB per bf16 input, a
+    512 MiB scrub between launches, one event pair per launch."""
+    import torch
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    g = torch.Generator(device=dev)
+    results = {}
+    for cols in ODD_ROW_WIDTHS:
+        rows = (32 << 20) // cols
+        g.manual_seed(cols)
+        rn = lambda *sh: torch.randn(*sh, device=dev, generator=g)
+        x = (rn(rows, cols) * 3).to(torch.bfloat16)
+        y = torch.empty_like(x)
+        for name, bpe in ODD_ROW_CASES:
+            if name.startswith("softmax"):
+                m = torch.where(torch.rand(rows, cols, device=dev, generator=g) < 0.1,
+                                float("-inf"), 0.0).to(torch.bfloat16)
+                fn = lambda: fs.row_softmax(x, m, 0.125, out=y)
+            elif name.startswith("LayerNorm"):
+                r = rn(rows, cols).to(torch.bfloat16)
+                ro = torch.empty_like(x)
+                gam = (rn(cols) * 0.1 + 1).to(torch.bfloat16)
+                bet = (rn(cols) * 0.1).to(torch.bfloat16)
+                fn = lambda: fs.layernorm_residual(x, r, gam, bet, 1e-5, out=y, residual_out=ro)
+            elif name.startswith("bias"):
+                b = (rn(cols) * 0.02).to(torch.bfloat16)
+                fn = lambda: fs.pointwise_chain(x, b, None, 1.0, "gelu_erf", out=y)
+            elif name.startswith("GEMM"):
+                b = (torch.rand(cols, device=dev, generator=g) - 0.5).to(torch.bfloat16)
+                sc = torch.rand(cols, device=dev, generator=g) + 0.5
+                o = torch.empty(rows, dtype=torch.float32, device=dev)
+                fn = lambda: fs.gemm_epilogue_reduce(x, b, sc, "sigmoid", "sum", out=o)
+            else:
+                o = torch.empty(rows, dtype=torch.float32, device=dev)
+                fn = lambda: fs.row_reduce(x, "sum", out=o)
+            fn()
+            torch.cuda.synchronize()
+            ts = []
+            for i in range(reps):
+                scrub.fill_(i & 0xFF)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            us = sorted(ts)[reps // 2]
+            results[(cols, name)] = (us, bpe * x.numel() / us / 1e3)
+            print(f"  {cols:>6} {name:<40} {us:8.1f} us {results[(cols, name)][1]:6.0f} GB/s",
+                  file=sys.stderr, flush=True)
+    names = [c[0] for c in ODD_ROW_CASES]
+    print("| columns | " + " | ".join(names) + " |")
+    print("|---" * (len(names) + 1) + "|")
+    for cols in ODD_ROW_WIDTHS:
+        cells = [f"{results[(cols, n)][1]:.0f}" for n in names]
+        print(f"| {cols} | " + " | ".join(cells) + " |")
+
+
+def short_kernel_name(name: str) -> str:
+    """A library kernel's name without the namespace, return type and
+    parameter list (its template arguments kept)."""
+    n = name.replace("(anonymous namespace)::", "").replace("void ", "").replace("fs::", "")
+    depth = 0
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return n[:i]
+    return n
+
+
+def report_counters(paths) -> None:
+    """Per-launch averages of the LDS and occupancy counters of the library's
+    kernels, from one or more rocprofv3 --pmc counter-collection CSVs (one
+    per counter pass); launches are grouped by kernel, grid and workgroup."""
+    import csv
+    acc = {}
+    meta = {}
+    for path in paths:
+        with open(path, newline="") as f:
+            for r in csv.DictReader(f):
+                if "fs::" not in r["Kernel_Name"]:
+                    continue
+                key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size"]),
+                       int(r["Workgroup_Size"]))
+                meta[key] = (int(r["VGPR_Count"]) + int(r.get("Accum_VGPR_Count") or 0),
+                             int(r["LDS_Block_Size"]))
+                d = acc.setdefault(key, {}).setdefault(r["Counter_Name"], {})
+                d[r["Dispatch_Id"]] = float(r["Counter_Value"])
+    avg = {k: {c: sum(v.values()) / len(v) for c, v in cs.items()} for k, cs in acc.items()}
+    cols = ("OccupancyPercent", "SQ_INSTS_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT",
+            "SQ_LDS_ADDR_CONFLICT", "LDSBankConflict")
+    print("| kernel | grid x wg | VGPRs | static LDS B | waves/CU (occupancy) | LDS instr | "
+          "LDS active cyc | bank-conflict cyc | conflict / active | addr-conflict cyc | "
+          "LDSBankConflict % |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+
+    def f(v, fmt):
+        return "--" if v is None else format(v, fmt)
+    for key in sorted(avg, key=lambda k: (k[0], k[1])):
+        a = avg[key]
+        occ, ins, act, bank, addr, pct = (a.get(c) for c in cols)
+        ratio = bank / act if bank is not None and act else None
+        waves = None if occ is None else occ * 32 / 100
+        print(f"| `{key[0]}` | {key[1] // key[2]} x {key[2]} | {meta[key][0]} | {meta[key][1]} | "
+              f"{f(waves, '.1f')} ({f(occ, '.0f')} %) | {f(ins, '.0f')} | {f(act, '.0f')} | "
+              f"{f(bank, '.0f')} | {f(ratio, '.4f')} | {f(addr, '.0f')} | {f(pct, '.3f')} |")
+
+
+# --copy-floor: each short block sub-kernel next to the calibration copy moving
+# the same number of bytes (half read, half written), in this order every
+# repetition, each launch after a read-only pass over 1 GiB (HBM-cold inputs
+# and no dirty lines left in the Infinity Cache, as in the bench step)
+FLOOR_CASES = (("copy_64MiB", 64 << 20), ("blk_ln1", None), ("copy_96MiB", 96 << 20),
+               ("blk_res", None), ("copy_128MiB", 128 << 20), ("blk_ln2", None))
+FLOOR_REPS = 15
+
+
+def copy_floor(reps: int = FLOOR_REPS) -> None:
+    import torch
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    T, H = 16384, 1024
+    bf = torch.bfloat16
+    rn = lambda *sh: torch.randn(*sh, device=dev, generator=g).to(bf)
+    x, r, att = rn(T, H), rn(T, H), rn(T, H)
+    gam, bet = (rn(H) * 0.1 + 1).to(bf), (rn(H) * 0.1).to(bf)
+    a, m, h1, out = (torch.empty(T, H, dtype=bf, device=dev) for _ in range(4))
+    span = 1 << 30
+    src = torch.empty(span, dtype=torch.uint8, device=dev)
+    dst = torch.empty(span, dtype=torch.uint8, device=dev)
+    scrub = torch.zeros(8192, 65536, dtype=bf, device=dev)          # 1 GiB, read only
+    sink = torch.empty(8192, dtype=torch.float32, device=dev)
+    offs = {}
+
+    def copy(nbytes):
+        half = nbytes // 2
+        def fn():
+            o = offs.get(nbytes, 0)
+            o = 0 if o + half > span else o
+            fs.copy_(dst[o:o + half], src[o:o + half])
+            offs[nbytes] = o + half
+        return fn
+    kern = {
+        "blk_ln1": lambda: fs.layernorm_residual(x, None, gam, bet, 1e-5, out=a),
+        "blk_res": lambda: fs.pointwise_chain(x, None, r, 1.0, "none", out=out),
+        "blk_ln2": lambda: fs.layernorm_residual(att, x, gam, bet, 1e-5, out=m, residual_out=h1),
+    }
+    cases = [(name, copy(nb) if nb else kern[name]) for name, nb in FLOOR_CASES]
+    times = {name: [] for name, _ in cases}
+    for rep in range(reps + 1):            # the first repetition is a warm-up
+        for name, fn in cases:
+            fs.row_reduce(scrub, "sum", out=sink)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                times[name].append(e0.elapsed_time(e1) * 1e3)
+    print("| case | median us (events) | min us |")
+    print("|---|---|---|")
+    for name, _ in cases:
+        ts = sorted(times[name])
+        print(f"| {name} | {ts[len(ts) // 2]:.2f} | {ts[0]:.2f} |")
+
+
+def floor_bytes(label: str) -> int:
+    for name, nb in FLOOR_CASES:
+        if name == label and nb:
+            return nb
+    return STEP_BYTES[label]
+
+
+def report_floor(trace_csv: str) -> None:
+    """Median dispatch duration of every --copy-floor case from a rocprofv3
+    kernel-trace CSV: the copies and kernels are told apart by their fixed
+    order within each repetition (the read-only passes between them are
+    skipped, the warm-up repetition dropped)."""
+    import csv
+    import re
+    labels = [name for name, _ in FLOOR_CASES]
+    pats = [r"copy128_kernel" if nb else KERNEL_PATTERNS[name] for name, nb in FLOOR_CASES]
+    seq = []
+    with open(trace_csv, newline="") as f:
+        for row in csv.DictReader(f):
+            n = row["Kernel_Name"].replace("(anonymous namespace)::", "")
+            if any(re.search(p, n) for p in pats):
+                seq.append((n, (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3))
+    per = len(labels)
+    if len(seq) % per:
+        raise ValueError(f"{len(seq)} matching dispatches is not a multiple of {per}")
+    got = {l: [] for l in labels}
+    for i, (n, us) in enumerate(seq):
+        label, pat = labels[i % per], pats[i % per]
+        if not re.search(pat, n):
+            raise ValueError(f"dispatch {i}: expected {label}, got {n}")
+        if i >= per:
+            got[label].append(us)
+    med = {l: sorted(v)[len(v) // 2] for l, v in got.items()}
+    print("| case | dispatches | median us | min us | bytes | GB/s | % of 8 TB/s | vs same-size copy |")
+    print("|---|---|---|---|---|---|---|---|")
+    copy_of = {}
+    for i, (name, nb) in enumerate(FLOOR_CASES):
+        if nb:
+            copy_of[FLOOR_CASES[i + 1][0]] = name
+    for name, nb in FLOOR_CASES:
+        b = floor_bytes(name)
+        gbs = b / med[name] / 1e3
+        ratio = f"{med[name] / med[copy_of[name]]:.3f}" if name in copy_of else "--"
+        print(f"| {name} | {len(got[name])} | {med[name]:.2f} | {min(got[name]):.2f} | {b} | "
+              f"{gbs:.0f} | {100 * gbs / PEAK_HBM_GBS:.1f} | {ratio} |")
+
+
 def main():
     args = parse()
     if args.long_rows:
         long_rows()
+        return
+    if args.copy_floor:
+        copy_floor()
+        return
+    if args.odd_rows:
+        odd_rows()
+        return
+    if args.report_counters:
+        report_counters(args.report_counters)
+        return
+    if args.report_floor:
+        report_floor(args.report_floor)
         return
     if args.report_trace:
         report_trace(args.report_trace, args.all_kernels)

@@ -134,3 +134,72 @@ def test_more_than_one_gpu_exits_with_the_reason():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr and r.stdout == ""
+
+
+def _trace(path, seq):
+    with open(path, "w") as f:
+        f.write("Kernel_Name,Start_Timestamp,End_Timestamp\n")
+        t = 0
+        for name, us in seq:
+            f.write(f'"{name}",{t},{t + int(us * 1000)}\n')
+            t += int(us * 1000) + 5000
+
+
+def test_report_floor_splits_the_dispatches_by_order(tmp_path, capsys):
+    scrub = "void fs::reduce_kernel<unsigned short, 0, 8, 4, true, false>(unsigned short const*, long)"
+    copy = NAMES["copy_1GiB"]
+    order = [(copy, 12.0), (NAMES["blk_ln1"], 13.0), (copy, 17.0), (NAMES["blk_res"], 16.0),
+             (copy, 23.0), (NAMES["blk_ln2"], 23.5)]
+    seq = []
+    for rep in range(3):                        # the first repetition is the warm-up
+        for name, us in order:
+            seq.append((scrub, 100.0))
+            seq.append((name, us * 10 if rep == 0 else us + rep * 0.1))
+    p = tmp_path / "trace.csv"
+    _trace(p, seq)
+    bench.report_floor(str(p))
+    out = capsys.readouterr().out
+    rows = {l.split("|")[1].strip(): l.split("|") for l in out.splitlines()[2:]}
+    assert float(rows["blk_ln1"][3]) == pytest.approx(13.2)          # median of 13.1, 13.2
+    assert rows["blk_ln1"][8].strip() == f"{13.2 / 12.2:.3f}"         # against copy_64MiB
+    assert rows["copy_96MiB"][2].strip() == "2"
+    # a dispatch out of order is an error, not a silent relabelling
+    bad = seq[:]
+    bad[3], bad[7] = bad[7], bad[3]
+    _trace(p, bad)
+    with pytest.raises(ValueError):
+        bench.report_floor(str(p))
+
+
+def test_short_kernel_name_keeps_template_arguments():
+    n = ("void fs::(anonymous namespace)::softmax_cached_kernel<unsigned short, unsigned short, "
+         "true, false, true, 32, 32, false>(unsigned short const*, long, float)")
+    assert bench.short_kernel_name(n) == ("softmax_cached_kernel<unsigned short, unsigned short, "
+                                          "true, false, true, 32, 32, false>")
+
+
+def test_report_counters_groups_launches_and_averages(tmp_path, capsys):
+    hdr = ("Correlation_Id,Dispatch_Id,Agent_Id,Queue_Id,Process_Id,Thread_Id,Grid_Size,Kernel_Id,"
+           "Kernel_Name,Workgroup_Size,LDS_Block_Size,Scratch_Size,VGPR_Count,Accum_VGPR_Count,"
+           "SGPR_Count,Counter_Name,Counter_Value,Start_Timestamp,End_Timestamp\n")
+    k = "void fs::(anonymous namespace)::epilogue_lds_kernel<unsigned short, 2>(unsigned short const*)"
+    lds = tmp_path / "lds.csv"
+    occ = tmp_path / "occ.csv"
+    with open(lds, "w") as f:
+        f.write(hdr)
+        for d, (act, bank) in enumerate([(1000, 10), (3000, 30)]):
+            for c, v in (("SQ_LDS_IDX_ACTIVE", act), ("SQ_LDS_BANK_CONFLICT", bank)):
+                f.write(f'1,{d},1,1,1,1,262144,3,"{k}",512,0,0,28,0,32,{c},{v},0,1\n')
+        f.write(f'1,9,1,1,1,1,4096,3,"__amd_rocclr_fillBuffer",256,0,0,8,0,16,SQ_LDS_IDX_ACTIVE,5,0,1\n')
+    with open(occ, "w") as f:
+        f.write(hdr)
+        for d, v in enumerate([50.0, 100.0]):
+            f.write(f'1,{10 + d},1,1,1,1,262144,3,"{k}",512,0,0,28,0,32,OccupancyPercent,{v},0,1\n')
+    bench.report_counters([str(lds), str(occ)])
+    out = capsys.readouterr().out.splitlines()
+    rows = [l for l in out if l.startswith("| `")]
+    assert len(rows) == 1                                     # runtime kernels are skipped
+    cells = [c.strip() for c in rows[0].split("|")]
+    assert cells[2] == "512 x 512" and cells[3] == "28"
+    assert cells[5] == "24.0 (75 %)"                          # mean occupancy 75 % of 32 waves
+    assert cells[7] == "2000" and cells[8] == "20" and cells[9] == "0.0100"
