@@ -105,13 +105,17 @@ fs_status check_ld(const char* name, int64_t ld, int64_t rows, int64_t cols) {
   return FS_OK;
 }
 
+// Row strides are only bounded by the overflow guard when there are several
+// rows, so the byte products below are taken in uint64 arithmetic: exact mod
+// 16, since 2^64 is a multiple of 16.
 bool vec_ok(const void* p, int64_t ld, int es) {
-  return p == nullptr || (aligned(p, 16) && (ld * es) % 16 == 0);
+  return p == nullptr || (aligned(p, 16) && (uint64_t(ld) * uint64_t(es)) % 16 == 0);
 }
 
 // q (or NULL) starts every row at the same offset within a 16-byte unit as p
 bool same_phase(const void* p, int64_t ld, const void* q, int64_t ldq, int es) {
-  return q == nullptr || ((addr(p) - addr(q)) % 16 == 0 && ((ld - ldq) * es) % 16 == 0);
+  return q == nullptr ||
+         ((addr(p) - addr(q)) % 16 == 0 && ((uint64_t(ld) - uint64_t(ldq)) * uint64_t(es)) % 16 == 0);
 }
 
 }  // namespace
