@@ -93,6 +93,16 @@ def rho_from_distances(d_opt, d_ref, ref_scale):
 RHO_LIMIT = 10.0
 
 
+def record_diag(case, **values):
+    """Append {case, **values} to the FS_RHO_LOG file as one JSON line (when
+    set) and print it."""
+    path = os.environ.get("FS_RHO_LOG")
+    if path:
+        with open(path, "a") as f:
+            f.write(json.dumps({"case": case, **{k: float(v) for k, v in values.items()}}) + "\n")
+    print(f"[diag] {case}: {values}", flush=True)
+
+
 def record_rho(case, d_opt, d_ref, ref_scale, limit=RHO_LIMIT):
     """Check the Gate-3 ratio of one case and, when FS_RHO_LOG names a file,
     append {case, rho, d_opt, d_ref} to it as one JSON line."""
