@@ -202,6 +202,11 @@ def parse():
                          "variants) and print a Markdown table")
     ap.add_argument("--report-counters", nargs="+", metavar="COUNTER_CSV",
                     help="LDS and occupancy table from rocprofv3 --pmc counter-collection CSVs")
+    ap.add_argument("--epilogue-context", action="store_true",
+                    help="launch the GEMM epilogue in four contexts separated by pauses "
+                         "(run under a kernel trace)")
+    ap.add_argument("--report-context", metavar="TRACE_CSV",
+                    help="the --epilogue-context table from a rocprofv3 kernel-trace CSV")
     ap.add_argument("--copy-floor", action="store_true",
                     help="time the short block kernels next to copies moving the same bytes, "
                          "each after a read-only 1 GiB pass (run under a kernel trace)")
@@ -752,6 +757,74 @@ def report_counters(paths) -> None:
               f"{f(bank, '.0f')} | {f(ratio, '.4f')} | {f(addr, '.0f')} | {f(pct, '.3f')} |")
 
 
+# --epilogue-context: the GEMM epilogue (a read-only stream with a sigmoid per
+# element) launched in four contexts, each a warm-up of 3 and then CONTEXT_REPS
+# repetitions, every block of launches separated by a pause
+CONTEXTS = ("inside full bench steps", "right after the [16384, 4096] LayerNorm",
+            "after a read-only 1 GiB pass", "back to back")
+CONTEXT_REPS = 20
+CONTEXT_PAUSE_S = 0.3
+
+
+def epilogue_context(seed: int = 0) -> None:
+    import torch
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    wl = Workload(seed)
+    k = {name: fn for name, _, _, fn in wl.kernels}
+    scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")     # 1 GiB
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    ep = k["ep_8192x8192"]
+    fns = (wl.step, lambda: (k["ln_16384x4096"](), ep()),
+           lambda: (fs.row_reduce(scrub, "sum", out=sink), ep()), ep)
+    for fn in fns:
+        for n in (3, CONTEXT_REPS):
+            torch.cuda.synchronize()
+            time.sleep(CONTEXT_PAUSE_S)
+            for _ in range(n):
+                fn()
+    torch.cuda.synchronize()
+    time.sleep(CONTEXT_PAUSE_S)
+
+
+def report_context(trace_csv: str) -> None:
+    """Median epilogue dispatch time per context of --epilogue-context: the
+    trace is split at pauses (gaps above half the pause), and the last
+    2 x len(CONTEXTS) blocks holding epilogue launches are the warm-up and
+    timed blocks of each context, in order."""
+    import csv
+    import re
+    rows = []
+    with open(trace_csv, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
+                         r["Kernel_Name"].replace("(anonymous namespace)::", "")))
+    rows.sort()
+    blocks, cur, last = [], [], None
+    for s, e, n in rows:
+        if last is not None and s - last > CONTEXT_PAUSE_S * 0.5e9:
+            blocks.append(cur)
+            cur = []
+        cur.append((s, e, n))
+        last = e
+    blocks.append(cur)
+    pat = KERNEL_PATTERNS["ep_8192x8192"]
+    eps = [[(e - s) / 1e3 for s, e, n in b if re.search(pat, n)] for b in blocks]
+    eps = [v for v in eps if v]
+    need = 2 * len(CONTEXTS)
+    if len(eps) < need:
+        raise ValueError(f"{len(eps)} blocks with epilogue launches, expected at least {need}")
+    timed = eps[-need:][1::2]
+    print("| context | launches | median us | q1 us | q3 us | min us | max us | % of 8 TB/s (median) |")
+    print("|---|---|---|---|---|---|---|---|")
+    for name, v in zip(CONTEXTS, timed):
+        v = sorted(v)
+        med = v[len(v) // 2]
+        print(f"| {name} | {len(v)} | {med:.2f} | {v[len(v) // 4]:.2f} | {v[3 * len(v) // 4]:.2f} | "
+              f"{v[0]:.2f} | {v[-1]:.2f} | "
+              f"{100 * STEP_BYTES['ep_8192x8192'] / med / 1e3 / PEAK_HBM_GBS:.1f} |")
+
+
 # --copy-floor: each short block sub-kernel next to the calibration copy moving
 # the same number of bytes (half read, half written), in this order every
 # repetition, each launch after a read-only pass over 1 GiB (HBM-cold inputs
@@ -867,6 +940,12 @@ def main():
         return
     if args.copy_floor:
         copy_floor()
+        return
+    if args.epilogue_context:
+        epilogue_context(args.seed)
+        return
+    if args.report_context:
+        report_context(args.report_context)
         return
     if args.odd_rows:
         odd_rows()

@@ -203,3 +203,28 @@ def test_report_counters_groups_launches_and_averages(tmp_path, capsys):
     assert cells[2] == "512 x 512" and cells[3] == "28"
     assert cells[5] == "24.0 (75 %)"                          # mean occupancy 75 % of 32 waves
     assert cells[7] == "2000" and cells[8] == "20" and cells[9] == "0.0100"
+
+
+def test_report_context_takes_the_timed_blocks(tmp_path, capsys):
+    ep = NAMES["ep_8192x8192"]
+    other = NAMES["ln_16384x4096"]
+    pause = int(bench.CONTEXT_PAUSE_S * 1e9)
+    rows, t = [], 0
+    # setup launches first (one epilogue), then warm-up / timed blocks per context
+    blocks = [[(ep, 30.0)]]
+    for i, _ in enumerate(bench.CONTEXTS):
+        blocks.append([(ep, 99.0)] * 3)
+        blocks.append([(other, 90.0), (ep, 20.0 + i)] * 5)
+    with open(tmp_path / "t.csv", "w") as f:
+        f.write("Kernel_Name,Start_Timestamp,End_Timestamp\n")
+        for b in blocks:
+            t += pause
+            for name, us in b:
+                f.write(f'"{name}",{t},{t + int(us * 1000)}\n')
+                t += int(us * 1000) + 3000
+    bench.report_context(str(tmp_path / "t.csv"))
+    out = [l for l in capsys.readouterr().out.splitlines()[2:]]
+    assert len(out) == len(bench.CONTEXTS)
+    for i, line in enumerate(out):
+        cells = [c.strip() for c in line.split("|")]
+        assert cells[2] == "5" and float(cells[3]) == 20.0 + i
