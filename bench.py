@@ -24,9 +24,12 @@ resident and is latency-bound).
 
 Timing: the K timed steps are bracketed by two events; inside them only the
 dominant kernel (the longest, picked from the warmup steps) is bracketed, for
-`roofline.achieved`.  A HIP event costs the GPU about 3 us, so events after
-every kernel would lengthen the step by about 10 %; the per-kernel breakdown
-therefore comes from a separate pass after the timed region.
+`roofline.achieved`.  Every event is a timing-only HIP event (created with
+hipEventDisableSystemFence: recording it skips the system-scope cache
+writeback and invalidation of a default event, which costs the GPU about 3 us
+per event; a timing-only one costs about 1 us).  Events after every kernel
+would still lengthen the step by about 3 %, so the per-kernel breakdown comes
+from a separate pass after the timed region.
 
 Prints one JSON line.  Two GPU-free modes turn rocprofv3 CSV output of this
 script into the summaries under profiles/:
@@ -57,6 +60,58 @@ KERNEL_SOURCES = {
     "pw": "pointwise.hip", "sm": "softmax.hip", "ln": "layernorm.hip", "ep": "epilogue.hip",
 }
 
+
+
+_HIP = None
+
+
+class TimingEvent:
+    """A HIP event used only for timing, recorded on torch's current stream.
+
+    It is created with hipEventDisableSystemFence, so recording it performs no
+    system-scope release (no writeback and invalidation of the caches, which
+    is most of a default event's cost on the GPU).  Its timestamps are read
+    only after a device synchronisation.  The HIP runtime is the one torch
+    has loaded (looked up, never loaded anew), so streams are shared."""
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self):
+        global _HIP
+        import ctypes
+        if _HIP is None:
+            import torch  # noqa: F401  (loads the HIP runtime)
+            hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD)
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                                    ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            _HIP = hip
+        self._ctypes = ctypes
+        self.ev = ctypes.c_void_p()
+        rc = _HIP.hipEventCreateWithFlags(ctypes.byref(self.ev), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self):
+        import torch
+        rc = _HIP.hipEventRecord(self.ev, self._ctypes.c_void_p(
+            torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, end: "TimingEvent") -> float:
+        """Milliseconds from this event to ``end`` (both recorded, device synchronised)."""
+        ms = self._ctypes.c_float()
+        rc = _HIP.hipEventElapsedTime(self._ctypes.byref(ms), self.ev, end.ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        if _HIP is not None and self.ev:
+            _HIP.hipEventDestroy(self.ev)
 
 # Each bench kernel by its (demangled, anonymous-namespace-free) kernel name in
 # rocprofv3 output: the template arguments tell the launches apart.
@@ -345,7 +400,7 @@ class Workload:
         dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
         fs.copy_(dst, src)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = TimingEvent(), TimingEvent()
         e0.record()
         for _ in range(iters):
             fs.copy_(dst, src)
@@ -364,7 +419,7 @@ class Workload:
                                         out=p["y"])
         fn()
         torch.cuda.synchronize()
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        evs = [(TimingEvent(), TimingEvent())
                for _ in range(reps)]
         for a, b in evs:
             a.record()
@@ -387,7 +442,7 @@ class Workload:
         out = []
         for nbytes in sizes:
             half = (nbytes // 2 + 4095) // 4096 * 4096
-            evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            evs = [TimingEvent() for _ in range(reps + 1)]
             off = 0
             evs[0].record()
             for i in range(reps):
@@ -609,8 +664,8 @@ def long_rows(reps: int = 9) -> None:
             ts = []
             for i in range(reps):
                 scrub.fill_(i & 0xFF)
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
+                e0 = TimingEvent()
+                e1 = TimingEvent()
                 e0.record()
                 fn()
                 e1.record()
@@ -685,8 +740,8 @@ def odd_rows(reps: int = 9) -> None:
             ts = []
             for i in range(reps):
                 scrub.fill_(i & 0xFF)
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
+                e0 = TimingEvent()
+                e1 = TimingEvent()
                 e0.record()
                 fn()
                 e1.record()
@@ -872,7 +927,7 @@ def copy_floor(reps: int = FLOOR_REPS) -> None:
     for rep in range(reps + 1):            # the first repetition is a warm-up
         for name, fn in cases:
             fs.row_reduce(scrub, "sum", out=sink)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = TimingEvent(), TimingEvent()
             e0.record()
             fn()
             e1.record()
@@ -979,7 +1034,7 @@ def main():
 
     def interval_pass(steps, reduce=lambda v: sum(v) / len(v)):
         """Per-kernel intervals between events recorded after every kernel."""
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)]
+        evs = [[TimingEvent() for _ in range(nk + 1)]
                for _ in range(steps)]
         for s in range(steps):
             evs[s][0].record()
@@ -998,12 +1053,12 @@ def main():
     torch.cuda.synchronize()
 
     # timed region: exactly K steps.  Events mark its two ends and bracket the
-    # dominant kernel of every step; no other event sits between kernels (an
-    # event costs the GPU about 3 us, so one after every kernel would inflate
-    # the step by about 10 %).
-    t_beg = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    dev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    # dominant kernel of every step; no other event sits between kernels (a
+    # timing-only event still costs the GPU about 1 us, so one after every
+    # kernel would inflate the step by about 3 %).
+    t_beg = TimingEvent()
+    t_end = TimingEvent()
+    dev = [(TimingEvent(), TimingEvent())
            for _ in range(args.steps)]
     dom_fn = wl.kernels[dom][3]
     torch.cuda.synchronize()
@@ -1077,7 +1132,8 @@ def main():
                      "algorithmic_bytes": dbytes, "launch_us": round(dom_ms * 1e3, 2)},
         "per_kernel": per_kernel,
         "per_kernel_note": "intervals between events recorded after every kernel, in a pass "
-                           "after the timed region; each includes the cost of one event. "
+                           "after the timed region; each includes the cost of one timing-only event "
+                           "(about 1 us). "
                            "same_size_copy_us: the calibration copy moving the same bytes "
                            "(half read, half written), timed the same way",
         "copy_calibration_GBs": round(copy_gbs, 1),

@@ -228,3 +228,26 @@ def test_report_context_takes_the_timed_blocks(tmp_path, capsys):
     for i, line in enumerate(out):
         cells = [c.strip() for c in line.split("|")]
         assert cells[2] == "5" and float(cells[3]) == 20.0 + i
+
+
+def test_timing_events_use_the_runtime_torch_loaded():
+    """The timing-only events resolve HIP from the runtime torch has already
+    loaded (the same one that owns torch's streams), never a second copy."""
+    import ctypes
+    import torch  # noqa: F401
+    if torch.cuda.is_available():
+        ev = bench.TimingEvent()
+        assert ev.ev.value
+    else:
+        with pytest.raises(RuntimeError, match="hipEventCreateWithFlags"):
+            bench.TimingEvent()
+    addr = ctypes.cast(bench._HIP.hipEventCreateWithFlags, ctypes.c_void_p).value
+    spans = []
+    for line in open("/proc/self/maps").read().splitlines():
+        parts = line.split()
+        if len(parts) >= 6 and "libamdhip64" in parts[5]:
+            lo, hi = (int(v, 16) for v in parts[0].split("-"))
+            spans.append((lo, hi, parts[5]))
+    owners = {p for lo, hi, p in spans if lo <= addr < hi}
+    assert len({p for _, _, p in spans}) == 1, spans
+    assert len(owners) == 1
