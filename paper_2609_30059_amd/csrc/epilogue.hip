@@ -7,8 +7,11 @@
 //
 // Design (gfx950).  (C + b) * s is evaluated as C * s + b * s (one FMA per
 // element); for the sigmoid the factor -log2(e) is folded into both
-// coefficients so that sigmoid = 1 / (1 + 2^u) costs one v_exp_f32 and one
-// v_rcp_f32.  The per-column coefficients (s, b*s) are staged once per block
+// coefficients so that sigmoid = 1 / (1 + 2^u) costs one v_exp_f32, and the
+// row kernels sum four sigmoids as one fraction with a single v_rcp_f32
+// (epi_sum4): the transcendentals are quarter-rate, and inside a streaming
+// workload that keeps the clock below its peak they, not HBM, would set the
+// pace.  The per-column coefficients (s, b*s) are staged once per block
 // in LDS; then every wave reduces whole rows on its own -- no block barrier
 // in the row loop.  A wave reads its row in chunks of CH 16-byte vectors per
 // lane and software-pipelines them: the loads of the next chunk (of this row
@@ -37,6 +40,9 @@
 #ifndef FS_EPI_WPE
 #define FS_EPI_WPE 8
 #endif
+#ifndef FS_EPI_SIG4
+#define FS_EPI_SIG4 1
+#endif
 #if FS_EPI_WPE > 0
 #define FS_EPI_OCC __attribute__((amdgpu_waves_per_eu(FS_EPI_WPE, FS_EPI_WPE)))
 #else
@@ -58,6 +64,38 @@ __device__ __forceinline__ float epi_act(float u) {
     return u > 0.f ? u : 0.f;
   } else {
     return u;
+  }
+}
+
+// act over four columns, summed.  For the sigmoid, with p = 1 + 2^u:
+//   1/p0 + 1/p1 + 1/p2 + 1/p3 = n/d,  d = p0 p1 p2 p3,
+// built one factor at a time (n' = n p + d, d' = d p), so four terms take
+// one reciprocal instead of four.  u is capped at 31 so that d stays below
+// 2^125 (a capped term counts 1/(1 + 2^31) < 4.7e-10 instead of its smaller
+// exact value); the cap is a NaN-propagating minimum, so a NaN in C still
+// reaches the row's result.
+constexpr float kSigmoidCap = 31.f;
+
+template <int ACT>
+__device__ __forceinline__ float epi_sum4(const float* x, const f32x4& s4, const f32x4& b4) {
+  if constexpr (ACT == FS_ACT_SIGMOID && FS_EPI_SIG4) {
+    float p[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float u = __builtin_elementwise_minimum(fmaf(x[e], s4[e], b4[e]), kSigmoidCap);
+      p[e] = 1.f + __builtin_amdgcn_exp2f(u);
+    }
+    float n = p[0] + p[1], d = p[0] * p[1];
+    n = fmaf(n, p[2], d);
+    d *= p[2];
+    n = fmaf(n, p[3], d);
+    d *= p[3];
+    return n * __builtin_amdgcn_rcpf(d);
+  } else {
+    float t = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) t += epi_act<ACT>(fmaf(x[e], s4[e], b4[e]));
+    return t;
   }
 }
 
@@ -200,8 +238,7 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
           for (int h = 0; h < H; ++h) {
             const f32x4 s4 = sc[(kq * H + h) * 64 + li];
             const f32x4 b4 = bs[(kq * H + h) * 64 + li];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) part += epi_act<ACT>(fmaf(v[h * 4 + e], s4[e], b4[e]));
+            part += epi_sum4<ACT>(v + h * 4, s4, b4);
           }
           acc += (FULL || vi < nvec) ? part : 0.f;
         }

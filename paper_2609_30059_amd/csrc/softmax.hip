@@ -141,10 +141,16 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   int64_t row0 = (int64_t(blockIdx.x) * G + g) * R;
   const int q = int(q_len);
   const int coff = cols - q;                 // cols - q_len
+  // A power-of-two q_len (the usual sequence length) takes a mask instead of
+  // a division; the step's remainder is formed only by waves that take a
+  // second trip (with the grid of one trip per wave, none does).  The load
+  // addresses depend on the position, so this sits on every wave's path to
+  // its first load.
   int pos0 = 0, step_mod = 0;
+  const bool q_pow2 = q > 0 && (q & (q - 1)) == 0;
   if (q > 0) {
-    pos0 = int(row0 % q_len);
-    step_mod = int(step % q_len);
+    pos0 = q_pow2 ? int(row0 & (q - 1)) : int(row0 % q_len);
+    if (row0 + step < rows) step_mod = q_pow2 ? int(step & (q - 1)) : int(step % q_len);
   }
   for (; row0 < rows; row0 += step) {
     Raw<T, V> rx[R][NV];

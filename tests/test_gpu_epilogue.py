@@ -43,6 +43,67 @@ def test_sign_flip_symmetry():
     np.testing.assert_allclose(o1 + o2, 8192.0, atol=2 * SUM_ATOL)
 
 
+def _saturating_c(cols, torch_dtype):
+    """C whose sigmoid arguments reach far past the fp32 range of 2^u:
+    row 0 all -300 (every term about 0), row 1 all +300 (every term 1),
+    row 2 alternating, row 3 uniform in [-120, 120], the other rows N(0, 1)
+    with one entry in ten replaced by +-U(40, 200)."""
+    g = torch.Generator().manual_seed(11)
+    rows = 24
+    c = torch.randn(rows, cols, generator=g, dtype=torch.float64)
+    c[0] = -300.0
+    c[1] = 300.0
+    c[2] = 300.0 * (1 - 2 * (torch.arange(cols) % 2))
+    c[3] = torch.rand(cols, generator=g, dtype=torch.float64) * 240 - 120
+    big = torch.rand(rows - 4, cols, generator=g) < 0.1
+    mag = (torch.rand(rows - 4, cols, generator=g, dtype=torch.float64) * 160 + 40) * \
+        torch.where(torch.rand(rows - 4, cols, generator=g) < 0.5, -1.0, 1.0).double()
+    c[4:] = torch.where(big, mag, c[4:])
+    return c.to(torch_dtype)
+
+
+@pytest.mark.parametrize("c_dtype", ["bf16", "f32"])
+def test_sigmoid_saturated_arguments(c_dtype):
+    """Arguments whose 2^u overflows fp32 (and every size in between): the
+    four-term sum caps u at 31, which moves a term by less than 4.7e-10."""
+    cols = 4096
+    tdt = torch.bfloat16 if c_dtype == "bf16" else torch.float32
+    c = _saturating_c(cols, tdt)
+    g = torch.Generator().manual_seed(12)
+    bias = (torch.rand(cols, generator=g) - 0.5).to(tdt)
+    scale = torch.rand(cols, generator=g) + 0.5
+    announce("epilogue saturated sigmoid", c_dtype)
+    got = host64(fs.gemm_epilogue_reduce(c.cuda(), bias.cuda(), scale.cuda(), "sigmoid", "sum"))
+    with np.errstate(over="ignore"):
+        ref = oracle.gemm_epilogue_reduce(c.double().numpy(), bias.double().numpy(),
+                                          scale.double().numpy(), "sigmoid", "sum")
+    assert np.isfinite(got).all()
+    assert_close(f"saturated {c_dtype}", got, ref, SUM_ATOL * cols / 8192, 1e-6)
+    assert 0.0 <= got[0] <= cols * 5e-10
+    assert got[1] == cols
+
+
+@pytest.mark.parametrize("c_dtype", ["bf16", "f32"])
+def test_nan_and_infinities_in_c(c_dtype):
+    """A NaN in C gives its row NaN and no other; +-inf give terms 1 and 0."""
+    cols = 8192
+    d = fd.epilogue_inputs(13, 9, cols, c_dtype)
+    c = dev(d["c"])
+    c[3, 17] = float("nan")
+    c[5, 4000] = float("inf")
+    c[6, 5] = float("-inf")
+    c[7, 8191] = float("nan")
+    announce("epilogue NaN and inf in C", c_dtype)
+    got = host64(fs.gemm_epilogue_reduce(c, dev(d["bias"]), dev(d["col_scale"]), "sigmoid", "sum"))
+    with np.errstate(over="ignore", invalid="ignore"):
+        ref = oracle.gemm_epilogue_reduce(host64(c), d["bias"].f64(), d["col_scale"].f64(),
+                                          "sigmoid", "sum")
+    nan_rows = [3, 7]
+    assert np.isnan(got[nan_rows]).all() and np.isnan(ref[nan_rows]).all()
+    keep = [i for i in range(9) if i not in nan_rows]
+    assert_close(f"{c_dtype} finite rows", got[keep], ref[keep], SUM_ATOL, 0.0)
+
+
 @pytest.mark.parametrize("c_dtype,b_dtype", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
                                              ("f32", "bf16")])
 # staged rungs up to 16384 columns; rows that are not whole vectors, from two

@@ -98,6 +98,22 @@ def test_causal_attention_scores(seed):
         np.testing.assert_array_equal(got[r], one_hot)
 
 
+@pytest.mark.parametrize("q_len", [512, 64, 100, 48])
+def test_causal_rows_beyond_one_trip_per_wave(q_len):
+    """More rows than the one-wave grid covers in one trip, so waves advance
+    their causal position by the grid step (power-of-two and other q_len)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rows_per_trip = cus * 8 * 16 * 4 * 2       # grid cap x (4 waves x 2 rows) per block
+    rows, cols = 2 * rows_per_trip + 13, 64
+    d = fd.softmax_inputs(q_len, rows, cols, "bf16", mask_dtype=None)
+    announce("softmax causal looping waves", q_len, rows)
+    got = host64(fs.row_softmax(dev(d["x"]), None, d["scale"], causal_q_len=q_len))
+    ref = oracle.row_softmax(d["x"].f64(), None, d["scale"], causal_q_len=q_len)
+    assert_close(f"causal looping q_len {q_len}", got, ref, *TOL["bf16"])
+    masked = oracle.causal_mask(rows, cols, q_len)
+    softmax_supplementary(f"causal looping q_len {q_len}", got, ref, masked)
+
+
 @pytest.mark.parametrize("q_len,cols", [(3, 10), (64, 512), (100, 4096), (512, 512), (37, 1001),
                                         (64, 4095), (9, 12289)])
 def test_causal_offsets_and_widths(q_len, cols):
