@@ -6,6 +6,7 @@ produces, next to this file,
   * libfusedsub.so -- the fused sub-kernels behind the C ABI of include/fusedsub.h
   * libfsgemm.so   -- the hipBLASLt GEMM wrapper of include/fsgemm.h
   * issue_rate     -- the issue-rate calibration program of tiers.py
+  * libclockprobe.so -- the engine-clock probe of bench.py's clock-transient mode
 
 Every HIP translation unit is compiled with the packed-FP32 target feature
 switched off (ordinary fp32 code only).  Objects go to ``_build/`` (ignored
@@ -38,6 +39,7 @@ HIP_FLAGS = [
 LIB_FUSEDSUB = os.path.join(HERE, "libfusedsub.so")
 LIB_FSGEMM = os.path.join(HERE, "libfsgemm.so")
 ISSUE_RATE = os.path.join(HERE, "issue_rate")     # calibration program of tiers.py
+LIB_CLOCK_PROBE = os.path.join(HERE, "libclockprobe.so")   # bench.py --clock-transient
 
 
 def _hipcc() -> str:
@@ -82,9 +84,14 @@ def build(verbose: bool = False, jobs: int = 8) -> None:
                         verbose)
         probe = ex.submit(_run, [_hipcc(), *HIP_FLAGS, os.path.join(CSRC, "issue_rate.hip"),
                                  "-o", ISSUE_RATE + ".tmp"], verbose)
+        clock = ex.submit(_run, [_hipcc(), *HIP_FLAGS, "-shared",
+                                 os.path.join(CSRC, "clock_probe.hip"), "-o",
+                                 LIB_CLOCK_PROBE + ".tmp"], verbose)
         fut.result()
         probe.result()
+        clock.result()
     os.replace(ISSUE_RATE + ".tmp", ISSUE_RATE)
+    os.replace(LIB_CLOCK_PROBE + ".tmp", LIB_CLOCK_PROBE)
     _link(objs, LIB_FUSEDSUB, [], verbose)
     _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
           f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
@@ -104,7 +111,7 @@ def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8
 
 def clean() -> None:
     shutil.rmtree(BUILD, ignore_errors=True)
-    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE):
+    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE, LIB_CLOCK_PROBE):
         if os.path.exists(p):
             os.remove(p)
 

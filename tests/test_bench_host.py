@@ -251,3 +251,42 @@ def test_timing_events_use_the_runtime_torch_loaded():
     owners = {p for lo, hi, p in spans if lo <= addr < hi}
     assert len({p for _, _, p in spans}) == 1, spans
     assert len(owners) == 1
+
+
+def test_report_transient_pairs_steps_with_clocks(tmp_path, capsys):
+    """Warm-up steps before the first probe fold into step 0 (its last
+    launches count); each probe closes a step; the dip steps are those below
+    90 % of the median clock of the last 60 steps."""
+    order = ["pw_256x1024", "sm_8192x4096", "ln_16384x4096", "ep_8192x8192", "blk_ln1",
+             "blk_sm", "blk_ln2", "blk_gelu", "blk_res"]
+    probe = "void (anonymous namespace)::clock_probe_kernel(unsigned long long*, int, int)"
+    steps = 80
+    clocks = [1500 if 2 <= s < 12 else 2000 for s in range(steps)]
+    t = 0
+    with open(tmp_path / "t.csv", "w") as f:
+        f.write("Kernel_Name,Start_Timestamp,End_Timestamp\n")
+        for _ in range(3):                          # warm-up steps, no probe
+            for k in order:
+                f.write(f'"{NAMES[k]}",{t},{t + 99000}\n')
+                t += 100000
+        t += 500_000_000
+        for s in range(steps):
+            for k in order:
+                us = 30.0 if (k == "ep_8192x8192" and clocks[s] < 2000) else 20.0
+                f.write(f'"{NAMES[k]}",{t},{t + int(us * 1000)}\n')
+                t += int(us * 1000) + 1000
+            f.write(f'"{probe}",{t},{t + 7000}\n')
+            t += 8000
+    with open(tmp_path / "log", "w") as f:
+        for s in range(steps):
+            f.write(f"clock step {s} {clocks[s]} MHz\n")
+    tab = bench.transient_table(str(tmp_path / "t.csv"), str(tmp_path / "log"))
+    assert len(tab) == steps
+    assert tab[0][1] == 0.0 and tab[0][3]["ep_8192x8192"] == 20.0
+    assert [row[2] for row in tab] == clocks
+    bench.report_transient(str(tmp_path / "t.csv"), str(tmp_path / "log"))
+    out = capsys.readouterr().out
+    assert "sustained clock (median of the last 60 steps): 2000 MHz; 10 steps below" in out
+    ep_line = [l for l in out.splitlines() if l.startswith("| ep_8192x8192 |")][0]
+    cells = [c.strip() for c in ep_line.split("|")]
+    assert float(cells[2]) == 30.0 and float(cells[3]) == 20.0 and float(cells[4]) == 1.5
