@@ -828,13 +828,25 @@ def report_counters(paths) -> None:
 # --epilogue-context: the GEMM epilogue (a read-only stream with a sigmoid per
 # element) launched in four contexts, each a warm-up of 3 and then CONTEXT_REPS
 # repetitions, every block of launches separated by a pause
-CONTEXTS = ("inside full bench steps", "right after the [16384, 4096] LayerNorm",
-            "after a read-only 1 GiB pass", "back to back")
-CONTEXT_REPS = 20
+CONTEXT_STEPS, CONTEXT_STEP_TAIL, CONTEXT_REPS = 100, 60, 20
+# (label, measured kernel, launches after the 3 warm-up ones)
+CONTEXTS = (("inside full bench steps", "ep", CONTEXT_STEPS),
+            ("a plain row sum over the same C in its place in full bench steps", "rowsum",
+             CONTEXT_STEPS),
+            ("right after the [16384, 4096] LayerNorm", "ep", CONTEXT_REPS),
+            ("after a read-only 1 GiB pass", "ep", CONTEXT_REPS),
+            ("back to back", "ep", CONTEXT_REPS))
 CONTEXT_PAUSE_S = 0.3
+CONTEXT_PATTERNS = {"ep": KERNEL_PATTERNS["ep_8192x8192"],
+                    "rowsum": r"reduce_kernel<unsigned short,"}
+CONTEXT_BYTES = {"ep": STEP_BYTES["ep_8192x8192"], "rowsum": 8192 * 8192 * 2 + 8192 * 4}
 
 
 def epilogue_context(seed: int = 0) -> None:
+    """The GEMM epilogue on the bench's C in the contexts of CONTEXTS, each
+    block of launches after a pause (run under a kernel trace).  The second
+    context runs the bench step with a plain row sum over the same C (the
+    read-only floor of those bytes) where the epilogue would be."""
     import torch
     import paper_2609_30059_amd as fs
     torch.cuda.set_device(0)
@@ -843,10 +855,19 @@ def epilogue_context(seed: int = 0) -> None:
     scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")     # 1 GiB
     sink = torch.empty(8192, dtype=torch.float32, device="cuda")
     ep = k["ep_8192x8192"]
-    fns = (wl.step, lambda: (k["ln_16384x4096"](), ep()),
+    c = wl.ep["c"]
+
+    def step_with_rowsum():
+        for name, _, _, fn in wl.kernels:
+            if name == "ep_8192x8192":
+                fs.row_reduce(c, "sum", out=sink)
+            else:
+                fn()
+
+    fns = (wl.step, step_with_rowsum, lambda: (k["ln_16384x4096"](), ep()),
            lambda: (fs.row_reduce(scrub, "sum", out=sink), ep()), ep)
-    for fn in fns:
-        for n in (3, CONTEXT_REPS):
+    for fn, (_, _, reps) in zip(fns, CONTEXTS):
+        for n in (3, reps):
             torch.cuda.synchronize()
             time.sleep(CONTEXT_PAUSE_S)
             for _ in range(n):
@@ -856,10 +877,12 @@ def epilogue_context(seed: int = 0) -> None:
 
 
 def report_context(trace_csv: str) -> None:
-    """Median epilogue dispatch time per context of --epilogue-context: the
-    trace is split at pauses (gaps above half the pause), and the last
-    2 x len(CONTEXTS) blocks holding epilogue launches are the warm-up and
-    timed blocks of each context, in order."""
+    """Median dispatch time of each context's kernel in --epilogue-context:
+    the trace is split at pauses (gaps above half the pause); the last
+    2 x len(CONTEXTS) blocks are the warm-up and timed blocks of each
+    context, in order.  Step contexts report their last CONTEXT_STEP_TAIL
+    launches (the first milliseconds of load after a pause run at a lower
+    engine clock)."""
     import csv
     import re
     rows = []
@@ -876,21 +899,23 @@ def report_context(trace_csv: str) -> None:
         cur.append((s, e, n))
         last = e
     blocks.append(cur)
-    pat = KERNEL_PATTERNS["ep_8192x8192"]
-    eps = [[(e - s) / 1e3 for s, e, n in b if re.search(pat, n)] for b in blocks]
-    eps = [v for v in eps if v]
     need = 2 * len(CONTEXTS)
-    if len(eps) < need:
-        raise ValueError(f"{len(eps)} blocks with epilogue launches, expected at least {need}")
-    timed = eps[-need:][1::2]
-    print("| context | launches | median us | q1 us | q3 us | min us | max us | % of 8 TB/s (median) |")
-    print("|---|---|---|---|---|---|---|---|")
-    for name, v in zip(CONTEXTS, timed):
+    if len(blocks) < need:
+        raise ValueError(f"{len(blocks)} blocks in the trace, expected at least {need}")
+    timed = blocks[-need:][1::2]
+    print("| context | kernel | launches | median us | q1 us | q3 us | min us | max us | "
+          "% of 8 TB/s (median) |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for (name, kind, reps), b in zip(CONTEXTS, timed):
+        v = [(e - s) / 1e3 for s, e, n in b if re.search(CONTEXT_PATTERNS[kind], n)]
+        if reps == CONTEXT_STEPS:
+            v = v[-CONTEXT_STEP_TAIL:]
         v = sorted(v)
         med = v[len(v) // 2]
-        print(f"| {name} | {len(v)} | {med:.2f} | {v[len(v) // 4]:.2f} | {v[3 * len(v) // 4]:.2f} | "
-              f"{v[0]:.2f} | {v[-1]:.2f} | "
-              f"{100 * STEP_BYTES['ep_8192x8192'] / med / 1e3 / PEAK_HBM_GBS:.1f} |")
+        label = "epilogue" if kind == "ep" else "row sum"
+        print(f"| {name} | {label} | {len(v)} | {med:.2f} | {v[len(v) // 4]:.2f} | "
+              f"{v[3 * len(v) // 4]:.2f} | {v[0]:.2f} | {v[-1]:.2f} | "
+              f"{100 * CONTEXT_BYTES[kind] / med / 1e3 / PEAK_HBM_GBS:.1f} |")
 
 
 # --copy-floor: each short block sub-kernel next to the calibration copy moving

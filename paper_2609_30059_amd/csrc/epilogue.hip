@@ -40,6 +40,9 @@
 #ifndef FS_EPI_WPE
 #define FS_EPI_WPE 8
 #endif
+#ifndef FS_EPI_NBUF
+#define FS_EPI_NBUF 2   // chunk buffers of the staged kernel (prefetch depth + 1)
+#endif
 #ifndef FS_EPI_SIG4
 #define FS_EPI_SIG4 1
 #endif
@@ -170,11 +173,13 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
   const int64_t stride = int64_t(gridDim.x) * W;
   int64_t row = int64_t(blockIdx.x) * W + wave;
 
-  // raw chunks: CH vectors of 4 dwords each, double-buffered.  Loads are
-  // unconditional (a lane past the row end re-reads the row's last vector,
-  // FULL rows have none) so the next chunk stays in flight while the
-  // current one is evaluated.
-  u32x4 buf[2][CH];
+  // raw chunks: CH vectors of 4 dwords each, in NB buffers: while chunk j is
+  // evaluated, chunks j+1 .. j+NB-1 are in flight.  Loads are unconditional
+  // (a lane past the row end re-reads the row's last vector, FULL rows have
+  // none).  NB > 2 needs NCH % NB == 0, so that chunk j of every row sits in
+  // buffer j % NB.
+  constexpr int NB = (FS_EPI_NBUF > 2 && NCH % FS_EPI_NBUF == 0) ? FS_EPI_NBUF : 2;
+  u32x4 buf[NB][CH];
   auto load_chunk = [&](u32x4 (&dst)[CH], int64_t r, int j, auto full) {
     const CT* cr = c + r * ld_c;
 #pragma unroll
@@ -189,9 +194,11 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
   // slower with one row per wave).
   auto rot_of = [&](int64_t r) { return FS_EPI_ROTATE ? int(r & (NCH - 1)) : 0; };
   int rot = rot_of(row);
-  // the first chunk is in flight while the coefficients are staged (a wave
-  // without a row reads the last row and exits after the barrier)
-  load_chunk(buf[0], row < rows ? row : rows - 1, rot, std::false_type{});
+  // the first NB-1 chunks are in flight while the coefficients are staged (a
+  // wave without a row reads the last row and exits after the barrier)
+#pragma unroll
+  for (int i = 0; i + 1 < NB; ++i)
+    load_chunk(buf[i], row < rows ? row : rows - 1, (rot + i) & (NCH - 1), std::false_type{});
 
   // stage (s, b*s): the null checks sit outside the loop so that each body is
   // branch-free and its loads are issued together
@@ -215,23 +222,24 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
       // of loop-invariant LDS reads into registers (which would spill)
       int li = lane;
       asm volatile("" : "+v"(li));
-      // the last chunk prefetches the first chunk of the wave's next row; on
-      // its last row every wave re-reads chunk 0 of row 0 instead, which keeps
-      // the loads free of branches and costs HBM traffic once per cache (a
-      // wave's own streamed chunk is not kept in the cache: re-reading it
-      // measured 3 % more traffic)
+      // the last NB-1 chunks prefetch the first chunks of the wave's next row;
+      // on its last row every wave re-reads row 0 instead, which keeps the
+      // loads free of branches and costs HBM traffic once per cache (a wave's
+      // own streamed chunk is not kept in the cache: re-reading it measured
+      // 3 % more traffic)
       const int64_t pre_row = next < rows ? next : 0;
       const int pre_chunk = next < rows ? rot_of(next) : 0;
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        if (j + 1 < NCH) load_chunk(buf[(j + 1) & 1], row, (j + 1 + rot) & (NCH - 1), full);
-        else load_chunk(buf[(j + 1) & 1], pre_row, pre_chunk, full);
+        const int jp = j + NB - 1;                 // the chunk loaded now
+        if (jp < NCH) load_chunk(buf[jp % NB], row, (jp + rot) & (NCH - 1), full);
+        else load_chunk(buf[jp % NB], pre_row, (jp - NCH + pre_chunk) & (NCH - 1), full);
         const int pj = (j + rot) & (NCH - 1);
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
           const int vi = (pj * CH + q) * 64 + lane;
           float v[V];
-          Elem<CT>::unpack(buf[j & 1][q], v);
+          Elem<CT>::unpack(buf[j % NB][q], v);
           const int kq = pj * CH + q;
           float part = 0.f;
 #pragma unroll
@@ -248,7 +256,7 @@ __global__ __launch_bounds__(64 * W) FS_EPI_OCC void epilogue_lds_kernel(
       if (next >= rows) break;
       row = next;
       rot = rot_of(row);
-      if constexpr (NCH % 2 == 1) {
+      if constexpr (NB == 2 && NCH % 2 == 1) {
         // with an odd chunk count the next row's chunk 0 landed in buf[1]
 #pragma unroll
         for (int q = 0; q < CH; ++q) buf[0][q] = buf[1][q];

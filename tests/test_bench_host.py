@@ -207,14 +207,19 @@ def test_report_counters_groups_launches_and_averages(tmp_path, capsys):
 
 def test_report_context_takes_the_timed_blocks(tmp_path, capsys):
     ep = NAMES["ep_8192x8192"]
+    rowsum = "void fs::reduce_kernel<unsigned short, 0, 1, 16, 4, 1>(unsigned short const*, long)"
     other = NAMES["ln_16384x4096"]
     pause = int(bench.CONTEXT_PAUSE_S * 1e9)
-    rows, t = [], 0
-    # setup launches first (one epilogue), then warm-up / timed blocks per context
-    blocks = [[(ep, 30.0)]]
-    for i, _ in enumerate(bench.CONTEXTS):
-        blocks.append([(ep, 99.0)] * 3)
-        blocks.append([(other, 90.0), (ep, 20.0 + i)] * 5)
+    t = 0
+    # setup launches first, then a warm-up and a timed block per context; step
+    # contexts report only their last CONTEXT_STEP_TAIL launches
+    blocks = [[(ep, 30.0), (other, 90.0)]]
+    for i, (_, kind, reps) in enumerate(bench.CONTEXTS):
+        name = ep if kind == "ep" else rowsum
+        blocks.append([(name, 99.0)] * 3)
+        head = reps - bench.CONTEXT_STEP_TAIL if reps == bench.CONTEXT_STEPS else 0
+        blocks.append([(other, 90.0), (name, 50.0)] * head
+                      + [(other, 90.0), (name, 20.0 + i)] * (reps - head))
     with open(tmp_path / "t.csv", "w") as f:
         f.write("Kernel_Name,Start_Timestamp,End_Timestamp\n")
         for b in blocks:
@@ -225,9 +230,11 @@ def test_report_context_takes_the_timed_blocks(tmp_path, capsys):
     bench.report_context(str(tmp_path / "t.csv"))
     out = [l for l in capsys.readouterr().out.splitlines()[2:]]
     assert len(out) == len(bench.CONTEXTS)
-    for i, line in enumerate(out):
+    for i, (line, (_, kind, reps)) in enumerate(zip(out, bench.CONTEXTS)):
         cells = [c.strip() for c in line.split("|")]
-        assert cells[2] == "5" and float(cells[3]) == 20.0 + i
+        n = bench.CONTEXT_STEP_TAIL if reps == bench.CONTEXT_STEPS else reps
+        assert cells[2] == ("epilogue" if kind == "ep" else "row sum")
+        assert cells[3] == str(n) and float(cells[4]) == 20.0 + i
 
 
 def test_timing_events_use_the_runtime_torch_loaded():
