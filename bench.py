@@ -58,6 +58,8 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+from paper_2609_30059_amd.timing import TimingEvent  # noqa: E402
+
 PEAK_HBM_GBS = 8000.0
 SETTLE_MS = 25.0       # back-to-back steps before the warmup (do_bench-style warm-up)
 METRIC = "achieved HBM GB/s and % of MI355X peak per fused sub-kernel; oracle match"
@@ -67,57 +69,6 @@ KERNEL_SOURCES = {
 }
 
 
-
-_HIP = None
-
-
-class TimingEvent:
-    """A HIP event used only for timing, recorded on torch's current stream.
-
-    It is created with hipEventDisableSystemFence, so recording it performs no
-    system-scope release (no writeback and invalidation of the caches, which
-    is most of a default event's cost on the GPU).  Its timestamps are read
-    only after a device synchronisation.  The HIP runtime is the one torch
-    has loaded (looked up, never loaded anew), so streams are shared."""
-    DISABLE_SYSTEM_FENCE = 0x20000000
-
-    def __init__(self):
-        global _HIP
-        import ctypes
-        if _HIP is None:
-            import torch  # noqa: F401  (loads the HIP runtime)
-            hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD)
-            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p),
-                                                    ctypes.c_uint]
-            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
-                                                ctypes.c_void_p, ctypes.c_void_p]
-            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
-            _HIP = hip
-        self._ctypes = ctypes
-        self.ev = ctypes.c_void_p()
-        rc = _HIP.hipEventCreateWithFlags(ctypes.byref(self.ev), self.DISABLE_SYSTEM_FENCE)
-        if rc != 0:
-            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
-
-    def record(self):
-        import torch
-        rc = _HIP.hipEventRecord(self.ev, self._ctypes.c_void_p(
-            torch.cuda.current_stream().cuda_stream))
-        if rc != 0:
-            raise RuntimeError(f"hipEventRecord failed ({rc})")
-
-    def elapsed_time(self, end: "TimingEvent") -> float:
-        """Milliseconds from this event to ``end`` (both recorded, device synchronised)."""
-        ms = self._ctypes.c_float()
-        rc = _HIP.hipEventElapsedTime(self._ctypes.byref(ms), self.ev, end.ev)
-        if rc != 0:
-            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
-        return ms.value
-
-    def __del__(self):
-        if _HIP is not None and self.ev:
-            _HIP.hipEventDestroy(self.ev)
 
 # Each bench kernel by its (demangled, anonymous-namespace-free) kernel name in
 # rocprofv3 output: the template arguments tell the launches apart.

@@ -31,6 +31,8 @@ import subprocess
 import sys
 from typing import Callable, Dict, Optional
 
+from .timing import TimingEvent
+
 GAMMA = 1.03
 
 VARIANTS = ("fused", "eager_subkernels", "eager", "compiled")
@@ -68,7 +70,7 @@ def do_bench(fn: Callable[[], object], warmup_ms: float = 25.0, rep_ms: float = 
     fn()
     torch.cuda.synchronize()
     flush = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda") if flush_bytes else None
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = TimingEvent(), TimingEvent()
     e0.record()
     for _ in range(5):
         fn()
@@ -77,8 +79,8 @@ def do_bench(fn: Callable[[], object], warmup_ms: float = 25.0, rep_ms: float = 
     n_warm, n_rep = bench_plan(e0.elapsed_time(e1) / 5, warmup_ms, rep_ms)
     for _ in range(n_warm):
         fn()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_rep)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(n_rep)]
+    starts = [TimingEvent() for _ in range(n_rep)]
+    ends = [TimingEvent() for _ in range(n_rep)]
     for i in range(n_rep):
         if flush is not None:
             flush.zero_()

@@ -39,13 +39,14 @@ from typing import Dict
 from . import ops
 from .block import TransformerBlock
 from .gate import do_bench
+from .timing import TimingEvent
 
 LLC_FLUSH_BYTES = 512 << 20
 
 
 def _events(n):
     import torch
-    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    return [TimingEvent() for _ in range(n)]
 
 
 def time_pair(first, second, reps: int = 30, flush: bool = True) -> Dict[str, float]:

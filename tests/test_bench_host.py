@@ -242,13 +242,14 @@ def test_timing_events_use_the_runtime_torch_loaded():
     loaded (the same one that owns torch's streams), never a second copy."""
     import ctypes
     import torch  # noqa: F401
+    from paper_2609_30059_amd import timing
     if torch.cuda.is_available():
         ev = bench.TimingEvent()
         assert ev.ev.value
     else:
         with pytest.raises(RuntimeError, match="hipEventCreateWithFlags"):
             bench.TimingEvent()
-    addr = ctypes.cast(bench._HIP.hipEventCreateWithFlags, ctypes.c_void_p).value
+    addr = ctypes.cast(timing._HIP.hipEventCreateWithFlags, ctypes.c_void_p).value
     spans = []
     for line in open("/proc/self/maps").read().splitlines():
         parts = line.split()
