@@ -298,3 +298,26 @@ def test_report_transient_pairs_steps_with_clocks(tmp_path, capsys):
     ep_line = [l for l in out.splitlines() if l.startswith("| ep_8192x8192 |")][0]
     cells = [c.strip() for c in ep_line.split("|")]
     assert float(cells[2]) == 30.0 and float(cells[3]) == 20.0 and float(cells[4]) == 1.5
+
+
+def test_clock_probe_refuses_bad_arguments_before_any_launch():
+    """The engine-clock probe checks its arguments on the host and launches
+    nothing for a null buffer, a slot out of range, an empty grid or a
+    negative trip count (the pointer below is never dereferenced)."""
+    import ctypes
+    import subprocess
+    from paper_2609_30059_amd import build as B
+    lib = ctypes.CDLL(B.LIB_CLOCK_PROBE)
+    f = lib.fsx_clock_probe
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                  ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    fake = ctypes.c_void_p(64)
+    assert f(None, 0, 1, 1, 1, None) == -1
+    assert f(fake, -1, 4, 1, 1, None) == -1
+    assert f(fake, 4, 4, 1, 1, None) == -1
+    assert f(fake, 0, 4, 0, 1, None) == -1
+    assert f(fake, 0, 4, 1, -1, None) == -1
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_CLOCK_PROBE], capture_output=True,
+                         text=True).stdout
+    assert {l.split()[-1] for l in out.splitlines() if " T " in l} == {"fsx_clock_probe"}
