@@ -44,6 +44,9 @@
 #ifndef FS_SM_CACHE_GROUP_WORDS
 #define FS_SM_CACHE_GROUP_WORDS 8   // raw load registers per slot group of the row cache
 #endif
+#ifndef FS_SM_ONE_TRIP_MIN_W
+#define FS_SM_ONE_TRIP_MIN_W 2   // vector rungs of at least this many waves per row have a one-trip form
+#endif
 #ifndef FS_SM_GRID_SCALE
 #define FS_SM_GRID_SCALE 64
 #endif
@@ -105,11 +108,16 @@ __device__ __forceinline__ void store_until(T* row, int c0, int end, const float
 // in) to its last; the head and tail (at most V-1 columns each) are one
 // extra element for each of the group's first lanes: lanes below h take
 // the head, the next ones the tail.
+// LOOP: groups walk the rows with a grid stride; without it every group
+// takes one trip (the host launches that form when the grid covers the
+// rows), as straight-line code with nothing computed for later trips.
+// The arguments a wave needs before its first loads (x, the mask, rows,
+// q_len, cols) fill the first 64 bytes of the argument block.
 template <typename T, typename MT, bool HAS_MASK, int W, int EPT, bool VEC, bool SHIFT, int G,
-          int R>
+          int R, bool LOOP>
 __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
     const T* __restrict__ x, int64_t ld_x, const MT* __restrict__ mask, int64_t ld_m,
-    T* y, int64_t ld_y, int64_t rows, int cols, float scale, int64_t q_len, int trim_shift) {
+    int64_t rows, int64_t q_len, int cols, int trim_shift, float scale, T* y, int64_t ld_y) {
   constexpr int kThreads = 64 * W;
   constexpr int V = VEC || SHIFT ? Elem<T>::kVec : 1;
   constexpr int NV = EPT / V;                       // vectors per thread
@@ -150,7 +158,9 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
   const bool q_pow2 = q > 0 && (q & (q - 1)) == 0;
   if (q > 0) {
     pos0 = q_pow2 ? int(row0 & (q - 1)) : int(row0 % q_len);
-    if (row0 + step < rows) step_mod = q_pow2 ? int(step & (q - 1)) : int(step % q_len);
+    if constexpr (LOOP) {
+      if (row0 + step < rows) step_mod = q_pow2 ? int(step & (q - 1)) : int(step % q_len);
+    }
   }
   for (; row0 < rows; row0 += step) {
     Raw<T, V> rx[R][NV];
@@ -208,7 +218,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         if constexpr (HAS_MASK) em[r] = mr[ce];
       }
     }
-    if (q > 0) {
+    if (LOOP && q > 0) {
       pos0 += step_mod;
       if (pos0 >= q) pos0 -= q;
     }
@@ -353,6 +363,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         }
       }
     }
+    if constexpr (!LOOP) break;
   }
 }
 
@@ -649,16 +660,22 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
   // smallest capacity >= cols; the vector path needs EPT >= V
   const int64_t c = a.cols;
-  auto launch = [&](auto kern, int threads, int rows_per_block, int blocks_per_cu) {
+  // kern_loop walks rows with a grid stride; kern_one (same arithmetic, one
+  // trip per row group) is launched when the grid holds every row group
+  auto launch = [&](auto kern_loop, auto kern_one, int threads, int rows_per_block,
+                    int blocks_per_cu) {
     int64_t want = (a.rows + rows_per_block - 1) / rows_per_block;
     int64_t cap = int64_t(cus) * blocks_per_cu * FS_SM_GRID_SCALE / 4;
     int grid = int(want < cap ? want : cap);
     if (grid < 1) grid = 1;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s,
-                       static_cast<const T*>(a.x), a.ld_x, static_cast<const MT*>(a.mask),
-                       a.ld_mask, static_cast<T*>(a.y), a.ld_y, a.rows, int(a.cols),
-                       a.scale, a.causal_q_len, a.trim_shift);
-    return hipGetLastError();
+    auto go = [&](auto kern) {
+      hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), 0, s, static_cast<const T*>(a.x),
+                         a.ld_x, static_cast<const MT*>(a.mask), a.ld_mask, a.rows,
+                         a.causal_q_len, int(a.cols), a.trim_shift, a.scale,
+                         static_cast<T*>(a.y), a.ld_y);
+      return hipGetLastError();
+    };
+    return want <= cap ? go(kern_one) : go(kern_loop);
   };
   // Variant ladder, in order: the first rung with at least min_w waves per row
   // and a row capacity 64 * W * EPT >= cols is launched.
@@ -672,7 +689,8 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
       constexpr int VS = Elem<T>::kVec;
 #define FS_SMS(Wv, E, Gv, BPC)                                                                  \
   if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E)                                      \
-    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, false, true, Gv, RowsPerGroup<Wv, E>::value>, \
+    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, false, true, Gv, RowsPerGroup<Wv, E>::value, true>, \
+                  softmax_kernel<T, MT, HAS_MASK, Wv, E, false, true, Gv, RowsPerGroup<Wv, E>::value, true>, \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
       if constexpr (VS <= 4) { FS_SMS(1, 4, 4, 8) }
       FS_SMS(1, 8, 4, 8)
@@ -695,7 +713,9 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
 #define FS_SM(Wv, E, Gv, BPC)                                                       \
   if (small_q && Wv >= min_w && c <= int64_t(64) * Wv * E &&                     \
       (VEC || c <= (a.shifted ? FS_SM_SHIFT_REG_COLS : FS_SM_ELEMENTWISE_REG_COLS)))  \
-    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, false, Gv, RowsPerGroup<Wv, E>::value>, \
+    return launch(softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, false, Gv, RowsPerGroup<Wv, E>::value, true>, \
+                  softmax_kernel<T, MT, HAS_MASK, Wv, E, VEC, false, Gv, RowsPerGroup<Wv, E>::value,  \
+                                 !VEC || Wv < FS_SM_ONE_TRIP_MIN_W>,                                   \
                   64 * Wv * Gv, Gv * RowsPerGroup<Wv, E>::value, BPC);
   if constexpr (V <= 1) { FS_SM(1, 1, 4, 8) }
   if constexpr (V <= 2) { FS_SM(1, 2, 4, 8) }
