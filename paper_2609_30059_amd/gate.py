@@ -13,10 +13,11 @@ leaks from one into the next.
 
 Here M(k0) is the same pre-LN block with the same hipBLASLt GEMM calls but
 its five sub-kernels computed by PyTorch eager operators (the unfused
-baseline), and M(k0 -> k) is the block with the libfusedsub kernels.  Two
-more models are timed for context only: the whole block written in plain
-PyTorch eager (its GEMMs included), and that eager block under
-torch.compile.
+baseline), and M(k0 -> k) is the block with the libfusedsub kernels.  Three
+more models are timed for context only: the fused block captured once as a
+HIP graph and replayed (the same launches without per-launch host work), the
+whole block written in plain PyTorch eager (its GEMMs included), and that
+eager block under torch.compile.
 
 Run ``python -m paper_2609_30059_amd.gate`` for the JSON report.
 """
@@ -35,7 +36,7 @@ from .timing import TimingEvent
 
 GAMMA = 1.03
 
-VARIANTS = ("fused", "eager_subkernels", "eager", "compiled")
+VARIANTS = ("fused", "fused_graph", "eager_subkernels", "eager", "compiled")
 
 
 def perf_gate(tau_candidate: float, tau_baseline: float, gamma: float = GAMMA) -> bool:
@@ -188,12 +189,14 @@ def measure(variant: str, seed: int = 0, warmup_ms: float = 25.0, rep_ms: float 
     if variant not in VARIANTS:
         raise ValueError(f"variant must be one of {VARIANTS}")
     params, x, heads, eps = _device_inputs(seed, dims)
-    if variant in ("fused", "eager_subkernels"):
-        cls = TransformerBlock if variant == "fused" else _baseline_block_class()
+    if variant in ("fused", "fused_graph", "eager_subkernels"):
+        cls = _baseline_block_class() if variant == "eager_subkernels" else TransformerBlock
         blk = cls(params, heads=heads, eps=eps)
         buf = blk.alloc(*x.shape[:2], x.device)
         fn = lambda: blk.forward(x, buf)              # noqa: E731
         get = lambda: buf["out"]                      # noqa: E731
+        if variant == "fused_graph":
+            fn = _captured(fn)
     else:
         f = eager_block if variant == "eager" else torch.compile(eager_block)
         res = {}
@@ -204,6 +207,23 @@ def measure(variant: str, seed: int = 0, warmup_ms: float = 25.0, rep_ms: float 
     t.update(variant=variant, out_abs_mean=float(out.abs().mean()),
              out_finite=bool(torch.isfinite(out).all()))
     return t
+
+
+def _captured(fn: Callable[[], object]) -> Callable[[], object]:
+    """fn captured once as a HIP graph (after a warm-up call on a side stream
+    that creates the GEMM plans and loads every kernel); returns its replay."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g.replay
 
 
 def run_isolated(variant: str, seed: int, warmup_ms: float, rep_ms: float,
@@ -229,6 +249,8 @@ def report(results: Dict[str, Dict[str, object]], gamma: float = GAMMA) -> Dict[
     for ctx in ("eager", "compiled"):
         if ctx in results:
             out[f"speedup_vs_{ctx}"] = results[ctx]["median_ms"] / tf
+    if "fused_graph" in results:
+        out["graph_replay_speedup"] = tf / results["fused_graph"]["median_ms"]
     return out
 
 
@@ -244,7 +266,8 @@ def main(argv=None) -> int:
     if a.variant:
         print(json.dumps(measure(a.variant, a.seed, a.warmup_ms, a.rep_ms)), flush=True)
         return 0
-    variants = ["fused", "eager_subkernels", "eager"] + (["compiled"] if a.compile else [])
+    variants = (["fused", "fused_graph", "eager_subkernels", "eager"]
+                + (["compiled"] if a.compile else []))
     results = {}
     for v in variants:
         results[v] = run_isolated(v, a.seed, a.warmup_ms, a.rep_ms)

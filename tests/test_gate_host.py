@@ -45,6 +45,12 @@ def test_report_uses_the_baseline_model():
     assert math.isclose(r["speedup_vs_eager"], 2.0)
     r = gate.report({"fused": {"median_ms": 3.2}, "eager_subkernels": {"median_ms": 3.0}})
     assert not r["pass"]
+    assert "graph_replay_speedup" not in r
+    # the graph replay is context: it never enters the verdict
+    r = gate.report({"fused": {"median_ms": 2.0}, "fused_graph": {"median_ms": 1.6},
+                     "eager_subkernels": {"median_ms": 2.1}})
+    assert r["pass"] and math.isclose(r["speedup"], 1.05)
+    assert math.isclose(r["graph_replay_speedup"], 1.25)
 
 
 @pytest.mark.parametrize("seed", [0, 1])

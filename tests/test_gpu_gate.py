@@ -45,11 +45,13 @@ def test_baseline_models_match_oracle(seed):
 def test_fused_block_passes_the_gate_at_full_shape():
     announce("gate full shape")
     t = {v: gate.measure(v, seed=0, warmup_ms=10.0, rep_ms=60.0)
-         for v in ("fused", "eager_subkernels")}
+         for v in ("fused", "fused_graph", "eager_subkernels")}
     for v in t.values():
         assert v["out_finite"]
     # the two models compute the same block: their outputs agree in mean size
     assert abs(t["fused"]["out_abs_mean"] / t["eager_subkernels"]["out_abs_mean"] - 1) < 1e-2
+    # the graph replays the fused block's own launches: the same output
+    assert t["fused_graph"]["out_abs_mean"] == t["fused"]["out_abs_mean"]
     r = gate.report(t)
     print("gate", r, flush=True)
     assert r["pass"], r

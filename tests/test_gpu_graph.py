@@ -1,0 +1,196 @@
+"""HIP graph capture of the sub-kernels and of the stitched block.
+
+Every libfusedsub entry point only validates on the host and enqueues kernels
+(no allocation, memset or synchronisation), so a compiled graph's sub-kernels
+can be captured once and replayed; the block adds the hipBLASLt calls of the
+fixed library part (Def. 1) with plans cached and the workspace allocated
+before capture.  Each graph is replayed several times with eager work and
+host synchronisations between the replays, and every replay is compared with
+the eager result of the same calls: bit for bit, because the same kernels
+run on the same inputs.  A replay after the captured input buffers are
+refilled must match an eager run on the new values (the graph reads the live
+buffers, not a snapshot).
+"""
+import math
+
+import pytest
+import torch
+
+import paper_2609_30059_amd as fs
+from gpu_util import announce
+
+pytestmark = pytest.mark.gpu
+
+BF = torch.bfloat16
+
+
+def bits(t: torch.Tensor) -> torch.Tensor:
+    """Raw storage as integers, so NaN payloads and signed zeros compare too."""
+    if t.dtype == BF:
+        return t.view(torch.int16)
+    if t.dtype == torch.float32:
+        return t.view(torch.int32)
+    return t
+
+
+def poison(t: torch.Tensor) -> None:
+    if t.dtype in (BF, torch.float32):
+        t.fill_(float("nan"))
+    else:
+        t.fill_(-7)
+
+
+def eager_noise(dev) -> None:
+    """Unrelated eager work between replays (a GEMM and a reduction)."""
+    a = torch.randn(512, 512, device=dev)
+    (a @ a).sum().item()
+
+
+def replay_and_check(graph, step, outs, refill=None, replays=3):
+    """Replay `graph` `replays` times against the eager results of `step`;
+    then refill the inputs, run `step` eagerly for new references and replay
+    once more."""
+    dev = outs[0].device
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    for rep in range(replays):
+        for o in outs:
+            poison(o)
+        eager_noise(dev)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (o, r) in enumerate(zip(outs, ref)):
+            assert torch.equal(bits(o), bits(r)), f"replay {rep}: output {i} differs from eager"
+    if refill is None:
+        return
+    refill()
+    step()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    for o in outs:
+        poison(o)
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    for i, (o, r) in enumerate(zip(outs, ref)):
+        assert torch.equal(bits(o), bits(r)), f"replay after refill: output {i} differs"
+
+
+def capture(step):
+    """Warm up on a side stream (plans, cached device properties, code
+    objects), then capture one call of `step`."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    return g
+
+
+def test_subkernels_captured_in_one_graph():
+    announce("graph: every sub-kernel entry point")
+    dev = "cuda"
+    gen = torch.Generator(device=dev).manual_seed(0)
+
+    def rnd(*shape, dtype=torch.float32, s=1.0):
+        return (s * torch.randn(*shape, device=dev, generator=gen)).to(dtype)
+
+    # pointwise fp32 [300, 1000] with bias and residual; bf16 bias + GELU [640, 4096]
+    xp, bp, rp = rnd(300, 1000), rnd(1000, s=0.3), rnd(300, 1000)
+    xg, bg = rnd(640, 4096, dtype=BF), rnd(4096, dtype=BF, s=0.02)
+    # masked softmax bf16 [257, 4096] (column 0 never masked) and causal [2, 4, 512, 512]
+    xs = rnd(257, 4096, dtype=BF, s=3.0)
+    ms = torch.where(torch.rand(257, 4096, device=dev, generator=gen) < 0.1,
+                     float("-inf"), 0.0).to(BF)
+    ms[:, 0] = 0
+    sc = rnd(2, 4, 512, 512, dtype=BF)
+    # LayerNorm + residual [333, 4096]; one-wave LayerNorm [640, 1024]; RMSNorm [100, 2048]
+    xl, rl = rnd(333, 4096, dtype=BF), rnd(333, 4096, dtype=BF)
+    gl, bl = (1 + rnd(4096, s=0.1)).to(BF), rnd(4096, dtype=BF, s=0.1)
+    x1 = rnd(640, 1024, dtype=BF)
+    g1, b1 = (1 + rnd(1024, s=0.1)).to(BF), rnd(1024, dtype=BF, s=0.1)
+    xr, rr, gr = rnd(100, 2048, dtype=BF), rnd(100, 2048, dtype=BF), (1 + rnd(2048, s=0.1)).to(BF)
+    # epilogue on C bf16 [300, 8192]; row reductions fp32 [77, 5000]
+    ce = rnd(300, 8192, dtype=BF)
+    be, se = rnd(8192, dtype=BF, s=0.3), 0.5 + torch.rand(8192, device=dev, generator=gen)
+    xq = rnd(77, 5000)
+    # head split of a [96, 3 * 4 * 64] projection
+    qkv = rnd(96, 768, dtype=BF)
+
+    outs = {
+        "pw": torch.empty_like(xp), "gelu": torch.empty_like(xg), "sm": torch.empty_like(xs),
+        "causal": torch.empty_like(sc), "ln": torch.empty_like(xl), "ln_h": torch.empty_like(xl),
+        "ln1": torch.empty_like(x1), "rms": torch.empty_like(xr), "rms_h": torch.empty_like(xr),
+        "ep": torch.empty(300, device=dev), "sum": torch.empty(77, device=dev),
+        "max": torch.empty(77, device=dev),
+        "arg": torch.empty(77, dtype=torch.int64, device=dev),
+        "heads": torch.empty(12, 96, 64, dtype=BF, device=dev),
+    }
+
+    def step():
+        fs.pointwise_chain(xp, bp, rp, 0.7, "gelu_erf", out=outs["pw"])
+        fs.pointwise_chain(xg, bg, None, 1.0, "gelu_erf", out=outs["gelu"])
+        fs.row_softmax(xs, ms, 0.125, out=outs["sm"])
+        fs.row_softmax(sc, None, 0.125, causal_q_len=512, out=outs["causal"])
+        fs.layernorm_residual(xl, rl, gl, bl, 1e-5, out=outs["ln"], residual_out=outs["ln_h"])
+        fs.layernorm_residual(x1, None, g1, b1, 1e-5, out=outs["ln1"])
+        fs.rmsnorm_residual(xr, rr, gr, 1e-6, out=outs["rms"], residual_out=outs["rms_h"])
+        fs.gemm_epilogue_reduce(ce, be, se, "sigmoid", "sum", out=outs["ep"])
+        fs.row_reduce(xq, "sum", out=outs["sum"])
+        fs.row_reduce(xq, "max", out=outs["max"])
+        fs.row_argmax(xq, out=outs["arg"])
+        fs.copy_strided(outs["heads"], qkv, rows=96, cols=64, batch=12, ld_src=768,
+                        stride_src=64, ld_dst=64, stride_dst=96 * 64)
+
+    g = capture(step)
+
+    def refill():
+        for t, s in ((xp, 1.0), (xs, 3.0), (xl, 1.0), (ce, 1.0), (xq, 1.0), (qkv, 1.0),
+                     (sc, 1.0)):
+            t.copy_((s * torch.randn(t.shape, device=dev, generator=gen)).to(t.dtype))
+
+    replay_and_check(g, step, list(outs.values()), refill=refill)
+
+
+def test_block_forward_captured_in_a_graph():
+    """The stitched block (five sub-kernels, two layout copies and the
+    hipBLASLt GEMMs) at [2, 128, 256] with 4 heads, captured as one graph."""
+    announce("graph: stitched block [2, 128, 256], 4 heads")
+    dev = "cuda"
+    gen = torch.Generator(device=dev).manual_seed(1)
+    B, S, H, NH, F = 2, 128, 256, 4, 1024
+
+    def w(*shape, s=0.02):
+        return (s * torch.randn(*shape, device=dev, generator=gen)).to(BF)
+
+    params = {"w_qkv": w(H, 3 * H), "b_qkv": w(3 * H), "w_o": w(H, H), "b_o": w(H),
+              "w_1": w(H, F), "b_1": w(F), "w_2": w(F, H), "b_2": w(H),
+              "ln1_gamma": (1 + w(H, s=0.1).float()).to(BF), "ln1_beta": w(H, s=0.1),
+              "ln2_gamma": (1 + w(H, s=0.1).float()).to(BF), "ln2_beta": w(H, s=0.1)}
+    blk = fs.TransformerBlock(params, NH)
+    x = w(B, S, H, s=1.0)
+    buf = blk.alloc(B, S, x.device)
+
+    def step():
+        blk.forward(x, buf)
+
+    step()
+    torch.cuda.synchronize()
+    first = buf["out"].clone()
+    step()
+    torch.cuda.synchronize()
+    # hipBLASLt picks one algorithm per shape; the eager forward repeats bit for bit
+    assert torch.equal(bits(first), bits(buf["out"])), "eager forward is not repeatable"
+    g = capture(step)
+    keys = ["a", "qkv", "probs", "o", "att", "h1", "m", "g", "d", "out"]
+
+    def refill():
+        x.copy_(torch.randn(x.shape, device=dev, generator=gen).to(BF))
+
+    replay_and_check(g, step, [buf[k] for k in keys], refill=refill)
+    assert math.isfinite(float(buf["out"].float().abs().max()))
