@@ -231,6 +231,12 @@ def parse():
                     help="the --clock-transient table from its kernel trace and printed lines")
     ap.add_argument("--report-floor", metavar="TRACE_CSV",
                     help="the --copy-floor table from a rocprofv3 kernel-trace CSV")
+    ap.add_argument("--access-floors", action="store_true",
+                    help="time every step sub-kernel next to its access-shape floor "
+                         "(libaccessfloor.so), each after a read-only 1 GiB pass (run under "
+                         "a kernel trace)")
+    ap.add_argument("--report-floors", metavar="TRACE_CSV",
+                    help="the --access-floors table from a rocprofv3 kernel-trace CSV")
     return ap.parse_args()
 
 
@@ -978,6 +984,135 @@ def report_floor(trace_csv: str) -> None:
 
 
 
+# --access-floors: every sub-kernel of the step next to its access-shape floor
+# (libaccessfloor.so: a kernel moving the same bytes in the same launch shape
+# with none of the arithmetic), alternating, each launch after a read-only
+# pass over 1 GiB, in this order every repetition
+FLOOR_SHAPES = ("pw_256x1024", "pw_262144x1024", "sm_8192x4096", "ln_16384x4096",
+                "ep_8192x8192", "blk_ln1", "blk_sm", "blk_ln2", "blk_gelu", "blk_res")
+ACCESS_FLOOR_REPS = 10
+
+
+def access_floor_operands(wl):
+    """(in0, in1, out0, out1) of each step launch, in fsx_access_floor's shape
+    order: the floor reads the sub-kernel's own inputs and writes its outputs."""
+    T, H = wl.bx.shape[0] * wl.bx.shape[1], wl.bx.shape[2]
+    x2, buf = wl.bx.view(T, H), wl.buf
+    return {
+        "pw_256x1024": (wl.pw["x"], wl.pw["r"], wl.pw["y"], None),
+        "pw_262144x1024": (wl.pwbw["x"], wl.pwbw["r"], wl.pwbw["y"], None),
+        "sm_8192x4096": (wl.sm["x"], wl.sm["m"], wl.sm["y"], None),
+        "ln_16384x4096": (wl.ln["x"], wl.ln["r"], wl.ln["y"], wl.ln["ro"]),
+        "ep_8192x8192": (wl.ep["c"], None, wl.ep["out"], None),
+        "blk_ln1": (x2, None, buf["a"], None),
+        "blk_sm": (buf["scores"], None, buf["probs"], None),
+        "blk_ln2": (buf["att"], x2, buf["m"], buf["h1"]),
+        "blk_gelu": (buf["u"], None, buf["g"], None),
+        "blk_res": (buf["d"], buf["h1"], buf["out"], None),
+    }
+
+
+def access_floors(seed: int = 0, reps: int = ACCESS_FLOOR_REPS) -> None:
+    """Prints the median event interval of every step sub-kernel and of its
+    floor; run under a kernel trace for dispatch durations (--report-floors)."""
+    import ctypes
+    import torch
+    from paper_2609_30059_amd import build as B
+    if not os.path.exists(B.LIB_ACCESS_FLOOR):
+        raise RuntimeError(f"{B.LIB_ACCESS_FLOOR} is not built (python -m paper_2609_30059_amd.build)")
+    lib = ctypes.CDLL(B.LIB_ACCESS_FLOOR)
+    sz = ctypes.c_size_t
+    lib.fsx_access_floor.argtypes = [ctypes.c_int, ctypes.c_void_p, sz, ctypes.c_void_p, sz,
+                                     ctypes.c_void_p, sz, ctypes.c_void_p, sz, ctypes.c_int,
+                                     ctypes.c_void_p]
+    lib.fsx_access_floor.restype = ctypes.c_int
+    lib.fsx_access_floor_shapes.restype = ctypes.c_int
+    if lib.fsx_access_floor_shapes() != len(FLOOR_SHAPES):
+        raise RuntimeError("libaccessfloor.so does not match bench.py's shape list")
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    wl = Workload(seed)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    ops = access_floor_operands(wl)
+    real = {name: fn for name, _, _, fn in wl.kernels}
+    real["pw_262144x1024"] = lambda: fs.pointwise_chain(
+        wl.pwbw["x"], wl.pw["b"], wl.pwbw["r"], wl.pw["s"], "gelu_erf", out=wl.pwbw["y"])
+
+    def floor(shape):
+        args = []
+        for t in ops[FLOOR_SHAPES[shape]]:
+            args += [None, 0] if t is None else [t.data_ptr(), t.numel() * t.element_size()]
+        def fn():
+            rc = lib.fsx_access_floor(shape, *args, cus, torch.cuda.current_stream().cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"fsx_access_floor({FLOOR_SHAPES[shape]}) returned {rc}")
+        return fn
+
+    scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")   # 1 GiB, read only
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    cases = []
+    for i, name in enumerate(FLOOR_SHAPES):
+        cases += [(name, "kernel", real[name]), (name, "floor", floor(i))]
+    times = {(n, k): [] for n, k, _ in cases}
+    for rep in range(reps + 1):            # the first repetition is a warm-up
+        for name, kind, fn in cases:
+            fs.row_reduce(scrub, "sum", out=sink)
+            e0, e1 = TimingEvent(), TimingEvent()
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                times[(name, kind)].append(e0.elapsed_time(e1) * 1e3)
+    print("| kernel | kernel us (events) | floor us (events) | kernel / floor |")
+    print("|---|---|---|---|")
+    for name in FLOOR_SHAPES:
+        k, f = (sorted(times[(name, c)])[reps // 2] for c in ("kernel", "floor"))
+        print(f"| {name} | {k:.2f} | {f:.2f} | {k / f:.3f} |")
+
+
+def report_floors(trace_csv: str) -> None:
+    """Median dispatch durations of every --access-floors case from a rocprofv3
+    kernel-trace CSV.  Each repetition launches, per step kernel, a read-only
+    pass, the kernel, a read-only pass and its floor; the read-only passes
+    are dropped and the rest assigned in that fixed order (the warm-up
+    repetition dropped).  The sub-kernels must match their kernel-name
+    patterns and the floors floor_rows_kernel."""
+    import csv
+    import re
+    seq = []
+    with open(trace_csv, newline="") as f:
+        for row in csv.DictReader(f):
+            n = row["Kernel_Name"].replace("(anonymous namespace)::", "")
+            seq.append((int(row["Start_Timestamp"]), n,
+                        (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3))
+    seq.sort()
+    # the measured launches begin after the Workload setup: from the first
+    # floor dispatch back to the kernel launched right before it
+    first = next(i for i, (_, n, _) in enumerate(seq) if "floor_rows_kernel" in n)
+    pats = [KERNEL_PATTERNS[n] for n in FLOOR_SHAPES] + [r"floor_rows_kernel"]
+    body = [(n, us) for _, n, us in seq[first - 2:] if any(re.search(p, n) for p in pats)]
+    per = 2 * len(FLOOR_SHAPES)
+    if len(body) % per:
+        raise ValueError(f"{len(body)} measured dispatches is not a multiple of {per}")
+    got = {}
+    for i, (n, us) in enumerate(body):
+        name, kind = FLOOR_SHAPES[(i % per) // 2], ("kernel", "floor")[i % 2]
+        pat = KERNEL_PATTERNS[name] if kind == "kernel" else r"floor_rows_kernel"
+        if not re.search(pat, n):
+            raise ValueError(f"dispatch {i}: expected the {kind} of {name}, got {n[:120]}")
+        if i >= per:
+            got.setdefault((name, kind), []).append(us)
+    print("| kernel | compulsory bytes | kernel us | floor us | kernel / floor | kernel % of 8 TB/s "
+          "| floor % of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|")
+    for name in FLOOR_SHAPES:
+        k, f = (sorted(got[(name, c)])[len(got[(name, c)]) // 2] for c in ("kernel", "floor"))
+        b = STEP_BYTES[name]
+        print(f"| {name} | {b} | {k:.2f} | {f:.2f} | {k / f:.3f} | "
+              f"{100 * b / k / 1e3 / PEAK_HBM_GBS:.1f} | {100 * b / f / 1e3 / PEAK_HBM_GBS:.1f} |")
+
+
 # ---------------------------------------------------------------------------
 # clock transient: the step after an idle pause, with an engine-clock reading
 # after every step
@@ -1093,6 +1228,12 @@ def main():
         return
     if args.copy_floor:
         copy_floor()
+        return
+    if args.access_floors:
+        access_floors(args.seed)
+        return
+    if args.report_floors:
+        report_floors(args.report_floors)
         return
     if args.clock_transient:
         clock_transient()

@@ -7,6 +7,7 @@ produces, next to this file,
   * libfsgemm.so   -- the hipBLASLt GEMM wrapper of include/fsgemm.h
   * issue_rate     -- the issue-rate calibration program of tiers.py
   * libclockprobe.so -- the engine-clock probe of bench.py's clock-transient mode
+  * libaccessfloor.so -- the access-shape floor kernels of bench.py's access-floors mode
 
 Every HIP translation unit is compiled with the packed-FP32 target feature
 switched off (ordinary fp32 code only).  Objects go to ``_build/`` (ignored
@@ -40,6 +41,7 @@ LIB_FUSEDSUB = os.path.join(HERE, "libfusedsub.so")
 LIB_FSGEMM = os.path.join(HERE, "libfsgemm.so")
 ISSUE_RATE = os.path.join(HERE, "issue_rate")     # calibration program of tiers.py
 LIB_CLOCK_PROBE = os.path.join(HERE, "libclockprobe.so")   # bench.py --clock-transient
+LIB_ACCESS_FLOOR = os.path.join(HERE, "libaccessfloor.so")   # bench.py --access-floors
 
 
 def _hipcc() -> str:
@@ -87,11 +89,16 @@ def build(verbose: bool = False, jobs: int = 8) -> None:
         clock = ex.submit(_run, [_hipcc(), *HIP_FLAGS, "-shared",
                                  os.path.join(CSRC, "clock_probe.hip"), "-o",
                                  LIB_CLOCK_PROBE + ".tmp"], verbose)
+        floor = ex.submit(_run, [_hipcc(), *HIP_FLAGS, "-shared",
+                                 os.path.join(CSRC, "access_floor.hip"), "-o",
+                                 LIB_ACCESS_FLOOR + ".tmp"], verbose)
         fut.result()
         probe.result()
         clock.result()
+        floor.result()
     os.replace(ISSUE_RATE + ".tmp", ISSUE_RATE)
     os.replace(LIB_CLOCK_PROBE + ".tmp", LIB_CLOCK_PROBE)
+    os.replace(LIB_ACCESS_FLOOR + ".tmp", LIB_ACCESS_FLOOR)
     _link(objs, LIB_FUSEDSUB, [], verbose)
     _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
           f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
@@ -111,7 +118,7 @@ def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8
 
 def clean() -> None:
     shutil.rmtree(BUILD, ignore_errors=True)
-    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE, LIB_CLOCK_PROBE):
+    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE, LIB_CLOCK_PROBE, LIB_ACCESS_FLOOR):
         if os.path.exists(p):
             os.remove(p)
 

@@ -171,6 +171,71 @@ def test_report_floor_splits_the_dispatches_by_order(tmp_path, capsys):
         bench.report_floor(str(p))
 
 
+def test_report_floors_pairs_each_kernel_with_its_floor(tmp_path, capsys):
+    scrub = "void fs::reduce_kernel<unsigned short, 0, 8, 4, true, false>(unsigned short const*, long)"
+    floor = ("void (anonymous namespace)::floor_rows_kernel<2, 1, 4, 1, 1, 1, false, false>"
+             "(unsigned int __vector(4) const*, long)")
+    # the setup launches every step kernel (and a block forward) before the
+    # measured repetitions; those dispatches are not part of the table
+    seq = [(NAMES[n], 50.0) for n in bench.FLOOR_SHAPES]
+    for rep in range(4):                        # the first repetition is the warm-up
+        for i, name in enumerate(bench.FLOOR_SHAPES):
+            seq.append((scrub, 150.0))
+            seq.append((NAMES[name], 1000.0 if rep == 0 else 20.0 + i + rep * 0.1))
+            seq.append((scrub, 150.0))
+            seq.append((floor, 1000.0 if rep == 0 else 10.0 + i))
+    p = tmp_path / "trace.csv"
+    _trace(p, seq)
+    bench.report_floors(str(p))
+    out = capsys.readouterr().out
+    rows = {l.split("|")[1].strip(): [c.strip() for c in l.split("|")] for l in out.splitlines()[2:]}
+    assert set(rows) == set(bench.FLOOR_SHAPES)
+    ln = rows["ln_16384x4096"]                  # shape 3: kernel 23.2 (median of 23.1..23.3), floor 13
+    assert float(ln[3]) == pytest.approx(23.2) and float(ln[4]) == pytest.approx(13.0)
+    assert ln[5] == f"{23.2 / 13.0:.3f}"
+    assert int(ln[2]) == bench.STEP_BYTES["ln_16384x4096"]
+    # a floor where a kernel belongs is an error, not a silent relabelling
+    bad = seq[:]
+    k = len(bench.FLOOR_SHAPES) + 4 * 3 + 1     # the kernel of the fourth case, first repetition
+    bad[k] = (floor, 20.0)
+    _trace(p, bad)
+    with pytest.raises(ValueError):
+        bench.report_floors(str(p))
+
+
+def test_access_floor_refuses_bad_arguments_before_any_launch():
+    """The access-floor library checks shapes, buffer sizes, alignment and the
+    CU count on the host and launches nothing when one is wrong (the pointers
+    below are never dereferenced)."""
+    import ctypes
+    import subprocess
+    from paper_2609_30059_amd import build as B
+    lib = ctypes.CDLL(B.LIB_ACCESS_FLOOR)
+    f = lib.fsx_access_floor
+    sz = ctypes.c_size_t
+    f.argtypes = [ctypes.c_int, ctypes.c_void_p, sz, ctypes.c_void_p, sz, ctypes.c_void_p, sz,
+                  ctypes.c_void_p, sz, ctypes.c_int, ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    lib.fsx_access_floor_shapes.restype = ctypes.c_int
+    assert lib.fsx_access_floor_shapes() == len(bench.FLOOR_SHAPES)
+    p, big = 1 << 20, 1 << 31                   # a 16-byte-aligned stand-in address, ample sizes
+    ln = bench.FLOOR_SHAPES.index("ln_16384x4096")
+    need = 16384 * 4096 * 2
+    assert f(-1, p, big, p, big, p, big, p, big, 256, None) == -2
+    assert f(len(bench.FLOOR_SHAPES), p, big, p, big, p, big, p, big, 256, None) == -2
+    assert f(ln, p, big, p, big, p, big, p, big, 0, None) == -3
+    assert f(ln, None, big, p, big, p, big, p, big, 256, None) == -1
+    assert f(ln, p + 8, big, p, big, p, big, p, big, 256, None) == -1      # misaligned
+    assert f(ln, p, need - 16, p, big, p, big, p, big, 256, None) == -1    # x too small
+    assert f(ln, p, need, p, need, p, need, None, 0, 256, None) == -1      # residual_out missing
+    ep = bench.FLOOR_SHAPES.index("ep_8192x8192")
+    assert f(ep, p, 8192 * 8192 * 2, None, 0, p, 8, None, 0, 256, None) == -1   # out < 16 bytes
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_ACCESS_FLOOR], capture_output=True,
+                         text=True).stdout
+    assert {l.split()[-1] for l in out.splitlines() if " T " in l} == {
+        "fsx_access_floor", "fsx_access_floor_shapes"}
+
+
 def test_short_kernel_name_keeps_template_arguments():
     n = ("void fs::(anonymous namespace)::softmax_cached_kernel<unsigned short, unsigned short, "
          "true, false, true, 32, 32, false>(unsigned short const*, long, float)")
