@@ -510,13 +510,24 @@ __global__ __launch_bounds__(256) void epilogue_wide_kernel(
 #define FS_EPI_WAVES 16
 #endif
 #ifndef FS_EPI_CHUNK
-#define FS_EPI_CHUNK 2
+#define FS_EPI_CHUNK 2   // vectors per pipelined chunk
+#endif
+#ifndef FS_EPI_CHUNK_FULL
+#define FS_EPI_CHUNK_FULL 4   // the same for rows that fill 2..16 vectors per lane
 #endif
 #ifndef FS_EPI_BLOCKS_PER_CU
 #define FS_EPI_BLOCKS_PER_CU 2
 #endif
 constexpr int kLdsW = FS_EPI_WAVES;    // waves per block of the staged kernel
 constexpr int kLdsCH = FS_EPI_CHUNK;   // vectors per pipelined chunk
+// Full rows of up to 16 vectors per lane read 4-vector chunks: twice the
+// bytes in flight per wave.  In the benchmark step the 2-vector form of the
+// 8192-column epilogue ran either at 22 us or, on many boxes in most
+// launches, at 28 us with its waves resident longer at an unchanged clock;
+// the 4-vector form stays at about 23 us.  Wider or partial rows keep
+// 2-vector chunks (4 would spill at 64 VGPRs).
+template <int NV>
+constexpr int kLdsChFull = NV <= 16 ? FS_EPI_CHUNK_FULL : FS_EPI_CHUNK;
 
 template <typename CT, typename BT, int ACT>
 hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
@@ -540,7 +551,7 @@ hipError_t dispatch(const EpilogueArgs& a, int cus, hipStream_t s) {
 #define FS_EPI_RUNG(NV)                                                                 \
   if (per_lane <= NV)                                                                    \
     return nvec == int64_t(NV) * 64                                                      \
-               ? staged(epilogue_lds_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, true>, NV)   \
+               ? staged(epilogue_lds_kernel<CT, BT, ACT, NV, kLdsChFull<NV>, kLdsW, true>, NV) \
                : staged(epilogue_lds_kernel<CT, BT, ACT, NV, kLdsCH, kLdsW, false>, NV);
     FS_EPI_RUNG(2)
     FS_EPI_RUNG(4)
