@@ -1338,7 +1338,10 @@ def main():
 
     # per-kernel breakdown (context, after the timed region): K more steps with
     # an event after every kernel; each interval includes that event's cost
-    per = interval_pass(args.steps)
+    # medians (do_bench's statistic) and means of the same intervals
+    per_all = interval_pass(args.steps, lambda v: v)
+    per = [sorted(v)[len(v) // 2] for v in per_all]
+    per_mean = [sum(v) / len(v) for v in per_all]
     # the practical ceiling of a kernel that moves as many bytes: a copy of
     # that size, measured the same way
     copies = ([float("nan")] * nk if args.no_copy_reference
@@ -1349,9 +1352,10 @@ def main():
 
     traffic = load_traffic()
     per_kernel = {}
-    for (name, kind, nbytes, _), ms, cms in zip(wl.kernels, per, copies):
+    for (name, kind, nbytes, _), ms, mms, cms in zip(wl.kernels, per, per_mean, copies):
         gbs = nbytes / (ms * 1e-3) / 1e9
-        per_kernel[name] = {"us": round(ms * 1e3, 2), "bytes": nbytes, "GB/s": round(gbs, 1),
+        per_kernel[name] = {"us": round(ms * 1e3, 2), "mean_us": round(mms * 1e3, 2),
+                            "bytes": nbytes, "GB/s": round(gbs, 1),
                             "frac": round(gbs / PEAK_HBM_GBS, 4),
                             "same_size_copy_us": None if cms != cms else round(cms * 1e3, 2)}
     dname, dkind, dbytes, _ = wl.kernels[dom]
@@ -1390,8 +1394,9 @@ def main():
                      "algorithmic_bytes": dbytes, "launch_us": round(dom_ms * 1e3, 2)},
         "per_kernel": per_kernel,
         "per_kernel_note": "intervals between events recorded after every kernel, in a pass "
-                           "after the timed region; each includes the cost of one timing-only event "
-                           "(about 1 us). "
+                           "of K steps after the timed region; us, GB/s and frac from the median "
+                           "interval, mean_us the mean; each interval includes the cost of one "
+                           "timing-only event (about 1 us). "
                            "same_size_copy_us: the calibration copy moving the same bytes "
                            "(half read, half written), timed the same way",
         "copy_calibration_GBs": round(copy_gbs, 1),
