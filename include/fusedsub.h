@@ -30,11 +30,14 @@
  * exactly on load and rounded to nearest even once, on the final store
  * (Appendix A, Executor prompt: accumulate in fp32, cast on the final store).
  *
- * Alignment: every pointer must be aligned to its element size
- * (FS_ERR_BAD_ARGUMENT otherwise).  Base pointers aligned to 16 bytes with ld*sizeof(elem) a
- * multiple of 16 (and cols a multiple of the 16-byte vector width) take the
- * 128-bit vector path; anything else takes a correct scalar path.  This is
- * never an error.
+ * Alignment: every pointer must be aligned to its element size (a float at a
+ * multiple of 4 bytes, a bf16 value at a multiple of 2; FS_ERR_BAD_ARGUMENT
+ * otherwise).  Within that, any address, row stride and width is accepted:
+ * base pointers aligned to 16 bytes with ld*sizeof(elem) a multiple of 16 (and
+ * cols a multiple of the 16-byte vector width) take the 128-bit vector path,
+ * rows whose operands share one offset within a 16-byte unit load their
+ * aligned body 16 bytes at a time, and anything else takes a correct
+ * element-wise path.
  *
  * Errors: every entry point validates its arguments on the host, before any
  * HIP call, and returns a status; it never aborts.  A launch failure returns
