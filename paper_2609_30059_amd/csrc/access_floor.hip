@@ -158,3 +158,19 @@ extern "C" __attribute__((visibility("default"))) int fsx_access_floor(
 extern "C" __attribute__((visibility("default"))) int fsx_access_floor_shapes(void) {
   return kNumShapes;
 }
+
+// Bytes one launch of shape `shape` reads and writes (whole 16-byte vectors;
+// the causal shape reads each row up to its last live vector), or -1 for an
+// unknown shape: the caller compares them with the sub-kernel's compulsory
+// bytes.
+extern "C" __attribute__((visibility("default"))) int64_t fsx_access_floor_bytes(int shape) {
+  if (shape < 0 || shape >= kNumShapes) return -1;
+  const Geometry& s = kShapes[shape];
+  int64_t read_vecs = s.rows * s.ld;
+  if (shape == 6) {   // causal rows of 512 bf16 (8 per vector) in periods of 512 rows
+    int64_t per_period = 0;
+    for (int pos = 0; pos < 512; ++pos) per_period += pos / 8 + 1;
+    read_vecs = s.rows / 512 * per_period;
+  }
+  return 16 * (read_vecs * s.nin + s.rows * s.ld * s.nout);
+}

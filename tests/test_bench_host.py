@@ -233,7 +233,32 @@ def test_access_floor_refuses_bad_arguments_before_any_launch():
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_ACCESS_FLOOR], capture_output=True,
                          text=True).stdout
     assert {l.split()[-1] for l in out.splitlines() if " T " in l} == {
-        "fsx_access_floor", "fsx_access_floor_shapes"}
+        "fsx_access_floor", "fsx_access_floor_shapes", "fsx_access_floor_bytes"}
+
+
+def test_access_floors_move_the_sub_kernels_bytes():
+    """Each floor reads and writes the compulsory bytes of the step launch it
+    stands in for: exactly, less the broadcast vectors (bias, gamma/beta,
+    column scales) and the epilogue's row sums it does not move; the causal
+    shape reads whole 16-byte vectors up to each row's diagonal, 1.4 % above
+    the element count of the lower triangle."""
+    import ctypes
+    from paper_2609_30059_amd import build as B
+    lib = ctypes.CDLL(B.LIB_ACCESS_FLOOR)
+    lib.fsx_access_floor_bytes.restype = ctypes.c_int64
+    lib.fsx_access_floor_bytes.argtypes = [ctypes.c_int]
+    small = {"pw_256x1024": 1024 * 4, "pw_262144x1024": 1024 * 4, "ln_16384x4096": 2 * 4096 * 2,
+             "ep_8192x8192": 8192 * (2 + 4) + 8192 * 4, "blk_ln1": 2 * 1024 * 2,
+             "blk_ln2": 2 * 1024 * 2, "blk_gelu": 4096 * 2}
+    for i, name in enumerate(bench.FLOOR_SHAPES):
+        got = lib.fsx_access_floor_bytes(i)
+        want = bench.STEP_BYTES[name] - small.get(name, 0)
+        if name == "blk_sm":
+            assert want < got < want * 1.015, (name, got, want)
+        else:
+            assert got == want, (name, got, want)
+    assert lib.fsx_access_floor_bytes(-1) == -1
+    assert lib.fsx_access_floor_bytes(len(bench.FLOOR_SHAPES)) == -1
 
 
 def test_short_kernel_name_keeps_template_arguments():
