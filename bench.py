@@ -34,7 +34,10 @@ hipEventDisableSystemFence: recording it skips the system-scope cache
 writeback and invalidation of a default event, which costs the GPU about 3 us
 per event; a timing-only one costs about 1 us).  Events after every kernel
 would still lengthen the step by about 3 %, so the per-kernel breakdown comes
-from a separate pass after the timed region.
+from a separate pass after the timed region (medians, with the means beside
+them), followed by the same pass over the step's access-shape floors
+(libaccessfloor.so: each launch's bytes moved in its launch shape with none of
+the arithmetic) when that library is built.
 
 Prints one JSON line.  Two GPU-free modes turn rocprofv3 CSV output of this
 script into the summaries under profiles/:
@@ -1012,14 +1015,15 @@ def access_floor_operands(wl):
     }
 
 
-def access_floors(seed: int = 0, reps: int = ACCESS_FLOOR_REPS) -> None:
-    """Prints the median event interval of every step sub-kernel and of its
-    floor; run under a kernel trace for dispatch durations (--report-floors)."""
+def floor_launchers(wl):
+    """{step launch name: closure launching its access-shape floor on the
+    current stream} from libaccessfloor.so, or None when it is not built.
+    The floors read the sub-kernels' inputs and overwrite their outputs."""
     import ctypes
     import torch
     from paper_2609_30059_amd import build as B
     if not os.path.exists(B.LIB_ACCESS_FLOOR):
-        raise RuntimeError(f"{B.LIB_ACCESS_FLOOR} is not built (python -m paper_2609_30059_amd.build)")
+        return None
     lib = ctypes.CDLL(B.LIB_ACCESS_FLOOR)
     sz = ctypes.c_size_t
     lib.fsx_access_floor.argtypes = [ctypes.c_int, ctypes.c_void_p, sz, ctypes.c_void_p, sz,
@@ -1029,14 +1033,8 @@ def access_floors(seed: int = 0, reps: int = ACCESS_FLOOR_REPS) -> None:
     lib.fsx_access_floor_shapes.restype = ctypes.c_int
     if lib.fsx_access_floor_shapes() != len(FLOOR_SHAPES):
         raise RuntimeError("libaccessfloor.so does not match bench.py's shape list")
-    import paper_2609_30059_amd as fs
-    torch.cuda.set_device(0)
-    wl = Workload(seed)
-    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    cus = torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
     ops = access_floor_operands(wl)
-    real = {name: fn for name, _, _, fn in wl.kernels}
-    real["pw_262144x1024"] = lambda: fs.pointwise_chain(
-        wl.pwbw["x"], wl.pw["b"], wl.pwbw["r"], wl.pw["s"], "gelu_erf", out=wl.pwbw["y"])
 
     def floor(shape):
         args = []
@@ -1047,12 +1045,29 @@ def access_floors(seed: int = 0, reps: int = ACCESS_FLOOR_REPS) -> None:
             if rc != 0:
                 raise RuntimeError(f"fsx_access_floor({FLOOR_SHAPES[shape]}) returned {rc}")
         return fn
+    return {name: floor(i) for i, name in enumerate(FLOOR_SHAPES)}
+
+
+def access_floors(seed: int = 0, reps: int = ACCESS_FLOOR_REPS) -> None:
+    """Prints the median event interval of every step sub-kernel and of its
+    floor; run under a kernel trace for dispatch durations (--report-floors)."""
+    import torch
+    from paper_2609_30059_amd import build as B
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    wl = Workload(seed)
+    floors = floor_launchers(wl)
+    if floors is None:
+        raise RuntimeError(f"{B.LIB_ACCESS_FLOOR} is not built (python -m paper_2609_30059_amd.build)")
+    real = {name: fn for name, _, _, fn in wl.kernels}
+    real["pw_262144x1024"] = lambda: fs.pointwise_chain(
+        wl.pwbw["x"], wl.pw["b"], wl.pwbw["r"], wl.pw["s"], "gelu_erf", out=wl.pwbw["y"])
 
     scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")   # 1 GiB, read only
     sink = torch.empty(8192, dtype=torch.float32, device="cuda")
     cases = []
-    for i, name in enumerate(FLOOR_SHAPES):
-        cases += [(name, "kernel", real[name]), (name, "floor", floor(i))]
+    for name in FLOOR_SHAPES:
+        cases += [(name, "kernel", real[name]), (name, "floor", floors[name])]
     times = {(n, k): [] for n, k, _ in cases}
     for rep in range(reps + 1):            # the first repetition is a warm-up
         for name, kind, fn in cases:
@@ -1350,14 +1365,37 @@ def main():
     bw_ms = wl.pointwise_bandwidth_scale(max(args.steps // 5, 5))
     bw_bytes = STEP_BYTES["pw_262144x1024"]
 
+    # access-shape floors (libaccessfloor.so): K steps of the step's launches
+    # each replaced by its floor, timed like the per-kernel pass.  Last of the
+    # GPU measurements: the floors overwrite the sub-kernels' outputs.
+    floors = floor_launchers(wl)
+    floor_med = [None] * nk
+    if floors is not None:
+        fl_fns = [floors[name] for name, _, _, _ in wl.kernels]
+        for f in fl_fns:
+            f()
+        torch.cuda.synchronize()
+        fev = [[TimingEvent() for _ in range(nk + 1)] for _ in range(args.steps)]
+        for row in fev:
+            row[0].record()
+            for i, f in enumerate(fl_fns):
+                f()
+                row[i + 1].record()
+        torch.cuda.synchronize()
+        floor_med = [sorted(fev[st][i].elapsed_time(fev[st][i + 1]) for st in range(args.steps))
+                     [args.steps // 2] for i in range(nk)]
+
     traffic = load_traffic()
     per_kernel = {}
-    for (name, kind, nbytes, _), ms, mms, cms in zip(wl.kernels, per, per_mean, copies):
+    for (name, kind, nbytes, _), ms, mms, cms, fms in zip(wl.kernels, per, per_mean, copies,
+                                                          floor_med):
         gbs = nbytes / (ms * 1e-3) / 1e9
         per_kernel[name] = {"us": round(ms * 1e3, 2), "mean_us": round(mms * 1e3, 2),
                             "bytes": nbytes, "GB/s": round(gbs, 1),
                             "frac": round(gbs / PEAK_HBM_GBS, 4),
-                            "same_size_copy_us": None if cms != cms else round(cms * 1e3, 2)}
+                            "same_size_copy_us": None if cms != cms else round(cms * 1e3, 2),
+                            "floor_us": None if fms is None else round(fms * 1e3, 2),
+                            "vs_floor": None if fms is None else round(ms / fms, 3)}
     dname, dkind, dbytes, _ = wl.kernels[dom]
     achieved = dbytes / (dom_ms * 1e-3) / 1e9
     t = traffic.get(dname)
@@ -1398,7 +1436,10 @@ def main():
                            "interval, mean_us the mean; each interval includes the cost of one "
                            "timing-only event (about 1 us). "
                            "same_size_copy_us: the calibration copy moving the same bytes "
-                           "(half read, half written), timed the same way",
+                           "(half read, half written), timed the same way; floor_us: the launch's "
+                           "access-shape floor (libaccessfloor.so: the same bytes in the same "
+                           "launch shape, none of the arithmetic), median over K steps of floors "
+                           "timed the same way; vs_floor = us / floor_us",
         "copy_calibration_GBs": round(copy_gbs, 1),
         "context": {"pointwise_bandwidth_scale": {
                         "shape": [262144, 1024], "dtype": "f32", "bytes": bw_bytes,
