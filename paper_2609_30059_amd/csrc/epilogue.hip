@@ -521,11 +521,11 @@ __global__ __launch_bounds__(256) void epilogue_wide_kernel(
 constexpr int kLdsW = FS_EPI_WAVES;    // waves per block of the staged kernel
 constexpr int kLdsCH = FS_EPI_CHUNK;   // vectors per pipelined chunk
 // Full rows of up to 16 vectors per lane read 4-vector chunks: twice the
-// bytes in flight per wave.  In the benchmark step the 2-vector form of the
-// 8192-column epilogue ran either at 22 us or, on many boxes in most
-// launches, at 28 us with its waves resident longer at an unchanged clock;
-// the 4-vector form stays at about 23 us.  Wider or partial rows keep
-// 2-vector chunks (4 would spill at 64 VGPRs).
+// bytes in flight per wave.  Between other bandwidth-bound kernels the
+// 2-vector form of the 8192-column epilogue ran either at 22 us or, in many
+// runs for most of its launches, at 28 us with its waves resident longer at
+// an unchanged clock; the 4-vector form stays near 23 us.  Wider or partial
+// rows keep 2-vector chunks (4 would spill at 64 VGPRs).
 template <int NV>
 constexpr int kLdsChFull = NV <= 16 ? FS_EPI_CHUNK_FULL : FS_EPI_CHUNK;
 

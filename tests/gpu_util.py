@@ -26,7 +26,8 @@ requires_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a
 
 
 def announce(*parts):
-    """Name the case on stdout before the GPU step runs (survives a lost box)."""
+    """Name the case on stdout before the GPU step runs (it survives a lost
+    process)."""
     print("[case]", *parts, flush=True)
     sys.stdout.flush()
 
