@@ -8,6 +8,8 @@ produces, next to this file,
   * issue_rate     -- the issue-rate calibration program of tiers.py
   * libclockprobe.so -- the engine-clock probe of bench.py's clock-transient mode
   * libaccessfloor.so -- the access-shape floor kernels of bench.py's access-floors mode
+  * abi_consumer   -- tests/abi_consumer.cpp, a plain C++ program that calls
+                      libfusedsub.so through include/fusedsub.h (GPU test of the ABI)
 
 Every HIP translation unit is compiled with the packed-FP32 target feature
 switched off (ordinary fp32 code only).  Objects go to ``_build/`` (ignored
@@ -42,6 +44,7 @@ LIB_FSGEMM = os.path.join(HERE, "libfsgemm.so")
 ISSUE_RATE = os.path.join(HERE, "issue_rate")     # calibration program of tiers.py
 LIB_CLOCK_PROBE = os.path.join(HERE, "libclockprobe.so")   # bench.py --clock-transient
 LIB_ACCESS_FLOOR = os.path.join(HERE, "libaccessfloor.so")   # bench.py --access-floors
+ABI_CONSUMER = os.path.join(HERE, "abi_consumer")   # tests/test_gpu_abi_consumer.py
 
 
 def _hipcc() -> str:
@@ -103,6 +106,13 @@ def build(verbose: bool = False, jobs: int = 8) -> None:
     _run(["g++", "-shared", "-fPIC", gemm_obj, "-o", LIB_FSGEMM + ".tmp", f"-L{ROCM}/lib",
           f"-Wl,-rpath,{ROCM}/lib", "-lhipblaslt", "-lamdhip64"], verbose)
     os.replace(LIB_FSGEMM + ".tmp", LIB_FSGEMM)
+    # a host-only C++ caller of the ABI, linked against the library just built
+    # (found next to the program at run time)
+    _run(["g++", "-O2", "-std=c++17", "-Wall", "-D__HIP_PLATFORM_AMD__", f"-I{INCLUDE}",
+          f"-I{ROCM}/include", os.path.join(ROOT, "tests", "abi_consumer.cpp"),
+          "-o", ABI_CONSUMER + ".tmp", f"-L{HERE}", "-lfusedsub", f"-L{ROCM}/lib",
+          "-lamdhip64", "-Wl,-rpath,$ORIGIN", f"-Wl,-rpath,{ROCM}/lib"], verbose)
+    os.replace(ABI_CONSUMER + ".tmp", ABI_CONSUMER)
 
 
 def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8) -> str:
@@ -118,7 +128,8 @@ def build_variant(out_dir: str, defines=(), verbose: bool = False, jobs: int = 8
 
 def clean() -> None:
     shutil.rmtree(BUILD, ignore_errors=True)
-    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE, LIB_CLOCK_PROBE, LIB_ACCESS_FLOOR):
+    for p in (LIB_FUSEDSUB, LIB_FSGEMM, ISSUE_RATE, LIB_CLOCK_PROBE, LIB_ACCESS_FLOOR,
+              ABI_CONSUMER):
         if os.path.exists(p):
             os.remove(p)
 

@@ -299,3 +299,16 @@ def test_causal_softmax_trimmed_validation():
     assert ct(dtype=9) == 4
     assert ct(y=A + 2) == 5
     assert ct(rows=0, x=NULL, y=NULL) == 0
+
+
+def test_plain_cpp_consumer_is_built_against_the_in_tree_library():
+    """tests/abi_consumer.cpp (run on the GPU by test_gpu_abi_consumer.py)
+    links the in-tree libfusedsub.so and refuses a bad command line before
+    any HIP call."""
+    from paper_2609_30059_amd.build import ABI_CONSUMER
+    assert os.access(ABI_CONSUMER, os.X_OK), "run python -m paper_2609_30059_amd.build"
+    deps = subprocess.run(["ldd", ABI_CONSUMER], capture_output=True, text=True).stdout
+    line = next(l for l in deps.splitlines() if "libfusedsub.so" in l)
+    assert os.path.realpath(line.split("=>")[1].split()[0]) == os.path.realpath(N.LIB_FUSEDSUB)
+    r = subprocess.run([ABI_CONSUMER], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 1 and "usage" in r.stderr
