@@ -69,8 +69,9 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
 class Tensor:
     """A host tensor in its storage dtype.
 
-    ``data`` holds float32 values for ``dtype == "f32"`` and uint16 bf16 bit
-    patterns for ``dtype == "bf16"``.
+    ``data`` holds float32 values for ``dtype == "f32"``, uint16 bf16 bit
+    patterns for ``dtype == "bf16"`` and bytes for ``dtype == "u8"`` (a byte
+    mask; ``f64`` gives the byte values themselves).
     """
     data: np.ndarray
     dtype: str
@@ -84,6 +85,8 @@ class Tensor:
             return self.data.astype(np.float64)
         if self.dtype == "bf16":
             return bf16_bits_to_f64(self.data)
+        if self.dtype == "u8":
+            return self.data.astype(np.float64)
         raise ValueError(self.dtype)
 
     def rows(self, idx) -> "Tensor":
@@ -137,6 +140,11 @@ def softmax_inputs(seed: int, rows: int, cols: int, dtype: str = "bf16",
     Each mask element is -inf independently with probability ``p_masked``
     (draw order: logits, then one U(0,1) per mask element).  A row that comes
     out fully masked gets column 0 unmasked, so no row is empty.
+
+    ``mask_dtype="u8"`` stores the same pattern as a byte mask: 0 where the
+    additive mask is 0, and at each masked position a byte drawn uniformly
+    from 1..255 (one more draw per element, after the others, so the logits
+    and the pattern equal those of the other mask dtypes for the seed).
     """
     rng = np.random.default_rng(seed)
     x = _normal(rng, (rows, cols), 0.0, sigma)
@@ -147,8 +155,13 @@ def softmax_inputs(seed: int, rows: int, cols: int, dtype: str = "bf16",
         full = masked.all(axis=1)
         if full.any():
             masked[full, 0] = False
-        m = np.where(masked, NEG_INF, 0.0)
-        out["mask"] = _store(m, mask_dtype)
+        if mask_dtype == "u8":
+            b = rng.integers(1, 256, size=(rows, cols), dtype=np.uint8)
+            out["mask"] = Tensor(np.ascontiguousarray(np.where(masked, b, 0).astype(np.uint8)),
+                                 "u8")
+        else:
+            m = np.where(masked, NEG_INF, 0.0)
+            out["mask"] = _store(m, mask_dtype)
     return out
 
 

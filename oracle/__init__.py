@@ -9,14 +9,14 @@ Parity status: every function here is pinned by the CPU tests
 ``tests/test_oracle_*.py`` to closed forms, invariants, special cases and
 printed reference values (``tests/golden/``).
 """
-from .subkernels import (ACTS, apply_act, causal_mask, causal_written_width, gelu_erf, gemm_epilogue_reduce,
+from .subkernels import (ACTS, apply_act, byte_mask_additive, causal_mask, causal_written_width, gelu_erf, gemm_epilogue_reduce,
                          layernorm_residual, pointwise_chain, relu, residual_store_bf16,
                          rmsnorm_residual, round_to_bf16, row_argmax, row_reduce, row_softmax,
                          sigmoid, strided_copy)
 from .block import block_forward, block_forward_sequence, STAGES
 
 __all__ = [
-    "ACTS", "apply_act", "causal_mask", "causal_written_width", "gelu_erf", "gemm_epilogue_reduce",
+    "ACTS", "apply_act", "byte_mask_additive", "causal_mask", "causal_written_width", "gelu_erf", "gemm_epilogue_reduce",
     "layernorm_residual", "pointwise_chain", "relu", "residual_store_bf16",
     "rmsnorm_residual", "row_reduce", "row_argmax",
     "round_to_bf16", "row_softmax", "sigmoid", "strided_copy", "block_forward",

@@ -29,7 +29,9 @@ Readings where the paper is silent (each is also listed in the design notes):
   * The pointwise chain applies scale, then bias, then the activation, then
     the residual add; the bias broadcasts along rows (one value per column).
   * Softmax uses an additive mask; a row whose every entry is masked yields
-    an all-zero output row (no NaN).
+    an all-zero output row (no NaN).  A byte mask (one byte per element, as
+    boolean attention masks are stored) stands for the additive mask with
+    -inf where the byte is nonzero and 0 where it is zero.
   * The causal rule masks element (r, j) iff j > (r mod q_len) + (cols - q_len).
   * LayerNorm uses the biased variance with eps inside the square root; its
     input is h = x + residual, and the stored residual is the float32 sum
@@ -45,7 +47,7 @@ from scipy import special as _sp
 
 __all__ = [
     "ACTS", "gelu_erf", "sigmoid", "relu", "apply_act",
-    "pointwise_chain", "causal_mask", "row_softmax", "layernorm_residual",
+    "pointwise_chain", "causal_mask", "byte_mask_additive", "row_softmax", "layernorm_residual",
     "rmsnorm_residual", "residual_store_bf16", "round_to_bf16", "gemm_epilogue_reduce",
     "row_reduce", "row_argmax",
 ]
@@ -128,6 +130,15 @@ def causal_written_width(rows: int, cols: int, q_len: int, block: int) -> np.nda
     s = np.arange(rows, dtype=np.int64) % q_len
     w = (s // block + 1) * block + (cols - q_len)
     return np.clip(w, 0, cols)
+
+
+def byte_mask_additive(m):
+    """Additive mask of a byte mask: -inf where the byte is nonzero (the
+    position is excluded), 0 where it is zero.  The paper's fused softmax
+    takes an additive mask (Appendix A, Planner item 9); a byte mask is the
+    same {0, -inf} mask stored in one byte per element."""
+    m = np.asarray(m)
+    return np.where(m != 0, -np.inf, 0.0)
 
 
 def row_softmax(x, mask=None, scale: float = 1.0, causal_q_len: int = 0):

@@ -34,6 +34,17 @@ def test_softmax_mask_rate_and_no_empty_row():
     assert (~np.isinf(d["mask"].f64())).any(axis=1).all()
 
 
+def test_byte_mask_has_the_pattern_of_the_additive_mask():
+    a = fd.softmax_inputs(5, 300, 96, "bf16")
+    b = fd.softmax_inputs(5, 300, 96, "bf16", mask_dtype="u8")
+    np.testing.assert_array_equal(a["x"].data, b["x"].data)
+    assert b["mask"].dtype == "u8" and b["mask"].data.dtype == np.uint8
+    np.testing.assert_array_equal(b["mask"].data != 0, np.isinf(a["mask"].f64()))
+    vals = b["mask"].data[b["mask"].data != 0]
+    assert vals.min() >= 1 and len(np.unique(vals)) > 100   # many byte values, not just 1
+    np.testing.assert_array_equal(b["mask"].f64(), b["mask"].data.astype(np.float64))
+
+
 def test_distributions():
     d = fd.layernorm_inputs(1, 256, 1024)
     assert abs(d["x"].f64().std() - 1.0) < 0.01

@@ -141,6 +141,31 @@ class TestSoftmax:
                                    rtol=1e-14)
         assert y[0, 1] == 0.0 and y[1, 0] == 0.0 and y[1, 2] == 0.0
 
+    def test_byte_mask_keeps_the_zero_bytes_only(self):
+        # brute force: the softmax of a row under a byte mask is the softmax
+        # of its kept entries alone (zero bytes), placed back, with exact
+        # zeros at the nonzero bytes -- whatever their value (1, 7, 255)
+        rng = np.random.default_rng(4)
+        x = rng.standard_normal((3, 8)) * 2
+        m = np.array([[0, 1, 0, 255, 0, 0, 7, 0],
+                      [1, 1, 1, 1, 1, 1, 1, 0],
+                      [0, 0, 0, 0, 0, 0, 0, 0]], dtype=np.uint8)
+        add = oracle.byte_mask_additive(m)
+        assert add.dtype == np.float64
+        np.testing.assert_array_equal(np.isinf(add), m != 0)
+        assert np.all(add[m == 0] == 0.0) and np.all(add[m != 0] < 0)
+        y = oracle.row_softmax(x, add, 0.5)
+        for r in range(3):
+            keep = [j for j in range(8) if m[r, j] == 0]
+            e = [math.exp(0.5 * x[r, j]) for j in keep]
+            want = np.zeros(8)
+            for j, v in zip(keep, e):
+                want[j] = v / sum(e)
+            np.testing.assert_allclose(y[r], want, rtol=1e-14, atol=0)
+        assert np.all(y[m != 0] == 0.0)
+        np.testing.assert_array_equal(y[1], [0, 0, 0, 0, 0, 0, 0, 1])
+        np.testing.assert_array_equal(y[2], oracle.row_softmax(x[2:], None, 0.5)[0])
+
     def test_fully_masked_row_is_zero(self):
         y = oracle.row_softmax(np.ones((1, 3)), np.full((1, 3), -np.inf), 1.0)
         np.testing.assert_array_equal(y, 0.0)
