@@ -279,6 +279,8 @@ class Workload:
         self.host["softmax_8192x4096"] = h2
         self.sm = dict(x=d(h2["x"]), m=d(h2["mask"]), s=h2["scale"])
         self.sm["y"] = torch.empty_like(self.sm["x"])
+        # the same mask as bytes (nonzero = excluded), measured as context
+        self.sm["m8"] = (self.sm["m"] != 0).to(torch.uint8)
         # layernorm_16384x4096
         h3 = fd.make_inputs("layernorm_16384x4096", seed)
         self.host["layernorm_16384x4096"] = h3
@@ -401,6 +403,30 @@ class Workload:
         torch.cuda.synchronize()
         ts = sorted(a.elapsed_time(b) for a, b in evs)
         return ts[reps // 2]
+
+    def softmax_byte_mask(self, reps):
+        """Median launch intervals of the [8192, 4096] softmax with its mask
+        as bytes and, alternating with it, as the additive bf16 mask; each
+        launch follows a read-only pass over 1 GiB (inputs come from HBM) and
+        is bracketed by its own two events.  Returns (byte us, additive us)."""
+        torch, fs, p = self.torch, self.fs, self.sm
+        scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")
+        sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+        fns = [lambda: fs.row_softmax(p["x"], p["m8"], p["s"], out=p["y"]),
+               lambda: fs.row_softmax(p["x"], p["m"], p["s"], out=p["y"])]
+        ts = [[], []]
+        for rep in range(reps + 1):            # the first repetition is a warm-up
+            for i, fn in enumerate(fns):
+                fs.row_reduce(scrub, "sum", out=sink)
+                a, b = TimingEvent(), TimingEvent()
+                a.record()
+                fn()
+                b.record()
+                torch.cuda.synchronize()
+                if rep:
+                    ts[i].append(a.elapsed_time(b))
+        del scrub
+        return tuple(sorted(t)[reps // 2] * 1e3 for t in ts)
 
     def same_size_copies(self, sizes, reps):
         """Median interval of a calibration copy moving the same number of
@@ -1364,6 +1390,8 @@ def main():
 
     bw_ms = wl.pointwise_bandwidth_scale(max(args.steps // 5, 5))
     bw_bytes = STEP_BYTES["pw_262144x1024"]
+    sm8_us, sm_add_us = wl.softmax_byte_mask(max(args.steps // 5, 5))
+    sm8_bytes = 8192 * 4096 * (2 + 1 + 2)
 
     # access-shape floors (libaccessfloor.so): K steps of the step's launches
     # each replaced by its floor, timed like the per-kernel pass.  Last of the
@@ -1446,6 +1474,13 @@ def main():
                         "us": round(bw_ms * 1e3, 2),
                         "GB/s": round(bw_bytes / (bw_ms * 1e-3) / 1e9, 1),
                         "frac": round(bw_bytes / (bw_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+                    "softmax_byte_mask": {
+                        "shape": [8192, 4096], "dtype": "bf16", "mask": "u8", "bytes": sm8_bytes,
+                        "us": round(sm8_us, 2),
+                        "GB/s": round(sm8_bytes / (sm8_us * 1e-6) / 1e9, 1),
+                        "frac": round(sm8_bytes / (sm8_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                        "additive_bf16_mask_us": round(sm_add_us, 2),
+                        "note": "each launch after a 1 GiB read-only pass, with its own events"},
                     "block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
                     "gemm_8192x8192x4096_ms": round(wl.gemm_8192x8192x4096_ms, 3),
                     "wall_s_warmup_and_timed": round(wall_s, 4), "setup_s": round(setup_s, 1),

@@ -32,7 +32,7 @@
  *
  * Alignment: every pointer must be aligned to its element size (a float at a
  * multiple of 4 bytes, a bf16 value at a multiple of 2; FS_ERR_BAD_ARGUMENT
- * otherwise).  Within that, any address, row stride and width is accepted:
+ * otherwise; a byte mask may start anywhere).  Within that, any address, row stride and width is accepted:
  * base pointers aligned to 16 bytes with ld*sizeof(elem) a multiple of 16 (and
  * cols a multiple of the 16-byte vector width) take the 128-bit vector path,
  * rows whose operands share one offset within a 16-byte unit load their
@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 1
+#define FS_ABI_VERSION 2
 #define FS_API __attribute__((visibility("default")))
 
 typedef enum fs_status {
@@ -75,7 +75,10 @@ typedef enum fs_status {
   FS_ERR_HIP = 7                /* the HIP runtime reported an error           */
 } fs_status;
 
-typedef enum fs_dtype { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
+/* FS_U8 is a byte mask, accepted only as the mask_dtype of fs_row_softmax: a
+ * nonzero byte excludes its position (the additive value -inf), a zero byte
+ * keeps it (0).  Added in ABI version 2. */
+typedef enum fs_dtype { FS_F32 = 0, FS_BF16 = 1, FS_U8 = 2 } fs_dtype;
 
 typedef enum fs_act {
   FS_ACT_NONE = 0,
@@ -113,6 +116,12 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  *
  * x, y   : [rows, cols] of `dtype`; y may be x exactly (in place).
  * mask   : [rows, cols] of `mask_dtype` with row stride ld_mask, or NULL.
+ *          FS_U8 (a byte mask: nonzero = excluded, i.e. -inf; zero = 0) reads
+ *          1 byte per element instead of 2 or 4; it takes the 16-byte path of
+ *          x with 8-byte (bf16 x) or 4-byte (fp32 x) mask loads when the mask
+ *          rows start at multiples of that many bytes, else the element-wise
+ *          path.  The result is the same, bit for bit, as with the additive
+ *          mask of 0 and -inf it stands for.
  * causal_q_len > 0 additionally masks element (r, j) when
  *          j > (r mod causal_q_len) + (cols - causal_q_len); masked
  *          elements are not read and are written as +0.  0 = off.

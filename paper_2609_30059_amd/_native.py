@@ -26,11 +26,11 @@ FS_OK = 0
 STATUS_NAMES = {0: "FS_OK", 1: "FS_ERR_NULL_POINTER", 2: "FS_ERR_BAD_SHAPE",
                 3: "FS_ERR_BAD_STRIDE", 4: "FS_ERR_UNSUPPORTED_DTYPE", 5: "FS_ERR_ALIASING",
                 6: "FS_ERR_BAD_ARGUMENT", 7: "FS_ERR_HIP"}
-FS_F32, FS_BF16 = 0, 1
+FS_F32, FS_BF16, FS_U8 = 0, 1, 2
 ACTS = {"none": 0, "gelu_erf": 1, "sigmoid": 2, "relu": 3}
 REDUCES = {"sum": 0, "mean": 1}
 ROW_OPS = {"sum": 0, "mean": 1, "max": 2}
-FS_ABI_VERSION = 1
+FS_ABI_VERSION = 2
 FS_SOFTMAX_MAX_COLS = 16777216
 FS_LAYERNORM_MAX_COLS = 16777216
 

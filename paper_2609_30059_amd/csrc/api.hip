@@ -49,7 +49,8 @@ fs_status device_cus(int* cus) {
   return FS_OK;
 }
 
-int elem_size(fs_dtype d) { return d == FS_F32 ? 4 : 2; }
+int elem_size(fs_dtype d) { return d == FS_F32 ? 4 : d == FS_BF16 ? 2 : 1; }
+// data dtypes; the byte mask FS_U8 is accepted by fs_row_softmax's mask only
 bool dtype_ok(int d) { return d == FS_F32 || d == FS_BF16; }
 int vec_width(fs_dtype d) { return 16 / elem_size(d); }
 
@@ -108,8 +109,8 @@ fs_status check_ld(const char* name, int64_t ld, int64_t rows, int64_t cols) {
 // Row strides are only bounded by the overflow guard when there are several
 // rows, so the byte products below are taken in uint64 arithmetic: exact mod
 // 16, since 2^64 is a multiple of 16.
-bool vec_ok(const void* p, int64_t ld, int es) {
-  return p == nullptr || (aligned(p, 16) && (uint64_t(ld) * uint64_t(es)) % 16 == 0);
+bool vec_ok(const void* p, int64_t ld, int es, int unit = 16) {
+  return p == nullptr || (aligned(p, unit) && (uint64_t(ld) * uint64_t(es)) % uint64_t(unit) == 0);
 }
 
 // q (or NULL) starts every row at the same offset within a 16-byte unit as p
@@ -181,7 +182,7 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
                          float scale, int64_t causal_q_len, fs_dtype dtype, hipStream_t stream) {
   clear_msg();
   if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
-  if (mask && !dtype_ok(mask_dtype))
+  if (mask && !dtype_ok(mask_dtype) && mask_dtype != FS_U8)
     return fail(FS_ERR_UNSUPPORTED_DTYPE, "mask_dtype=%d", int(mask_dtype));
   if (!mask) mask_dtype = dtype;
   if (!std::isfinite(scale)) return fail(FS_ERR_BAD_ARGUMENT, "scale is not finite");
@@ -204,8 +205,10 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
 
   fs::SoftmaxArgs a{x, ld_x, mask, ld_mask, mask_dtype, y, ld_y, rows, cols, scale,
                     causal_q_len, dtype, false};
+  // the mask's share of a 16-byte vector of x: 16 bytes, or 8 / 4 of a byte mask
+  const int mask_unit = std::min(16, vec_width(dtype) * ms);
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
-          vec_ok(mask, ld_mask, ms);
+          vec_ok(mask, ld_mask, ms, mask_unit);
   a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && (mask == nullptr || ms == es) &&
               same_phase(x, ld_x, y, ld_y, es) && same_phase(x, ld_x, mask, ld_mask, es);
   int cus = 0;

@@ -137,15 +137,31 @@ __device__ __forceinline__ void ldv(const T* p, float* out) {
 // clamp out-of-range addresses onto an in-bounds vector and mask the values
 // afterwards, so the compiler can keep every load of a row in flight at once
 // (a load under a per-lane branch forces a wait for all older loads).
+// A byte mask (uint8_t) is held as loaded, four bytes per dword, and unpacks
+// to the additive value it stands for: -inf where the byte is nonzero (an
+// excluded position), 0 where it is zero.
 template <typename T, int V>
 struct Raw {
   static constexpr int kBytes = int(sizeof(T)) * V;
-  static constexpr int kWords = V == 1 ? 1 : kBytes / 4;
+  static constexpr int kWords = V == 1 ? 1 : (kBytes + 3) / 4;
   uint32_t w[kWords];
 
   template <bool NT = true>
   __device__ __forceinline__ void load(const T* p) {
-    if constexpr (V == 1) {
+    if constexpr (sizeof(T) == 1) {
+      static_assert(V == 1 || V == 4 || V == 8, "byte vectors of 1, 4 or 8");
+      if constexpr (V == 1) {
+        w[0] = *p;
+      } else if constexpr (V == 4) {
+        if constexpr (NT && kNtLoad) w[0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
+        else w[0] = *reinterpret_cast<const uint32_t*>(p);
+      } else {
+        u32x2 v;
+        if constexpr (NT && kNtLoad) v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+        else v = *reinterpret_cast<const u32x2*>(p);
+        w[0] = v.x; w[1] = v.y;
+      }
+    } else if constexpr (V == 1) {
       w[0] = __float_as_uint(Elem<T>::load1(p));
     } else if constexpr (kBytes == 16) {
       const u32x4 v = ld128<NT>(p);
@@ -163,7 +179,11 @@ struct Raw {
     }
   }
   __device__ __forceinline__ void unpack(float* out) const {
-    if constexpr (V == 1) {
+    if constexpr (sizeof(T) == 1) {
+#pragma unroll
+      for (int i = 0; i < V; ++i)
+        out[i] = ((w[i / 4] >> (8 * (i % 4))) & 0xffu) != 0u ? -INFINITY : 0.f;
+    } else if constexpr (V == 1) {
       out[0] = __uint_as_float(w[0]);
     } else if constexpr (sizeof(T) == 4) {
 #pragma unroll

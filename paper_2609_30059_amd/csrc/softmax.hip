@@ -774,10 +774,14 @@ hipError_t by_vec(const SoftmaxArgs& a, int cus, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s) {
-  const bool mbf16 = a.mask_dtype == FS_BF16;
-  if (a.dtype == FS_BF16)
-    return mbf16 ? by_vec<uint16_t, uint16_t>(a, cus, s) : by_vec<uint16_t, float>(a, cus, s);
-  return mbf16 ? by_vec<float, uint16_t>(a, cus, s) : by_vec<float, float>(a, cus, s);
+  if (a.dtype == FS_BF16) {
+    if (a.mask_dtype == FS_U8) return by_vec<uint16_t, uint8_t>(a, cus, s);
+    if (a.mask_dtype == FS_BF16) return by_vec<uint16_t, uint16_t>(a, cus, s);
+    return by_vec<uint16_t, float>(a, cus, s);
+  }
+  if (a.mask_dtype == FS_U8) return by_vec<float, uint8_t>(a, cus, s);
+  if (a.mask_dtype == FS_BF16) return by_vec<float, uint16_t>(a, cus, s);
+  return by_vec<float, float>(a, cus, s);
 }
 
 }  // namespace fs

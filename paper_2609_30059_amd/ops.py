@@ -147,9 +147,20 @@ def pointwise_chain(x: torch.Tensor, bias: Optional[torch.Tensor] = None,
     return out
 
 
+def mask_dtype(m: torch.Tensor) -> int:
+    """fs_dtype of a softmax mask: float32 and bfloat16 masks are additive;
+    bool and uint8 masks are byte masks (FS_U8), where a nonzero element
+    excludes its position (True = masked out, as in ``masked_fill``)."""
+    if m.dtype in (torch.bool, torch.uint8):
+        return N.FS_U8
+    return fs_dtype(m)
+
+
 def row_softmax(x: torch.Tensor, mask: Optional[torch.Tensor] = None, scale: float = 1.0,
                 causal_q_len: int = 0, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """softmax(x * scale + mask) along the last dim (fs_row_softmax)."""
+    """softmax(x * scale + mask) along the last dim (fs_row_softmax).  A bool
+    or uint8 mask excludes the positions where it is nonzero (see
+    ``mask_dtype``)."""
     rows, cols, ld_x = as_rows(x)
     if out is None:
         out = torch.empty_like(x, memory_format=torch.contiguous_format)
@@ -159,7 +170,7 @@ def row_softmax(x: torch.Tensor, mask: Optional[torch.Tensor] = None, scale: flo
     if mask is not None:
         if mask.shape != x.shape:
             raise ValueError("mask must have the shape of x")
-        ld_m, mdt = as_rows(mask)[2], fs_dtype(mask)
+        ld_m, mdt = as_rows(mask)[2], mask_dtype(mask)
     st = N.fs_row_softmax(x.data_ptr(), ld_x, _ptr(mask), ld_m, mdt, out.data_ptr(), ld_y, rows,
                           cols, float(scale), int(causal_q_len), fs_dtype(x), _stream())
     N.check("fs_row_softmax", st)

@@ -113,6 +113,31 @@ static void fixed_cases() {
              FS_ERR_BAD_ARGUMENT, "q_len");
   EXPECT(fs_row_softmax(P(A), 1 << 25, nullptr, 0, FS_BF16, W(B), 1 << 25, 4, FS_SOFTMAX_MAX_COLS + 1,
                         1.f, 0, FS_BF16, 0) == FS_ERR_BAD_SHAPE, "too wide");
+  // byte masks: the 16-byte path of x with 8-byte (bf16 x) or 4-byte (fp32 x)
+  // mask vectors; any byte address is accepted
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 8), 136, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             rec::sm.vec && rec::sm.mask_dtype == FS_U8, "byte mask, 8-byte vectors");
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 4), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.vec && !rec::sm.shifted, "byte mask off its 8-byte unit: element path");
+  EXPECT(fs_row_softmax(P(A), 128, P(C), 132, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.vec, "byte mask rows 132 bytes apart: element path");
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 4), 132, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_F32, 0) == FS_OK &&
+             rec::sm.vec, "byte mask, 4-byte vectors for fp32 x");
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 3), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_F32, 0) == FS_OK &&
+             !rec::sm.vec, "byte mask at an odd address");
+  EXPECT(fs_row_softmax(P(A), 1001, P(C), 1001, FS_U8, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.vec && !rec::sm.shifted, "byte mask: no aligned-body path");
+  EXPECT(fs_row_softmax(P(A), 128, P(B + 511), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) ==
+             FS_ERR_ALIASING, "byte mask's last byte inside y");
+  EXPECT(fs_row_softmax(P(A), 128, P(B + 1024 + 0), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK,
+         "byte mask just past y");
+  EXPECT(fs_row_softmax(P(A), 128, nullptr, 0, FS_BF16, W(B), 128, 4, 128, 0.125f, 0, FS_U8, 0) ==
+             FS_ERR_UNSUPPORTED_DTYPE, "bytes are a mask dtype only");
+  EXPECT(fs_pointwise_chain(P(A), 64, nullptr, nullptr, 0, W(B), 64, 4, 64, 1.f, FS_ACT_NONE, FS_U8, 0) ==
+             FS_ERR_UNSUPPORTED_DTYPE, "no byte pointwise chain");
+  EXPECT(fs_gemm_epilogue_reduce(P(A), 64, FS_BF16, P(C), FS_U8, nullptr, FS_ACT_NONE, FS_REDUCE_SUM,
+                                 reinterpret_cast<float*>(W(B)), 4, 64, 0) == FS_ERR_UNSUPPORTED_DTYPE,
+         "no byte bias");
   EXPECT(fs_causal_softmax_trimmed(P(A), 512, W(B), 512, 1024, 512, 0.125f, 512, 3, FS_BF16, 0) ==
              FS_ERR_BAD_ARGUMENT, "block not a power of two");
   EXPECT(fs_causal_softmax_trimmed(P(A), 512, W(B), 512, 1024, 512, 0.125f, 512, 128, FS_BF16, 0) == FS_OK &&

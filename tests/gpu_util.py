@@ -37,6 +37,8 @@ def dev(t: fd.Tensor, device="cuda") -> torch.Tensor:
         return None
     if t.dtype == "f32":
         return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
+    if t.dtype == "u8":
+        return torch.from_numpy(np.ascontiguousarray(t.data)).to(device)
     return torch.from_numpy(np.ascontiguousarray(t.data).view(np.int16)).view(
         torch.bfloat16).to(device)
 

@@ -1,0 +1,140 @@
+"""GPU parity of fs_row_softmax with a byte mask (FS_U8) against the float64
+oracle, and bit for bit against the same call with the additive {0, -inf}
+mask the bytes stand for (the kernels add the same fp32 values)."""
+import numpy as np
+import pytest
+import torch
+
+import fusedsub_data as fd
+import oracle
+import paper_2609_30059_amd as fs
+from gpu_util import (SEEDS, TOL, announce, assert_close, bf16_ulp_close, dev, host64,
+                      softmax_supplementary)
+
+pytestmark = pytest.mark.gpu
+
+
+def additive(d, dtype):
+    """The additive mask of d's byte mask, stored in `dtype` on the device."""
+    a = oracle.byte_mask_additive(d["mask"].data)
+    if dtype == "f32":
+        return torch.from_numpy(a.astype(np.float32)).cuda()
+    return torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).cuda()
+
+
+def bits(t):
+    return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
+
+
+def check(name, d, y, dtype, causal_q_len=0, y_additive=None):
+    got = host64(y)
+    ref = oracle.row_softmax(d["x"].f64(), oracle.byte_mask_additive(d["mask"].data),
+                             d["scale"], causal_q_len=causal_q_len)
+    assert_close(name, got, ref, *TOL[dtype])
+    if dtype == "bf16":
+        bf16_ulp_close(name, got, ref, ulps=1.0, atol=1e-7)
+    assert np.all(got[d["mask"].data != 0] == 0.0), name + ": masked entries not zero"
+    if y_additive is not None:
+        np.testing.assert_array_equal(bits(y), bits(y_additive), err_msg=name + " vs additive")
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_8192x4096_five_seeds_every_row(seed):
+    d = fd.softmax_inputs(seed, 8192, 4096, "bf16", mask_dtype="u8")
+    announce("softmax byte mask [8192, 4096]", seed)
+    x, m = dev(d["x"]), dev(d["mask"])
+    y = fs.row_softmax(x, m, d["scale"])
+    ya = fs.row_softmax(x, additive(d, "bf16"), d["scale"])
+    got = host64(y)
+    ref = oracle.row_softmax(d["x"].f64(), oracle.byte_mask_additive(d["mask"].data), d["scale"])
+    assert_close(f"seed {seed}", got, ref, *TOL["bf16"])
+    softmax_supplementary(f"seed {seed}", got, ref, d["mask"].data != 0)
+    np.testing.assert_array_equal(bits(y), bits(ya))
+
+
+def test_bool_mask_is_a_byte_mask():
+    d = fd.softmax_inputs(9, 64, 4096, "bf16", mask_dtype="u8")
+    announce("softmax bool mask")
+    x = dev(d["x"])
+    yb = fs.row_softmax(x, dev(d["mask"]) != 0, d["scale"])
+    yu = fs.row_softmax(x, dev(d["mask"]), d["scale"])
+    np.testing.assert_array_equal(bits(yb), bits(yu))
+    check("bool mask", d, yb, "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+# the vector and element-wise register rungs, the row cache (past 32768
+# columns) and its streamed tail (past 65536)
+@pytest.mark.parametrize("cols", [1, 3, 8, 37, 512, 513, 1000, 4096, 4104, 8192, 16392, 40000,
+                                  65536, 70000, 70001])
+def test_widths(dtype, cols):
+    rows = 7 if cols <= 16392 else 3
+    d = fd.softmax_inputs(cols + 1, rows, cols, dtype, mask_dtype="u8")
+    announce("softmax byte mask width", cols, dtype)
+    x = dev(d["x"])
+    y = fs.row_softmax(x, dev(d["mask"]), d["scale"])
+    ya = fs.row_softmax(x, additive(d, dtype), d["scale"])
+    # bit for bit where both masks take the same path: rows of whole 16-byte
+    # vectors, or too short for the aligned-body path (which a byte mask
+    # never takes; there the two differ only in summation order)
+    v = 8 if dtype == "bf16" else 4
+    same_path = cols % v == 0 or cols < 2 * v
+    check(f"cols {cols} {dtype}", d, y, dtype, y_additive=ya if same_path else None)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("offset", [0, 1, 4, 8])
+def test_mask_rows_at_any_byte_offset(dtype, offset):
+    # a [rows, cols] byte mask inside a wider buffer, its rows `ld` bytes
+    # apart, starting `offset` bytes in: 16-byte x with 4- or 8-byte mask
+    # vectors where the offsets allow, else the element-wise path
+    rows, cols, ld = 33, 2048, 2048 + 8
+    d = fd.softmax_inputs(50 + offset, rows, cols, dtype, mask_dtype="u8")
+    announce("softmax byte mask offset", offset, dtype)
+    buf = torch.full((rows * ld + 16,), 0xAB, dtype=torch.uint8, device="cuda")
+    view = buf[offset:offset + rows * ld].view(rows, ld)[:, :cols]
+    view.copy_(dev(d["mask"]))
+    x = dev(d["x"])
+    y = fs.row_softmax(x, view, d["scale"])
+    ya = fs.row_softmax(x, additive(d, dtype), d["scale"])
+    # the byte mask keeps the vector path when its rows start on its vector
+    # unit (8 bytes for bf16 x, 4 for fp32): bit for bit there
+    unit = 8 if dtype == "bf16" else 4
+    check(f"offset {offset} {dtype}", d, y, dtype,
+          y_additive=ya if offset % unit == 0 else None)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_causal_with_byte_mask(dtype):
+    # [2, 4, 512, 512] scores, causal over 512 positions and a byte mask on top
+    d = fd.softmax_inputs(77, 2 * 4 * 512, 512, dtype, mask_dtype="u8")
+    # keep the diagonal: every row then has a live entry under both masks
+    d["mask"].data[np.arange(4096), np.arange(4096) % 512] = 0
+    announce("softmax byte mask causal", dtype)
+    x = dev(d["x"])
+    y = fs.row_softmax(x, dev(d["mask"]), d["scale"], causal_q_len=512)
+    ya = fs.row_softmax(x, additive(d, dtype), d["scale"], causal_q_len=512)
+    check(f"causal {dtype}", d, y, dtype, causal_q_len=512, y_additive=ya)
+    upper = oracle.causal_mask(4096, 512, 512)
+    assert np.all(host64(y)[upper] == 0.0)
+
+
+@pytest.mark.parametrize("rows,cols", [(300000, 64), (2 * 256 + 3, 40000)])
+def test_rows_beyond_one_trip(rows, cols):
+    # more rows than the grid holds in one trip (one-wave rows), and more rows
+    # than compute units for the row cache: every row against the oracle
+    d = fd.softmax_inputs(rows, rows, cols, "bf16", mask_dtype="u8")
+    announce("softmax byte mask many rows", rows, cols)
+    x = dev(d["x"])
+    y = fs.row_softmax(x, dev(d["mask"]), d["scale"])
+    ya = fs.row_softmax(x, additive(d, "bf16"), d["scale"])
+    check(f"[{rows}, {cols}]", d, y, "bf16", y_additive=ya)
+
+
+def test_in_place_with_byte_mask():
+    d = fd.softmax_inputs(5, 40, 4096, "bf16", mask_dtype="u8")
+    announce("softmax byte mask in place")
+    x = dev(d["x"])
+    y = fs.row_softmax(x, dev(d["mask"]), d["scale"], out=x)
+    assert y.data_ptr() == x.data_ptr()
+    check("in place", d, y, "bf16")
