@@ -125,6 +125,16 @@ static void fixed_cases() {
              rec::sm.vec, "byte mask, 4-byte vectors for fp32 x");
   EXPECT(fs_row_softmax(P(A), 128, P(C + 3), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_F32, 0) == FS_OK &&
              !rec::sm.vec, "byte mask at an odd address");
+  // a bf16 mask beside fp32 x: 8 bytes of mask per 16-byte vector of x
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 8), 132, FS_BF16, W(B), 128, 4, 128, 0.125f, 0, FS_F32, 0) == FS_OK &&
+             rec::sm.vec, "bf16 mask on 8-byte boundaries with fp32 x");
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 4), 132, FS_BF16, W(B), 128, 4, 128, 0.125f, 0, FS_F32, 0) == FS_OK &&
+             !rec::sm.vec, "bf16 mask off its 8-byte unit");
+  // an fp32 mask beside bf16 x: 32 bytes of mask per vector, 16-byte loads
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 16), 132, FS_F32, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             rec::sm.vec, "fp32 mask on 16-byte boundaries with bf16 x");
+  EXPECT(fs_row_softmax(P(A), 128, P(C + 8), 132, FS_F32, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.vec, "fp32 mask off its 16-byte unit");
   EXPECT(fs_row_softmax(P(A), 1001, P(C), 1001, FS_U8, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
              !rec::sm.vec && !rec::sm.shifted, "byte mask: no aligned-body path");
   EXPECT(fs_row_softmax(P(A), 128, P(B + 511), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) ==

@@ -182,6 +182,28 @@ def test_strided_misaligned_in_place_and_guards(dtype):
         mg.check_untouched("softmax mask")
 
 
+@pytest.mark.parametrize("offset", [0, 4, 8])
+def test_bf16_mask_with_fp32_x_at_8_byte_offsets(offset):
+    # fp32 x reads 4 mask elements (8 bytes of a bf16 mask) per 16-byte vector:
+    # mask rows on 8-byte boundaries take the vector path, others the
+    # element-wise one; both against the oracle, and bit for bit against the
+    # same mask in a contiguous copy where both take the vector path
+    rows, cols, ld = 19, 2048, 2048 + 4              # mask rows 4104 bytes apart
+    d = fd.softmax_inputs(60 + offset, rows, cols, "f32", mask_dtype="bf16")
+    announce("softmax fp32 x, bf16 mask offset", offset)
+    buf = torch.zeros(rows * ld + 16, dtype=torch.bfloat16, device="cuda")
+    e = offset // 2
+    mview = buf[e:e + rows * ld].view(rows, ld)[:, :cols]
+    mview.copy_(dev(d["mask"]))
+    x = dev(d["x"])
+    y = fs.row_softmax(x, mview, d["scale"])
+    ref = oracle.row_softmax(d["x"].f64(), d["mask"].f64(), d["scale"])
+    assert_close(f"offset {offset}", host64(y), ref, *TOL["f32"])
+    if offset % 8 == 0:
+        yc = fs.row_softmax(x, dev(d["mask"]), d["scale"])
+        assert torch.equal(y.view(torch.int32), yc.view(torch.int32))
+
+
 def test_repeatable():
     d = fd.softmax_inputs(5, 64, 4096)
     x, m = dev(d["x"]), dev(d["mask"])
