@@ -117,11 +117,13 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  * x, y   : [rows, cols] of `dtype`; y may be x exactly (in place).
  * mask   : [rows, cols] of `mask_dtype` with row stride ld_mask, or NULL.
  *          FS_U8 (a byte mask: nonzero = excluded, i.e. -inf; zero = 0) reads
- *          1 byte per element instead of 2 or 4; it takes the 16-byte path of
- *          x with 8-byte (bf16 x) or 4-byte (fp32 x) mask loads when the mask
- *          rows start at multiples of that many bytes, else the element-wise
- *          path.  The result is the same, bit for bit, as with the additive
- *          mask of 0 and -inf it stands for.
+ *          1 byte per element instead of 2 or 4.  The 16-byte path of x reads
+ *          the mask elements of each x vector at once: 8 bytes (bf16 x) or 4
+ *          (fp32 x) of a byte mask, 8 of a bf16 mask beside fp32 x, 16 bytes
+ *          otherwise; it needs the mask's rows to start at multiples of that
+ *          many bytes, else the row takes the element-wise path.  A byte mask
+ *          gives the same result, bit for bit, as the additive mask of 0 and
+ *          -inf it stands for, on the same path.
  * causal_q_len > 0 additionally masks element (r, j) when
  *          j > (r mod causal_q_len) + (cols - causal_q_len); masked
  *          elements are not read and are written as +0.  0 = off.
