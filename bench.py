@@ -616,6 +616,7 @@ LONG_ROW_WIDTHS = (16392, 32768, 49152, 50257, 65536, 98304, 131072, 262144)
 # (name, dtype, bytes per element of one launch): compulsory reads + writes
 LONG_ROW_CASES = (
     ("softmax bf16 + bf16 mask", "bf16", 6),
+    ("softmax bf16 + byte mask", "bf16", 5),
     ("softmax bf16", "bf16", 4),
     ("softmax fp32", "f32", 8),
     ("LayerNorm + residual bf16", "bf16", 8),
@@ -644,9 +645,11 @@ def long_rows(reps: int = 9) -> None:
             y = torch.empty_like(x)
             if name.startswith("softmax"):
                 m = None
-                if "mask" in name:
+                if "bf16 mask" in name:
                     m = torch.where(torch.rand(rows, cols, device=dev, generator=g) < 0.1,
                                     float("-inf"), 0.0).to(tdt)
+                elif "byte mask" in name:
+                    m = (torch.rand(rows, cols, device=dev, generator=g) < 0.1).to(torch.uint8)
                 fn = lambda: fs.row_softmax(x, m, 0.125, out=y)
             else:
                 r = torch.randn(rows, cols, device=dev, generator=g).to(tdt)
@@ -689,6 +692,7 @@ def long_rows(reps: int = 9) -> None:
 ODD_ROW_WIDTHS = (1001, 4095, 16383)
 ODD_ROW_CASES = (
     ("softmax bf16 + bf16 mask", 6),
+    ("softmax bf16 + byte mask", 5),
     ("LayerNorm + residual bf16", 8),
     ("bias + GELU bf16", 4),
     ("GEMM epilogue bf16 (sigmoid, row sum)", 2),
@@ -714,8 +718,11 @@ def odd_rows(reps: int = 9) -> None:
         y = torch.empty_like(x)
         for name, bpe in ODD_ROW_CASES:
             if name.startswith("softmax"):
-                m = torch.where(torch.rand(rows, cols, device=dev, generator=g) < 0.1,
-                                float("-inf"), 0.0).to(torch.bfloat16)
+                masked = torch.rand(rows, cols, device=dev, generator=g) < 0.1
+                if "byte mask" in name:
+                    m = masked.to(torch.uint8)
+                else:
+                    m = torch.where(masked, float("-inf"), 0.0).to(torch.bfloat16)
                 fn = lambda: fs.row_softmax(x, m, 0.125, out=y)
             elif name.startswith("LayerNorm"):
                 r = rn(rows, cols).to(torch.bfloat16)

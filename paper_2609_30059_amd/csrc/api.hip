@@ -119,6 +119,15 @@ bool same_phase(const void* p, int64_t ld, const void* q, int64_t ldq, int es) {
          ((addr(p) - addr(q)) % 16 == 0 && ((uint64_t(ld) - uint64_t(ldq)) * uint64_t(es)) % 16 == 0);
 }
 
+// the byte mask q (or NULL) starts every row at the same element offset
+// within its v-byte unit as p (elements of es bytes) within its 16-byte unit:
+// the aligned body of p's rows then meets whole v-byte units of q's
+bool same_byte_phase(const void* p, int64_t ld, int es, const void* q, int64_t ldq, int v) {
+  return q == nullptr ||
+         ((addr(p) / uintptr_t(es) - addr(q)) % uintptr_t(v) == 0 &&
+          (uint64_t(ld) - uint64_t(ldq)) % uint64_t(v) == 0);
+}
+
 }  // namespace
 
 extern "C" {
@@ -209,8 +218,9 @@ fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t 
   const int mask_unit = std::min(16, vec_width(dtype) * ms);
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(mask, ld_mask, ms, mask_unit);
-  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && (mask == nullptr || ms == es) &&
-              same_phase(x, ld_x, y, ld_y, es) && same_phase(x, ld_x, mask, ld_mask, es);
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && same_phase(x, ld_x, y, ld_y, es) &&
+              (mask_dtype == FS_U8 ? same_byte_phase(x, ld_x, es, mask, ld_mask, vec_width(dtype))
+                                   : ms == es && same_phase(x, ld_x, mask, ld_mask, es));
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_softmax(a, cus, stream);

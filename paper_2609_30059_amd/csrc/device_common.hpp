@@ -92,6 +92,8 @@ template <> struct Elem<uint16_t> {   // bf16 bit patterns
 // is used keeps the wait for the load at the use, not at the load.
 __device__ __forceinline__ float raw_f32(float v) { return v; }
 __device__ __forceinline__ float raw_f32(uint16_t v) { return bf16_to_f32(v); }
+// a byte-mask element: the additive value it stands for
+__device__ __forceinline__ float raw_f32(uint8_t v) { return v != 0 ? -INFINITY : 0.f; }
 
 // 128-bit loads/stores.  Streaming data is touched once, so it is loaded and
 // stored non-temporally (it should not displace reused data from the caches);

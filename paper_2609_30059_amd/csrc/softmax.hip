@@ -684,7 +684,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
   const bool small_q = a.causal_q_len < (int64_t(1) << 30);
   // rows that share a 16-byte phase: the vector ladder over each row's
   // aligned body (a row of c columns has at most c / V whole vectors in it)
-  if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T))) {
+  if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T) || sizeof(MT) == 1)) {
     if (a.shifted && c <= FS_SM_SHIFT_REG_COLS) {
       constexpr int VS = Elem<T>::kVec;
 #define FS_SMS(Wv, E, Gv, BPC)                                                                  \
@@ -749,7 +749,7 @@ hipError_t dispatch(const SoftmaxArgs& a, int cus, hipStream_t s) {
       return hipGetLastError();
     };
     constexpr int64_t kSlot = int64_t(1024) * V;
-    if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T))) {
+    if constexpr (!VEC && (!HAS_MASK || sizeof(MT) == sizeof(T) || sizeof(MT) == 1)) {
       if (a.shifted) {
         // 16-byte slots over each row's aligned body
         constexpr int64_t kVSlot = int64_t(1024) * Elem<T>::kVec;

@@ -135,8 +135,20 @@ static void fixed_cases() {
              rec::sm.vec, "fp32 mask on 16-byte boundaries with bf16 x");
   EXPECT(fs_row_softmax(P(A), 128, P(C + 8), 132, FS_F32, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK &&
              !rec::sm.vec, "fp32 mask off its 16-byte unit");
+  // odd widths: the aligned-body path when the byte mask's rows start at x's
+  // element phase within their 8-byte (bf16 x) or 4-byte (fp32 x) units
   EXPECT(fs_row_softmax(P(A), 1001, P(C), 1001, FS_U8, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
-             !rec::sm.vec && !rec::sm.shifted, "byte mask: no aligned-body path");
+             !rec::sm.vec && rec::sm.shifted, "contiguous byte mask: aligned body");
+  EXPECT(fs_row_softmax(P(A + 6), 1001, P(C + 3), 1009, FS_U8, W(B + 6), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) ==
+             FS_OK && rec::sm.shifted, "byte mask at x's phase, rows 8 bytes wider");
+  EXPECT(fs_row_softmax(P(A), 1001, P(C + 1), 1001, FS_U8, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.vec && !rec::sm.shifted, "byte mask off x's phase: element path");
+  EXPECT(fs_row_softmax(P(A), 1001, P(C), 1005, FS_U8, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.shifted, "byte mask rows drifting from x's phase: element path");
+  EXPECT(fs_row_softmax(P(A + 4), 1001, P(C + 1), 1001, FS_U8, W(B + 4), 1001, 4, 1001, 0.125f, 0, FS_F32, 0) ==
+             FS_OK && rec::sm.shifted, "fp32 x one element in, byte mask one byte in");
+  EXPECT(fs_row_softmax(P(A), 1001, P(C), 1001, FS_F32, W(B), 1001, 4, 1001, 0.125f, 0, FS_BF16, 0) == FS_OK &&
+             !rec::sm.shifted, "fp32 mask beside bf16 x: element path");
   EXPECT(fs_row_softmax(P(A), 128, P(B + 511), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) ==
              FS_ERR_ALIASING, "byte mask's last byte inside y");
   EXPECT(fs_row_softmax(P(A), 128, P(B + 1024 + 0), 128, FS_U8, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK,

@@ -74,12 +74,10 @@ def test_widths(dtype, cols):
     x = dev(d["x"])
     y = fs.row_softmax(x, dev(d["mask"]), d["scale"])
     ya = fs.row_softmax(x, additive(d, dtype), d["scale"])
-    # bit for bit where both masks take the same path: rows of whole 16-byte
-    # vectors, or too short for the aligned-body path (which a byte mask
-    # never takes; there the two differ only in summation order)
-    v = 8 if dtype == "bf16" else 4
-    same_path = cols % v == 0 or cols < 2 * v
-    check(f"cols {cols} {dtype}", d, y, dtype, y_additive=ya if same_path else None)
+    # contiguous masks of either kind take the same path as each other (the
+    # vector path, the aligned body of rows that are not whole vectors, or
+    # the element-wise one): bit for bit
+    check(f"cols {cols} {dtype}", d, y, dtype, y_additive=ya)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -102,6 +100,29 @@ def test_mask_rows_at_any_byte_offset(dtype, offset):
     unit = 8 if dtype == "bf16" else 4
     check(f"offset {offset} {dtype}", d, y, dtype,
           y_additive=ya if offset % unit == 0 else None)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cols,ld,offset", [(1001, 1009, 0), (1001, 1009, 3), (1001, 1005, 0),
+                                            (4095, 4103, 5), (40001, 40009, 0), (70001, 70001, 1)])
+def test_odd_rows_with_strided_byte_masks(dtype, cols, ld, offset):
+    # rows that are not whole 16-byte vectors: a byte mask whose rows start
+    # at x's element phase within its 8-byte (bf16 x) or 4-byte (fp32 x)
+    # units shares x's aligned body; one that drifts (ld 1005) or starts off
+    # the phase takes the element-wise path.  x and y contiguous.
+    rows = 9 if cols < 30000 else 3
+    d = fd.softmax_inputs(cols + ld + offset, rows, cols, dtype, mask_dtype="u8")
+    announce("softmax byte mask odd rows", cols, ld, offset, dtype)
+    buf = torch.full((rows * ld + 16,), 0x5A, dtype=torch.uint8, device="cuda")
+    view = buf[offset:offset + rows * ld].view(rows, ld)[:, :cols]
+    view.copy_(dev(d["mask"]))
+    x = dev(d["x"])
+    y = fs.row_softmax(x, view, d["scale"])
+    ya = fs.row_softmax(x, additive(d, dtype), d["scale"])
+    v = 8 if dtype == "bf16" else 4
+    aligned_body = offset % v == 0 and (ld - cols) % v == 0
+    check(f"cols {cols} ld {ld} offset {offset} {dtype}", d, y, dtype,
+          y_additive=ya if aligned_body else None)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
