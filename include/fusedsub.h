@@ -121,9 +121,11 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  *          the mask elements of each x vector at once: 8 bytes (bf16 x) or 4
  *          (fp32 x) of a byte mask, 8 of a bf16 mask beside fp32 x, 16 bytes
  *          otherwise; it needs the mask's rows to start at multiples of that
- *          many bytes, else the row takes the element-wise path.  A byte mask
- *          gives the same result, bit for bit, as the additive mask of 0 and
- *          -inf it stands for, on the same path.
+ *          many bytes.  For rows that are not whole 16-byte vectors, a byte
+ *          mask whose rows start at x's element offset within those units
+ *          (contiguous tensors, for instance) shares x's aligned body below.
+ *          A byte mask gives the same result, bit for bit, as the additive
+ *          mask of 0 and -inf it stands for, on the same path.
  * causal_q_len > 0 additionally masks element (r, j) when
  *          j > (r mod causal_q_len) + (cols - causal_q_len); masked
  *          elements are not read and are written as +0.  0 = off.
@@ -137,8 +139,9 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  * Rows that are not whole 16-byte vectors load one element per lane, except
  * rows of at least two vectors whose x, mask (of x's dtype) and y start each
  * row at the same offset within a 16-byte unit (contiguous tensors, for
- * instance): there the aligned body of every row is loaded 16 bytes at a
- * time.  Rows may be up to FS_SOFTMAX_MAX_COLS columns.
+ * instance), or with a byte mask at x's element phase: there the aligned
+ * body of every row is loaded 16 bytes at a time.  Rows may be up to
+ * FS_SOFTMAX_MAX_COLS columns.
  * scale must be finite; mask values may be any float or -inf.
  */
 #define FS_SOFTMAX_MAX_COLS 16777216
