@@ -47,7 +47,7 @@ from scipy import special as _sp
 
 __all__ = [
     "ACTS", "gelu_erf", "sigmoid", "relu", "apply_act",
-    "pointwise_chain", "causal_mask", "byte_mask_additive", "row_softmax", "layernorm_residual",
+    "pointwise_chain", "PROGRAM_OPS", "pointwise_program", "causal_mask", "byte_mask_additive", "row_softmax", "layernorm_residual",
     "rmsnorm_residual", "residual_store_bf16", "round_to_bf16", "gemm_epilogue_reduce",
     "row_reduce", "row_argmax",
 ]
@@ -106,6 +106,73 @@ def pointwise_chain(x, bias=None, residual=None, scale: float = 1.0, act: str = 
     if residual is not None:
         y = y + np.asarray(residual, dtype=np.float64)
     return y
+
+
+# ---------------------------------------------------------------------------
+# a1, general form: a fused pointwise program
+# ---------------------------------------------------------------------------
+# Each operation maps the running value v (starting at x) to a new value;
+# the names and their parameters:
+PROGRAM_OPS = {
+    "scale": 1,          # v * a
+    "shift": 1,          # v + a
+    "add_bias": 0,       # v + bias[j]
+    "mul_column": 0,     # v * col[j]
+    "add_residual": 0,   # v + residual[r, j]
+    "mul_residual": 0,   # v * residual[r, j]
+    "clamp": 2,          # min(max(v, a), b)  (hardtanh for a = -1, b = 1)
+    "gelu_erf": 0,       # v * Phi(v)
+    "sigmoid": 0,        # 1 / (1 + exp(-v))
+    "relu": 0,           # max(v, 0)
+    "tanh": 0,           # tanh(v)
+    "silu": 0,           # v * sigmoid(v)
+    "leaky_relu": 1,     # v if v >= 0 else a * v
+}
+
+
+def pointwise_program(x, ops, bias=None, col=None, residual=None):
+    """y = f_n(... f_1(x) ...) elementwise, each f_i an operation of
+    ``PROGRAM_OPS`` given as (name, *params).
+
+    The general form of the fused pointwise chain: a compiled graph's group
+    of adjacent elementwise operations (a linear layer's output followed by
+    a multiply, a hardtanh and a GELU, say) evaluated as one pass (Section 3,
+    merging adjacent fusible kernels; Appendix A, Fusion Agent: pointwise +
+    pointwise, activation + bias fusion).  ``bias`` and ``col`` are [cols]
+    vectors broadcast over rows; ``residual`` has the shape of ``x``.
+    """
+    v = np.asarray(x, dtype=np.float64)
+    for op in ops:
+        name, prm = op[0], [float(p) for p in op[1:]]
+        if name not in PROGRAM_OPS or len(prm) != PROGRAM_OPS[name]:
+            raise ValueError(f"bad program operation {op!r}")
+        if name == "scale":
+            v = v * prm[0]
+        elif name == "shift":
+            v = v + prm[0]
+        elif name == "add_bias":
+            v = v + np.asarray(bias, dtype=np.float64)[None, :]
+        elif name == "mul_column":
+            v = v * np.asarray(col, dtype=np.float64)[None, :]
+        elif name == "add_residual":
+            v = v + np.asarray(residual, dtype=np.float64)
+        elif name == "mul_residual":
+            v = v * np.asarray(residual, dtype=np.float64)
+        elif name == "clamp":
+            v = np.minimum(np.maximum(v, prm[0]), prm[1])
+        elif name == "gelu_erf":
+            v = gelu_erf(v)
+        elif name == "sigmoid":
+            v = sigmoid(v)
+        elif name == "relu":
+            v = relu(v)
+        elif name == "tanh":
+            v = np.tanh(v)
+        elif name == "silu":
+            v = v * sigmoid(v)
+        else:   # leaky_relu
+            v = np.where(v >= 0.0, v, prm[0] * v)
+    return v
 
 
 # ---------------------------------------------------------------------------

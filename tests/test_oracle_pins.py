@@ -99,6 +99,66 @@ class TestPointwise:
               1 / (1 + math.exp(-0.5)), 1 / (1 + math.exp(-2))]], rtol=1e-15)
 
 
+class TestPointwiseProgram:
+    def test_empty_program_is_identity(self):
+        x = np.array([[1.5, -2.0, 0.0]])
+        np.testing.assert_array_equal(oracle.pointwise_program(x, []), x)
+
+    def test_order_is_the_listed_order(self):
+        x = np.array([[3.0]])
+        assert oracle.pointwise_program(x, [("scale", 2), ("shift", 1)])[0, 0] == 7.0
+        assert oracle.pointwise_program(x, [("shift", 1), ("scale", 2)])[0, 0] == 8.0
+
+    def test_linear_mul_hardtanh_gelu_chain(self):
+        # the paper's fused group (a multiply, a hardtanh, a GELU after a
+        # linear layer) on values whose results the normal table gives:
+        # 3 * 0.5 = 1.5 clamps to 1 -> Phi(1); 1 * 0.5 = 0.5 passes ->
+        # 0.5 Phi(0.5); -1 * 0.5 -> -0.5 Phi(-0.5) = -0.5 (1 - Phi(0.5));
+        # -8 * 0.5 = -4 clamps to -1 -> -(1 - Phi(1))
+        x = np.array([[3.0, 1.0, -1.0, -8.0]])
+        y = oracle.pointwise_program(x, [("scale", 0.5), ("clamp", -1, 1), ("gelu_erf",)])
+        want = [PHI[1.0], 0.5 * PHI[0.5], -0.5 * (1 - PHI[0.5]), -(1 - PHI[1.0])]
+        np.testing.assert_allclose(y[0], want, rtol=0, atol=1e-15)
+
+    def test_clamp_leaky_relu_and_relu(self):
+        x = np.array([[-2.0, -0.5, 0.0, 0.5, 2.0]])
+        np.testing.assert_array_equal(oracle.pointwise_program(x, [("clamp", -1, 1)]),
+                                      [[-1, -0.5, 0, 0.5, 1]])
+        np.testing.assert_allclose(oracle.pointwise_program(x, [("leaky_relu", 0.1)]),
+                                   [[-0.2, -0.05, 0, 0.5, 2.0]], rtol=1e-15)
+        np.testing.assert_array_equal(oracle.pointwise_program(x, [("relu",)]),
+                                      [[0, 0, 0, 0.5, 2.0]])
+
+    def test_tanh_and_silu_closed_forms(self):
+        # tanh(ln(3) / 2) = (3 - 1) / (3 + 1) = 1/2 and tanh is odd;
+        # silu(ln 3) = ln 3 * 3/4 (sigmoid(ln 3) = 3/4), silu(0) = 0,
+        # silu(-ln 3) = -ln 3 / 4
+        l3 = math.log(3.0)
+        y = oracle.pointwise_program(np.array([[l3 / 2, -l3 / 2, 0.0]]), [("tanh",)])
+        np.testing.assert_allclose(y[0], [0.5, -0.5, 0.0], rtol=1e-15, atol=1e-16)
+        y = oracle.pointwise_program(np.array([[l3, 0.0, -l3]]), [("silu",)])
+        np.testing.assert_allclose(y[0], [0.75 * l3, 0.0, -0.25 * l3], rtol=1e-15)
+        y = oracle.pointwise_program(np.array([[l3]]), [("sigmoid",)])
+        assert y[0, 0] == pytest.approx(0.75, rel=1e-15)
+
+    def test_vectors_broadcast_per_column_and_residual_per_element(self):
+        x = np.array([[1.0, 2.0], [3.0, 4.0]])
+        b = np.array([10.0, 20.0])
+        c = np.array([2.0, -1.0])
+        r = np.array([[1.0, 0.0], [-1.0, 5.0]])
+        y = oracle.pointwise_program(x, [("add_bias",), ("mul_column",), ("add_residual",)],
+                                     bias=b, col=c, residual=r)
+        np.testing.assert_array_equal(y, [[23.0, -22.0], [25.0, -19.0]])
+        y = oracle.pointwise_program(x, [("mul_residual",)], residual=r)
+        np.testing.assert_array_equal(y, [[1.0, 0.0], [-3.0, 20.0]])
+
+    def test_rejects_unknown_or_malformed_operations(self):
+        with pytest.raises(ValueError):
+            oracle.pointwise_program(np.zeros((1, 1)), [("softplus",)])
+        with pytest.raises(ValueError):
+            oracle.pointwise_program(np.zeros((1, 1)), [("clamp", -1)])
+
+
 # ---------------------------------------------------------------------------
 # a2 row softmax
 # ---------------------------------------------------------------------------
