@@ -428,6 +428,37 @@ class Workload:
         del scrub
         return tuple(sorted(t)[reps // 2] * 1e3 for t in ts)
 
+    def pointwise_program(self, reps):
+        """Median launch intervals of a fused pointwise program -- bias, a
+        multiply, a hardtanh and a GELU on the block's bf16 [16384, 4096]
+        MLP activations -- and, alternating with it, of the fixed bias + GELU
+        chain on the same tensors; each launch after a read-only pass over
+        1 GiB, with its own events.  Returns (program us, chain us, bytes)."""
+        torch, fs = self.torch, self.fs
+        g = torch.Generator(device="cuda").manual_seed(7)
+        x = (0.5 * torch.randn(16384, 4096, device="cuda", generator=g)).to(torch.bfloat16)
+        b = (0.02 * torch.randn(4096, device="cuda", generator=g)).to(torch.bfloat16)
+        y = torch.empty_like(x)
+        ops = [("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0), ("gelu_erf",)]
+        scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")
+        sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+        fns = [lambda: fs.pointwise_program(x, ops, bias=b, out=y),
+               lambda: fs.pointwise_chain(x, b, None, 1.0, "gelu_erf", out=y)]
+        ts = [[], []]
+        for rep in range(reps + 1):            # the first repetition is a warm-up
+            for i, fn in enumerate(fns):
+                fs.row_reduce(scrub, "sum", out=sink)
+                e0, e1 = TimingEvent(), TimingEvent()
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                if rep:
+                    ts[i].append(e0.elapsed_time(e1))
+        del scrub, x, y
+        nbytes = 16384 * 4096 * 2 * 2 + 4096 * 2
+        return (*(sorted(t)[reps // 2] * 1e3 for t in ts), nbytes)
+
     def same_size_copies(self, sizes, reps):
         """Median interval of a calibration copy moving the same number of
         bytes as each kernel (half read, half written), timed like the
@@ -1399,6 +1430,7 @@ def main():
     bw_bytes = STEP_BYTES["pw_262144x1024"]
     sm8_us, sm_add_us = wl.softmax_byte_mask(max(args.steps // 5, 5))
     sm8_bytes = 8192 * 4096 * (2 + 1 + 2)
+    prog_us, prog_chain_us, prog_bytes = wl.pointwise_program(max(args.steps // 5, 5))
 
     # access-shape floors (libaccessfloor.so): K steps of the step's launches
     # each replaced by its floor, timed like the per-kernel pass.  Last of the
@@ -1487,6 +1519,14 @@ def main():
                         "GB/s": round(sm8_bytes / (sm8_us * 1e-6) / 1e9, 1),
                         "frac": round(sm8_bytes / (sm8_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                         "additive_bf16_mask_us": round(sm_add_us, 2),
+                        "note": "each launch after a 1 GiB read-only pass, with its own events"},
+                    "pointwise_program": {
+                        "ops": "add_bias, scale 0.5, clamp [-1, 1], gelu_erf",
+                        "shape": [16384, 4096], "dtype": "bf16", "bytes": prog_bytes,
+                        "us": round(prog_us, 2),
+                        "GB/s": round(prog_bytes / (prog_us * 1e-6) / 1e9, 1),
+                        "frac": round(prog_bytes / (prog_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                        "fixed_bias_gelu_chain_us": round(prog_chain_us, 2),
                         "note": "each launch after a 1 GiB read-only pass, with its own events"},
                     "block_forward_ms_with_gemms": round(wl.block_e2e_ms, 3),
                     "gemm_8192x8192x4096_ms": round(wl.gemm_8192x8192x4096_ms, 3),

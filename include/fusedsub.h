@@ -108,6 +108,51 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
                              fs_dtype dtype, hipStream_t stream);
 
 /*
+ * Fused pointwise program: the general form of the chain above, for the
+ * groups of adjacent elementwise operations a compiled graph merges into one
+ * kernel (Section 3: adjacent fusible groups, e.g. a multiply, a hardtanh and
+ * a GELU after a linear layer; Appendix A, Fusion Agent: pointwise +
+ * pointwise, activation + bias fusion).
+ *
+ *   v = x[r, j];  for i < n_ops: v = op_i(v);  y[r, j] = v
+ *
+ * Every step is evaluated in fp32 registers (one rounding per step); y is
+ * rounded to `dtype` once.  x, residual, y: [rows, cols] of `dtype` with row
+ * strides ld_x, ld_r, ld_y; bias, col: [cols] of `dtype`.  bias, col and
+ * residual may be NULL unless an operation reads them (FS_ERR_NULL_POINTER).
+ * y may be x or residual exactly (in place) and must not overlap bias or
+ * col.  ops: n_ops (0 ... FS_PROGRAM_MAX_OPS) operations, read on the host
+ * during the call (the caller keeps ownership); a and b as listed, finite
+ * (clamp bounds may be infinite, with a <= b), else FS_ERR_BAD_ARGUMENT.
+ * Rows of whole 16-byte vectors are read and written 16 bytes at a time;
+ * other rows element by element.
+ */
+#define FS_PROGRAM_MAX_OPS 16
+typedef enum fs_op_code {
+  FS_OP_SCALE = 0,          /* v * a                                       */
+  FS_OP_SHIFT = 1,          /* v + a                                       */
+  FS_OP_ADD_BIAS = 2,       /* v + bias[j]                                 */
+  FS_OP_MUL_COLUMN = 3,     /* v * col[j]                                  */
+  FS_OP_ADD_RESIDUAL = 4,   /* v + residual[r, j]                          */
+  FS_OP_MUL_RESIDUAL = 5,   /* v * residual[r, j]                          */
+  FS_OP_CLAMP = 6,          /* min(max(v, a), b); hardtanh: a = -1, b = 1  */
+  FS_OP_GELU_ERF = 7,       /* v * (1 + erf(v / sqrt 2)) / 2               */
+  FS_OP_SIGMOID = 8,        /* 1 / (1 + exp(-v))                           */
+  FS_OP_RELU = 9,           /* max(v, 0)                                   */
+  FS_OP_TANH = 10,          /* tanh(v)                                     */
+  FS_OP_SILU = 11,          /* v * sigmoid(v)                              */
+  FS_OP_LEAKY_RELU = 12     /* v >= 0 ? v : a * v                          */
+} fs_op_code;
+typedef struct fs_op {
+  int32_t code;             /* an fs_op_code                               */
+  float a, b;               /* parameters (unused ones are ignored)        */
+} fs_op;
+FS_API fs_status fs_pointwise_program(const void* x, int64_t ld_x, const fs_op* ops, int n_ops,
+                                      const void* bias, const void* col, const void* residual,
+                                      int64_t ld_r, void* y, int64_t ld_y, int64_t rows,
+                                      int64_t cols, fs_dtype dtype, hipStream_t stream);
+
+/*
  * Fused row softmax with pre-scale and additive mask (Appendix A, Planner
  * item 9 and Codegen prompt: fused softmax, online softmax).
  *

@@ -9,8 +9,8 @@ library raises ``NativeLibraryError`` -- there is no CPU fallback.
 from ._native import (FS_LAYERNORM_MAX_COLS, FS_SOFTMAX_MAX_COLS, FusedSubError,  # noqa: F401
                       GemmError, NativeLibraryError)
 from .ops import (as_rows, causal_softmax_trimmed, copy_, copy_strided, gemm, gemm_epilogue_reduce, gemm_strided_batched,  # noqa: F401
-                  layernorm_residual, pointwise_chain, rmsnorm_residual, row_argmax, row_reduce,
-                  row_softmax)
+                  layernorm_residual, pointwise_chain, pointwise_program, rmsnorm_residual,
+                  row_argmax, row_reduce, row_softmax)
 from .block import TransformerBlock  # noqa: F401
 
 __version__ = "0.1.0"

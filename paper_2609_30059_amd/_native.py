@@ -35,7 +35,8 @@ FS_SOFTMAX_MAX_COLS = 16777216
 FS_LAYERNORM_MAX_COLS = 16777216
 
 # every symbol the headers declare
-FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_row_softmax", "fs_causal_softmax_trimmed",
+FUSEDSUB_SYMBOLS = ("fs_pointwise_chain", "fs_pointwise_program", "fs_row_softmax",
+                    "fs_causal_softmax_trimmed",
                     "fs_layernorm_residual",
                     "fs_rmsnorm_residual", "fs_row_reduce", "fs_row_argmax",
                     "fs_gemm_epilogue_reduce", "fs_copy_strided", "fs_copy",
@@ -59,8 +60,23 @@ _I64 = ctypes.c_int64
 _I = ctypes.c_int
 _F = ctypes.c_float
 
+FS_PROGRAM_MAX_OPS = 16
+# fs_op_code by the oracle's operation names, with the parameter count
+PROGRAM_OPS = {"scale": (0, 1), "shift": (1, 1), "add_bias": (2, 0), "mul_column": (3, 0),
+               "add_residual": (4, 0), "mul_residual": (5, 0), "clamp": (6, 2),
+               "gelu_erf": (7, 0), "sigmoid": (8, 0), "relu": (9, 0), "tanh": (10, 0),
+               "silu": (11, 0), "leaky_relu": (12, 1)}
+
+
+class FsOp(ctypes.Structure):
+    """struct fs_op of fusedsub.h."""
+    _fields_ = [("code", ctypes.c_int32), ("a", ctypes.c_float), ("b", ctypes.c_float)]
+
+
 _SIGS = {
     "fs_pointwise_chain": [_P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64, _F, _I, _I, _P],
+    "fs_pointwise_program": [_P, _I64, ctypes.POINTER(FsOp), _I, _P, _P, _P, _I64, _P, _I64, _I64,
+                             _I64, _I, _P],
     "fs_row_softmax": [_P, _I64, _P, _I64, _I, _P, _I64, _I64, _I64, _F, _I64, _I, _P],
     "fs_layernorm_residual": [_P, _I64, _P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _F, _I,
                               _P],
@@ -139,6 +155,12 @@ def fs_pointwise_chain(x, ld_x, bias, residual, ld_r, y, ld_y, rows, cols, scale
                        stream):
     return fusedsub().fs_pointwise_chain(x, ld_x, bias, residual, ld_r, y, ld_y, rows, cols,
                                          scale, act, dtype, stream)
+
+
+def fs_pointwise_program(x, ld_x, ops, n_ops, bias, col, residual, ld_r, y, ld_y, rows, cols,
+                         dtype, stream):
+    return fusedsub().fs_pointwise_program(x, ld_x, ops, n_ops, bias, col, residual, ld_r, y, ld_y,
+                                           rows, cols, dtype, stream)
 
 
 def fs_row_softmax(x, ld_x, mask, ld_mask, mask_dtype, y, ld_y, rows, cols, scale, causal_q_len,

@@ -186,6 +186,75 @@ fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bias, cons
   return e == hipSuccess ? FS_OK : hip_fail(e, "pointwise_chain launch");
 }
 
+fs_status fs_pointwise_program(const void* x, int64_t ld_x, const fs_op* ops, int n_ops,
+                               const void* bias, const void* col, const void* residual,
+                               int64_t ld_r, void* y, int64_t ld_y, int64_t rows, int64_t cols,
+                               fs_dtype dtype, hipStream_t stream) {
+  clear_msg();
+  if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
+  if (n_ops < 0 || n_ops > FS_PROGRAM_MAX_OPS)
+    return fail(FS_ERR_BAD_ARGUMENT, "n_ops=%d outside 0..%d", n_ops, FS_PROGRAM_MAX_OPS);
+  if (n_ops > 0 && !ops) return fail(FS_ERR_NULL_POINTER, "ops is NULL with n_ops=%d", n_ops);
+  fs::ProgramArgs a{};
+  bool need_bias = false, need_col = false, need_res = false;
+  for (int k = 0; k < n_ops; ++k) {
+    const fs_op& o = ops[k];
+    switch (o.code) {
+      case FS_OP_SCALE: case FS_OP_SHIFT: case FS_OP_LEAKY_RELU:
+        if (!std::isfinite(o.a)) return fail(FS_ERR_BAD_ARGUMENT, "ops[%d].a is not finite", k);
+        break;
+      case FS_OP_CLAMP:
+        if (std::isnan(o.a) || std::isnan(o.b) || o.a > o.b)
+          return fail(FS_ERR_BAD_ARGUMENT, "ops[%d]: clamp bounds must be ordered, not NaN", k);
+        break;
+      case FS_OP_ADD_BIAS: need_bias = true; break;
+      case FS_OP_MUL_COLUMN: need_col = true; break;
+      case FS_OP_ADD_RESIDUAL: case FS_OP_MUL_RESIDUAL: need_res = true; break;
+      case FS_OP_GELU_ERF: case FS_OP_SIGMOID: case FS_OP_RELU: case FS_OP_TANH: case FS_OP_SILU:
+        break;
+      default: return fail(FS_ERR_BAD_ARGUMENT, "ops[%d].code=%d", k, int(o.code));
+    }
+    a.prog.code[k] = o.code;
+    a.prog.a[k] = o.a;
+    a.prog.b[k] = o.b;
+  }
+  a.prog.n = n_ops;
+  fs_status st = check_shape(rows, cols, INT32_MAX / 2);
+  if (st != FS_OK) return st;
+  if ((st = check_ld("ld_x", ld_x, rows, cols)) != FS_OK) return st;
+  if ((st = check_ld("ld_y", ld_y, rows, cols)) != FS_OK) return st;
+  if (need_res && (st = check_ld("ld_r", ld_r, rows, cols)) != FS_OK) return st;
+  if (rows == 0 || cols == 0) return FS_OK;
+  if (!x || !y) return fail(FS_ERR_NULL_POINTER, "x and y are required");
+  if ((need_bias && !bias) || (need_col && !col) || (need_res && !residual))
+    return fail(FS_ERR_NULL_POINTER, "the program reads a NULL bias, col or residual");
+  // operands the program does not read are not touched
+  if (!need_bias) bias = nullptr;
+  if (!need_col) col = nullptr;
+  if (!need_res) residual = nullptr;
+  const int es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(y, es) || !aligned(bias, es) || !aligned(col, es) ||
+      !aligned(residual, es))
+    return fail(FS_ERR_BAD_ARGUMENT, "pointers must be aligned to the element size");
+  const Extent ex = mat_extent(x, rows, cols, ld_x, es), ey = mat_extent(y, rows, cols, ld_y, es);
+  const Extent er = residual ? mat_extent(residual, rows, cols, ld_r, es) : Extent{};
+  const Extent eb = bias ? vec_extent(bias, cols, es) : Extent{};
+  const Extent ec = col ? vec_extent(col, cols, es) : Extent{};
+  if ((overlap(ey, ex) && !identical(ey, ex)) || (overlap(ey, er) && !identical(ey, er)) ||
+      overlap(ey, eb) || overlap(ey, ec))
+    return fail(FS_ERR_ALIASING, "y overlaps an input other than exactly x or residual");
+
+  a.x = x; a.ld_x = ld_x; a.bias = bias; a.col = col; a.res = residual; a.ld_r = ld_r;
+  a.y = y; a.ld_y = ld_y; a.rows = rows; a.cols = cols; a.dtype = dtype;
+  a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
+          vec_ok(residual, ld_r, es) && (bias == nullptr || aligned(bias, 16)) &&
+          (col == nullptr || aligned(col, 16));
+  int cus = 0;
+  if ((st = device_cus(&cus)) != FS_OK) return st;
+  hipError_t e = fs::launch_program(a, cus, stream);
+  return e == hipSuccess ? FS_OK : hip_fail(e, "pointwise_program launch");
+}
+
 fs_status fs_row_softmax(const void* x, int64_t ld_x, const void* mask, int64_t ld_mask,
                          fs_dtype mask_dtype, void* y, int64_t ld_y, int64_t rows, int64_t cols,
                          float scale, int64_t causal_q_len, fs_dtype dtype, hipStream_t stream) {

@@ -64,7 +64,7 @@ __device__ __forceinline__ float epi_act(float u) {
   } else if constexpr (ACT == FS_ACT_GELU_ERF) {
     return gelu_erf(u);
   } else if constexpr (ACT == FS_ACT_RELU) {
-    return u > 0.f ? u : 0.f;
+    return u < 0.f ? 0.f : u;   // a NaN stays NaN
   } else {
     return u;
   }

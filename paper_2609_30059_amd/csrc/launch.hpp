@@ -70,6 +70,25 @@ struct EpilogueArgs {
 
 // `cus` is the compute-unit count of the current device.
 hipError_t launch_pointwise(const PointwiseArgs& a, int cus, hipStream_t s);
+// A pointwise program as the kernel takes it: by value, in the argument block.
+struct Program {
+  int n;
+  int32_t code[FS_PROGRAM_MAX_OPS];
+  float a[FS_PROGRAM_MAX_OPS], b[FS_PROGRAM_MAX_OPS];
+};
+
+struct ProgramArgs {
+  const void* x; int64_t ld_x;
+  const void* bias; const void* col;
+  const void* res; int64_t ld_r;   // NULL unless an operation reads it
+  void* y; int64_t ld_y;
+  int64_t rows, cols;
+  fs_dtype dtype;
+  bool vec;
+  Program prog;
+};
+
+hipError_t launch_program(const ProgramArgs& a, int cus, hipStream_t s);
 hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s);
 hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs& a, int cus, hipStream_t s);

@@ -42,7 +42,7 @@ __device__ __forceinline__ float act_fn(float z) {
   } else if constexpr (ACT == FS_ACT_SIGMOID) {
     return sigmoid(z);
   } else if constexpr (ACT == FS_ACT_RELU) {
-    return z > 0.f ? z : 0.f;
+    return z < 0.f ? 0.f : z;   // a NaN stays NaN
   } else {
     return z;
   }

@@ -1,0 +1,162 @@
+// Fused pointwise program: y = op_n(... op_1(x) ...), the operations of
+// fs_op_code applied in fp32 registers, one load of every input and one
+// store of y.
+//
+// KernelOPT merges adjacent fusible elementwise kernels of a compiled graph
+// into one (Section 3; its example group is a multiply, a hardtanh and a
+// GELU after a linear layer) and fuses pointwise chains and activations
+// with their bias (Appendix A, Fusion Agent).  The fixed chain of
+// pointwise.hip covers act(x * s + b) + r; this kernel takes the group as
+// data, so one compiled kernel serves every such group.
+//
+// Design (gfx950): the launch shape of the pointwise chain -- a block of 256
+// threads owns a slab of 256 column vectors (16 bytes each) and walks down
+// the rows, U rows per trip with all their loads issued before any use; the
+// column vectors (bias, col) stay in registers.  The program sits in the
+// kernel's argument block and is read with scalar loads: the operation loop
+// is uniform across the wave, outside the loops over the trip's U x V
+// values, so each operation costs one scalar branch per trip and the
+// arithmetic of the U x V values it applies to.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+#ifndef FS_PROG_ROWS_PER_TRIP
+#define FS_PROG_ROWS_PER_TRIP 4
+#endif
+#ifndef FS_PROG_BLOCKS_PER_CU
+#define FS_PROG_BLOCKS_PER_CU 16
+#endif
+
+namespace fs {
+namespace {
+
+constexpr int kBlock = 256;
+
+// tanh(v) = sign(v) (1 - e) / (1 + e) with e = exp(-2 |v|) in (0, 1]: no
+// overflow for any v, +-1 at +-inf, NaN for NaN; absolute error a few units
+// of 2^-24 (relative error larger only where |tanh v| is below about 1e-3)
+__device__ __forceinline__ float tanh_fn(float v) {
+  const float e = __builtin_amdgcn_exp2f(-2.f * kLog2e * fabsf(v));
+  return copysignf((1.f - e) * __builtin_amdgcn_rcpf(1.f + e), v);
+}
+
+template <typename T, bool HAS_RES, bool VEC, int U>
+__global__ __launch_bounds__(kBlock) void program_kernel(
+    const T* x, int64_t ld_x, const T* __restrict__ bias, const T* __restrict__ col, const T* res,
+    int64_t ld_r, T* y, int64_t ld_y, int64_t rows, int cols, int col_blocks, Program prog) {
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  const int cb = blockIdx.x % col_blocks;
+  const int64_t rg = blockIdx.x / col_blocks;
+  const int64_t nrg = gridDim.x / col_blocks;
+  const int c0 = (cb * kBlock + threadIdx.x) * V;
+  if (c0 >= cols) return;               // no barriers below: early exit is safe
+
+  float bv[V], cv[V];
+#pragma unroll
+  for (int i = 0; i < V; ++i) bv[i] = cv[i] = 0.f;
+  if (bias) {
+    Raw<T, V> rb;
+    rb.template load<false>(bias + c0);
+    rb.unpack(bv);
+  }
+  if (col) {
+    Raw<T, V> rc;
+    rc.template load<false>(col + c0);
+    rc.unpack(cv);
+  }
+
+  for (int64_t r0 = rg * U; r0 < rows; r0 += nrg * U) {
+    // all loads of the trip first; rows past the end re-read the last row
+    // (in bounds) and are not stored
+    Raw<T, V> rx[U], rr[HAS_RES ? U : 1];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t r = r0 + u < rows ? r0 + u : rows - 1;
+      rx[u].load(x + r * ld_x + c0);
+      if constexpr (HAS_RES) rr[u].load(res + r * ld_r + c0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    float v[U][V], rv[HAS_RES ? U : 1][V];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      rx[u].unpack(v[u]);
+      if constexpr (HAS_RES) rr[u].unpack(rv[u]);
+    }
+    for (int k = 0; k < prog.n; ++k) {
+      const int code = prog.code[k];
+      const float pa = prog.a[k], pb = prog.b[k];
+#define FS_EACH(expr)                               \
+  _Pragma("unroll") for (int u = 0; u < U; ++u)     \
+    _Pragma("unroll") for (int i = 0; i < V; ++i) { \
+      const float t = v[u][i];                      \
+      v[u][i] = (expr);                             \
+    }
+      switch (code) {
+        case FS_OP_SCALE: FS_EACH(t * pa) break;
+        case FS_OP_SHIFT: FS_EACH(t + pa) break;
+        case FS_OP_ADD_BIAS: FS_EACH(t + bv[i]) break;
+        case FS_OP_MUL_COLUMN: FS_EACH(t * cv[i]) break;
+        case FS_OP_ADD_RESIDUAL:
+          if constexpr (HAS_RES) { FS_EACH(t + rv[u][i]) }
+          break;
+        case FS_OP_MUL_RESIDUAL:
+          if constexpr (HAS_RES) { FS_EACH(t * rv[u][i]) }
+          break;
+        // clamp and ReLU by comparisons, so that a NaN stays NaN (fminf and
+        // fmaxf would return the other operand)
+        case FS_OP_CLAMP: FS_EACH(t < pa ? pa : (t > pb ? pb : t)) break;
+        case FS_OP_GELU_ERF: FS_EACH(gelu_erf(t)) break;
+        case FS_OP_SIGMOID: FS_EACH(sigmoid(t)) break;
+        case FS_OP_RELU: FS_EACH(t < 0.f ? 0.f : t) break;
+        case FS_OP_TANH: FS_EACH(tanh_fn(t)) break;
+        case FS_OP_SILU: FS_EACH(t * sigmoid(t)) break;
+        default: FS_EACH(t >= 0.f ? t : pa * t) break;   // FS_OP_LEAKY_RELU
+      }
+#undef FS_EACH
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (r0 + u < rows) stv<T, V>(y + (r0 + u) * ld_y + c0, v[u]);
+  }
+}
+
+template <typename T, bool HAS_RES, bool VEC>
+hipError_t dispatch(const ProgramArgs& a, int cus, hipStream_t s) {
+  constexpr int V = VEC ? Elem<T>::kVec : 1;
+  const int64_t vecs = (a.cols + V - 1) / V;
+  const int col_blocks = int((vecs + kBlock - 1) / kBlock);
+  const int64_t target_blocks = int64_t(cus) * FS_PROG_BLOCKS_PER_CU;
+  auto go = [&](auto kern, int64_t grid) {
+    hipLaunchKernelGGL(kern, dim3(unsigned(grid)), dim3(kBlock), 0, s, static_cast<const T*>(a.x),
+                       a.ld_x, static_cast<const T*>(a.bias), static_cast<const T*>(a.col),
+                       static_cast<const T*>(a.res), a.ld_r, static_cast<T*>(a.y), a.ld_y, a.rows,
+                       int(a.cols), col_blocks, a.prog);
+    return hipGetLastError();
+  };
+  constexpr int U = FS_PROG_ROWS_PER_TRIP;
+  const int64_t row_groups_needed = (a.rows + U - 1) / U;
+  if (row_groups_needed < int64_t(cus) * 2) {
+    // small problem: one row per trip, as many blocks as rows (up to the target)
+    const int64_t r1 = a.rows < target_blocks ? a.rows : target_blocks;
+    return go(program_kernel<T, HAS_RES, VEC, 1>, r1 * col_blocks);
+  }
+  int64_t rg = target_blocks / col_blocks;
+  if (rg < 1) rg = 1;
+  if (rg > row_groups_needed) rg = row_groups_needed;
+  return go(program_kernel<T, HAS_RES, VEC, U>, rg * col_blocks);
+}
+
+template <typename T>
+hipError_t by_res(const ProgramArgs& a, int cus, hipStream_t s) {
+  if (a.res)
+    return a.vec ? dispatch<T, true, true>(a, cus, s) : dispatch<T, true, false>(a, cus, s);
+  return a.vec ? dispatch<T, false, true>(a, cus, s) : dispatch<T, false, false>(a, cus, s);
+}
+
+}  // namespace
+
+hipError_t launch_program(const ProgramArgs& a, int cus, hipStream_t s) {
+  return a.dtype == FS_BF16 ? by_res<uint16_t>(a, cus, s) : by_res<float>(a, cus, s);
+}
+
+}  // namespace fs

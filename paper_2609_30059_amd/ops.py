@@ -147,6 +147,53 @@ def pointwise_chain(x: torch.Tensor, bias: Optional[torch.Tensor] = None,
     return out
 
 
+def program_ops(ops) -> "ctypes.Array":
+    """An fs_op array from operations given as (name, *params) with the
+    names of fusedsub.h's fs_op_code in lower case (``("scale", 0.5)``,
+    ``("clamp", -1, 1)``, ``("gelu_erf",)``, ...)."""
+    ops = list(ops)
+    arr = (N.FsOp * max(len(ops), 1))()
+    for k, op in enumerate(ops):
+        name, prm = op[0], list(op[1:])
+        if name not in N.PROGRAM_OPS:
+            raise ValueError(f"unknown operation {name!r}")
+        code, n = N.PROGRAM_OPS[name]
+        if len(prm) != n:
+            raise ValueError(f"{name} takes {n} parameter(s), got {len(prm)}")
+        prm += [0.0] * (2 - n)
+        arr[k] = N.FsOp(code, float(prm[0]), float(prm[1]))
+    return arr
+
+
+def pointwise_program(x: torch.Tensor, ops, bias: Optional[torch.Tensor] = None,
+                      col: Optional[torch.Tensor] = None,
+                      residual: Optional[torch.Tensor] = None,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y = op_n(... op_1(x) ...) elementwise (fs_pointwise_program); see
+    ``program_ops`` for the form of ``ops``."""
+    ops = list(ops)
+    arr = program_ops(ops)
+    rows, cols, ld_x = as_rows(x)
+    if out is None:
+        out = torch.empty_like(x, memory_format=torch.contiguous_format)
+    _cuda(x=x, bias=bias, col=col, residual=residual, out=out)
+    ld_y = _like(out, x, "out")
+    ld_r = 0
+    if residual is not None:
+        if residual.shape != x.shape or residual.dtype != x.dtype:
+            raise ValueError("residual must match x")
+        ld_r = as_rows(residual)[2]
+    for name, v in (("bias", bias), ("col", col)):
+        if v is not None and v.dtype != x.dtype:
+            raise ValueError(f"{name} dtype must match x")
+        _vec(v, cols, name)
+    st = N.fs_pointwise_program(x.data_ptr(), ld_x, arr, len(ops), _ptr(bias), _ptr(col),
+                                _ptr(residual), ld_r, out.data_ptr(), ld_y, rows, cols,
+                                fs_dtype(x), _stream())
+    N.check("fs_pointwise_program", st)
+    return out
+
+
 def mask_dtype(m: torch.Tensor) -> int:
     """fs_dtype of a softmax mask: float32 and bfloat16 masks are additive;
     bool and uint8 masks are byte masks (FS_U8), where a nonzero element

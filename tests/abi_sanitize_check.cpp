@@ -15,6 +15,7 @@
 // Exit status 0 means every check passed; the sanitizers abort on their own
 // reports (-fno-sanitize-recover).
 #include <climits>
+#include <cmath>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -40,6 +41,7 @@ namespace rec {
 int launches = 0;
 hipError_t result = hipSuccess;
 fs::PointwiseArgs pw;
+fs::ProgramArgs pg;
 fs::SoftmaxArgs sm;
 fs::LayerNormArgs ln;
 fs::EpilogueArgs ep;
@@ -50,6 +52,7 @@ int64_t copy_bytes = 0;
 
 namespace fs {
 hipError_t launch_pointwise(const PointwiseArgs& a, int, hipStream_t) { ++rec::launches; rec::pw = a; return rec::result; }
+hipError_t launch_program(const ProgramArgs& a, int, hipStream_t) { ++rec::launches; rec::pg = a; return rec::result; }
 hipError_t launch_softmax(const SoftmaxArgs& a, int, hipStream_t) { ++rec::launches; rec::sm = a; return rec::result; }
 hipError_t launch_layernorm(const LayerNormArgs& a, int, hipStream_t) { ++rec::launches; rec::ln = a; return rec::result; }
 hipError_t launch_epilogue(const EpilogueArgs& a, int, hipStream_t) { ++rec::launches; rec::ep = a; return rec::result; }
@@ -103,6 +106,40 @@ static void fixed_cases() {
   rec::result = hipSuccess;
   EXPECT(pw(P(A), 64, nullptr, nullptr, 0, W(B), 64, 4, 64, 1.f, 0, 0) == FS_OK && fs_last_error_message()[0] == 0,
          "message cleared");
+
+  // pointwise program: operations validated and copied, operands it does
+  // not read dropped, the vector path for aligned rows
+  {
+    const fs_op chain[4] = {{FS_OP_ADD_BIAS, 0.f, 0.f}, {FS_OP_SCALE, 0.5f, 0.f},
+                            {FS_OP_CLAMP, -1.f, 1.f}, {FS_OP_GELU_ERF, 0.f, 0.f}};
+    EXPECT(fs_pointwise_program(P(A), 64, chain, 4, P(C), P(D), P(D + 4096), 64, W(B), 64, 4, 64,
+                                FS_F32, 0) == FS_OK &&
+               rec::pg.prog.n == 4 && rec::pg.prog.code[2] == FS_OP_CLAMP && rec::pg.prog.b[2] == 1.f &&
+               rec::pg.bias == P(C) && rec::pg.col == nullptr && rec::pg.res == nullptr && rec::pg.vec,
+           "program recorded");
+    EXPECT(fs_pointwise_program(P(A), 63, chain, 4, P(C), nullptr, nullptr, 0, W(B), 63, 4, 63, FS_F32, 0) ==
+               FS_OK && !rec::pg.vec, "odd width: element path");
+    EXPECT(fs_pointwise_program(P(A), 64, chain, 4, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32, 0) ==
+               FS_ERR_NULL_POINTER, "bias read but NULL");
+    EXPECT(fs_pointwise_program(P(A), 64, chain, 4, P(B + 64), nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32,
+                                0) == FS_ERR_ALIASING, "bias inside y");
+    const fs_op bad_clamp[1] = {{FS_OP_CLAMP, 1.f, -1.f}};
+    EXPECT(fs_pointwise_program(P(A), 64, bad_clamp, 1, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32,
+                                0) == FS_ERR_BAD_ARGUMENT, "clamp bounds out of order");
+    const fs_op open_clamp[1] = {{FS_OP_CLAMP, -INFINITY, 0.f}};
+    EXPECT(fs_pointwise_program(P(A), 64, open_clamp, 1, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32,
+                                0) == FS_OK, "one-sided clamp");
+    const fs_op bad_code[1] = {{13, 0.f, 0.f}};
+    EXPECT(fs_pointwise_program(P(A), 64, bad_code, 1, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32,
+                                0) == FS_ERR_BAD_ARGUMENT, "unknown code");
+    EXPECT(fs_pointwise_program(P(A), 64, chain, FS_PROGRAM_MAX_OPS + 1, P(C), nullptr, nullptr, 0, W(B), 64,
+                                4, 64, FS_F32, 0) == FS_ERR_BAD_ARGUMENT, "too many operations");
+    EXPECT(fs_pointwise_program(P(A), 64, nullptr, 0, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_BF16,
+                                0) == FS_OK && rec::pg.prog.n == 0, "empty program: a copy");
+    const fs_op res_op[1] = {{FS_OP_MUL_RESIDUAL, 0.f, 0.f}};
+    EXPECT(fs_pointwise_program(P(A), 64, res_op, 1, nullptr, nullptr, P(B), 64, W(B), 64, 4, 64, FS_BF16, 0) ==
+               FS_OK && rec::pg.res == P(B), "in place on the residual");
+  }
 
   // softmax
   EXPECT(fs_row_softmax(P(A), 128, P(C), 128, FS_BF16, W(B), 128, 4, 128, 0.125f, 0, FS_BF16, 0) == FS_OK, "ok");
@@ -258,6 +295,17 @@ static void sweep(int n) {
       EXPECT(st == FS_OK && !empty && rec::pw.rows == rows && rec::pw.cols == cols && rec::pw.ld_x == l1 &&
                  rec::pw.x == P(p1) && rec::pw.y == W(p4),
              "pointwise sweep %d", i);
+    }
+    before = rec::launches;
+    {
+      fs_op prog[FS_PROGRAM_MAX_OPS];
+      const int n_ops = int(next() % (FS_PROGRAM_MAX_OPS + 3)) - 1;   // -1 .. max + 1
+      for (fs_op& o : prog) o = fs_op{int32_t(next() % 15) - 1, pick_float(), pick_float()};
+      st = fs_pointwise_program(P(p1), l1, n_ops > 0 ? prog : nullptr, n_ops, P(p2), P(p3), P(p5), l2,
+                                W(p4), l3, rows, cols, fs_dtype(e2), 0);
+      if (rec::launches != before)
+        EXPECT(st == FS_OK && !empty && rec::pg.rows == rows && rec::pg.prog.n == n_ops,
+               "program sweep %d", i);
     }
     before = rec::launches;
     st = fs_row_softmax(P(p1), l1, P(p2), l2, fs_dtype(e3), W(p4), l3, rows, cols, f, pick_int(),

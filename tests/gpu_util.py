@@ -60,7 +60,8 @@ def assert_close(name, got, ref, atol, rtol):
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, f"{name}: shape {got.shape} vs {ref.shape}"
-    err = np.abs(got - ref)
+    with np.errstate(invalid="ignore"):          # inf - inf where both are infinite
+        err = np.abs(got - ref)
     ok = err <= atol + rtol * np.abs(ref)
     ok &= ~np.isnan(got)
     # identical infinities are equal

@@ -92,6 +92,56 @@ def test_pointwise_empty_problem_is_ok_without_pointers():
     assert N.fs_last_error_message() == ""
 
 
+# ---- pointwise program ---------------------------------------------------------
+def ops_array(*ops):
+    arr = (N.FsOp * max(len(ops), 1))()
+    for k, (code, a, b) in enumerate(ops):
+        arr[k] = N.FsOp(code, a, b)
+    return arr
+
+
+def pp(**kw):
+    a = dict(x=A, ld_x=64, ops=ops_array((2, 0.0, 0.0), (0, 0.5, 0.0), (6, -1.0, 1.0), (7, 0, 0)),
+             n_ops=4, bias=C, col=NULL, residual=NULL, ld_r=64, y=B, ld_y=64, rows=4, cols=64,
+             dtype=0, stream=None)
+    a.update(kw)
+    return N.fs_pointwise_program(**a)
+
+
+def test_pointwise_program_validation():
+    assert pp(dtype=2) == 4                                  # bytes are a mask dtype only
+    assert pp(n_ops=N.FS_PROGRAM_MAX_OPS + 1) == 6
+    assert pp(n_ops=-1) == 6
+    assert pp(ops=None) == 1
+    assert pp(ops=ops_array((13, 0, 0)), n_ops=1) == 6      # unknown code
+    assert pp(ops=ops_array((0, float("nan"), 0)), n_ops=1) == 6
+    assert pp(ops=ops_array((12, float("inf"), 0)), n_ops=1) == 6
+    assert pp(ops=ops_array((6, 1.0, -1.0)), n_ops=1) == 6  # clamp bounds out of order
+    assert pp(ops=ops_array((6, float("nan"), 1.0)), n_ops=1) == 6
+    assert pp(bias=NULL) == 1                                # the program adds a bias
+    assert pp(ops=ops_array((5, 0, 0)), n_ops=1) == 1       # it multiplies by a NULL residual
+    assert pp(ops=ops_array((3, 0, 0)), n_ops=1, bias=NULL) == 1   # and a NULL column vector
+    assert pp(ld_y=63) == 3
+    assert pp(x=A + 2) == 6
+    assert pp(bias=B + 64) == 5                              # bias inside y
+    assert pp(y=A + 4) == 5                                  # y partly over x
+    # checks that end before any HIP call: an empty problem, open clamp bounds
+    assert pp(rows=0, x=NULL, y=NULL) == 0
+    assert pp(ops=ops_array((6, float("-inf"), float("inf"))), n_ops=1, rows=0) == 0
+    assert pp(ops=None, n_ops=0, rows=0) == 0
+    # operations the program does not use leave their operands unread
+    assert pp(ops=ops_array((7, 0, 0)), n_ops=1, bias=NULL, rows=0) == 0
+
+
+def test_program_operation_table_matches_the_header():
+    txt = open(os.path.join(ROOT, "include", "fusedsub.h")).read()
+    codes = dict(re.findall(r"FS_OP_([A-Z_]+) = (\d+)", txt))
+    assert {k.lower(): int(v) for k, v in codes.items()} == \
+        {name: code for name, (code, _) in N.PROGRAM_OPS.items()}
+    m = re.search(r"#define FS_PROGRAM_MAX_OPS (\d+)", txt)
+    assert int(m.group(1)) == N.FS_PROGRAM_MAX_OPS
+
+
 # ---- softmax -----------------------------------------------------------------
 def sm(**kw):
     a = dict(x=A, ld_x=128, mask=NULL, ld_mask=128, mask_dtype=1, y=B, ld_y=128, rows=4,
