@@ -14,9 +14,10 @@
 // the rows, U rows per trip with all their loads issued before any use; the
 // column vectors (bias, col) stay in registers.  The program sits in the
 // kernel's argument block and is read with scalar loads: the operation loop
-// is uniform across the wave, outside the loops over the trip's U x V
-// values, so each operation costs one scalar branch per trip and the
-// arithmetic of the U x V values it applies to.
+// is uniform across the wave and runs once per group of rows of the trip
+// holding 16 values per lane (only they are live across it, which keeps the
+// register count low), so each operation costs a scalar load, a few compares
+// and branches per 16 values, and their arithmetic.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -45,6 +46,8 @@ __global__ __launch_bounds__(kBlock) void program_kernel(
     const T* x, int64_t ld_x, const T* __restrict__ bias, const T* __restrict__ col, const T* res,
     int64_t ld_r, T* y, int64_t ld_y, int64_t rows, int cols, int col_blocks, Program prog) {
   constexpr int V = VEC ? Elem<T>::kVec : 1;
+  constexpr int RG = 16 / V < U ? (16 / V > 0 ? 16 / V : 1) : U;   // rows per operation dispatch
+  static_assert(U % RG == 0, "row groups split the trip");
   const int cb = blockIdx.x % col_blocks;
   const int64_t rg = blockIdx.x / col_blocks;
   const int64_t nrg = gridDim.x / col_blocks;
@@ -76,47 +79,54 @@ __global__ __launch_bounds__(kBlock) void program_kernel(
       if constexpr (HAS_RES) rr[u].load(res + r * ld_r + c0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    float v[U][V], rv[HAS_RES ? U : 1][V];
+    // the trip's rows go through the program in groups of RG rows, RG x V =
+    // 16 values per lane (2 bf16 rows, 4 fp32 rows): each operation's
+    // dispatch is shared by 16 values while only those stay live across the
+    // operation loop
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      rx[u].unpack(v[u]);
-      if constexpr (HAS_RES) rr[u].unpack(rv[u]);
-    }
-    for (int k = 0; k < prog.n; ++k) {
-      const int code = prog.code[k];
-      const float pa = prog.a[k], pb = prog.b[k];
-#define FS_EACH(expr)                               \
-  _Pragma("unroll") for (int u = 0; u < U; ++u)     \
-    _Pragma("unroll") for (int i = 0; i < V; ++i) { \
-      const float t = v[u][i];                      \
-      v[u][i] = (expr);                             \
-    }
-      switch (code) {
-        case FS_OP_SCALE: FS_EACH(t * pa) break;
-        case FS_OP_SHIFT: FS_EACH(t + pa) break;
-        case FS_OP_ADD_BIAS: FS_EACH(t + bv[i]) break;
-        case FS_OP_MUL_COLUMN: FS_EACH(t * cv[i]) break;
-        case FS_OP_ADD_RESIDUAL:
-          if constexpr (HAS_RES) { FS_EACH(t + rv[u][i]) }
-          break;
-        case FS_OP_MUL_RESIDUAL:
-          if constexpr (HAS_RES) { FS_EACH(t * rv[u][i]) }
-          break;
-        // clamp and ReLU by comparisons, so that a NaN stays NaN (fminf and
-        // fmaxf would return the other operand)
-        case FS_OP_CLAMP: FS_EACH(t < pa ? pa : (t > pb ? pb : t)) break;
-        case FS_OP_GELU_ERF: FS_EACH(gelu_erf(t)) break;
-        case FS_OP_SIGMOID: FS_EACH(sigmoid(t)) break;
-        case FS_OP_RELU: FS_EACH(t < 0.f ? 0.f : t) break;
-        case FS_OP_TANH: FS_EACH(tanh_fn(t)) break;
-        case FS_OP_SILU: FS_EACH(t * sigmoid(t)) break;
-        default: FS_EACH(t >= 0.f ? t : pa * t) break;   // FS_OP_LEAKY_RELU
+    for (int u0 = 0; u0 < U; u0 += RG) {
+      float v[RG][V], rv[HAS_RES ? RG : 1][V];
+#pragma unroll
+      for (int g = 0; g < RG; ++g) {
+        rx[u0 + g].unpack(v[g]);
+        if constexpr (HAS_RES) rr[u0 + g].unpack(rv[g]);
       }
-#undef FS_EACH
+      for (int k = 0; k < prog.n; ++k) {
+        const int code = prog.code[k];
+        const float pa = prog.a[k], pb = prog.b[k];
+#define FS_EACH(expr)                               \
+  _Pragma("unroll") for (int g = 0; g < RG; ++g)    \
+    _Pragma("unroll") for (int i = 0; i < V; ++i) { \
+      const float t = v[g][i];                      \
+      v[g][i] = (expr);                             \
     }
+        switch (code) {
+          case FS_OP_SCALE: FS_EACH(t * pa) break;
+          case FS_OP_SHIFT: FS_EACH(t + pa) break;
+          case FS_OP_ADD_BIAS: FS_EACH(t + bv[i]) break;
+          case FS_OP_MUL_COLUMN: FS_EACH(t * cv[i]) break;
+          case FS_OP_ADD_RESIDUAL:
+            if constexpr (HAS_RES) { FS_EACH(t + rv[g][i]) }
+            break;
+          case FS_OP_MUL_RESIDUAL:
+            if constexpr (HAS_RES) { FS_EACH(t * rv[g][i]) }
+            break;
+          // clamp and ReLU by comparisons, so that a NaN stays NaN (fminf
+          // and fmaxf would return the other operand)
+          case FS_OP_CLAMP: FS_EACH(t < pa ? pa : (t > pb ? pb : t)) break;
+          case FS_OP_GELU_ERF: FS_EACH(gelu_erf(t)) break;
+          case FS_OP_SIGMOID: FS_EACH(sigmoid(t)) break;
+          case FS_OP_RELU: FS_EACH(t < 0.f ? 0.f : t) break;
+          case FS_OP_TANH: FS_EACH(tanh_fn(t)) break;
+          case FS_OP_SILU: FS_EACH(t * sigmoid(t)) break;
+          default: FS_EACH(t >= 0.f ? t : pa * t) break;   // FS_OP_LEAKY_RELU
+        }
+#undef FS_EACH
+      }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (r0 + u < rows) stv<T, V>(y + (r0 + u) * ld_y + c0, v[u]);
+      for (int g = 0; g < RG; ++g)
+        if (r0 + u0 + g < rows) stv<T, V>(y + (r0 + u0 + g) * ld_y + c0, v[g]);
+    }
   }
 }
 
