@@ -4,9 +4,9 @@
  *
  * A compiled model is a set of generated sub-kernels plus fixed vendor
  * library calls (KernelOPT, Def. 1 in Section 3).  The GEMMs stay library
- * calls; this library implements the generated part: fused pointwise chains,
- * row reductions (softmax, LayerNorm with residual) and GEMM epilogues with a
- * row reduction (Appendix A, Codegen and Fusion Agent prompts: epilogue
+ * calls; this library implements the generated part: fused pointwise chains
+ * and programs, row reductions (softmax, LayerNorm and RMSNorm with residual,
+ * sum, mean, max, argmax) and GEMM epilogues with a row reduction (Appendix A, Codegen and Fusion Agent prompts: epilogue
  * fusion, cross-reduction fusion, pointwise + pointwise, residual + norm).
  *
  * Conventions shared by every entry point
