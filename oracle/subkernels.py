@@ -330,10 +330,16 @@ def gemm_epilogue_reduce(c, bias=None, col_scale=None, act: str = "sigmoid",
 # plain row reductions
 # ---------------------------------------------------------------------------
 def row_reduce(x, op: str = "sum"):
-    """out[i] = sum_j x[i, j] ("sum"), that divided by cols ("mean") or
-    max_j x[i, j] ("max").  Section 6 lists sum/mean reductions among the
-    optimised sub-kernel classes; the reduction + pointwise fusion pattern is
-    in Appendix A (Fusion Agent)."""
+    """out[i] = sum_j x[i, j] ("sum"), that divided by cols ("mean"),
+    max_j x[i, j] ("max") or log sum_j exp(x[i, j]) ("logsumexp").  Section 6
+    lists sum/mean reductions among the optimised sub-kernel classes; the
+    reduction + pointwise fusion pattern is in Appendix A (Fusion Agent); the
+    paper's level-2 case study chains a linear layer with sum, max, mean and
+    log-sum-exp reductions along the row.
+
+    logsumexp is evaluated as m + log(sum_j exp(x[i, j] - m)) with m the row
+    maximum (the same value, without overflow): a row of -inf gives -inf, a
+    +inf entry gives +inf and a NaN gives NaN."""
     x = np.asarray(x, dtype=np.float64)
     if op == "sum":
         return x.sum(axis=1)
@@ -341,6 +347,15 @@ def row_reduce(x, op: str = "sum"):
         return x.sum(axis=1) / x.shape[1]
     if op == "max":
         return x.max(axis=1)
+    if op == "logsumexp":
+        m = x.max(axis=1)
+        out = np.empty(x.shape[0])
+        for i in range(x.shape[0]):
+            if np.isnan(m[i]) or np.isinf(m[i]):
+                out[i] = m[i]          # NaN, +inf, or a row of -inf
+            else:
+                out[i] = m[i] + math.log(np.exp(x[i] - m[i]).sum())
+        return out
     raise ValueError(f"unknown reduction {op!r}")
 
 

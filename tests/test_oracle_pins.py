@@ -580,6 +580,27 @@ class TestRowReduce:
 # ---------------------------------------------------------------------------
 # layout transform
 # ---------------------------------------------------------------------------
+    def test_logsumexp_closed_forms(self):
+        l3 = math.log(3.0)
+        x = np.array([[0.0, l3, -np.inf],          # log(1 + 3) = log 4
+                      [5.0, 5.0, 5.0],             # 5 + log 3
+                      [1000.0, 1000.0, -1000.0],   # no overflow: 1000 + log 2
+                      [-np.inf, -np.inf, -np.inf], # empty sum: -inf
+                      [1.0, np.inf, 0.0],          # +inf
+                      [np.nan, 0.0, 1.0]])         # NaN
+        y = oracle.row_reduce(x, "logsumexp")
+        np.testing.assert_allclose(y[:3], [math.log(4.0), 5.0 + l3, 1000.0 + math.log(2.0)],
+                                   rtol=1e-15)
+        assert y[3] == -np.inf and y[4] == np.inf and np.isnan(y[5])
+
+    def test_logsumexp_shift_and_bounds(self):
+        # lse(x + c) = lse(x) + c, and max <= lse <= max + log(cols)
+        rng = np.random.default_rng(8)
+        x = rng.standard_normal((6, 50)) * 4
+        y = oracle.row_reduce(x, "logsumexp")
+        np.testing.assert_allclose(oracle.row_reduce(x + 7.5, "logsumexp"), y + 7.5, rtol=1e-14)
+        assert np.all(x.max(axis=1) <= y) and np.all(y <= x.max(axis=1) + math.log(50))
+
 class TestStridedCopy:
     def test_head_split_is_a_numpy_transpose(self):
         # [tokens, 3, heads, dh] -> [3, heads, tokens, dh]; catches swapped
