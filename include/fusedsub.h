@@ -89,7 +89,12 @@ typedef enum fs_act {
 
 typedef enum fs_reduce { FS_REDUCE_SUM = 0, FS_REDUCE_MEAN = 1 } fs_reduce;
 
-typedef enum fs_row_op { FS_ROW_SUM = 0, FS_ROW_MEAN = 1, FS_ROW_MAX = 2 } fs_row_op;
+typedef enum fs_row_op {
+  FS_ROW_SUM = 0,
+  FS_ROW_MEAN = 1,
+  FS_ROW_MAX = 2,
+  FS_ROW_LOGSUMEXP = 3   /* added in ABI version 2 */
+} fs_row_op;
 
 /*
  * Fused pointwise chain (Appendix A, Fusion Agent: pointwise + pointwise and
@@ -281,11 +286,16 @@ FS_API fs_status fs_rmsnorm_residual(const void* x, int64_t ld_x, const void* re
  *   out[i] = sum_j x[i, j]   (FS_ROW_SUM)
  *          = that / cols     (FS_ROW_MEAN)
  *          = max_j x[i, j]   (FS_ROW_MAX; a NaN in the row gives NaN)
+ *          = log sum_j exp(x[i, j])   (FS_ROW_LOGSUMEXP, as m + log sum_j
+ *            exp(x[i, j] - m) with running maxima m, so it never overflows;
+ *            a row of -inf gives -inf, a +inf gives +inf, a NaN gives NaN;
+ *            the reductions the paper's level-2 case study chains after a
+ *            linear layer: sum, max, mean, log-sum-exp)
  *
  * x   : [rows, cols] of `dtype`, row stride ld_x.  Rows of any length: the
  *       row is streamed, not held in registers.
  * out : [rows] fp32, contiguous; must not overlap x.
- * cols == 0 with rows > 0: SUM writes zeros, MEAN and MAX return
+ * cols == 0 with rows > 0: SUM writes zeros, MEAN, MAX and LOGSUMEXP return
  * FS_ERR_BAD_SHAPE.
  */
 FS_API fs_status fs_row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op,

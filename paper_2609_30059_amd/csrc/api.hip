@@ -388,7 +388,8 @@ fs_status row_reduce(const void* x, int64_t ld_x, fs_dtype dtype, fs_row_op op, 
                      int64_t* out_i, int64_t rows, int64_t cols, hipStream_t stream) {
   clear_msg();
   if (!dtype_ok(dtype)) return fail(FS_ERR_UNSUPPORTED_DTYPE, "dtype=%d", int(dtype));
-  if (!out_i && op != FS_ROW_SUM && op != FS_ROW_MEAN && op != FS_ROW_MAX)
+  if (!out_i && op != FS_ROW_SUM && op != FS_ROW_MEAN && op != FS_ROW_MAX &&
+      op != FS_ROW_LOGSUMEXP)
     return fail(FS_ERR_BAD_ARGUMENT, "op=%d", int(op));
   fs_status st = check_shape(rows, cols, INT32_MAX / 2);
   if (st != FS_OK) return st;

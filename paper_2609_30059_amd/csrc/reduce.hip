@@ -1,5 +1,5 @@
-// Plain row reductions: sum, mean, max (fp32 out) and bit-exact argmax
-// (int64 out, lowest index on ties, first NaN wins).
+// Plain row reductions: sum, mean, max, log-sum-exp (fp32 out) and bit-exact
+// argmax (int64 out, lowest index on ties, first NaN wins).
 //
 // KernelOPT Section 6 counts sum/mean reductions among the optimised
 // sub-kernel classes; Appendix A (Executor prompt) asks for fp32 accumulation.
@@ -49,17 +49,38 @@ struct ArgP {
   }
 };
 
-constexpr int kOpSum = 0, kOpMax = 2, kOpArg = 3;   // MEAN runs as SUM
+// (m, s): the largest value seen and the sum of exp(v - m) over the values
+// seen, for a log-sum-exp.  Merging rescales the sum of the smaller maximum
+// by exp(m - M); a part whose maximum equals M keeps its sum as it is, so
+// infinite maxima merge without inf - inf.  NaN propagates through M.
+struct LseP {
+  float m, s;
+  __device__ __forceinline__ static float scaled(float s, float m, float M) {
+    const float ms = M == -INFINITY ? 0.f : M;   // all -inf: every sum is 0
+    return m == M ? s : s * __builtin_amdgcn_exp2f((m - ms) * kLog2e);
+  }
+  __device__ __forceinline__ static LseP combine(const LseP& a, const LseP& b) {
+    const float M = __builtin_elementwise_maximum(a.m, b.m);
+    return {M, scaled(a.s, a.m, M) + scaled(b.s, b.m, M)};
+  }
+  template <class F> __device__ __forceinline__ static LseP map(const LseP& a, F f) {
+    return {f(a.m), f(a.s)};
+  }
+};
+
+constexpr int kOpSum = 0, kOpMax = 2, kOpArg = 3, kOpLse = 4;   // MEAN runs as SUM
 
 template <int OP> struct AccOf;
 template <> struct AccOf<kOpSum> { using type = SumP; };
 template <> struct AccOf<kOpMax> { using type = MaxP; };
 template <> struct AccOf<kOpArg> { using type = ArgP; };
+template <> struct AccOf<kOpLse> { using type = LseP; };
 
 template <int OP>
 __device__ __forceinline__ typename AccOf<OP>::type identity() {
   if constexpr (OP == kOpSum) return SumP{0.f};
   else if constexpr (OP == kOpMax) return MaxP{-INFINITY};
+  else if constexpr (OP == kOpLse) return LseP{-INFINITY, 0.f};
   else return ArgP{-INFINITY, 0x7fffffff};
 }
 
@@ -75,6 +96,8 @@ __device__ __forceinline__ void accumulate(typename AccOf<OP>::type& acc, float 
     acc.s += v;
   } else if constexpr (OP == kOpMax) {
     acc.m = __builtin_elementwise_maximum(acc.m, v);
+  } else if constexpr (OP == kOpLse) {
+    acc = LseP::combine(acc, LseP{v, 1.f});
   } else {
     const bool upd = first || (!(v <= acc.v) && acc.v == acc.v);
     acc.v = upd ? v : acc.v;
@@ -128,17 +151,48 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
         rv[u].load(xr + (c0 < bend ? c0 : (SHIFT ? blast : clast)));
       }
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (OP == kOpLse) {
+        // the trip's values at once: their maximum tm, the sum of
+        // exp(v - tm) over them (independent terms), then one merge into the
+        // running pair -- about one exponential per value and one dependent
+        // merge per trip.  A value equal to tm counts 1 (so +inf does not
+        // meet inf - inf); vectors past the row end count nothing.
+        float vals[U][V];
+        float tm = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int c0 = h + ((t * U + u) * kThreads + tid) * V;
-        // the lane's first vector holds its lowest columns; if it lies past
-        // the row end, so do all the lane's vectors
-        const bool first = t == 0 && u == 0;
-        float v[V];
-        rv[u].unpack(v);
-        if (c0 < bend) {   // the whole vector is in the row (or body)
+        for (int u = 0; u < U; ++u) {
+          const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+          rv[u].unpack(vals[u]);
 #pragma unroll
-          for (int i = 0; i < V; ++i) accumulate<OP>(acc[i], v[i], c0 + i, first);
+          for (int i = 0; i < V; ++i)
+            tm = c0 < bend ? __builtin_elementwise_maximum(tm, vals[u][i]) : tm;
+        }
+        const float tms = tm == -INFINITY ? 0.f : tm;
+        float ts = 0.f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+#pragma unroll
+          for (int i = 0; i < V; ++i) {
+            const float e = vals[u][i] == tm ? 1.f
+                                             : __builtin_amdgcn_exp2f((vals[u][i] - tms) * kLog2e);
+            ts += c0 < bend ? e : 0.f;
+          }
+        }
+        acc[0] = LseP::combine(acc[0], LseP{tm, ts});
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+          // the lane's first vector holds its lowest columns; if it lies past
+          // the row end, so do all the lane's vectors
+          const bool first = t == 0 && u == 0;
+          float v[V];
+          rv[u].unpack(v);
+          if (c0 < bend) {   // the whole vector is in the row (or body)
+#pragma unroll
+            for (int i = 0; i < V; ++i) accumulate<OP>(acc[i], v[i], c0 + i, first);
+          }
         }
       }
     }
@@ -159,6 +213,7 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
     if (tid == 0) {
       if constexpr (OP == kOpArg) out_i[row] = tot.i;
       else if constexpr (OP == kOpSum) out_f[row] = tot.s * post_scale;
+      else if constexpr (OP == kOpLse) out_f[row] = tot.m + logf(tot.s);   // -inf + -inf, inf + log s
       else out_f[row] = tot.m;
     }
   }
@@ -199,6 +254,7 @@ template <typename T>
 hipError_t by_op(const ReduceArgs& a, bool argmax, int cus, hipStream_t s) {
   if (argmax) return by_path<T, kOpArg>(a, cus, s);
   if (a.op == FS_ROW_MAX) return by_path<T, kOpMax>(a, cus, s);
+  if (a.op == FS_ROW_LOGSUMEXP) return by_path<T, kOpLse>(a, cus, s);
   return by_path<T, kOpSum>(a, cus, s);
 }
 

@@ -306,7 +306,7 @@ def rmsnorm_residual(x: torch.Tensor, residual: Optional[torch.Tensor] = None,
 
 
 def row_reduce(x: torch.Tensor, op: str = "sum", out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Row sum / mean / max as float32 [rows]  (fs_row_reduce)."""
+    """Row sum / mean / max / logsumexp as float32 [rows]  (fs_row_reduce)."""
     rows, cols, ld_x = as_rows(x)
     if out is None:
         out = torch.empty(rows, dtype=torch.float32, device=x.device)

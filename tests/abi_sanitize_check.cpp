@@ -224,6 +224,10 @@ static void fixed_cases() {
   EXPECT(fs_row_reduce(P(A), 4096, FS_BF16, FS_ROW_SUM, of, 16, 4096, 0) == FS_OK && rec::rd.vec, "sum");
   EXPECT(fs_row_reduce(P(A), 4096, FS_BF16, fs_row_op(7), of, 16, 4096, 0) == FS_ERR_BAD_ARGUMENT, "op");
   EXPECT(fs_row_reduce(P(A), 0, FS_BF16, FS_ROW_MAX, of, 16, 0, 0) == FS_ERR_BAD_SHAPE, "max of nothing");
+  EXPECT(fs_row_reduce(P(A), 0, FS_BF16, FS_ROW_LOGSUMEXP, of, 16, 0, 0) == FS_ERR_BAD_SHAPE,
+         "log-sum-exp of nothing");
+  EXPECT(fs_row_reduce(P(A), 4096, FS_BF16, FS_ROW_LOGSUMEXP, of, 16, 4096, 0) == FS_OK &&
+             rec::rd.op == FS_ROW_LOGSUMEXP && rec::rd.vec, "log-sum-exp");
   EXPECT(fs_row_argmax(P(A), 4095, FS_BF16, oi, 16, 4095, 0) == FS_OK && rec::rd.out_i == oi && rec::rd.shifted,
          "argmax aligned body");
   EXPECT(fs_row_argmax(P(A), 4095, FS_BF16, nullptr, 16, 4095, 0) == FS_ERR_NULL_POINTER, "argmax out");

@@ -221,6 +221,8 @@ def test_row_reduce_and_argmax_validation():
     assert red(out=B + 2) == 6              # misaligned float*
     assert red(cols=0, op=1) == 2           # mean of nothing
     assert red(cols=0, op=2) == 2           # max of nothing
+    assert red(cols=0, op=3) == 2           # log-sum-exp of nothing
+    assert red(op=4) == 6                   # one past the last reduction
     assert red(rows=0, x=NULL, out=NULL) == 0
     assert arg(out=NULL) == 1
     assert arg(cols=0, ld_x=0) == 2

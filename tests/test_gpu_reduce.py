@@ -130,3 +130,48 @@ def test_strided_and_misaligned(dtype):
         np.testing.assert_array_equal(fs.row_argmax(g.view).cpu().numpy(), oracle.row_argmax(x.f64()))
         assert_close("sum", host64(fs.row_reduce(g.view, "sum")), oracle.row_reduce(x.f64(), "sum"),
                      sum_tol(x.f64()), 0)
+
+
+# log-sum-exp: LSE = m + log S with S = sum_j exp(x_j - m) >= 1, so its
+# absolute error is about the relative error of S -- fp32 terms from
+# v_exp_f32 (a few units of 2^-24 each) summed in fp32, sequentially per lane
+# and then in a tree -- plus the fp32 rounding of m + log S
+LSE_ATOL, LSE_RTOL = 2e-5, 2e-6
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_logsumexp_seeds(seed, dtype):
+    x = fd.row_inputs(seed, 97, 4096, dtype, mean=0.25, std=2.0)
+    announce("row_reduce logsumexp seeds", seed, dtype)
+    got = host64(fs.row_reduce(dev(x), "logsumexp"))
+    assert_close("logsumexp", got, oracle.row_reduce(x.f64(), "logsumexp"), LSE_ATOL, LSE_RTOL)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+# the vector path, the aligned body of odd rows, one element per lane, long rows
+@pytest.mark.parametrize("rows,cols", [(5, 1), (5, 3), (9, 8), (33, 1000), (33, 1003), (7, 9001),
+                                       (3, 70000), (2000, 64)])
+def test_logsumexp_widths(dtype, rows, cols):
+    x = fd.row_inputs(cols + rows, rows, cols, dtype, mean=-1.0, std=6.0)
+    announce("row_reduce logsumexp width", rows, cols, dtype)
+    got = host64(fs.row_reduce(dev(x), "logsumexp"))
+    assert_close(f"logsumexp {rows}x{cols}", got, oracle.row_reduce(x.f64(), "logsumexp"),
+                 LSE_ATOL, LSE_RTOL)
+
+
+def test_logsumexp_special_rows():
+    inf, nan = float("inf"), float("nan")
+    x = torch.full((8, 1024), -3.0, device="cuda")
+    x[0] = -inf                           # empty sum: -inf
+    x[1, 500] = inf                       # +inf
+    x[2, 7] = nan                         # NaN
+    x[3, 100:200] = -inf                  # masked entries add nothing
+    x[4] = 88.0                           # exp(88) near the fp32 limit: no overflow
+    x[5, 0] = 1e30                        # one huge entry: the row is that entry
+    x[6, :] = torch.arange(1024, device="cuda", dtype=torch.float32)   # rising maxima
+    x[7, :] = -torch.arange(1024, device="cuda", dtype=torch.float32)  # falling
+    got = host64(fs.row_reduce(x, "logsumexp"))
+    ref = oracle.row_reduce(host64(x), "logsumexp")
+    assert got[0] == -np.inf and got[1] == np.inf and np.isnan(got[2])
+    assert_close("finite rows", got[3:], ref[3:], LSE_ATOL, LSE_RTOL)
