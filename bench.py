@@ -212,6 +212,10 @@ def parse():
     ap.add_argument("--measured-at", default="", help="commit the counter runs measured")
     ap.add_argument("--commands", nargs=2, default=("", ""), metavar=("FETCH_CMD", "WRITE_CMD"),
                     help="the rocprofv3 commands of the two counter runs (recorded)")
+    ap.add_argument("--program-costs", action="store_true",
+                    help="pointwise programs of growing arithmetic against the fixed chain, and "
+                         "the row reductions (sum, max, log-sum-exp), each launch after a "
+                         "read-only 1 GiB pass")
     ap.add_argument("--long-rows", action="store_true",
                     help="time long-row softmax and LayerNorm/RMSNorm and print a Markdown table")
     ap.add_argument("--odd-rows", action="store_true",
@@ -729,6 +733,63 @@ ODD_ROW_CASES = (
     ("GEMM epilogue bf16 (sigmoid, row sum)", 2),
     ("row sum bf16", 2),
 )
+
+
+def program_costs(reps: int = 11) -> None:
+    """Median event interval of pointwise programs of growing arithmetic on
+    bf16 [16384, 4096] against the fixed chain, and of the row reductions on
+    bf16 [16384, 4096] and fp32 [8192, 4096]; every launch follows a
+    read-only pass over 1 GiB."""
+    import torch
+    import paper_2609_30059_amd as fs
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    x = (0.5 * torch.randn(16384, 4096, device="cuda", generator=g)).to(torch.bfloat16)
+    b = (0.02 * torch.randn(4096, device="cuda", generator=g)).to(torch.bfloat16)
+    y = torch.empty_like(x)
+    scrub = torch.zeros(8192, 65536, dtype=torch.bfloat16, device="cuda")
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    prog = lambda ops, **kw: (lambda: fs.pointwise_program(x, ops, out=y, **kw))   # noqa: E731
+    cases = [
+        ("fixed chain: none", 4, lambda: fs.pointwise_chain(x, None, None, 1.0, "none", out=y)),
+        ("fixed chain: bias + GELU", 4, lambda: fs.pointwise_chain(x, b, None, 1.0, "gelu_erf",
+                                                                   out=y)),
+        ("program: (empty, a copy)", 4, prog([])),
+        ("program: scale", 4, prog([("scale", 0.5)])),
+        ("program: GELU", 4, prog([("gelu_erf",)])),
+        ("program: bias, GELU", 4, prog([("add_bias",), ("gelu_erf",)], bias=b)),
+        ("program: bias, scale, GELU", 4, prog([("add_bias",), ("scale", 0.5), ("gelu_erf",)],
+                                               bias=b)),
+        ("program: bias, scale, clamp, GELU", 4,
+         prog([("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0), ("gelu_erf",)], bias=b)),
+        ("program: 8 x scale", 4, prog([("scale", 1.0)] * 8)),
+        ("program: GELU, GELU", 4, prog([("gelu_erf",), ("gelu_erf",)])),
+    ]
+    xf = (2 * torch.randn(8192, 4096, device="cuda", generator=g))
+    o = torch.empty(16384, device="cuda")
+    for name, t in (("bf16 [16384, 4096]", x), ("fp32 [8192, 4096]", xf)):
+        for op in ("sum", "max", "logsumexp"):
+            cases.append((f"row {op}, {name}", 0,
+                          (lambda t=t, op=op: fs.row_reduce(t, op, out=o[:t.shape[0]]))))
+    times = {n: [] for n, _, _ in cases}
+    for rep in range(reps + 1):            # the first repetition is a warm-up
+        for name, _, fn in cases:
+            fs.row_reduce(scrub, "sum", out=sink)
+            e0, e1 = TimingEvent(), TimingEvent()
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                times[name].append(e0.elapsed_time(e1) * 1e3)
+    print("| case | us (events) | GB/s | % of 8 TB/s |")
+    print("|---|---|---|---|")
+    for name, bpe, _ in cases:
+        us = sorted(times[name])[reps // 2]
+        nbytes = (x.numel() * bpe if bpe else
+                  (x.numel() * 2 if "bf16" in name else xf.numel() * 4))
+        gbs = nbytes / us / 1e3
+        print(f"| {name} | {us:.2f} | {gbs:.0f} | {100 * gbs / PEAK_HBM_GBS:.1f} |")
 
 
 def odd_rows(reps: int = 9) -> None:
@@ -1302,6 +1363,9 @@ def report_transient(trace_csv: str, log: str) -> None:
 
 def main():
     args = parse()
+    if args.program_costs:
+        program_costs()
+        return
     if args.long_rows:
         long_rows()
         return
