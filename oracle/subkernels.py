@@ -308,8 +308,10 @@ def gemm_epilogue_reduce(c, bias=None, col_scale=None, act: str = "sigmoid",
     """out[i] = reduce_j act((C[i, j] + bias[j]) * col_scale[j]).
 
     Appendix A (Codegen prompt: keep the matmul a library call, fuse only the
-    epilogue; Fusion Agent: reduction + pointwise).  ``reduce`` is "sum" or
-    "mean" over the columns.
+    epilogue; Fusion Agent: reduction + pointwise).  ``reduce`` is "sum",
+    "mean", "max" or "logsumexp" over the columns (the last two as in
+    ``row_reduce``: the reductions the paper's level-2 case study chains
+    after a linear layer).
     """
     c = np.asarray(c, dtype=np.float64)
     t = c
@@ -318,6 +320,8 @@ def gemm_epilogue_reduce(c, bias=None, col_scale=None, act: str = "sigmoid",
     if col_scale is not None:
         t = t * np.asarray(col_scale, dtype=np.float64)[None, :]
     v = apply_act(t, act)
+    if reduce in ("max", "logsumexp"):
+        return row_reduce(v, reduce)
     s = v.sum(axis=1)
     if reduce == "sum":
         return s

@@ -327,6 +327,21 @@ class TestLayerNorm:
 # a4 GEMM epilogue + row reduction
 # ---------------------------------------------------------------------------
 class TestEpilogue:
+    def test_max_and_logsumexp_reductions(self):
+        # C + b then * s, act, then the row's max or log-sum-exp: with
+        # relu over [-1, ln 3 - 1] + 1 -> [0, ln 3], max ln 3 and LSE log 4;
+        # sigmoid of 0 everywhere -> max 1/2 and LSE 1/2 + log(cols)
+        c = np.array([[-1.0, math.log(3.0) - 1.0]])
+        b, s = np.array([1.0, 1.0]), np.array([1.0, 1.0])
+        assert oracle.gemm_epilogue_reduce(c, b, s, "relu", "max")[0] == pytest.approx(
+            math.log(3.0), rel=1e-15)
+        assert oracle.gemm_epilogue_reduce(c, b, s, "relu", "logsumexp")[0] == pytest.approx(
+            math.log(4.0), rel=1e-15)
+        z = oracle.gemm_epilogue_reduce(np.zeros((2, 64)), None, None, "sigmoid", "logsumexp")
+        np.testing.assert_allclose(z, 0.5 + math.log(64.0), rtol=1e-15)
+        assert (oracle.gemm_epilogue_reduce(np.zeros((2, 64)), None, None, "sigmoid", "max")
+                == 0.5).all()
+
     def test_zero_input_gives_half_count(self):
         out = oracle.gemm_epilogue_reduce(np.zeros((3, 8192)), np.zeros(8192), np.ones(8192),
                                           "sigmoid", "sum")
