@@ -767,6 +767,15 @@ def program_costs(reps: int = 11) -> None:
     ]
     xf = (2 * torch.randn(8192, 4096, device="cuda", generator=g))
     o = torch.empty(16384, device="cuda")
+    # the GEMM epilogue with each reduction on a bf16 C [8192, 8192] (the sum
+    # and mean in one kernel family, max and log-sum-exp in another)
+    ce = (0.0256 * torch.randn(8192, 8192, device="cuda", generator=g)).to(torch.bfloat16)
+    be = (torch.rand(8192, device="cuda", generator=g) - 0.5).to(torch.bfloat16)
+    se = torch.rand(8192, device="cuda", generator=g) + 0.5
+    for red in ("sum", "max", "logsumexp"):
+        cases.append((f"epilogue sigmoid {red}, bf16 C [8192, 8192]", -1,
+                      (lambda red=red: fs.gemm_epilogue_reduce(ce, be, se, "sigmoid", red,
+                                                               out=o[:8192]))))
     for name, t in (("bf16 [16384, 4096]", x), ("fp32 [8192, 4096]", xf)):
         for op in ("sum", "max", "logsumexp"):
             cases.append((f"row {op}, {name}", 0,
@@ -786,7 +795,7 @@ def program_costs(reps: int = 11) -> None:
     print("|---|---|---|---|")
     for name, bpe, _ in cases:
         us = sorted(times[name])[reps // 2]
-        nbytes = (x.numel() * bpe if bpe else
+        nbytes = (x.numel() * bpe if bpe > 0 else ce.numel() * 2 if bpe < 0 else
                   (x.numel() * 2 if "bf16" in name else xf.numel() * 4))
         gbs = nbytes / us / 1e3
         print(f"| {name} | {us:.2f} | {gbs:.0f} | {100 * gbs / PEAK_HBM_GBS:.1f} |")

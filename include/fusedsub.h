@@ -87,7 +87,12 @@ typedef enum fs_act {
   FS_ACT_RELU = 3               /* max(z, 0)                                   */
 } fs_act;
 
-typedef enum fs_reduce { FS_REDUCE_SUM = 0, FS_REDUCE_MEAN = 1 } fs_reduce;
+typedef enum fs_reduce {
+  FS_REDUCE_SUM = 0,
+  FS_REDUCE_MEAN = 1,
+  FS_REDUCE_MAX = 2,        /* added in ABI version 2 */
+  FS_REDUCE_LOGSUMEXP = 3   /* added in ABI version 2 */
+} fs_reduce;
 
 typedef enum fs_row_op {
   FS_ROW_SUM = 0,
@@ -317,11 +322,15 @@ FS_API fs_status fs_row_argmax(const void* x, int64_t ld_x, fs_dtype dtype, int6
  *
  *   row_out[i] = reduce_j act((C[i, j] + bias[j]) * col_scale[j])
  *
+ * reduce: FS_REDUCE_SUM, FS_REDUCE_MEAN, FS_REDUCE_MAX (a NaN gives NaN) or
+ * FS_REDUCE_LOGSUMEXP (log sum_j exp(.), as max + log sum exp(. - max), so
+ * it never overflows; -inf for a row of -inf, +inf and NaN propagate): the
+ * reductions the paper's level-2 case study chains after a linear layer.
  * c         : [rows, cols] of c_dtype, row stride ld_c.
  * bias      : [cols] of bias_dtype, or NULL (0).
  * col_scale : [cols] fp32, or NULL (1).
  * row_out   : [rows] fp32 (contiguous).  With cols == 0 and rows > 0, SUM
- *             writes zeros and MEAN returns FS_ERR_BAD_SHAPE.
+ *             writes zeros and the other reductions return FS_ERR_BAD_SHAPE.
  * The sum is accumulated in fp32 (per-thread partial sums, then a tree).
  */
 FS_API fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype,

@@ -28,7 +28,7 @@ STATUS_NAMES = {0: "FS_OK", 1: "FS_ERR_NULL_POINTER", 2: "FS_ERR_BAD_SHAPE",
                 6: "FS_ERR_BAD_ARGUMENT", 7: "FS_ERR_HIP"}
 FS_F32, FS_BF16, FS_U8 = 0, 1, 2
 ACTS = {"none": 0, "gelu_erf": 1, "sigmoid": 2, "relu": 3}
-REDUCES = {"sum": 0, "mean": 1}
+REDUCES = {"sum": 0, "mean": 1, "max": 2, "logsumexp": 3}
 ROW_OPS = {"sum": 0, "mean": 1, "max": 2, "logsumexp": 3}
 FS_ABI_VERSION = 2
 FS_SOFTMAX_MAX_COLS = 16777216

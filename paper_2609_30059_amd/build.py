@@ -32,7 +32,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 
 FUSEDSUB_SOURCES = ["api.hip", "pointwise.hip", "program.hip", "softmax.hip", "layernorm.hip",
-                    "epilogue.hip", "reduce.hip", "copy.hip"]
+                    "epilogue.hip", "epilogue_maxlse.hip", "reduce.hip", "copy.hip"]
 HIP_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

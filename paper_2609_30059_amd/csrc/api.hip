@@ -461,14 +461,14 @@ fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype,
   if (!bias) bias_dtype = FS_F32;
   if (int(act) < FS_ACT_NONE || int(act) > FS_ACT_RELU)
     return fail(FS_ERR_BAD_ARGUMENT, "act=%d", int(act));
-  if (reduce != FS_REDUCE_SUM && reduce != FS_REDUCE_MEAN)
+  if (int(reduce) < FS_REDUCE_SUM || int(reduce) > FS_REDUCE_LOGSUMEXP)
     return fail(FS_ERR_BAD_ARGUMENT, "reduce=%d", int(reduce));
   fs_status st = check_shape(rows, cols, INT32_MAX / 2);
   if (st != FS_OK) return st;
   if ((st = check_ld("ld_c", ld_c, rows, cols)) != FS_OK) return st;
   if (rows == 0) return FS_OK;
-  if (cols == 0 && reduce == FS_REDUCE_MEAN)
-    return fail(FS_ERR_BAD_SHAPE, "mean over zero columns");
+  if (cols == 0 && reduce != FS_REDUCE_SUM)
+    return fail(FS_ERR_BAD_SHAPE, "this reduction needs cols >= 1");
   if (!row_out || (cols > 0 && !c)) return fail(FS_ERR_NULL_POINTER, "c and row_out are required");
   const int es = elem_size(c_dtype), bs = elem_size(bias_dtype);
   if (!aligned(c, es) || !aligned(bias, bs) || !aligned(col_scale, 4) || !aligned(row_out, 4))
@@ -487,7 +487,9 @@ fs_status fs_gemm_epilogue_reduce(const void* c, int64_t ld_c, fs_dtype c_dtype,
   a.shifted = !a.vec && cols >= 2 * vec_width(c_dtype);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
-  hipError_t e = fs::launch_epilogue(a, cus, stream);
+  hipError_t e = reduce == FS_REDUCE_MAX || reduce == FS_REDUCE_LOGSUMEXP
+                     ? fs::launch_epilogue_maxlse(a, cus, stream)
+                     : fs::launch_epilogue(a, cus, stream);
   return e == hipSuccess ? FS_OK : hip_fail(e, "gemm_epilogue_reduce launch");
 }
 

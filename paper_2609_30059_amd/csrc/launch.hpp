@@ -92,6 +92,8 @@ hipError_t launch_program(const ProgramArgs& a, int cus, hipStream_t s);
 hipError_t launch_softmax(const SoftmaxArgs& a, int cus, hipStream_t s);
 hipError_t launch_layernorm(const LayerNormArgs& a, int cus, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs& a, int cus, hipStream_t s);
+// FS_REDUCE_MAX and FS_REDUCE_LOGSUMEXP (epilogue_maxlse.hip)
+hipError_t launch_epilogue_maxlse(const EpilogueArgs& a, int cus, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int cus, hipStream_t s);
 
 struct CopyStridedArgs {

@@ -155,8 +155,7 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
         // the trip's values at once: their maximum tm, the sum of
         // exp(v - tm) over them (independent terms), then one merge into the
         // running pair -- about one exponential per value and one dependent
-        // merge per trip.  A value equal to tm counts 1 (so +inf does not
-        // meet inf - inf); vectors past the row end count nothing.
+        // merge per trip; vectors past the row end count nothing.
         float vals[U][V];
         float tm = -INFINITY;
 #pragma unroll
@@ -167,16 +166,29 @@ __global__ __launch_bounds__(64 * W * G) void reduce_kernel(
           for (int i = 0; i < V; ++i)
             tm = c0 < bend ? __builtin_elementwise_maximum(tm, vals[u][i]) : tm;
         }
-        const float tms = tm == -INFINITY ? 0.f : tm;
+        // exp(v - tm) as exp2((v - tm) log2e): the difference first, exact
+        // near the maximum at any magnitude (the one-fma form carries the
+        // rounding of tm log2e, which past |tm| ~ 1e9 overflows the
+        // exponent); a trip whose maximum is +inf counts its +inf values
+        // without inf - inf
         float ts = 0.f;
+        if (tm == INFINITY) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+          for (int u = 0; u < U; ++u) {
+            const int c0 = h + ((t * U + u) * kThreads + tid) * V;
 #pragma unroll
-          for (int i = 0; i < V; ++i) {
-            const float e = vals[u][i] == tm ? 1.f
-                                             : __builtin_amdgcn_exp2f((vals[u][i] - tms) * kLog2e);
-            ts += c0 < bend ? e : 0.f;
+            for (int i = 0; i < V; ++i) ts += c0 < bend && vals[u][i] == tm ? 1.f : 0.f;
+          }
+        } else {
+          const float tms = tm == -INFINITY ? 0.f : tm;
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const int c0 = h + ((t * U + u) * kThreads + tid) * V;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+              const float e = __builtin_amdgcn_exp2f((vals[u][i] - tms) * kLog2e);
+              ts += c0 < bend ? e : 0.f;
+            }
           }
         }
         acc[0] = LseP::combine(acc[0], LseP{tm, ts});

@@ -45,6 +45,7 @@ fs::ProgramArgs pg;
 fs::SoftmaxArgs sm;
 fs::LayerNormArgs ln;
 fs::EpilogueArgs ep;
+bool ep_maxlse = false;
 fs::ReduceArgs rd;
 fs::CopyStridedArgs cs;
 int64_t copy_bytes = 0;
@@ -55,7 +56,8 @@ hipError_t launch_pointwise(const PointwiseArgs& a, int, hipStream_t) { ++rec::l
 hipError_t launch_program(const ProgramArgs& a, int, hipStream_t) { ++rec::launches; rec::pg = a; return rec::result; }
 hipError_t launch_softmax(const SoftmaxArgs& a, int, hipStream_t) { ++rec::launches; rec::sm = a; return rec::result; }
 hipError_t launch_layernorm(const LayerNormArgs& a, int, hipStream_t) { ++rec::launches; rec::ln = a; return rec::result; }
-hipError_t launch_epilogue(const EpilogueArgs& a, int, hipStream_t) { ++rec::launches; rec::ep = a; return rec::result; }
+hipError_t launch_epilogue(const EpilogueArgs& a, int, hipStream_t) { ++rec::launches; rec::ep = a; rec::ep_maxlse = false; return rec::result; }
+hipError_t launch_epilogue_maxlse(const EpilogueArgs& a, int, hipStream_t) { ++rec::launches; rec::ep = a; rec::ep_maxlse = true; return rec::result; }
 hipError_t launch_reduce(const ReduceArgs& a, int, hipStream_t) { ++rec::launches; rec::rd = a; return rec::result; }
 hipError_t launch_copy(const void*, void*, int64_t bytes, int, hipStream_t) { ++rec::launches; rec::copy_bytes = bytes; return rec::result; }
 hipError_t launch_copy_strided(const CopyStridedArgs& a, int, hipStream_t) { ++rec::launches; rec::cs = a; return rec::result; }
@@ -139,6 +141,25 @@ static void fixed_cases() {
     const fs_op res_op[1] = {{FS_OP_MUL_RESIDUAL, 0.f, 0.f}};
     EXPECT(fs_pointwise_program(P(A), 64, res_op, 1, nullptr, nullptr, P(B), 64, W(B), 64, 4, 64, FS_BF16, 0) ==
                FS_OK && rec::pg.res == P(B), "in place on the residual");
+  }
+
+  // epilogue reductions: sum and mean in one kernel family, max and log-sum-exp in another
+  {
+    float* ofp = reinterpret_cast<float*>(W(D));
+    EXPECT(fs_gemm_epilogue_reduce(P(A), 8192, FS_BF16, P(B), FS_BF16, reinterpret_cast<const float*>(P(C)),
+                                   FS_ACT_SIGMOID, FS_REDUCE_SUM, ofp, 16, 8192, 0) == FS_OK && !rec::ep_maxlse,
+           "sum epilogue");
+    EXPECT(fs_gemm_epilogue_reduce(P(A), 8192, FS_BF16, P(B), FS_BF16, reinterpret_cast<const float*>(P(C)),
+                                   FS_ACT_RELU, FS_REDUCE_MAX, ofp, 16, 8192, 0) == FS_OK && rec::ep_maxlse &&
+               rec::ep.reduce == FS_REDUCE_MAX && rec::ep.vec && rec::ep.coef_vec,
+           "max epilogue");
+    EXPECT(fs_gemm_epilogue_reduce(P(A), 8192, FS_BF16, nullptr, FS_BF16, nullptr, FS_ACT_NONE,
+                                   FS_REDUCE_LOGSUMEXP, ofp, 16, 8192, 0) == FS_OK && rec::ep_maxlse &&
+               rec::ep.reduce == FS_REDUCE_LOGSUMEXP, "log-sum-exp epilogue");
+    EXPECT(fs_gemm_epilogue_reduce(P(A), 0, FS_BF16, nullptr, FS_BF16, nullptr, FS_ACT_NONE, FS_REDUCE_MAX, ofp,
+                                   16, 0, 0) == FS_ERR_BAD_SHAPE, "max over no columns");
+    EXPECT(fs_gemm_epilogue_reduce(P(A), 64, FS_BF16, nullptr, FS_BF16, nullptr, FS_ACT_NONE, fs_reduce(4), ofp,
+                                   16, 64, 0) == FS_ERR_BAD_ARGUMENT, "reduce out of range");
   }
 
   // softmax

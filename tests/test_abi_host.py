@@ -247,12 +247,15 @@ def test_epilogue_validation():
     assert ep(c_dtype=4) == 4
     assert ep(bias=C, bias_dtype=9) == 4
     assert ep(act=11) == 6
-    assert ep(reduce=3) == 6
+    assert ep(reduce=4) == 6                      # one past log-sum-exp
+    assert ep(reduce=-1) == 6
     assert ep(row_out=B + 2) == 6
     assert ep(row_out=A + 64) == 5                # row_out inside C
     assert ep(col_scale=B) == 5
     assert ep(rows=0, c=NULL, row_out=NULL) == 0
     assert ep(cols=0, reduce=1) == 2              # mean over zero columns
+    assert ep(cols=0, reduce=2) == 2              # max over zero columns
+    assert ep(cols=0, reduce=3) == 2              # log-sum-exp over zero columns
 
 
 def test_copy_validation():

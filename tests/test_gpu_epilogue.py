@@ -254,3 +254,52 @@ def test_rows_beyond_the_resident_waves(c_dtype, cols):
         for r0 in range(0, rows, 2048)])
     tol = max(SUM_ATOL * cols / 8192, 1e-5)
     assert_close(f"looping rows {cols}", host64(o), ref, tol, 1e-6)
+
+
+# max and log-sum-exp: the max is one of the fp32 values act((c + b) * s), so
+# it is within the fp32 rounding of that expression (a few units of 2^-24,
+# more through an activation's own error); log-sum-exp adds the relative
+# error of a sum of fp32 exponentials to it (see the row reduction tests)
+MAXLSE_ATOL, MAXLSE_RTOL = 2e-5, 2e-5
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("reduce", ["max", "logsumexp"])
+def test_max_and_logsumexp_reductions_five_seeds(seed, reduce):
+    d = fd.epilogue_inputs(seed, 128, 8192)
+    announce("epilogue", reduce, seed)
+    for act in ("none", "sigmoid", "gelu_erf", "relu"):
+        o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]), act, reduce)
+        ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                          act, reduce)
+        assert_close(f"{reduce} {act} seed {seed}", host64(o), ref, MAXLSE_ATOL, MAXLSE_RTOL)
+
+
+@pytest.mark.parametrize("reduce", ["max", "logsumexp"])
+@pytest.mark.parametrize("c_dtype,b_dtype", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
+                                             ("f32", "bf16")])
+# the vector path, odd widths (element-wise), one column, long rows
+@pytest.mark.parametrize("cols", [1, 7, 1000, 1003, 8192, 40000])
+def test_max_and_logsumexp_widths_and_dtypes(reduce, c_dtype, b_dtype, cols):
+    rows = 600 if cols <= 1003 else 40     # 600 rows: blocks loop over rows
+    d = fd.epilogue_inputs(cols, rows, cols, c_dtype, c_std=2.0, bias_dtype=b_dtype)
+    announce("epilogue width", reduce, c_dtype, b_dtype, cols)
+    o = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]), "none", reduce)
+    ref = oracle.gemm_epilogue_reduce(d["c"].f64(), d["bias"].f64(), d["col_scale"].f64(),
+                                      "none", reduce)
+    assert_close(f"{reduce} {c_dtype}/{b_dtype} {cols}", host64(o), ref, MAXLSE_ATOL, MAXLSE_RTOL)
+
+
+def test_max_and_logsumexp_special_values():
+    c = torch.zeros(6, 4096, device="cuda")
+    c[0] = -float("inf")                     # a row of -inf
+    c[1, 9] = float("inf")
+    c[2, 100] = float("nan")
+    c[3, :] = 50.0                           # all equal: max 50, LSE 50 + log 4096
+    c[4, 17] = 1e30                          # one huge entry
+    c[5, ::2] = -float("inf")                # half masked
+    for reduce in ("max", "logsumexp"):
+        o = host64(fs.gemm_epilogue_reduce(c, None, None, "none", reduce))
+        ref = oracle.gemm_epilogue_reduce(host64(c), None, None, "none", reduce)
+        assert o[0] == -np.inf and o[1] == np.inf and np.isnan(o[2]), (reduce, o[:3])
+        assert_close(f"{reduce} finite rows", o[3:], ref[3:], MAXLSE_ATOL, MAXLSE_RTOL)

@@ -175,3 +175,16 @@ def test_logsumexp_special_rows():
     ref = oracle.row_reduce(host64(x), "logsumexp")
     assert got[0] == -np.inf and got[1] == np.inf and np.isnan(got[2])
     assert_close("finite rows", got[3:], ref[3:], LSE_ATOL, LSE_RTOL)
+
+
+def test_logsumexp_huge_magnitudes():
+    # maxima far past the exponent range of exp2: the difference is taken
+    # before the scaling, so the row's maximum contributes exactly 1
+    x = torch.full((4, 2048), 0.0, device="cuda")
+    x[0, 5] = 1e30
+    x[1, :] = -1e30
+    x[2, ::3] = 3e38
+    x[3, :] = 2e9
+    got = host64(fs.row_reduce(x, "logsumexp"))
+    ref = oracle.row_reduce(host64(x), "logsumexp")
+    assert_close("huge magnitudes", got, ref, LSE_ATOL, LSE_RTOL)
