@@ -135,7 +135,7 @@ FS_API fs_status fs_pointwise_chain(const void* x, int64_t ld_x, const void* bia
  * during the call (the caller keeps ownership); a and b as listed, finite
  * (clamp bounds may be infinite, with a <= b), else FS_ERR_BAD_ARGUMENT.
  * Rows of whole 16-byte vectors are read and written 16 bytes at a time;
- * other rows element by element.
+ * other rows element by element.  Added in ABI version 2.
  */
 #define FS_PROGRAM_MAX_OPS 16
 typedef enum fs_op_code {
