@@ -6,13 +6,17 @@
 // Design (gfx950): one row per group of W wave64s; each thread holds EPT
 // elements of the row in registers, so HBM is read once and written once.
 // Per thread: logits a = x * scale + mask, the local max m, and the local
-// sum d of 2^(a*log2e - m*log2e) with the exponentials kept in registers.
-// The exponent is one fma, a*log2e - m', with m' = m*log2e rounded once, so
-// large logits keep full relative accuracy in their differences.  A single
-// all-reduce combines the (m', d) pairs:
-//     (m1, d1) + (m2, d2) = (M, d1 * 2^(m1 - M) + d2 * 2^(m2 - M)),  M = max
+// sum d of exp(a - m) = 2^((a - m) log2 e) with the exponentials kept in
+// registers.  The difference is taken before the scaling: exact near the
+// maximum at any magnitude, so large logits keep full relative accuracy and
+// rows filled with the most negative finite value (a common mask) stay
+// finite.  (An exponent formed as one fma, a log2e - round(m log2e), carries
+// the rounding of m log2e, which overflows the exponent once |m| passes
+// about 1.5e9, or m log2e itself overflows.)  A single all-reduce combines
+// the (m, d) pairs:
+//     (m1, d1) + (m2, d2) = (M, d1 * e^(m1 - M) + d2 * e^(m2 - M)),  M = max
 // with m = -inf acting as the identity (never evaluating -inf - -inf).  The
-// output is the stored exponential times 2^(m' - M) / D: one exp2 per element.
+// output is the stored exponential times e^(m - M) / D: one exp2 per element.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -65,7 +69,7 @@ struct MaxSumP {
     if (M == -INFINITY) return {-INFINITY, 0.f};
     const bool a_big = a.m > b.m;
     const float big = a_big ? a.d : b.d, small = a_big ? b.d : a.d;
-    const float e = __builtin_amdgcn_exp2f(-fabsf(a.m - b.m));   // 2^-inf = 0
+    const float e = __builtin_amdgcn_exp2f(-fabsf(a.m - b.m) * kLog2e);   // 2^-inf = 0
     return {M, fmaf(small, e, big)};
   }
   template <class F> __device__ __forceinline__ static MaxSumP map(const MaxSumP& a, F f) {
@@ -281,17 +285,19 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       Multi<SumP, R> sm;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        // M' = M log2(e) rounded once; an all-masked row keeps 0 (its
-        // exponentials are exp2(-inf) = 0)
-        const float ml2 = mx.p[r].m == -INFINITY ? 0.f : mx.p[r].m * kLog2e;
+        // exp((a - M)) as exp2((a - M) log2 e), the difference first: exact
+        // near the maximum at any magnitude (a row masked with the most
+        // negative finite value included); an all-masked row keeps M = 0
+        // (its exponentials are exp2(-inf) = 0)
+        const float ms = mx.p[r].m == -INFINITY ? 0.f : mx.p[r].m;
         float d = 0.f;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
-          a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2));
+          a[r][i] = __builtin_amdgcn_exp2f((a[r][i] - ms) * kLog2e);
           d += a[r][i];
         }
         if constexpr (SHIFT) {
-          ae[r] = __builtin_amdgcn_exp2f(fmaf(ae[r], kLog2e, -ml2));
+          ae[r] = __builtin_amdgcn_exp2f((ae[r] - ms) * kLog2e);
           d += ae[r];
         }
         sm.p[r].s = d;
@@ -301,8 +307,9 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
       for (int r = 0; r < R; ++r)
         f[r] = sm.p[r].s > 0.f ? __builtin_amdgcn_rcpf(sm.p[r].s) : 0.f;   // D >= 1 when live
     } else {
-      // Multi-wave rows: local (m', d) per thread in base-2 units with the
-      // exponentials kept in a[], one all-reduce of the pairs across waves
+      // Multi-wave rows: local (m, d) per thread with the exponentials
+      // exp2((a - m) log2 e) kept in a[], one all-reduce of the pairs across
+      // waves
       using P = Multi<MaxSumP, R>;
       P part;
       bool empty[R];
@@ -313,15 +320,15 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 #pragma unroll
         for (int i = 0; i < EPT; ++i) m = fmaxf(m, a[r][i]);
         empty[r] = (m == -INFINITY);
-        ml2[r] = empty[r] ? 0.f : m * kLog2e;   // m' (0 for an all-masked slice)
+        ml2[r] = empty[r] ? 0.f : m;   // the slice's max (0 for an all-masked slice)
         float d = 0.f;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
-          a[r][i] = __builtin_amdgcn_exp2f(fmaf(a[r][i], kLog2e, -ml2[r]));   // exp2(-inf) = 0
+          a[r][i] = __builtin_amdgcn_exp2f((a[r][i] - ml2[r]) * kLog2e);   // exp2(-inf) = 0
           d += a[r][i];
         }
         if constexpr (SHIFT) {
-          ae[r] = __builtin_amdgcn_exp2f(fmaf(ae[r], kLog2e, -ml2[r]));
+          ae[r] = __builtin_amdgcn_exp2f((ae[r] - ml2[r]) * kLog2e);
           d += ae[r];
         }
         part.p[r] = MaxSumP{empty[r] ? -INFINITY : ml2[r], d};
@@ -334,7 +341,7 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
         // 0*inf); a fully masked row has M = -inf and comes out all zeros
         const MaxSumP p = tot.p[r];
         f[r] = (empty[r] || p.m == -INFINITY) ? 0.f
-                                              : __builtin_amdgcn_exp2f(ml2[r] - p.m) / p.d;
+                                              : __builtin_amdgcn_exp2f((ml2[r] - p.m) * kLog2e) / p.d;
       }
     }
 
@@ -371,13 +378,13 @@ __global__ __launch_bounds__(64 * W * G) void softmax_kernel(
 // block of 16 waves per row keeps the exponentials of its first 64*16*CL
 // columns in LDS (fp32, CL per lane) and of the next 64*16*CR columns in
 // registers, so those columns are read from HBM once; with TAIL, the `tail`
-// slots per lane past both are streamed: read once for the running (m', d)
-// and again for the outputs.  Pass 1 runs one online (m', d) per lane over the LDS part,
+// slots per lane past both are streamed: read once for the running (m, d)
+// and again for the outputs.  Pass 1 runs one online (m, d) per lane over the LDS part,
 // the register part and the tail, combined once across the block; each
-// cached slot group keeps 2^(a*log2e - mg), mg the lane's running max after
-// the group.  Pass 2 writes 2^(a*log2e - M) / D as e * 2^(mg - M) / D from
-// the registers and from LDS (one product per element), and recomputes it
-// for the re-read tail.
+// cached slot group keeps exp(a - mg), mg the lane's running max after the
+// group.  Pass 2 writes exp(a - M) / D as e * exp(mg - M) / D from the
+// registers and from LDS (one product per element), and recomputes it for
+// the re-read tail.
 // Each lane reads back only the LDS words it wrote, so the cache needs no
 // barrier.  One block per compute unit holds one row at a time, so the loads
 // of the next row's first slot groups are issued before the block-wide
@@ -497,25 +504,27 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
 #pragma unroll
       for (int i = 0; i < V; ++i) a[i] = (c0 + i <= cur.lim) ? xv[i] : -INFINITY;
     };
-    // merge N logits into the lane's running (m', d); with KEEP the logits
-    // are replaced by their exponentials 2^(a*log2e - m'), m' the running max
-    // after this merge (returned), so pass 2 needs one product per element
+    // merge N logits into the lane's running (m, d); with KEEP the logits
+    // are replaced by their exponentials exp2((a - m) log2 e), m the running
+    // max after this merge (returned), so pass 2 needs one product per
+    // element; differences are taken before the scaling (exact near the
+    // maximum at any magnitude)
     float mrun = -INFINITY, drun = 0.f;
     auto absorb = [&](auto kn, auto keep, float* a) {
       constexpr int N = decltype(kn)::value;
       float tm = -INFINITY;
 #pragma unroll
       for (int i = 0; i < N; ++i) tm = fmaxf(tm, a[i]);
-      const float mnew = fmaxf(mrun, tm == -INFINITY ? -INFINITY : tm * kLog2e);
+      const float mnew = fmaxf(mrun, tm);
       const float msafe = mnew == -INFINITY ? 0.f : mnew;
       float dt = 0.f;
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -msafe));
+        const float e = __builtin_amdgcn_exp2f((a[i] - msafe) * kLog2e);
         dt += e;
         if constexpr (decltype(keep)::value) a[i] = e;
       }
-      drun = fmaf(drun, __builtin_amdgcn_exp2f(mrun - msafe), dt);   // 2^-inf = 0
+      drun = fmaf(drun, __builtin_amdgcn_exp2f((mrun - msafe) * kLog2e), dt);   // 2^-inf = 0
       mrun = mnew;
       return msafe;
     };
@@ -600,12 +609,12 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     auto emit = [&](int slot, const float* a) {
       float o[V];
 #pragma unroll
-      for (int i = 0; i < V; ++i) o[i] = __builtin_amdgcn_exp2f(fmaf(a[i], kLog2e, -M)) * inv_d;
+      for (int i = 0; i < V; ++i) o[i] = __builtin_amdgcn_exp2f((a[i] - M) * kLog2e) * inv_d;
       store_until(yr, col_of(slot), cur.wendb, o);
     };
     // a cached slot: its exponentials times 2^(mg - M) / D (at most 1 / D)
     auto emit_e = [&](int slot, const float* e) {
-      const float f = __builtin_amdgcn_exp2f(mg[slot / G] - M) * inv_d;
+      const float f = __builtin_amdgcn_exp2f((mg[slot / G] - M) * kLog2e) * inv_d;
       float o[V];
 #pragma unroll
       for (int i = 0; i < V; ++i) o[i] = e[i] * f;
@@ -639,7 +648,7 @@ __global__ __launch_bounds__(1024) void softmax_cached_kernel(
     }
     if constexpr (SHIFT) {
       if (has_x && ce < cur.wend) {
-        const float o = __builtin_amdgcn_exp2f(fmaf(ax, kLog2e, -M)) * inv_d;
+        const float o = __builtin_amdgcn_exp2f((ax - M) * kLog2e) * inv_d;
         stv<T, 1>(yr + ce, &o);
       }
     }

@@ -240,3 +240,26 @@ def test_huge_causal_q_len(q_len):
     ref = oracle.row_softmax(d["x"].f64(), None, 0.5, causal_q_len=q_len)
     np.testing.assert_array_equal(ref, 0.0)
     np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("cols", [64, 4096, 40000, 70000])
+def test_extreme_finite_logits_and_lowest_value_masks(cols):
+    # rows masked with the most negative finite value (a common padding
+    # mask), rows whose maximum is far past 1e9, and a fully masked row: the
+    # exponent differences are formed before the scaling, so every row stays
+    # finite and matches the oracle (a fully lowest-masked row is uniform)
+    low = float(np.finfo(np.float32).min)
+    x = torch.zeros(6, cols, device="cuda")
+    x[0, :] = low                                   # every position masked
+    x[1, : cols // 2] = low
+    x[2, :] = 1e30
+    x[2, 1] = 1e30 * (1 - 2 ** -20)
+    x[3, :] = 3e38
+    x[4, :] = torch.linspace(-5e9, 5e9, cols, device="cuda")
+    x[5, 3] = -3e9
+    announce("softmax extreme logits", cols)
+    y = host64(fs.row_softmax(x, None, 1.0))
+    ref = oracle.row_softmax(host64(x), None, 1.0)
+    assert np.isfinite(y).all()
+    assert_close(f"extreme logits {cols}", y, ref, *TOL["f32"])
+    np.testing.assert_allclose(y[0], 1.0 / cols, rtol=1e-5)
