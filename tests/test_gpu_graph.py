@@ -93,7 +93,7 @@ def capture(step):
 
 
 def test_subkernels_captured_in_one_graph():
-    announce("graph: every sub-kernel entry point")
+    announce("graph: every sub-kernel entry point and mode")
     dev = "cuda"
     gen = torch.Generator(device=dev).manual_seed(0)
 
@@ -121,6 +121,12 @@ def test_subkernels_captured_in_one_graph():
     xq = rnd(77, 5000)
     # head split of a [96, 3 * 4 * 64] projection
     qkv = rnd(96, 768, dtype=BF)
+    # a byte mask, a pointwise program with a bias and a residual
+    mb = torch.rand(257, 4096, device=dev, generator=gen) < 0.1
+    mb[:, 0] = False
+    xg2, rg2 = rnd(200, 2048, dtype=BF), rnd(200, 2048, dtype=BF)
+    bg2 = rnd(2048, dtype=BF, s=0.1)
+    prog = [("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0), ("gelu_erf",), ("add_residual",)]
 
     outs = {
         "pw": torch.empty_like(xp), "gelu": torch.empty_like(xg), "sm": torch.empty_like(xs),
@@ -130,6 +136,9 @@ def test_subkernels_captured_in_one_graph():
         "max": torch.empty(77, device=dev),
         "arg": torch.empty(77, dtype=torch.int64, device=dev),
         "heads": torch.empty(12, 96, 64, dtype=BF, device=dev),
+        "sm_bytes": torch.empty_like(xs), "prog": torch.empty_like(xg2),
+        "lse": torch.empty(77, device=dev), "ep_max": torch.empty(300, device=dev),
+        "ep_lse": torch.empty(300, device=dev),
     }
 
     def step():
@@ -146,12 +155,17 @@ def test_subkernels_captured_in_one_graph():
         fs.row_argmax(xq, out=outs["arg"])
         fs.copy_strided(outs["heads"], qkv, rows=96, cols=64, batch=12, ld_src=768,
                         stride_src=64, ld_dst=64, stride_dst=96 * 64)
+        fs.row_softmax(xs, mb, 0.125, out=outs["sm_bytes"])
+        fs.pointwise_program(xg2, prog, bias=bg2, residual=rg2, out=outs["prog"])
+        fs.row_reduce(xq, "logsumexp", out=outs["lse"])
+        fs.gemm_epilogue_reduce(ce, be, se, "sigmoid", "max", out=outs["ep_max"])
+        fs.gemm_epilogue_reduce(ce, be, se, "sigmoid", "logsumexp", out=outs["ep_lse"])
 
     g = capture(step)
 
     def refill():
         for t, s in ((xp, 1.0), (xs, 3.0), (xl, 1.0), (ce, 1.0), (xq, 1.0), (qkv, 1.0),
-                     (sc, 1.0)):
+                     (sc, 1.0), (xg2, 1.0)):
             t.copy_((s * torch.randn(t.shape, device=dev, generator=gen)).to(t.dtype))
 
     replay_and_check(g, step, list(outs.values()), refill=refill)
