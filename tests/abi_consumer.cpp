@@ -11,6 +11,10 @@
 //   softmax    x, mask (bf16)               -> y          fs_row_softmax
 //   layernorm  x, residual, gamma, beta     -> y, res_out fs_layernorm_residual
 //   epilogue   c, bias (bf16), scale (f32)  -> out (f32)  fs_gemm_epilogue_reduce, sigmoid sum
+//   program    x, bias, col, residual (bf16) -> y         fs_pointwise_program; the
+//              operations come from <dir>/ops.txt, one "code a b" line each
+//   softmax_u8 x (bf16), mask (u8)          -> y          fs_row_softmax, byte mask
+//   logsumexp  x (bf16)                     -> out (f32)  fs_row_reduce, FS_ROW_LOGSUMEXP
 // Exits 0 on success; on any failure prints the status and exits 1.
 #include <hip/hip_runtime_api.h>
 
@@ -87,7 +91,9 @@ struct Dev {
 }  // namespace
 
 int main(int argc, char** argv) {
-  if (argc != 3) die("usage: abi_consumer <pointwise|softmax|layernorm|epilogue> <dir>");
+  if (argc != 3)
+    die("usage: abi_consumer <pointwise|softmax|layernorm|epilogue|program|softmax_u8|logsumexp>"
+        " <dir>");
   const std::string kase = argv[1];
   g_dir = argv[2];
   int64_t rows = 0, cols = 0;
@@ -137,6 +143,39 @@ int main(int argc, char** argv) {
                                   static_cast<const float*>(s.p), FS_ACT_SIGMOID, FS_REDUCE_SUM,
                                   static_cast<float*>(out.p), rows, cols, null_stream),
           "fs_gemm_epilogue_reduce");
+    hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    write_file("out.bin", out.host());
+  } else if (kase == "program") {
+    std::vector<fs_op> ops;
+    {
+      const std::string path = g_dir + "/ops.txt";
+      FILE* f = std::fopen(path.c_str(), "r");
+      if (!f) die("cannot open ops.txt");
+      int code = 0;
+      double a = 0, b = 0;
+      while (std::fscanf(f, "%d %lf %lf", &code, &a, &b) == 3)
+        ops.push_back(fs_op{code, float(a), float(b)});
+      std::fclose(f);
+    }
+    Dev x(read_file("x.bin", n * 2)), b(read_file("bias.bin", size_t(cols) * 2)),
+        c(read_file("col.bin", size_t(cols) * 2)), r(read_file("residual.bin", n * 2)), y(n * 2);
+    fs_ok(fs_pointwise_program(x.p, cols, ops.data(), int(ops.size()), b.p, c.p, r.p, cols, y.p,
+                               cols, rows, cols, FS_BF16, null_stream),
+          "fs_pointwise_program");
+    hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    write_file("y.bin", y.host());
+  } else if (kase == "softmax_u8") {
+    Dev x(read_file("x.bin", n * 2)), m(read_file("mask.bin", n)), y(n * 2);
+    fs_ok(fs_row_softmax(x.p, cols, m.p, cols, FS_U8, y.p, cols, rows, cols, float(p1),
+                         int64_t(p2), FS_BF16, null_stream),
+          "fs_row_softmax");
+    hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    write_file("y.bin", y.host());
+  } else if (kase == "logsumexp") {
+    Dev x(read_file("x.bin", n * 2)), out(size_t(rows) * 4);
+    fs_ok(fs_row_reduce(x.p, cols, FS_BF16, FS_ROW_LOGSUMEXP, static_cast<float*>(out.p), rows,
+                        cols, null_stream),
+          "fs_row_reduce");
     hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize");
     write_file("out.bin", out.host());
   } else {

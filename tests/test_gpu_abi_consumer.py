@@ -18,6 +18,7 @@ import torch
 import fusedsub_data as fd
 import oracle
 import paper_2609_30059_amd as fs
+from paper_2609_30059_amd import _native as N
 from paper_2609_30059_amd.build import ABI_CONSUMER
 from gpu_util import (TOL, announce, assert_close, bf16_ulp_close, dev, host64,
                       softmax_supplementary)
@@ -133,4 +134,57 @@ def test_gemm_epilogue_sigmoid_sum(tmp_path):
     assert_close("epilogue via the C ABI (sum)", out.astype(np.float64), ref, SUM_ATOL, 0.0)
     ot = fs.gemm_epilogue_reduce(dev(d["c"]), dev(d["bias"]), dev(d["col_scale"]), "sigmoid",
                                  "sum")
+    np.testing.assert_array_equal(out.view(np.uint32), bits_of(ot))
+
+
+def test_pointwise_program_bf16(tmp_path):
+    # the paper's group after a linear layer (bias, multiply, hardtanh, GELU)
+    # with a column multiply, a residual and a leaky ReLU around it; the
+    # fs_op array is built by the C++ program from "code a b" lines
+    rows, cols = 300, 1000
+    ops = [("mul_column",), ("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0), ("gelu_erf",),
+           ("add_residual",), ("leaky_relu", 0.05)]
+    d = fd.pointwise_inputs(16, rows, cols, "bf16")
+    col = fd.Tensor(np.ascontiguousarray(d["bias"].data[::-1]), "bf16")
+    lines = []
+    for op in ops:
+        prm = list(op[1:]) + [0.0] * (2 - len(op[1:]))
+        lines.append(f"{N.PROGRAM_OPS[op[0]][0]} {prm[0]!r} {prm[1]!r}")
+    (tmp_path / "ops.txt").write_text("\n".join(lines) + "\n")
+    run_consumer("program", tmp_path, rows, cols, 0, 0,
+                 {"x": d["x"].data, "bias": d["bias"].data, "col": col.data,
+                  "residual": d["residual"].data})
+    yb = load(tmp_path, "y", np.uint16, (rows, cols))
+    ref = oracle.pointwise_program(d["x"].f64(), ops, d["bias"].f64(), col.f64(),
+                                   d["residual"].f64())
+    assert_close("program via the C ABI", fd.bf16_bits_to_f64(yb), ref, *TOL["bf16"])
+    yt = fs.pointwise_program(dev(d["x"]), ops, bias=dev(d["bias"]), col=dev(col),
+                              residual=dev(d["residual"]))
+    np.testing.assert_array_equal(yb, bits_of(yt))
+
+
+def test_byte_mask_softmax_bf16(tmp_path):
+    rows, cols = 257, 4096
+    d = fd.softmax_inputs(17, rows, cols, "bf16", mask_dtype="u8")
+    run_consumer("softmax_u8", tmp_path, rows, cols, d["scale"], 0,
+                 {"x": d["x"].data, "mask": d["mask"].data})
+    yb = load(tmp_path, "y", np.uint16, (rows, cols))
+    got = fd.bf16_bits_to_f64(yb)
+    ref = oracle.row_softmax(d["x"].f64(), oracle.byte_mask_additive(d["mask"].data), d["scale"])
+    assert_close("byte-mask softmax via the C ABI", got, ref, *TOL["bf16"])
+    softmax_supplementary("byte-mask softmax via the C ABI", got, ref, d["mask"].data != 0)
+    yt = fs.row_softmax(dev(d["x"]), dev(d["mask"]), d["scale"])
+    np.testing.assert_array_equal(yb, bits_of(yt))
+
+
+def test_row_logsumexp_bf16(tmp_path):
+    rows, cols = 300, 8192
+    x = fd.row_inputs(18, rows, cols, "bf16", mean=0.25, std=2.0)
+    run_consumer("logsumexp", tmp_path, rows, cols, 0, 0, {"x": x.data})
+    out = load(tmp_path, "out", np.float32, (rows,))
+    # the bound of the row-reduce tests: the relative error of the fp32 sum
+    # S >= 1 of exp(x - max) terms, plus the rounding of max + log S
+    assert_close("logsumexp via the C ABI", out.astype(np.float64),
+                 oracle.row_reduce(x.f64(), "logsumexp"), 2e-5, 2e-6)
+    ot = fs.row_reduce(dev(x), "logsumexp")
     np.testing.assert_array_equal(out.view(np.uint32), bits_of(ot))
