@@ -737,7 +737,8 @@ ODD_ROW_CASES = (
 
 def program_costs(reps: int = 11) -> None:
     """Median event interval of pointwise programs of growing arithmetic on
-    bf16 [16384, 4096] against the fixed chain, and of the row reductions on
+    bf16 [16384, 4096] against the fixed chain (and on rows of 4095 columns),
+    of the GEMM epilogue's reductions, and of the row reductions on
     bf16 [16384, 4096] and fp32 [8192, 4096]; every launch follows a
     read-only pass over 1 GiB."""
     import torch
@@ -764,6 +765,34 @@ def program_costs(reps: int = 11) -> None:
          prog([("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0), ("gelu_erf",)], bias=b)),
         ("program: 8 x scale", 4, prog([("scale", 1.0)] * 8)),
         ("program: GELU, GELU", 4, prog([("gelu_erf",), ("gelu_erf",)])),
+    ]
+    # rows of 4095 columns (not whole 16-byte vectors): the aligned-body path
+    # where x and y start each row at one phase, the element-wise path where
+    # y sits one element further (bytes per element scaled to [16384, 4095])
+    xo = x[:, :4095].contiguous()
+    yo = torch.empty_like(xo)
+    ye = torch.empty(xo.numel() + 1, dtype=xo.dtype, device="cuda")[1:].view(xo.shape)
+    odd = 4 * 4095 / 4096
+    bg = [("add_bias",), ("gelu_erf",)]
+    cases += [
+        ("fixed chain: bias + GELU, [16384, 4095]", odd,
+         lambda: fs.pointwise_chain(xo, b[:4095], None, 1.0, "gelu_erf", out=yo)),
+        ("program: (empty), [16384, 4095]", odd, lambda: fs.pointwise_program(xo, [], out=yo)),
+        ("program: (empty), [16384, 4095], y at another phase (element-wise)", odd,
+         lambda: fs.pointwise_program(xo, [], out=ye)),
+        ("program: bias, scale, [16384, 4095]", odd,
+         lambda: fs.pointwise_program(xo, [("add_bias",), ("scale", 0.5)], bias=b[:4095],
+                                      out=yo)),
+        ("program: bias, scale, [16384, 4095], y at another phase (element-wise)", odd,
+         lambda: fs.pointwise_program(xo, [("add_bias",), ("scale", 0.5)], bias=b[:4095],
+                                      out=ye)),
+        ("program: bias, GELU, [16384, 4095]", odd,
+         lambda: fs.pointwise_program(xo, bg, bias=b[:4095], out=yo)),
+        ("program: bias, GELU, [16384, 4095], y at another phase (element-wise)", odd,
+         lambda: fs.pointwise_program(xo, bg, bias=b[:4095], out=ye)),
+        ("program: bias, scale, clamp, GELU, [16384, 4095]", odd,
+         lambda: fs.pointwise_program(xo, [("add_bias",), ("scale", 0.5), ("clamp", -1.0, 1.0),
+                                           ("gelu_erf",)], bias=b[:4095], out=yo)),
     ]
     xf = (2 * torch.randn(8192, 4096, device="cuda", generator=g))
     o = torch.empty(16384, device="cuda")

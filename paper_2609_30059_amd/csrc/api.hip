@@ -249,6 +249,9 @@ fs_status fs_pointwise_program(const void* x, int64_t ld_x, const fs_op* ops, in
   a.vec = cols % vec_width(dtype) == 0 && vec_ok(x, ld_x, es) && vec_ok(y, ld_y, es) &&
           vec_ok(residual, ld_r, es) && (bias == nullptr || aligned(bias, 16)) &&
           (col == nullptr || aligned(col, 16));
+  // bias and col are staged element by element: their alignment does not matter
+  a.shifted = !a.vec && cols >= 2 * vec_width(dtype) && same_phase(x, ld_x, y, ld_y, es) &&
+              same_phase(x, ld_x, residual, ld_r, es);
   int cus = 0;
   if ((st = device_cus(&cus)) != FS_OK) return st;
   hipError_t e = fs::launch_program(a, cus, stream);

@@ -85,6 +85,7 @@ struct ProgramArgs {
   int64_t rows, cols;
   fs_dtype dtype;
   bool vec;
+  bool shifted = false;   // not vec, rows of at least two 16-byte vectors, one phase
   Program prog;
 };
 

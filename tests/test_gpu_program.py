@@ -161,3 +161,68 @@ def test_relu_keeps_nan_in_the_fixed_chain_and_the_epilogue(dtype):
     c[2, 100] = float("nan")
     o = host64(fs.gemm_epilogue_reduce(c, None, None, "relu", "sum"))
     assert np.isnan(o[2]) and (o[[0, 1, 3, 4]] == 0).all()
+
+
+PROGRAMS = {
+    "every": EVERY_OP,
+    "bias_only": [("scale", 1.5), ("add_bias",), ("gelu_erf",)],
+    "column_only": [("mul_column",), ("tanh",), ("add_residual",)],
+    "plain": [("shift", 0.25), ("silu",), ("clamp", -0.5, 2.0)],
+}
+
+
+def bits(t):
+    return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+# rows that are not whole 16-byte vectors: the aligned body (rows of at
+# least two vectors), with several trips of four rows per block and a ragged
+# last trip ([5001, 1003]), wide rows of several column blocks, and rows of
+# 9 columns (two fp32 vectors; fewer than two bf16 vectors: element-wise)
+@pytest.mark.parametrize("shape", [(5001, 1003), (130, 4099), (2050, 17), (3000, 9)])
+@pytest.mark.parametrize("prog", sorted(PROGRAMS))
+def test_odd_width_rows(dtype, shape, prog):
+    ops = PROGRAMS[prog]
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    d, col = inputs(shape[0] + shape[1], *shape, dtype)
+    announce("program odd rows", shape, dtype, prog)
+    x, b, c, r = dev(d["x"]), dev(d["bias"]), dev(col), dev(d["residual"])
+    y = fs.pointwise_program(x, ops, bias=b, col=c, residual=r)
+    ref = oracle.pointwise_program(d["x"].f64(), ops, d["bias"].f64(), col.f64(),
+                                   d["residual"].f64())
+    assert_close(f"{shape} {dtype} {prog}", host64(y), ref, *TOL[dtype])
+    # y one element into a wider buffer: its rows sit at another phase than
+    # x's, which takes the element-wise path -- the same fp32 arithmetic per
+    # element, so the same bits
+    buf = torch.zeros(shape[0] * shape[1] + 1, dtype=tdt, device="cuda")
+    ye = buf[1:].view(shape)
+    fs.pointwise_program(x, ops, bias=b, col=c, residual=r, out=ye)
+    np.testing.assert_array_equal(bits(y), bits(ye))
+    assert buf[0].item() == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_odd_width_rows_in_place_and_strided(dtype):
+    # x, residual and y in strided buffers whose rows start at one phase that
+    # changes from row to row (ld 1011): the aligned body in place on x and
+    # on the residual, nothing outside the rows written
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows, cols, ld = 1500, 1001, 1011
+    ops = [("mul_column",), ("add_residual",), ("gelu_erf",), ("add_bias",), ("mul_residual",)]
+    d, col = inputs(rows + cols, rows, cols, dtype)
+    announce("program odd rows in place", dtype)
+    ref = oracle.pointwise_program(d["x"].f64(), ops, d["bias"].f64(), col.f64(),
+                                   d["residual"].f64())
+    for target in ("x", "residual"):
+        xg = Guarded(rows, cols, ld, tdt, offset=3)
+        xg.view.copy_(dev(d["x"]))
+        rg = Guarded(rows, cols, ld, tdt, offset=3)
+        rg.view.copy_(dev(d["residual"]))
+        out = xg.view if target == "x" else rg.view
+        fs.pointwise_program(xg.view, ops, bias=dev(d["bias"]), col=dev(col), residual=rg.view,
+                             out=out)
+        torch.cuda.synchronize()
+        assert_close(f"in place on {target}", host64(out), ref, *TOL[dtype])
+        xg.check_untouched("x")
+        rg.check_untouched("residual")
