@@ -120,7 +120,9 @@ static void fixed_cases() {
                rec::pg.bias == P(C) && rec::pg.col == nullptr && rec::pg.res == nullptr && rec::pg.vec,
            "program recorded");
     EXPECT(fs_pointwise_program(P(A), 63, chain, 4, P(C), nullptr, nullptr, 0, W(B), 63, 4, 63, FS_F32, 0) ==
-               FS_OK && !rec::pg.vec, "odd width: element path");
+               FS_OK && !rec::pg.vec && rec::pg.shifted, "odd width, one phase: aligned body");
+    EXPECT(fs_pointwise_program(P(A), 63, chain, 4, P(C), nullptr, nullptr, 0, W(B), 63, 4, 7, FS_F32, 0) ==
+               FS_OK && !rec::pg.vec && !rec::pg.shifted, "rows under two vectors: element path");
     EXPECT(fs_pointwise_program(P(A), 64, chain, 4, nullptr, nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32, 0) ==
                FS_ERR_NULL_POINTER, "bias read but NULL");
     EXPECT(fs_pointwise_program(P(A), 64, chain, 4, P(B + 64), nullptr, nullptr, 0, W(B), 64, 4, 64, FS_F32,
